@@ -1,0 +1,380 @@
+"""Pins of the fp64 oracle against facts fixed by the paper and by mathematics.
+
+Each test checks the oracle through a route that does not reuse its code:
+closed forms, invariants, dense-matrix forms stated in the paper, numerical
+minimisation, brute-force sorting, or library routines on tiny inputs.
+"""
+import math
+
+import numpy as np
+import pytest
+from scipy.special import softmax
+
+from paper_2606_14782_amd import inputs
+
+TOL = 1e-12
+
+
+def _box(x, k):
+    """Centred, truncated box mean by a full numpy convolution."""
+    n, h, ones = len(x), k // 2, np.ones(k)
+    num = np.convolve(x, ones, mode="full")[h:h + n]
+    den = np.convolve(np.ones(n), ones, mode="full")[h:h + n]
+    return num / den
+
+
+def _rand(shape, seed, scale=1.0):
+    return (np.random.default_rng(seed).standard_normal(shape) * scale).astype(np.float32)
+
+
+# --------------------------------------------------------------- window scores
+
+def test_attention_rows_sum_to_one_and_are_causal(oracle):
+    """Softmax rows (Sec. 4.1, causal A) sum to 1 and vanish past their position."""
+    G, W, d, n = 3, 6, 16, 41
+    o = oracle.scores(_rand((G, W, d), 1), _rand((n, d), 2), want_attn=True)
+    A = o["attn"]
+    assert np.allclose(A.sum(axis=2), 1.0, atol=TOL, rtol=0)
+    for w in range(W):
+        t = n - W + w
+        assert np.all(A[:, w, t + 1:] == 0.0)
+        assert np.all(A[:, w, :t + 1] > 0.0)
+
+
+def test_scores_match_dense_masked_softmax(oracle):
+    """B and Q equal a dense masked softmax of the full logit block (library route)."""
+    G, W, d, n = 3, 5, 16, 37
+    q, k = _rand((G, W, d), 3), _rand((n, d), 4)
+    logits = np.einsum("gwc,ic->gwi", q.astype(np.float64), k.astype(np.float64)) / math.sqrt(d)
+    pos = n - W + np.arange(W)
+    mask = np.arange(n)[None, :] > pos[:, None]
+    logits = np.where(mask[None], -np.inf, logits)
+    A = softmax(logits, axis=2)
+    o = oracle.scores(q, k)
+    assert np.allclose(o["B"], A.mean(axis=(0, 1)), atol=TOL, rtol=0)
+    assert np.allclose(o["Q"], A[:, W - 1, :].mean(axis=0), atol=TOL, rtol=0)
+    from scipy.special import logsumexp
+    lse = logsumexp(logits, axis=2)
+    assert np.allclose(o["lse"], lse, atol=1e-12, rtol=0)
+
+
+def test_identical_keys_closed_form(oracle):
+    """All keys equal: A_{t,i} = 1/(t+1), so B and Q have exact rational forms."""
+    G, W, d, n = 2, 4, 8, 23
+    k = np.tile(_rand((1, d), 5), (n, 1))
+    o = oracle.scores(_rand((G, W, d), 6), k)
+    t = n - W + np.arange(W)
+    B_cf = np.array([sum(1.0 / (tw + 1) for tw in t if tw >= i) / W for i in range(n)])
+    assert np.allclose(o["B"], B_cf, atol=TOL, rtol=0)
+    assert np.allclose(o["Q"], 1.0 / n, atol=TOL, rtol=0)
+
+
+def test_window_and_last_query_scores_sum_to_one(oracle):
+    """B averages W probability rows (causal zeros included), so sum B = sum Q = 1."""
+    o = oracle.scores(_rand((4, 8, 32), 7), _rand((300, 32), 8))
+    assert abs(o["B"].sum() - 1.0) < 1e-12 and abs(o["Q"].sum() - 1.0) < 1e-12
+
+
+def test_gqa_scores_are_group_means(oracle):
+    """Group averaging: B, Q of a G=2 group are the means of the single-head B, Q."""
+    W, d, n = 5, 16, 50
+    q, k = _rand((2, W, d), 9), _rand((n, d), 10)
+    both = oracle.scores(q, k)
+    s0, s1 = oracle.scores(q[:1], k), oracle.scores(q[1:], k)
+    assert np.allclose(both["B"], (s0["B"] + s1["B"]) / 2, atol=TOL, rtol=0)
+    assert np.allclose(both["Q"], (s0["Q"] + s1["Q"]) / 2, atol=TOL, rtol=0)
+    dup = oracle.scores(np.concatenate([q[:1], q[:1]]), k)
+    assert np.allclose(dup["B"], s0["B"], atol=TOL, rtol=0)
+
+
+# --------------------------------------------------------------- residual E
+
+def test_residual_is_half_total_variation(oracle):
+    """E = [Q-B]_+ with sum Q = sum B = 1 gives sum E = |Q-B|_1 / 2 (Eq. boundary_residual)."""
+    o = oracle.scores(_rand((1, 8, 16), 11), _rand((120, 16), 12))
+    E = oracle.residual(o["B"], o["Q"])
+    assert np.all(E >= 0)
+    assert abs(E.sum() - 0.5 * np.abs(o["Q"] - o["B"]).sum()) < 1e-14
+    assert np.all(E[o["Q"] <= o["B"]] == 0.0)
+    assert not np.any(np.signbit(E)), "E must be +0, never -0"
+    m = o["Q"] > o["B"]
+    assert np.allclose(E[m], (o["Q"] - o["B"])[m], atol=0, rtol=0)
+
+
+# --------------------------------------------------------------- coherence L
+
+def _dense_P(n, r):
+    """The row-normalised neighbourhood operator built from its set definition."""
+    P = np.zeros((n, n))
+    for i in range(n):
+        nb = [u for u in range(n) if abs(u - i) <= r]
+        P[i, nb] = 1.0 / len(nb)
+    return P
+
+
+@pytest.mark.parametrize("n,r", [(1, 5), (7, 0), (20, 1), (40, 5), (12, 30)])
+def test_coherence_equals_dense_operator(oracle, n, r):
+    E = np.random.default_rng(n + r).random(n)
+    assert np.allclose(oracle.coherence(E, r), _dense_P(n, r) @ E, atol=TOL, rtol=0)
+
+
+def test_coherence_delta_response_and_fixed_point(oracle):
+    n, r, j = 30, 5, 2
+    E = np.zeros(n)
+    E[j] = 1.0
+    L = oracle.coherence(E, r)
+    for i in range(n):
+        cnt = min(n - 1, i + r) - max(0, i - r) + 1
+        assert L[i] == pytest.approx(1.0 / cnt if abs(i - j) <= r else 0.0, abs=TOL)
+    assert L[0] == pytest.approx(1.0 / (r + 1), abs=TOL)   # boundary row divides by r+1
+    assert np.allclose(oracle.coherence(np.full(n, 3.25), r), 3.25, atol=TOL, rtol=0)
+
+
+# --------------------------------------------------------------- pooling
+
+@pytest.mark.parametrize("n,k", [(1, 7), (9, 1), (50, 5), (50, 7), (6, 13)])
+def test_pool_matches_convolution(oracle, n, k):
+    x = np.random.default_rng(n * k).random(n)
+    ref = _box(x, k)
+    assert np.allclose(oracle.pool(x, k), ref, atol=TOL, rtol=0)
+    if k == 1:
+        assert np.array_equal(oracle.pool(x, k), x)
+
+
+# --------------------------------------------------------------- top-k
+
+@pytest.mark.parametrize("n,k,levels", [(1, 1, 3), (10, 3, 2), (64, 16, 5), (200, 50, 7),
+                                        (33, 40, 4), (25, 0, 3)])
+def test_topk_equals_bruteforce_sort_with_ties(oracle, n, k, levels):
+    """Exactly min(k, n) indices; order (score desc, index asc), emitted ascending."""
+    x = np.random.default_rng(n + k).integers(0, levels, n).astype(np.float64)
+    ref = sorted(sorted(range(n), key=lambda i: (-x[i], i))[:k])
+    got = oracle.topk(x, k)
+    assert got.tolist() == ref
+    assert len(got) == min(k, n)
+
+
+# --------------------------------------------------------------- lambda
+
+def _msel(B, n_cand, M):
+    return sorted(range(n_cand), key=lambda i: (-B[i], i))[:M]
+
+
+def test_lambda_is_argmin_of_objective(oracle):
+    """Closed form (Eq. lambda_solution) = numerical argmin of Eq. lambda_objective."""
+    rng = np.random.default_rng(13)
+    n, K, gamma = 300, 20, 0.7
+    B, V = rng.random(n), rng.random(n) * 5
+    n_cand = n - 10
+    o = oracle.lambda_(B, V, n_cand, K, rho=2.0, gamma=gamma, eps=0.0)
+    sel = _msel(B, n_cand, 2 * K)
+    sb, sv = np.std(B[sel]), np.std(V[sel])
+
+    def f(lam):
+        return (np.std(lam * V[sel]) - gamma * sb) ** 2
+
+    lo, hi = 0.0, 10.0 * gamma * sb / sv
+    phi = (math.sqrt(5) - 1) / 2
+    for _ in range(200):
+        a, b = hi - phi * (hi - lo), lo + phi * (hi - lo)
+        if f(a) < f(b):
+            hi = b
+        else:
+            lo = a
+    assert o["lambda"] == pytest.approx((lo + hi) / 2, rel=1e-6)
+    assert o["m_count"] == 2 * K
+    assert o["sigma_B"] == pytest.approx(sb, rel=1e-12)
+    assert o["sigma_V"] == pytest.approx(sv, rel=1e-12)
+
+
+def test_lambda_scale_invariance_and_set_size(oracle):
+    rng = np.random.default_rng(14)
+    B, V = rng.random(100), rng.random(100)
+    a = oracle.lambda_(B, V, 90, 10, eps=0.0)
+    b = oracle.lambda_(B, 8.0 * V, 90, 10, eps=0.0)
+    assert b["lambda"] == pytest.approx(a["lambda"] / 8.0, rel=1e-13)
+    # M = min(rho K, |I|): a budget larger than half the candidates clamps M
+    c = oracle.lambda_(B, V, 30, 20)
+    assert c["m_count"] == 30
+    assert oracle.lambda_(B, V, 0, 20)["lambda"] == 0.0
+    z = oracle.lambda_(B, np.zeros(100), 90, 10)
+    assert z["sigma_V"] == 0.0 and math.isfinite(z["lambda"])
+
+
+# --------------------------------------------------------------- whole layers
+
+def _wl_small(**kw):
+    base = inputs.Workload("pin", 6, 4, 2, 16, 4, 3, "fp32", (60, 45), (8, 50),
+                           ((5, 40), (5, 30)), 1, 1234)
+    return base.with_(**kw)
+
+
+def _run(oracle, wl, params=None, layers=None):
+    p = oracle.Prompt.for_workload(wl, params)
+    outs, ins = [], []
+    for l in range(layers or wl.num_layers):
+        x = inputs.layer_inputs(wl, l)
+        ins.append(x)
+        outs.append(p.layer(l, x["q_win"], x["k"]))
+    return p, outs, ins
+
+
+def test_persistence_uses_the_causal_layer_set(oracle):
+    """T^l = mean of E^j, j in [max(0, l-m), l) (Eq. inter_layer_persistence, 0-based)."""
+    wl = _wl_small()
+    p, outs, _ = _run(oracle, wl)
+    m = 4
+    assert np.all(outs[0]["T"] == 0.0)
+    assert np.allclose(outs[1]["T"], outs[0]["E"], atol=TOL, rtol=0)
+    for l in range(2, wl.num_layers):
+        js = range(max(0, l - m), l)
+        ref = oracle.persistence([outs[j]["E"].ravel() for j in js], outs[0]["E"].size)
+        assert np.allclose(outs[l]["T"].ravel(), ref, atol=TOL, rtol=0)
+        assert np.allclose(outs[l]["T"], np.mean([outs[j]["E"] for j in js], axis=0),
+                           atol=TOL, rtol=0)
+
+
+def test_layer_causality(oracle):
+    """Changing layer 2 leaves layers 0-1 unchanged and moves T of layer 3."""
+    wl = _wl_small(num_layers=4)
+    _, a, ins = _run(oracle, wl)
+    p = oracle.Prompt.for_workload(wl)
+    b = []
+    for l in range(4):
+        x = dict(ins[l])
+        if l == 2:
+            x["k"] = x["k"] * np.float32(1.5)
+        b.append(p.layer(l, x["q_win"], x["k"]))
+    for l in (0, 1):
+        for key in ("B", "E", "T", "S", "idx"):
+            assert np.array_equal(a[l][key], b[l][key])
+    assert not np.allclose(a[3]["T"], b[3]["T"])
+
+
+def _seq_view(p, r, key, b, h):
+    return r[key][h, p.cu[b]:p.cu[b + 1]]
+
+
+def test_layer_composition_vector_form(oracle):
+    """V = (I + P_r) e + t (Eq. structural_calibration_form), S = B + lambda V
+    with lambda the numerical argmin, pooled S and top-K by brute force."""
+    wl = _wl_small()
+    p, outs, _ = _run(oracle, wl)
+    r, W = 5, wl.window
+    for l in (0, 3, 5):
+        o = outs[l]
+        for b in range(wl.batch):
+            n = wl.seq_lens[b]
+            K = wl.budgets[b]
+            for h in range(wl.num_kv_heads):
+                B = _seq_view(p, o, "B", b, h)
+                Q = _seq_view(p, o, "Q", b, h)
+                e = np.where(Q > B, Q - B, 0.0)
+                t = _seq_view(p, o, "T", b, h)
+                v = (np.eye(n) + _dense_P(n, r)) @ e + t
+                assert np.allclose(_seq_view(p, o, "V", b, h), v, atol=1e-15, rtol=1e-12)
+                nc = n - W
+                M = min(2 * K, nc)
+                sel = _msel(B, nc, M)
+                sb, sv = np.std(B[sel]), np.std(v[sel])
+                lam = sb / (sv + 1e-12)
+                assert o["lambda"][b, h] == pytest.approx(lam, rel=1e-9)
+                S = B + lam * v
+                assert np.allclose(_seq_view(p, o, "S", b, h), S, atol=1e-15, rtol=1e-9)
+                Sp = _box(S[:nc], wl.pool_kernel)
+                assert np.allclose(_seq_view(p, o, "S_pool", b, h)[:nc], Sp, atol=1e-15,
+                                   rtol=1e-9)
+                ref = sorted(sorted(range(nc), key=lambda i: (-Sp[i], i))[:K])
+                assert p.idx_of(o, b, h).tolist() == ref
+
+
+@pytest.mark.parametrize("mode", ["no_last_query", "gamma0"])
+def test_snapkv_reduction(oracle, mode):
+    """Without the last-query term S = B: kept set = top-K of pooled window score."""
+    wl = _wl_small(num_layers=3)
+    params = oracle.Params(use_last_query=0) if mode == "no_last_query" else \
+        oracle.Params(gamma=0.0)
+    p, outs, _ = _run(oracle, wl, params)
+    for o in outs:
+        assert np.array_equal(o["S"], o["B"])
+        for b in range(wl.batch):
+            nc = wl.seq_lens[b] - wl.window
+            B = _seq_view(p, o, "B", b, 0)[:nc]
+            Bp = _box(B, wl.pool_kernel)
+            K = wl.budgets[b]
+            ref = sorted(sorted(range(nc), key=lambda i: (-Bp[i], i))[:K])
+            assert p.idx_of(o, b, 0).tolist() == ref
+
+
+def test_budget_exact_padding_and_window_only(oracle):
+    """Exactly K positions from I when |I| >= K; all of I then -1 when |I| < K;
+    nothing when W = N (empty candidate set)."""
+    wl = _wl_small(seq_lens=(60, 45, 4), budgets=(8, 50, 3), visual=((5, 40), (5, 30), (0, 0)),
+                   n_planted=0, num_layers=2)
+    p, outs, _ = _run(oracle, wl)
+    for o in outs:
+        for h in range(wl.num_kv_heads):
+            i0 = p.idx_of(o, 0, h)
+            assert len(i0) == 8 and len(set(i0.tolist())) == 8
+            assert np.all(np.diff(i0) > 0) and i0.min() >= 0 and i0.max() < 60 - 4
+            i1 = p.idx_of(o, 1, h)
+            assert i1.tolist() == list(range(41))
+            off = 8 * 2 + h * 50
+            assert np.all(o["idx"][off + 41:off + 50] == -1)
+            assert len(p.idx_of(o, 2, h)) == 0 and o["n_kept"][2, h] == 0
+            assert o["lambda"][2, h] == 0.0
+
+
+def test_compaction_rows(oracle):
+    """Compacted cache = kept rows ascending, then the W window rows, then zeros."""
+    wl = _wl_small(num_layers=1, seq_lens=(60, 45), budgets=(8, 50))
+    p = oracle.Prompt.for_workload(wl)
+    x = inputs.layer_inputs(wl, 0)
+    o = p.layer(0, x["q_win"], x["k"])
+    ko, vo = p.compact(o, x["k"], x["v"], 4)
+    ko = ko.view(np.float32).reshape(-1, wl.num_kv_heads, wl.head_dim)
+    vo = vo.view(np.float32).reshape(-1, wl.num_kv_heads, wl.head_dim)
+    row = 0
+    for b in range(wl.batch):
+        n, K, W = wl.seq_lens[b], wl.budgets[b], wl.window
+        for h in range(wl.num_kv_heads):
+            ids = p.idx_of(o, b, h)
+            rows = list(ids) + list(range(n - W, n))
+            src = p.cu[b] + np.asarray(rows)
+            got_k = ko[row:row + len(rows), h]
+            assert np.array_equal(got_k, x["k"][src, h])
+            assert np.array_equal(vo[row:row + len(rows), h], x["v"][src, h])
+            assert np.all(ko[row + len(rows):row + K + W, h] == 0)
+        row += K + W
+
+
+def test_planted_evidence_is_retained_tiny_workload(oracle):
+    """Keys aligned with the last query (sparse evidence, Sec. 3 finding 2) are kept
+    by BACON at every layer and head of the tiny workload."""
+    wl = inputs.workload(0)
+    p, outs, _ = _run(oracle, wl)
+    snap = oracle.Prompt.for_workload(wl, oracle.Params(use_last_query=0))
+    pos = inputs.planted_positions(wl)[0]
+    snap_kept = bacon_kept = total = 0
+    for l, o in enumerate(outs):
+        x = inputs.layer_inputs(wl, l)
+        so = snap.layer(l, x["q_win"], x["k"])
+        for h in range(wl.num_kv_heads):
+            kept = set(p.idx_of(o, 0, h).tolist())
+            skept = set(snap.idx_of(so, 0, h).tolist())
+            for q in pos[h]:
+                total += 1
+                bacon_kept += q in kept
+                snap_kept += q in skept
+            assert len(kept) == wl.budgets[0]
+    assert bacon_kept == total, f"BACON kept {bacon_kept}/{total} planted keys"
+    print(f"planted keys kept: BACON {bacon_kept}/{total}, window-only {snap_kept}/{total}")
+
+
+def test_terms_mask_zero_gives_window_score(oracle):
+    """With no evidence terms V = 0 and the score reduces to B."""
+    wl = _wl_small(num_layers=2)
+    _, outs, _ = _run(oracle, wl, oracle.Params(terms=0))
+    for o in outs:
+        assert np.all(o["V"] == 0.0)
+        assert np.array_equal(o["S"], o["B"])
