@@ -1,0 +1,193 @@
+/*
+ * bacon.h -- C ABI of the MI355X (gfx950) BACON prefill KV-compression pass.
+ *
+ * BACON (Boundary Attention CalibratiON) refines the observation-window
+ * importance score of a layer's KV cache with last-query evidence and keeps
+ * the top-K keys of every KV head.  For each layer l, sequence b and KV head h
+ * (paper Sec. 4):
+ *
+ *   B_i = mean over the W window rows (and the G query heads of the group)
+ *         of the causal attention A_{q,i} = softmax_i(q . k_i / sqrt(d))
+ *                                      (Sec. 4.1, Eq. window_score; App. A)
+ *   Q_i = A_{D,i}, D = last prompt position (Sec. 4.2, Eq. last_query_score)
+ *   E   = [Q - B]_+                     (Eq. boundary_residual)
+ *   L   = P_r E (truncated box mean)    (Sec. 4.3, Eqs. neighbor_matrix, intra_layer_coherence)
+ *   T   = mean of E over the previous min(m, l) layers (Eq. inter_layer_persistence)
+ *   V   = E + L + T                     (Eq. structurally_calibrated_evidence)
+ *   lambda = gamma Std_M(B) / (Std_M(V) + eps), M = top-min(rho K, |I|) of B over I
+ *                                      (Sec. 4.4, Eqs. scale_matching_size/set, lambda_solution)
+ *   S   = B + lambda V                  (Eq. bacon_score)
+ *   kept = TopK over I of avgpool_k(S)  (Eq. topk_selection, with the SnapKV pooling)
+ *   compacted cache = {K_i, V_i : i kept} followed by the W window rows.
+ *
+ * Conventions (readings of points the paper leaves open):
+ *   - Window rows are the last W prompt positions; the candidate set I is
+ *     positions [0, N_b - W); the window itself is always kept.
+ *   - GQA: attention is averaged over the G = num_q_heads / num_kv_heads query
+ *     heads before E is formed; the budget is per KV head.
+ *   - Every top-k orders by score descending, then position ascending.
+ *   - Std is the population standard deviation; pooling is a centred average
+ *     of odd width over I with the in-range count as divisor.
+ *
+ * Layouts (all device pointers, row-major, packed without padding):
+ *   q_win   [B*W, Hq, d]   last W queries of every sequence (post-RoPE)
+ *   k, v    [T, Hkv, d]    T = cu_seqlens[B]
+ *   score vectors  [Hkv, T] float32 (B, Q, E, V, S)
+ *   lse     [B, Hq, W] float32, natural-log normaliser of each window row
+ *   lambda  [B, Hkv] float32
+ *   idx     int32; sequence b owns Hkv*budget_b entries starting at
+ *           Hkv * sum_{b'<b} budget_b', head-major ([h][j]); entries are
+ *           positions relative to the sequence start, ascending, and -1 where
+ *           the candidate set holds fewer than budget_b positions.
+ *   k_out, v_out [sum_b (budget_b + W), Hkv, d]; for each (b, h) the rows are
+ *           the kept rows in ascending position, then the W window rows, then
+ *           zero rows up to budget_b + W.
+ *
+ * Element type: BACON_FP32 (float) or BACON_BF16 (bfloat16) for q, k, v and
+ * the compacted cache; all scores are float32.  head_dim is 64 or 128.
+ *
+ * Ownership: the caller owns every device buffer, including the workspace
+ * (size from bacon_workspace_bytes, 256-byte aligned), which holds the E
+ * history of the current prompt.  The library never allocates device memory;
+ * it owns only the host-side context.  One context per stream; a context is
+ * not thread-safe.  Device pointers must be 16-byte aligned.
+ *
+ * Errors: every argument check runs on the host before anything is enqueued;
+ * a failing call returns a status, enqueues nothing, and bacon_last_error()
+ * gives the reason (per calling thread).  No call synchronises the stream;
+ * device faults surface at the caller's next synchronisation.
+ */
+#ifndef BACON_H
+#define BACON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BACON_OK = 0,
+  BACON_ERR_INVALID = 1,      /* bad argument, shape, pointer or batch layout */
+  BACON_ERR_UNSUPPORTED = 2,  /* valid but outside what the kernels handle    */
+  BACON_ERR_ORDER = 3,        /* layer out of sequence, or no prompt begun    */
+  BACON_ERR_WORKSPACE = 4,    /* workspace too small or misaligned            */
+  BACON_ERR_HIP = 5           /* a HIP runtime call or kernel launch failed   */
+} bacon_status;
+
+typedef enum { BACON_FP32 = 0, BACON_BF16 = 1 } bacon_dtype;
+
+enum { BACON_TERM_E = 1, BACON_TERM_L = 2, BACON_TERM_T = 4 };
+
+/* Method parameters.  Defaults (bacon_default_params): radius 5 and
+ * persist_m 4 (Sec. 4.3), rho 2 (Sec. 4.4), gamma 1 and eps 1e-12 (the paper
+ * gives no value), pool_kernel 7, use_last_query 1, terms E|L|T. */
+typedef struct {
+  int32_t radius;          /* r of the coherence neighbourhood, 0..16        */
+  int32_t persist_m;       /* m, persistence depth, 0..16                    */
+  float rho;               /* scale-matching expansion, > 0                  */
+  float gamma;             /* calibration strength, >= 0                     */
+  float eps;               /* stabiliser in lambda, >= 0                     */
+  int32_t pool_kernel;     /* odd width of the average pool of S, 1..33      */
+  int32_t use_last_query;  /* 1 = BACON; 0 = window score only (S = B)       */
+  uint32_t terms;          /* subset of BACON_TERM_E|L|T included in V       */
+} bacon_params;
+
+/* Static shape of the model and the largest batch a context will see. */
+typedef struct {
+  int32_t num_layers;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;      /* num_q_heads % num_kv_heads == 0              */
+  int32_t head_dim;          /* 64 or 128                                    */
+  int32_t window;            /* W >= 1, and G*W <= 512                       */
+  int32_t max_batch;         /* 1..64                                        */
+  int64_t max_total_tokens;  /* upper bound of T                             */
+  bacon_dtype dtype;
+} bacon_shape;
+
+/* A packed batch.  Both arrays live in HOST memory and are copied by the call.
+ * cu_seqlens[0] = 0 and W <= N_b = cu_seqlens[b+1]-cu_seqlens[b] <= 32768. */
+typedef struct {
+  int32_t batch;
+  const int32_t *cu_seqlens;  /* [batch + 1] */
+  const int32_t *budgets;     /* [batch], keys kept per KV head, >= 1 */
+} bacon_batch;
+
+typedef struct bacon_ctx bacon_ctx;
+
+/* Fills *p with the defaults listed above. */
+void bacon_default_params(bacon_params *p);
+
+/* Bytes of device workspace a context of this shape needs; 0 if the shape or
+ * parameters are invalid (see bacon_last_error). */
+size_t bacon_workspace_bytes(const bacon_shape *shape, const bacon_params *params);
+
+/* Creates a context over the caller's workspace d_ws (ws_bytes >= the size
+ * above, 256-byte aligned).  params may be NULL for the defaults. */
+bacon_status bacon_init(bacon_ctx **ctx, const bacon_shape *shape, const bacon_params *params,
+                        void *d_ws, size_t ws_bytes);
+
+/* Destroys the host context (the workspace stays the caller's). */
+bacon_status bacon_free(bacon_ctx *ctx);
+
+/* Starts a prompt: fixes the batch layout used by every layer until the next
+ * call and resets the layer counter; the E history starts empty.  Enqueues a
+ * small clearing kernel on `stream` (a hipStream_t). */
+bacon_status bacon_begin_prompt(bacon_ctx *ctx, const bacon_batch *batch, void *stream);
+
+/* Window score and last-query score of one layer (Eqs. window_score,
+ * last_query_score): writes B and Q [Hkv, T] and, if d_lse is not NULL, the
+ * window-row normalisers [B, Hq, W].  Reads no history; any layer may be scored. */
+bacon_status bacon_score(bacon_ctx *ctx, int32_t layer, const bacon_batch *batch,
+                         const void *d_q_win, const void *d_k, float *d_lse,
+                         float *d_B, float *d_Q, void *stream);
+
+/* Calibration of one layer (Eqs. boundary_residual .. bacon_score): from B and
+ * Q writes S [Hkv, T] and lambda [B, Hkv]; E and V [Hkv, T] when not NULL.
+ * Appends E to the prompt's history, so `layer` must be the next layer of the
+ * prompt (0, 1, 2, ...) counting calibrate and compress_layer calls. */
+bacon_status bacon_calibrate(bacon_ctx *ctx, int32_t layer, const bacon_batch *batch,
+                             const float *d_B, const float *d_Q, float *d_S, float *d_lambda,
+                             float *d_E, float *d_V, void *stream);
+
+/* Pools S over the candidate set and keeps the top budget_b positions per KV
+ * head (Eq. topk_selection); writes idx in the layout above. */
+bacon_status bacon_select_topk(bacon_ctx *ctx, const bacon_batch *batch, const float *d_S,
+                               int32_t *d_idx, void *stream);
+
+/* Builds the compacted cache from idx (cache construction after Eq.
+ * topk_selection); rows are copied bit for bit. */
+bacon_status bacon_compact(bacon_ctx *ctx, const bacon_batch *batch, const void *d_k,
+                           const void *d_v, const int32_t *d_idx, void *d_k_out,
+                           void *d_v_out, void *stream);
+
+/* The whole pass for one layer: score, calibrate, select and compact, with the
+ * intermediates kept in the workspace.  Same ordering rule as calibrate. */
+bacon_status bacon_compress_layer(bacon_ctx *ctx, int32_t layer, const bacon_batch *batch,
+                                  const void *d_q_win, const void *d_k, const void *d_v,
+                                  int32_t *d_idx, void *d_k_out, void *d_v_out, void *stream);
+
+/* Sizes of the outputs for a batch: idx entries and compacted rows. */
+int64_t bacon_idx_count(const bacon_batch *batch, int32_t num_kv_heads);
+int64_t bacon_kept_rows(const bacon_batch *batch, int32_t window);
+
+/* Per-kernel timing with hipEvents around every launch of the context.
+ * bacon_profile_read waits for the recorded events, fills up to `max`
+ * entries (name, launches, total milliseconds) and returns the count. */
+typedef struct {
+  char name[32];
+  int64_t launches;
+  double total_ms;
+} bacon_kernel_time;
+
+bacon_status bacon_profile_enable(bacon_ctx *ctx, int32_t enable);
+int32_t bacon_profile_read(bacon_ctx *ctx, bacon_kernel_time *out, int32_t max);
+
+const char *bacon_status_string(bacon_status s);
+const char *bacon_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BACON_H */

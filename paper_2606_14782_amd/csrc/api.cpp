@@ -1,0 +1,591 @@
+// Host side of the C ABI declared in include/bacon.h: argument checks,
+// workspace carving, layer ordering, launch sequencing and event timing.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/bacon.h"
+#include "internal.h"
+
+using namespace bacon;
+
+namespace {
+
+thread_local std::string g_err;
+
+bacon_status fail(bacon_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+bacon_status hip_fail(hipError_t e, const char *what) {
+  return fail(BACON_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t ring, vec_b, vec_ept, partials, lse2, counters, lambda, total;
+  int rpad, slots;
+  int64_t chunks_cap;
+};
+
+bacon_status check_shape(const bacon_shape *s) {
+  if (!s) return fail(BACON_ERR_INVALID, "shape is NULL");
+  if (s->num_layers < 1) return fail(BACON_ERR_INVALID, "num_layers must be >= 1");
+  if (s->num_q_heads < 1 || s->num_kv_heads < 1)
+    return fail(BACON_ERR_INVALID, "head counts must be >= 1");
+  if (s->num_q_heads % s->num_kv_heads)
+    return fail(BACON_ERR_INVALID, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)",
+                s->num_q_heads, s->num_kv_heads);
+  if (s->window < 1) return fail(BACON_ERR_INVALID, "window must be >= 1");
+  if (s->max_batch < 1) return fail(BACON_ERR_INVALID, "max_batch must be >= 1");
+  if (s->max_total_tokens < 1) return fail(BACON_ERR_INVALID, "max_total_tokens must be >= 1");
+  if (s->dtype != BACON_FP32 && s->dtype != BACON_BF16)
+    return fail(BACON_ERR_UNSUPPORTED, "dtype %d is not supported", (int)s->dtype);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(BACON_ERR_UNSUPPORTED, "head_dim %d is not supported (64 or 128)", s->head_dim);
+  if (s->max_batch > kMaxBatch)
+    return fail(BACON_ERR_UNSUPPORTED, "max_batch %d exceeds %d", s->max_batch, kMaxBatch);
+  const int64_t rows = (int64_t)(s->num_q_heads / s->num_kv_heads) * s->window;
+  if (rows > kMaxRows)
+    return fail(BACON_ERR_UNSUPPORTED, "group*window = %lld exceeds %d", (long long)rows, kMaxRows);
+  if (s->max_total_tokens > ((int64_t)1 << 31) / 2)
+    return fail(BACON_ERR_UNSUPPORTED, "max_total_tokens too large");
+  return BACON_OK;
+}
+
+bacon_status check_params(const bacon_params *p) {
+  if (p->radius < 0 || p->radius > 16) return fail(BACON_ERR_INVALID, "radius must be in [0, 16]");
+  if (p->persist_m < 0 || p->persist_m > kMaxRing)
+    return fail(BACON_ERR_INVALID, "persist_m must be in [0, %d]", kMaxRing);
+  if (!(p->rho > 0.f) || !std::isfinite(p->rho)) return fail(BACON_ERR_INVALID, "rho must be > 0");
+  if (!(p->gamma >= 0.f) || !std::isfinite(p->gamma))
+    return fail(BACON_ERR_INVALID, "gamma must be >= 0");
+  if (!(p->eps >= 0.f) || !std::isfinite(p->eps)) return fail(BACON_ERR_INVALID, "eps must be >= 0");
+  if (p->pool_kernel < 1 || p->pool_kernel > 33 || (p->pool_kernel & 1) == 0)
+    return fail(BACON_ERR_INVALID, "pool_kernel must be odd and in [1, 33]");
+  if (p->use_last_query != 0 && p->use_last_query != 1)
+    return fail(BACON_ERR_INVALID, "use_last_query must be 0 or 1");
+  if (p->terms & ~7u) return fail(BACON_ERR_INVALID, "terms has unknown bits");
+  return BACON_OK;
+}
+
+Layout layout_of(const bacon_shape *s, const bacon_params *p) {
+  Layout L{};
+  const int G = s->num_q_heads / s->num_kv_heads;
+  L.rpad = ((G * s->window + 31) / 32) * 32;
+  L.slots = p->persist_m > 0 ? p->persist_m : 1;
+  const int tk = 32 * std::min(L.rpad / 32, 4);
+  L.chunks_cap = (s->max_total_tokens + tk - 1) / tk + s->max_batch;
+  const size_t vec = (size_t)s->num_kv_heads * (size_t)s->max_total_tokens * sizeof(float);
+  size_t off = 0;
+  L.ring = off;     off += align256((size_t)L.slots * vec);
+  L.vec_b = off;    off += align256(vec);
+  L.vec_ept = off;  off += align256(vec);
+  L.partials = off; off += align256((size_t)s->num_kv_heads * L.chunks_cap * L.rpad * sizeof(float2));
+  L.lse2 = off;     off += align256((size_t)s->max_batch * s->num_kv_heads * L.rpad * sizeof(float));
+  L.counters = off; off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(unsigned));
+  L.lambda = off;   off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(float));
+  L.total = off;
+  return L;
+}
+
+const char *kKernelNames[] = {"window_lse", "window_score", "window_score_calib",
+                              "select_fused", "select_calib", "select_topk", "calib_elem",
+                              "compact", "clear"};
+enum KernelId { KI_LSE, KI_SCORE, KI_FUSED, KI_SEL_FUSED, KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM,
+                KI_COMPACT, KI_CLEAR, KI_COUNT };
+
+}  // namespace
+
+struct bacon_ctx {
+  bacon_shape shape;
+  bacon_params params;
+  char *ws;
+  size_t ws_bytes;
+  Layout L;
+  bool prompt = false;
+  int next_layer = 0;
+  std::vector<int32_t> cu, budgets;
+  int chunk_stages_override = 0;
+  bool counters_clean = false;
+  // profiling
+  bool prof = false;
+  std::vector<hipEvent_t> ev_pool;
+  struct Pending { int kid; hipEvent_t a, b; };
+  std::vector<Pending> pending;
+  size_t ev_next = 0;
+  int64_t launches[KI_COUNT] = {};
+  double ms[KI_COUNT] = {};
+};
+
+namespace {
+
+// Records events around a launch when profiling is on.
+template <typename F>
+bacon_status timed(bacon_ctx *c, int kid, hipStream_t s, F &&launch) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (c->prof && c->ev_next + 2 <= c->ev_pool.size()) {
+    e0 = c->ev_pool[c->ev_next++];
+    e1 = c->ev_pool[c->ev_next++];
+    hipEventRecord(e0, s);
+  }
+  const hipError_t e = launch();
+  if (e != hipSuccess) return hip_fail(e, kKernelNames[kid]);
+  if (e0) {
+    hipEventRecord(e1, s);
+    c->pending.push_back({kid, e0, e1});
+  }
+  return BACON_OK;
+}
+
+bacon_status check_batch(const bacon_ctx *c, const bacon_batch *bt) {
+  if (!bt) return fail(BACON_ERR_INVALID, "batch is NULL");
+  if (bt->batch < 1 || bt->batch > c->shape.max_batch)
+    return fail(BACON_ERR_INVALID, "batch size %d outside [1, %d]", bt->batch, c->shape.max_batch);
+  if (!bt->cu_seqlens || !bt->budgets) return fail(BACON_ERR_INVALID, "batch arrays are NULL");
+  if (bt->cu_seqlens[0] != 0) return fail(BACON_ERR_INVALID, "cu_seqlens[0] must be 0");
+  for (int b = 0; b < bt->batch; ++b) {
+    const int64_t n = (int64_t)bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
+    if (n < c->shape.window)
+      return fail(BACON_ERR_INVALID, "sequence %d has %lld tokens, fewer than the window %d", b,
+                  (long long)n, c->shape.window);
+    if (n > kMaxSeqLen)
+      return fail(BACON_ERR_UNSUPPORTED, "sequence %d has %lld tokens (max %d)", b, (long long)n,
+                  kMaxSeqLen);
+    if (bt->budgets[b] < 1) return fail(BACON_ERR_INVALID, "budget of sequence %d must be >= 1", b);
+  }
+  if (bt->cu_seqlens[bt->batch] > c->shape.max_total_tokens)
+    return fail(BACON_ERR_INVALID, "total tokens %d exceed max_total_tokens %lld",
+                bt->cu_seqlens[bt->batch], (long long)c->shape.max_total_tokens);
+  return BACON_OK;
+}
+
+bacon_status check_prompt_batch(const bacon_ctx *c, const bacon_batch *bt) {
+  if (!c->prompt) return fail(BACON_ERR_ORDER, "no prompt begun (call bacon_begin_prompt)");
+  if (bt->batch + 1 != (int)c->cu.size() ||
+      memcmp(bt->cu_seqlens, c->cu.data(), c->cu.size() * sizeof(int32_t)) != 0 ||
+      memcmp(bt->budgets, c->budgets.data(), c->budgets.size() * sizeof(int32_t)) != 0)
+    return fail(BACON_ERR_INVALID, "batch differs from the one given to bacon_begin_prompt");
+  return BACON_OK;
+}
+
+bacon_status check_ptr(const void *p, const char *name, size_t align) {
+  if (!p) return fail(BACON_ERR_INVALID, "%s is NULL", name);
+  if (reinterpret_cast<uintptr_t>(p) % align)
+    return fail(BACON_ERR_INVALID, "%s is not %zu-byte aligned", name, align);
+  return BACON_OK;
+}
+
+#define TRY(x)                     \
+  do {                             \
+    bacon_status _s = (x);         \
+    if (_s != BACON_OK) return _s; \
+  } while (0)
+
+SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out) {
+  SeqTable st{};
+  st.batch = bt->batch;
+  const bool bf16 = c->shape.dtype == BACON_BF16;
+  const PassGeom g = pass_geom(PASS_FUSED, bf16, c->shape.head_dim, c->L.rpad);
+  int64_t stages = 0;
+  for (int b = 0; b < bt->batch; ++b) {
+    const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
+    stages += (n + g.tk - 1) / g.tk;
+  }
+  stages *= c->shape.num_kv_heads;
+  const int by_lds = std::max(1, (160 * 1024) / std::max(1, g.lds));
+  const int by_waves = std::max(1, 16 / g.nw);
+  const int64_t slots = 256LL * std::min(by_lds, by_waves);
+  int per_wg = (int)std::max<int64_t>(1, (stages + slots - 1) / slots);
+  if (c->chunk_stages_override > 0) per_wg = c->chunk_stages_override;
+  const int chunk = g.tk * per_wg;
+  int cb = 0, ib = 0, kb = 0;
+  for (int b = 0; b < bt->batch; ++b) {
+    const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
+    st.cu[b] = bt->cu_seqlens[b];
+    st.chunk_base[b] = cb;
+    st.budget[b] = bt->budgets[b];
+    st.idx_base[b] = ib;
+    st.kept_base[b] = kb;
+    cb += (n + chunk - 1) / chunk;
+    ib += bt->budgets[b];
+    kb += bt->budgets[b] + c->shape.window;
+  }
+  st.cu[bt->batch] = bt->cu_seqlens[bt->batch];
+  st.chunk_base[bt->batch] = cb;
+  st.total_chunks = cb;
+  *chunk_out = chunk;
+  return st;
+}
+
+PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void *q, const void *k) {
+  PassArgs a{};
+  const bacon_shape &s = c->shape;
+  a.q = q;
+  a.k = k;
+  a.Hq = s.num_q_heads;
+  a.Hkv = s.num_kv_heads;
+  a.G = s.num_q_heads / s.num_kv_heads;
+  a.W = s.window;
+  a.R = a.G * s.window;
+  a.Rpad = c->L.rpad;
+  a.chunk = chunk;
+  a.T = s.max_total_tokens;
+  a.c2 = (float)(1.4426950408889634 / std::sqrt((double)s.head_dim));
+  a.partials = reinterpret_cast<float2 *>(c->ws + c->L.partials);
+  a.lse2 = reinterpret_cast<float *>(c->ws + c->L.lse2);
+  a.counters = reinterpret_cast<unsigned *>(c->ws + c->L.counters);
+  a.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
+  a.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
+  a.vec_EpT = reinterpret_cast<float *>(c->ws + c->L.vec_ept);
+  a.terms = c->params.terms;
+  (void)st;
+  return a;
+}
+
+// Ring slots for layer `layer`: write slot and the slots of the previous
+// min(m, layer) layers, oldest first.
+void ring_slots(const bacon_ctx *c, int layer, int *wr, int *cnt, int *rd) {
+  const int m = c->params.persist_m, S = c->L.slots;
+  *cnt = std::min(m, layer);
+  for (int j = 0; j < *cnt; ++j) rd[j] = (layer - *cnt + j) % S;
+  *wr = layer % S;
+}
+
+SelArgs sel_args(const bacon_ctx *c) {
+  SelArgs a{};
+  const bacon_shape &s = c->shape;
+  const bacon_params &p = c->params;
+  a.Hkv = s.num_kv_heads;
+  a.W = s.window;
+  a.T = s.max_total_tokens;
+  a.radius = p.radius;
+  a.pool_half = p.pool_kernel / 2;
+  a.rho = p.rho;
+  a.gamma = p.gamma;
+  a.eps = p.eps;
+  a.use_last_query = p.use_last_query;
+  a.terms = p.terms;
+  a.vec_B = reinterpret_cast<const float *>(c->ws + c->L.vec_b);
+  a.vec_EpT = reinterpret_cast<const float *>(c->ws + c->L.vec_ept);
+  a.lambda_ws = reinterpret_cast<float *>(c->ws + c->L.lambda);
+  a.row_bytes = s.head_dim * (s.dtype == BACON_BF16 ? 2 : 4);
+  return a;
+}
+
+// The pass-1 arrival counters must start at zero; they reset themselves
+// after every pass, so one clear per context suffices.
+bacon_status ensure_counters(bacon_ctx *c, hipStream_t s) {
+  if (c->counters_clean) return BACON_OK;
+  const int64_t ncnt = (int64_t)c->shape.max_batch * c->shape.num_kv_heads;
+  TRY(timed(c, KI_CLEAR, s, [&] {
+    return launch_clear_u32(reinterpret_cast<unsigned *>(c->ws + c->L.counters), ncnt, s);
+  }));
+  c->counters_clean = true;
+  return BACON_OK;
+}
+
+int max_len(const bacon_batch *bt) {
+  int m = 0;
+  for (int b = 0; b < bt->batch; ++b) m = std::max(m, bt->cu_seqlens[b + 1] - bt->cu_seqlens[b]);
+  return m;
+}
+
+}  // namespace
+
+extern "C" {
+
+void bacon_default_params(bacon_params *p) {
+  if (!p) return;
+  p->radius = 5;
+  p->persist_m = 4;
+  p->rho = 2.0f;
+  p->gamma = 1.0f;
+  p->eps = 1e-12f;
+  p->pool_kernel = 7;
+  p->use_last_query = 1;
+  p->terms = BACON_TERM_E | BACON_TERM_L | BACON_TERM_T;
+}
+
+size_t bacon_workspace_bytes(const bacon_shape *shape, const bacon_params *params) {
+  bacon_params p;
+  if (params) p = *params; else bacon_default_params(&p);
+  if (check_shape(shape) != BACON_OK || check_params(&p) != BACON_OK) return 0;
+  return layout_of(shape, &p).total;
+}
+
+bacon_status bacon_init(bacon_ctx **ctx, const bacon_shape *shape, const bacon_params *params,
+                        void *d_ws, size_t ws_bytes) {
+  if (!ctx) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  *ctx = nullptr;
+  TRY(check_shape(shape));
+  bacon_params p;
+  if (params) p = *params; else bacon_default_params(&p);
+  TRY(check_params(&p));
+  if (!d_ws) return fail(BACON_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(d_ws) % 256)
+    return fail(BACON_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+  const Layout L = layout_of(shape, &p);
+  if (ws_bytes < L.total)
+    return fail(BACON_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, L.total);
+  bacon_ctx *c = new bacon_ctx();
+  c->shape = *shape;
+  c->params = p;
+  c->ws = static_cast<char *>(d_ws);
+  c->ws_bytes = ws_bytes;
+  c->L = L;
+  if (const char *e = std::getenv("BACON_CHUNK_STAGES")) c->chunk_stages_override = std::atoi(e);
+  c->counters_clean = false;   // cleared by the first enqueue on a stream
+  *ctx = c;
+  return BACON_OK;
+}
+
+bacon_status bacon_free(bacon_ctx *c) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  for (hipEvent_t e : c->ev_pool) hipEventDestroy(e);
+  delete c;
+  return BACON_OK;
+}
+
+bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  c->cu.assign(bt->cu_seqlens, bt->cu_seqlens + bt->batch + 1);
+  c->budgets.assign(bt->budgets, bt->budgets + bt->batch);
+  c->prompt = true;
+  c->next_layer = 0;
+  c->counters_clean = false;
+  return ensure_counters(c, static_cast<hipStream_t>(stream));
+}
+
+bacon_status bacon_score(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
+                         const void *d_k, float *d_lse, float *d_B, float *d_Q, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  if (layer < 0 || layer >= c->shape.num_layers)
+    return fail(BACON_ERR_INVALID, "layer %d outside [0, %d)", layer, c->shape.num_layers);
+  TRY(check_ptr(d_q_win, "q_win", 16));
+  TRY(check_ptr(d_k, "k", 16));
+  TRY(check_ptr(d_B, "B", 4));
+  TRY(check_ptr(d_Q, "Q", 4));
+  if (d_lse) TRY(check_ptr(d_lse, "lse", 4));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int chunk = 0;
+  const SeqTable st = make_table(c, bt, &chunk);
+  PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
+  a.T = bt->cu_seqlens[bt->batch];
+  a.lse_user = d_lse;
+  a.out_B = d_B;
+  a.out_Q = d_Q;
+  const bool bf16 = c->shape.dtype == BACON_BF16;
+  const bool w32 = c->shape.window == 32;
+  TRY(ensure_counters(c, s));
+  TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+  return timed(c, KI_SCORE, s, [&] { return launch_pass(PASS_SCORE, bf16, c->shape.head_dim, w32, a, st, s); });
+}
+
+bacon_status bacon_calibrate(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const float *d_B,
+                             const float *d_Q, float *d_S, float *d_lambda, float *d_E,
+                             float *d_V, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  TRY(check_prompt_batch(c, bt));
+  if (layer != c->next_layer)
+    return fail(BACON_ERR_ORDER, "layer %d given, layer %d expected next", layer, c->next_layer);
+  if (layer >= c->shape.num_layers)
+    return fail(BACON_ERR_ORDER, "layer %d beyond num_layers %d", layer, c->shape.num_layers);
+  TRY(check_ptr(d_B, "B", 4));
+  TRY(check_ptr(d_Q, "Q", 4));
+  TRY(check_ptr(d_S, "S", 4));
+  TRY(check_ptr(d_lambda, "lambda", 4));
+  if (d_E) TRY(check_ptr(d_E, "E", 4));
+  if (d_V) TRY(check_ptr(d_V, "V", 4));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int chunk = 0;
+  const SeqTable st = make_table(c, bt, &chunk);
+  const int64_t T = bt->cu_seqlens[bt->batch];
+  ElemArgs e{};
+  e.in_B = d_B;
+  e.in_Q = d_Q;
+  e.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
+  ring_slots(c, layer, &e.ring_write, &e.ring_cnt, e.ring_read);
+  e.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
+  e.vec_EpT = reinterpret_cast<float *>(c->ws + c->L.vec_ept);
+  e.Hkv = c->shape.num_kv_heads;
+  e.T = T;
+  e.terms = c->params.terms;
+  // the [Hkv, T] vectors of the split path use the batch's T as row length
+  TRY(timed(c, KI_ELEM, s, [&] { return launch_elem(e, s); }));
+  SelArgs a = sel_args(c);
+  a.T = T;
+  a.ring_E = e.ring + (int64_t)e.ring_write * c->shape.num_kv_heads * T;
+  a.out_S = d_S;
+  a.out_V = d_V;
+  a.out_E = d_E;
+  a.out_lambda = d_lambda;
+  TRY(timed(c, KI_SEL_CALIB, s, [&] { return launch_select(SEL_CALIB, max_len(bt), a, st, s); }));
+  c->next_layer = layer + 1;
+  return BACON_OK;
+}
+
+bacon_status bacon_select_topk(bacon_ctx *c, const bacon_batch *bt, const float *d_S,
+                               int32_t *d_idx, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  TRY(check_ptr(d_S, "S", 4));
+  TRY(check_ptr(d_idx, "idx", 4));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int chunk = 0;
+  const SeqTable st = make_table(c, bt, &chunk);
+  SelArgs a = sel_args(c);
+  a.T = bt->cu_seqlens[bt->batch];
+  a.in_S = d_S;
+  a.idx = d_idx;
+  return timed(c, KI_SEL_TOPK, s, [&] { return launch_select(SEL_TOPK, max_len(bt), a, st, s); });
+}
+
+bacon_status bacon_compact(bacon_ctx *c, const bacon_batch *bt, const void *d_k, const void *d_v,
+                           const int32_t *d_idx, void *d_k_out, void *d_v_out, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  TRY(check_ptr(d_k, "k", 16));
+  TRY(check_ptr(d_v, "v", 16));
+  TRY(check_ptr(d_idx, "idx", 4));
+  TRY(check_ptr(d_k_out, "k_out", 16));
+  TRY(check_ptr(d_v_out, "v_out", 16));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int chunk = 0;
+  const SeqTable st = make_table(c, bt, &chunk);
+  CompactArgs a{};
+  a.idx = d_idx;
+  a.k = d_k;
+  a.v = d_v;
+  a.k_out = d_k_out;
+  a.v_out = d_v_out;
+  a.Hkv = c->shape.num_kv_heads;
+  a.W = c->shape.window;
+  a.row_bytes = c->shape.head_dim * (c->shape.dtype == BACON_BF16 ? 2 : 4);
+  return timed(c, KI_COMPACT, s, [&] { return launch_compact(a, st, s); });
+}
+
+bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
+                                  const void *d_q_win, const void *d_k, const void *d_v,
+                                  int32_t *d_idx, void *d_k_out, void *d_v_out, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  TRY(check_prompt_batch(c, bt));
+  if (layer != c->next_layer)
+    return fail(BACON_ERR_ORDER, "layer %d given, layer %d expected next", layer, c->next_layer);
+  if (layer >= c->shape.num_layers)
+    return fail(BACON_ERR_ORDER, "layer %d beyond num_layers %d", layer, c->shape.num_layers);
+  TRY(check_ptr(d_q_win, "q_win", 16));
+  TRY(check_ptr(d_k, "k", 16));
+  TRY(check_ptr(d_v, "v", 16));
+  TRY(check_ptr(d_idx, "idx", 4));
+  TRY(check_ptr(d_k_out, "k_out", 16));
+  TRY(check_ptr(d_v_out, "v_out", 16));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int chunk = 0;
+  const SeqTable st = make_table(c, bt, &chunk);
+  const int64_t T = bt->cu_seqlens[bt->batch];
+  PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
+  a.T = T;
+  ring_slots(c, layer, &a.ring_write, &a.ring_cnt, a.ring_read);
+  const bool bf16 = c->shape.dtype == BACON_BF16;
+  const bool w32 = c->shape.window == 32;
+  TRY(ensure_counters(c, s));
+  TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+  TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
+  SelArgs sa = sel_args(c);
+  sa.T = T;
+  sa.ring_E = a.ring + (int64_t)a.ring_write * c->shape.num_kv_heads * T;
+  sa.idx = d_idx;
+  sa.k = d_k;
+  sa.v = d_v;
+  sa.k_out = d_k_out;
+  sa.v_out = d_v_out;
+  sa.do_gather = 1;
+  TRY(timed(c, KI_SEL_FUSED, s, [&] { return launch_select(SEL_FUSED, max_len(bt), sa, st, s); }));
+  c->next_layer = layer + 1;
+  return BACON_OK;
+}
+
+int64_t bacon_idx_count(const bacon_batch *bt, int32_t num_kv_heads) {
+  if (!bt || !bt->budgets || bt->batch < 1) return 0;
+  int64_t n = 0;
+  for (int b = 0; b < bt->batch; ++b) n += bt->budgets[b];
+  return n * num_kv_heads;
+}
+
+int64_t bacon_kept_rows(const bacon_batch *bt, int32_t window) {
+  if (!bt || !bt->budgets || bt->batch < 1) return 0;
+  int64_t n = 0;
+  for (int b = 0; b < bt->batch; ++b) n += bt->budgets[b] + window;
+  return n;
+}
+
+bacon_status bacon_profile_enable(bacon_ctx *c, int32_t enable) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  if (enable && c->ev_pool.empty()) {
+    c->ev_pool.resize(16384);
+    for (auto &e : c->ev_pool) {
+      const hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return hip_fail(r, "hipEventCreate");
+    }
+  }
+  c->prof = enable != 0;
+  return BACON_OK;
+}
+
+int32_t bacon_profile_read(bacon_ctx *c, bacon_kernel_time *out, int32_t max) {
+  if (!c) return -1;
+  for (const auto &p : c->pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      c->ms[p.kid] += ms;
+      c->launches[p.kid] += 1;
+    }
+  }
+  c->pending.clear();
+  c->ev_next = 0;
+  int n = 0;
+  for (int k = 0; k < KI_COUNT && n < max; ++k) {
+    if (!c->launches[k]) continue;
+    if (out) {
+      std::snprintf(out[n].name, sizeof out[n].name, "%s", kKernelNames[k]);
+      out[n].launches = c->launches[k];
+      out[n].total_ms = c->ms[k];
+    }
+    ++n;
+  }
+  return n;
+}
+
+const char *bacon_status_string(bacon_status s) {
+  switch (s) {
+    case BACON_OK: return "ok";
+    case BACON_ERR_INVALID: return "invalid argument";
+    case BACON_ERR_UNSUPPORTED: return "unsupported";
+    case BACON_ERR_ORDER: return "layer out of order";
+    case BACON_ERR_WORKSPACE: return "workspace too small";
+    case BACON_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char *bacon_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

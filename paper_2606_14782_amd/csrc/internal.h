@@ -1,0 +1,111 @@
+// Internal declarations shared by the gfx950 kernels and the host API.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bacon {
+
+constexpr int kMaxBatch = 64;       // sequences per batch (kernel-argument table)
+constexpr int kMaxSeqLen = 32768;   // positions per sequence held by the select kernel
+constexpr int kMaxRows = 256;       // G*W window rows per KV head (8 row tiles of 32)
+constexpr int kMaxRing = 16;        // persistence depth m
+constexpr int kSelThreads = 512;
+constexpr int kHistBins = 2048;     // 11-bit digits of the block select
+
+// Per-sequence layout, passed by value to every kernel.
+struct SeqTable {
+  int32_t batch;
+  int32_t total_chunks;                 // key chunks per KV head over the batch
+  int32_t cu[kMaxBatch + 1];            // token offsets
+  int32_t chunk_base[kMaxBatch + 1];    // first chunk of each sequence
+  int32_t budget[kMaxBatch];            // kept keys per KV head
+  int32_t idx_base[kMaxBatch];          // sum of budgets before b
+  int32_t kept_base[kMaxBatch];         // sum of (budget + W) before b
+};
+
+enum PassMode { PASS_LSE = 0, PASS_SCORE = 1, PASS_FUSED = 2 };
+
+// Arguments of the two K-streaming passes.
+struct PassArgs {
+  const void *q;        // [B*W, Hq, d]
+  const void *k;        // [T, Hkv, d]
+  int Hq, Hkv, G, W, R, Rpad;
+  int chunk;            // keys per chunk (multiple of the stage size)
+  int64_t T;            // row length of the [Hkv, T] vectors
+  float c2;             // log2(e) / sqrt(d)
+  // pass 1
+  float2 *partials;     // [Hkv, total_chunks, Rpad]  (max, sum) in log2 units
+  float *lse2;          // [B, Hkv, Rpad]  log2-domain normaliser, +inf for pad rows
+  float *lse_user;      // optional [B, Hq, W] natural-log normaliser
+  unsigned *counters;   // [B, Hkv] arrival counters of the chunk WGs
+  // pass 2
+  float *out_B, *out_Q; // PASS_SCORE: [Hkv, T]
+  float *ring;          // [slots, Hkv, T] E history
+  int ring_write;       // slot receiving this layer's E
+  int ring_cnt;         // number of earlier layers averaged into T
+  int ring_read[kMaxRing];
+  float *vec_B, *vec_EpT;  // PASS_FUSED: B and E+T (per the terms mask) [Hkv, T]
+  uint32_t terms;
+};
+
+enum SelMode { SEL_FUSED = 0, SEL_CALIB = 1, SEL_TOPK = 2 };
+
+struct SelArgs {
+  int Hkv, W;
+  int64_t T;
+  int radius, pool_half;
+  float rho, gamma, eps;
+  int use_last_query;
+  uint32_t terms;
+  const float *vec_B;      // [Hkv, T]
+  const float *vec_EpT;    // [Hkv, T]
+  const float *ring_E;     // this layer's E slot [Hkv, T]
+  const float *in_S;       // SEL_TOPK: user S [Hkv, T]
+  float *out_S, *out_V, *out_E;  // SEL_CALIB optional outputs [Hkv, T]
+  float *out_lambda;       // optional [B, Hkv]
+  float *lambda_ws;        // [B, Hkv]
+  int32_t *idx;            // SEL_FUSED / SEL_TOPK output
+  // fused gather
+  const void *k, *v;
+  void *k_out, *v_out;
+  int row_bytes;
+  int do_gather;
+};
+
+struct ElemArgs {           // split calibrate: E, T, ring update
+  const float *in_B, *in_Q;
+  float *ring;
+  int ring_write, ring_cnt;
+  int ring_read[kMaxRing];
+  float *vec_B, *vec_EpT;
+  float *out_E;
+  int Hkv;
+  int64_t T;
+  uint32_t terms;
+};
+
+struct CompactArgs {
+  const int32_t *idx;
+  const void *k, *v;
+  void *k_out, *v_out;
+  int Hkv, W, row_bytes;
+};
+
+// Launch geometry of the K-streaming passes for a given shape.
+struct PassGeom {
+  int nw;       // waves per workgroup = row tiles
+  int tk;       // keys per pipeline stage
+  int lds;      // dynamic LDS bytes
+};
+PassGeom pass_geom(int mode, bool bf16, int head_dim, int rpad);
+
+hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
+                       const SeqTable &st, hipStream_t s);
+hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,
+                         hipStream_t s);
+hipError_t launch_elem(const ElemArgs &a, hipStream_t s);
+hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_clear_u32(unsigned *p, int64_t n, hipStream_t s);
+
+}  // namespace bacon

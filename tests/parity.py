@@ -1,0 +1,131 @@
+"""Helpers shared by the GPU parity tests: run the oracle and the HIP path on
+the same seeded inputs and compare them with the tolerances of the contract."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+from oracle import ref
+from paper_2606_14782_amd import inputs
+
+# Score tolerance: |x - x_ref| <= RTOL * (|x_ref| + mean |x_ref|)
+RTOL = {"fp32": 1e-5, "bf16": 1e-2}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def params_for(wl, **kw):
+    from paper_2606_14782_amd import bacon
+    d = dict(pool_kernel=wl.pool_kernel)
+    d.update(kw)
+    return bacon.default_params(**d)
+
+
+def oracle_params(**kw):
+    return ref.Params(**kw)
+
+
+def make_ctx(wl, params=None, max_total=None):
+    from paper_2606_14782_amd import bacon
+    return bacon.Context(wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window,
+                         wl.batch, max_total or wl.total_tokens, wl.dtype,
+                         params or params_for(wl))
+
+
+def to_dev(x, wl):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    return t.to(torch.bfloat16) if wl.dtype == "bf16" else t
+
+
+def close(name, got, want, rtol):
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    assert got.shape == want.shape, f"{name}: shape {got.shape} vs {want.shape}"
+    assert np.all(np.isfinite(got)), f"{name}: non-finite values"
+    scale = np.abs(want) + np.mean(np.abs(want))
+    err = np.abs(got - want)
+    worst = float(np.max(err / np.maximum(scale, 1e-300))) if err.size else 0.0
+    bad = err > rtol * scale
+    assert not bad.any(), (f"{name}: {int(bad.sum())}/{bad.size} beyond rtol {rtol}; worst "
+                           f"{worst:.3g}; first at {np.argwhere(bad)[0].tolist()}")
+    return worst
+
+
+def seq_slices(wl):
+    cu = wl.cu_seqlens
+    return [(int(cu[b]), int(cu[b + 1])) for b in range(wl.batch)]
+
+
+def check_idx(name, got, r, wl, rtol):
+    """Kept sets equal the oracle's except for positions whose pooled oracle
+    score is within rtol of the K-th kept score; also counts strict matches."""
+    W, Hkv = wl.window, wl.num_kv_heads
+    stats = {"pairs": 0, "strict": 0, "swaps": 0}
+    base = 0
+    for b, (s0, s1) in enumerate(seq_slices(wl)):
+        K = wl.budgets[b]
+        nc = (s1 - s0) - W
+        for h in range(Hkv):
+            off = base * Hkv + h * K
+            g = np.asarray(got[off:off + K])
+            o = np.asarray(r["idx"][off:off + K])
+            kept = min(K, max(nc, 0))
+            assert np.all(g[kept:] == -1), f"{name} b{b} h{h}: padding"
+            gk = g[:kept]
+            assert np.all(np.diff(gk) > 0), f"{name} b{b} h{h}: not ascending/unique"
+            assert kept == 0 or (gk.min() >= 0 and gk.max() < nc), f"{name} b{b} h{h}: range"
+            gs, os_ = set(gk.tolist()), set(o[:kept].tolist())
+            stats["pairs"] += 1
+            if gs == os_:
+                stats["strict"] += 1
+                continue
+            P = r["S_pool"][h, s0:s0 + nc]
+            pK = float(P[list(os_)].min())
+            for i in gs ^ os_:
+                assert abs(P[i] - pK) <= rtol * abs(pK), (
+                    f"{name} b{b} h{h}: position {i} differs, oracle score {P[i]:.9g} vs "
+                    f"K-th {pK:.9g}")
+            stats["swaps"] += len(gs - os_)
+        base += K
+    return stats
+
+
+def gather_rows(x_bytes, idx, wl):
+    """Expected compacted rows for GPU indices (bit copy of the input rows)."""
+    W, Hkv = wl.window, wl.num_kv_heads
+    rows = int(np.sum(np.asarray(wl.budgets) + W))
+    row_b = x_bytes.shape[-1]
+    out = np.zeros((rows, Hkv, row_b), np.uint8)
+    base, r0 = 0, 0
+    for b, (s0, s1) in enumerate(seq_slices(wl)):
+        K = wl.budgets[b]
+        n = s1 - s0
+        for h in range(Hkv):
+            g = idx[(base * Hkv + h * K):(base * Hkv + h * K + K)]
+            kept = g[g >= 0]
+            src = np.concatenate([kept, np.arange(n - W, n)]).astype(np.int64)
+            out[r0:r0 + len(src), h] = x_bytes[s0 + src, h]
+        base += K
+        r0 += K + W
+    return out
+
+
+def as_bytes(x_f32, wl):
+    """Raw bytes of an input tensor in its storage type, [T, Hkv, d*es]."""
+    if wl.dtype == "bf16":
+        u = inputs.bf16_bits(x_f32)
+    else:
+        u = np.ascontiguousarray(x_f32, np.float32)
+    return u.view(np.uint8).reshape(x_f32.shape[0], x_f32.shape[1], -1)
+
+
+def tensor_bytes(t):
+    import torch
+    a = t.detach().cpu()
+    if a.dtype == torch.bfloat16:
+        a = a.view(torch.int16)
+    return a.numpy().view(np.uint8).reshape(a.shape[0], a.shape[1], -1)

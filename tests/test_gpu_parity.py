@@ -1,0 +1,233 @@
+"""GPU parity of the HIP path against the fp64 oracle (needs an MI355X).
+
+Every case draws seeded inputs, runs the oracle layer by layer, and runs the
+HIP path through the C ABI both as split calls (score, calibrate, select,
+compact) and as the fused per-layer call.  Scores are compared element by
+element with |x - x_ref| <= rtol (|x_ref| + mean|x_ref|) (rtol 1e-5 for fp32
+inputs, 1e-2 for bf16); kept sets must match except for ties within rtol of
+the K-th oracle score; the compacted cache must be a bit copy of the input
+rows named by the GPU's indices.
+"""
+import numpy as np
+import pytest
+
+import parity as P
+from oracle import ref
+from paper_2606_14782_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_14782_amd import bacon
+    bacon.lib()
+    ref.set_threads(16)
+
+
+def _small(idx, **kw):
+    return inputs.shrink(inputs.workload(idx), **kw)
+
+
+CASES = {
+    # model-shaped workloads at full sequence length and head count, fewer layers
+    "tiny-fp32": lambda: inputs.workload(0),
+    "llava-n2048": lambda: inputs.workload(1).with_(num_layers=6),
+    "qwen2vl-n8192": lambda: inputs.workload(2).with_(num_layers=6),
+    "video-n32768": lambda: inputs.workload(3).with_(num_layers=5),
+    "ragged-b8": lambda: inputs.workload(4).with_(num_layers=5),
+    # reduced shapes with ragged tails (lengths not multiples of the tile sizes)
+    "llava-small": lambda: _small(1, num_layers=5, max_len=1500, num_kv_heads=4),
+    "qwen2vl-small": lambda: _small(2, num_layers=5, max_len=2500, num_kv_heads=2),
+    "video-small": lambda: _small(3, num_layers=3, max_len=3000, num_kv_heads=2),
+    "ragged-small": lambda: _small(4, num_layers=5, max_len=3000, num_kv_heads=2),
+}
+
+
+def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True):
+    import torch
+    from paper_2606_14782_amd import bacon
+    rtol = P.RTOL[wl.dtype]
+    P.log(f"[{name}] {wl.name} B={wl.batch} L={wl.num_layers} Hq={wl.num_q_heads} "
+          f"Hkv={wl.num_kv_heads} d={wl.head_dim} W={wl.window} lens={wl.seq_lens[:8]}")
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    orc = ref.Prompt.for_workload(wl, P.oracle_params(**(orc_kw or {})))
+    ctx_s = P.make_ctx(wl, P.params_for(wl, **(gpu_kw or {}))) if split else None
+    ctx_f = P.make_ctx(wl, P.params_for(wl, **(gpu_kw or {}))) if fused else None
+    if split:
+        ctx_s.bacon_begin_prompt(batch)
+    if fused:
+        ctx_f.bacon_begin_prompt(batch)
+    worst = {}
+    stats = {"pairs": 0, "strict": 0, "swaps": 0}
+    for layer in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, layer)
+        r = orc.layer(layer, x["q_win"], x["k"])
+        q, k, v = P.to_dev(x["q_win"], wl), P.to_dev(x["k"], wl), P.to_dev(x["v"], wl)
+        kb, vb = P.as_bytes(x["k"], wl), P.as_bytes(x["v"], wl)
+        P.log(f"[{name}] layer {layer}")
+        idx_split = None
+        if split:
+            B, Q, lse = ctx_s.bacon_score(layer, batch, q, k, want_lse=True)
+            cal = ctx_s.bacon_calibrate(layer, batch, B, Q, want_E=True, want_V=True)
+            idx = ctx_s.bacon_select_topk(batch, cal["S"])
+            ko, vo = ctx_s.bacon_compact(batch, k, v, idx)
+            torch.cuda.synchronize()
+            for key, got in (("lse", lse), ("B", B), ("Q", Q), ("E", cal["E"]), ("V", cal["V"]),
+                             ("S", cal["S"]), ("lambda", cal["lambda"])):
+                w = P.close(f"{name} L{layer} {key}", got.cpu().numpy(), r[key], rtol)
+                worst[key] = max(worst.get(key, 0.0), w)
+            idx_split = idx.cpu().numpy()
+            P.check_idx(f"{name} L{layer} split", idx_split, r, wl, rtol)
+            assert np.array_equal(P.tensor_bytes(ko), P.gather_rows(kb, idx_split, wl))
+            assert np.array_equal(P.tensor_bytes(vo), P.gather_rows(vb, idx_split, wl))
+        if fused:
+            idx, ko, vo = ctx_f.bacon_compress_layer(layer, batch, q, k, v)
+            torch.cuda.synchronize()
+            gi = idx.cpu().numpy()
+            s = P.check_idx(f"{name} L{layer} fused", gi, r, wl, rtol)
+            for key in stats:
+                stats[key] += s[key]
+            assert np.array_equal(P.tensor_bytes(ko), P.gather_rows(kb, gi, wl)), "K gather"
+            assert np.array_equal(P.tensor_bytes(vo), P.gather_rows(vb, gi, wl)), "V gather"
+            if idx_split is not None:
+                assert np.array_equal(gi, idx_split), "fused and split paths disagree"
+        del q, k, v
+    P.log(f"[{name}] ok; worst rel err {worst}; kept sets strict {stats['strict']}/"
+          f"{stats['pairs']}, swaps {stats['swaps']}")
+    return worst, stats
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_workload_parity(name):
+    run_case(name, CASES[name]())
+
+
+EDGE = {
+    # generic row layout (G*W = 24, pad rows), d = 64, budget > |I|, budget = |I|
+    "gqa3-w8-d64": dict(wl=inputs.Workload("edge", 3, 6, 2, 64, 8, 5, "bf16", (40, 300, 77),
+                                           (5, 500, 69), ((0, 30), (10, 250), (5, 60)), 1, 7)),
+    # fp32 path with d = 128 and a window that is not a multiple of 32
+    "fp32-d128-w20": dict(wl=inputs.Workload("edge", 3, 4, 2, 128, 20, 3, "fp32", (333, 97),
+                                             (40, 7), ((10, 300), (5, 60)), 2, 8)),
+    # the window is the whole prompt: empty candidate set
+    "window-only": dict(wl=inputs.Workload("edge", 2, 4, 4, 64, 8, 5, "fp32", (8, 50),
+                                           (4, 4), ((0, 0), (0, 30)), 0, 9)),
+    # single window row, budget 1, MHA bf16
+    "w1-budget1": dict(wl=inputs.Workload("edge", 2, 2, 2, 128, 1, 1, "bf16", (129,), (1,),
+                                          ((0, 100),), 1, 10)),
+    # parameter variants on one workload
+    "radius0-m0": dict(wl=inputs.Workload("edge", 3, 4, 2, 64, 16, 5, "bf16", (600,), (32,),
+                                          ((40, 500),), 2, 11),
+                       gpu=dict(radius=0, persist_m=0), orc=dict(radius=0, persist_m=0)),
+    "m1-pool1-r9": dict(wl=inputs.Workload("edge", 4, 4, 2, 64, 16, 1, "bf16", (600,), (32,),
+                                           ((40, 500),), 2, 12),
+                        gpu=dict(radius=9, persist_m=1), orc=dict(radius=9, persist_m=1)),
+    "window-score-only": dict(wl=inputs.Workload("edge", 2, 8, 2, 128, 32, 7, "bf16", (1000,),
+                                                 (64,), ((30, 800),), 3, 13),
+                              gpu=dict(use_last_query=0), orc=dict(use_last_query=0)),
+    "gamma0": dict(wl=inputs.Workload("edge", 2, 8, 2, 128, 32, 7, "bf16", (1000,), (64,),
+                                      ((30, 800),), 3, 14),
+                   gpu=dict(gamma=0.0), orc=dict(gamma=0.0)),
+    "terms-E-T": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 7, "bf16", (1000,), (64,),
+                                         ((30, 800),), 3, 15),
+                      gpu=dict(terms=5), orc=dict(terms=5)),
+    "gamma-rho": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 7, "bf16", (1000, 700),
+                                         (64, 300), ((30, 800), (30, 600)), 3, 16),
+                      gpu=dict(gamma=0.5, rho=3.0), orc=dict(gamma=0.5, rho=3.0)),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_cases(name):
+    c = EDGE[name]
+    run_case(name, c["wl"], c.get("gpu"), c.get("orc"))
+
+
+def test_fused_pass_is_deterministic():
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = _small(4, num_layers=3, max_len=4000, num_kv_heads=2)
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    outs = []
+    for rep in range(2):
+        ctx = P.make_ctx(wl)
+        ctx.bacon_begin_prompt(batch)
+        got = []
+        for layer in range(wl.num_layers):
+            x = inputs.layer_inputs(wl, layer)
+            idx, ko, vo = ctx.bacon_compress_layer(layer, batch, P.to_dev(x["q_win"], wl),
+                                                   P.to_dev(x["k"], wl), P.to_dev(x["v"], wl))
+            torch.cuda.synchronize()
+            got.append((idx.cpu().numpy(), P.tensor_bytes(ko), P.tensor_bytes(vo)))
+        outs.append(got)
+    for a, b in zip(*outs):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+def test_outputs_stay_inside_their_buffers():
+    """Guard regions around every output are left untouched."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = _small(4, num_layers=2, max_len=2000, num_kv_heads=2)
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    ctx = P.make_ctx(wl)
+    ctx.bacon_begin_prompt(batch)
+    n_idx = batch.idx_count(wl.num_kv_heads)
+    rows = batch.kept_rows(wl.window)
+    G = 4096
+    idx_buf = torch.full((n_idx + 2 * G,), 0x5A5A5A5A, dtype=torch.int32, device="cuda")
+    row_elems = wl.num_kv_heads * wl.head_dim
+    k_buf = torch.full((rows * row_elems + 2 * G,), 3.0, dtype=torch.bfloat16, device="cuda")
+    v_buf = torch.full((rows * row_elems + 2 * G,), 5.0, dtype=torch.bfloat16, device="cuda")
+    for layer in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, layer)
+        out = (idx_buf[G:G + n_idx], k_buf[G:G + rows * row_elems].view(rows, wl.num_kv_heads, -1),
+               v_buf[G:G + rows * row_elems].view(rows, wl.num_kv_heads, -1))
+        ctx.bacon_compress_layer(layer, batch, P.to_dev(x["q_win"], wl), P.to_dev(x["k"], wl),
+                                 P.to_dev(x["v"], wl), out=out)
+    torch.cuda.synchronize()
+    for buf, fill in ((idx_buf, 0x5A5A5A5A), (k_buf, 3.0), (v_buf, 5.0)):
+        assert bool((buf[:G] == fill).all()) and bool((buf[-G:] == fill).all())
+
+
+def test_ragged_batch_equals_single_sequences(monkeypatch):
+    """Sequences of a packed batch are independent: a batch gives the same kept
+    positions as each sequence run alone (same chunking forced for both)."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    monkeypatch.setenv("BACON_CHUNK_STAGES", "2")
+    wl = _small(4, num_layers=3, max_len=2500, num_kv_heads=2)
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    ctx = P.make_ctx(wl)
+    ctx.bacon_begin_prompt(batch)
+    xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+    full = []
+    for layer, x in enumerate(xs):
+        idx, _, _ = ctx.bacon_compress_layer(layer, batch, P.to_dev(x["q_win"], wl),
+                                             P.to_dev(x["k"], wl), P.to_dev(x["v"], wl))
+        full.append(idx.cpu().numpy())
+    cu = wl.cu_seqlens
+    base = 0
+    for b in range(wl.batch):
+        one = wl.with_(seq_lens=(wl.seq_lens[b],), budgets=(wl.budgets[b],),
+                       visual=(wl.visual[b],))
+        bt = bacon.BatchLayout(one.cu_seqlens, one.budgets_arr)
+        c1 = P.make_ctx(one)
+        c1.bacon_begin_prompt(bt)
+        K = wl.budgets[b]
+        for layer, x in enumerate(xs):
+            q = x["q_win"][b * wl.window:(b + 1) * wl.window]
+            k = x["k"][cu[b]:cu[b + 1]]
+            v = x["v"][cu[b]:cu[b + 1]]
+            idx, _, _ = c1.bacon_compress_layer(layer, bt, P.to_dev(q, wl), P.to_dev(k, wl),
+                                                P.to_dev(v, wl))
+            got = idx.cpu().numpy()
+            want = full[layer][base * wl.num_kv_heads:(base + K) * wl.num_kv_heads]
+            assert np.array_equal(got, want), f"sequence {b} layer {layer}"
+        base += K
+    torch.cuda.synchronize()
