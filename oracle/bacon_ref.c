@@ -132,14 +132,19 @@ double bacon_ref_lambda(int n_cand, const double *B, const double *V, int budget
   }
   int32_t *sel = (int32_t *)malloc(sizeof(int32_t) * (size_t)M);
   bacon_ref_topk(n_cand, B, M, sel);
+  /* Population variance, two-pass; values are first shifted by the first
+   * member of the set (variance is shift-invariant), so constant data gives
+   * exactly 0 rather than rounding noise that eps would amplify. */
+  const double b0 = B[sel[0]], v0 = V[sel[0]];
   double mb = 0.0, mv = 0.0;
-  for (int j = 0; j < M; ++j) { mb += B[sel[j]]; mv += V[sel[j]]; }
+  for (int j = 0; j < M; ++j) { mb += B[sel[j]] - b0; mv += V[sel[j]] - v0; }
   mb /= (double)M;
   mv /= (double)M;
   double vb = 0.0, vv = 0.0;
   for (int j = 0; j < M; ++j) {
-    vb += (B[sel[j]] - mb) * (B[sel[j]] - mb);
-    vv += (V[sel[j]] - mv) * (V[sel[j]] - mv);
+    const double db = (B[sel[j]] - b0) - mb, dv = (V[sel[j]] - v0) - mv;
+    vb += db * db;
+    vv += dv * dv;
   }
   free(sel);
   const double sb = sqrt(vb / (double)M), sv = sqrt(vv / (double)M);

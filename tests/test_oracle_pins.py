@@ -199,6 +199,9 @@ def test_lambda_scale_invariance_and_set_size(oracle):
     assert oracle.lambda_(B, V, 0, 20)["lambda"] == 0.0
     z = oracle.lambda_(B, np.zeros(100), 90, 10)
     assert z["sigma_V"] == 0.0 and math.isfinite(z["lambda"])
+    # the standard deviation of a constant set is exactly zero, so lambda is 0
+    c = oracle.lambda_(np.full(100, 1.0 / 3.0), rng.random(100), 90, 10)
+    assert c["sigma_B"] == 0.0 and c["lambda"] == 0.0
 
 
 # --------------------------------------------------------------- whole layers
