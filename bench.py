@@ -1,0 +1,235 @@
+"""Benchmark of the BACON prefill KV-compression pass on one MI355X.
+
+One step = the whole pass of a prompt: bacon_begin_prompt and
+bacon_compress_layer for every layer (score -> calibrate -> select -> compact),
+on the 32K-token long-video GQA workload (32 layers, 32 query / 8 KV heads,
+d = 128, window 32, budget 256, bf16).  Inputs are synthetic, seeded, and
+resident in HBM before timing starts.
+
+Prints one JSON line: keys scored per second (positions x KV heads x layers
+per second), ms per step and per layer, a roofline entry for the dominant
+kernel (algorithmic bytes / mean launch time from HIP events recorded around
+each launch on the pass's stream) and the fp64 CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "KV compression pass ms/layer + keys scored/sec; HBM GB/s vs peak at N=32K"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(wl, persist_m=4):
+    """Bytes a layer must move at minimum: K once, Q_win, the E history read and
+    write, the gather of kept and window rows of K and V, and the indices."""
+    es = wl.elem_size
+    T, Hkv, d = wl.total_tokens, wl.num_kv_heads, wl.head_dim
+    k_bytes = T * Hkv * d * es
+    q_bytes = wl.batch * wl.window * wl.num_q_heads * d * es
+    kept_rows = sum(b + wl.window for b in wl.budgets)
+    gather = 2 * 2 * kept_rows * Hkv * d * es
+    idx = 4 * sum(wl.budgets) * Hkv
+    per_layer = []
+    for l in range(wl.num_layers):
+        ring = (min(persist_m, l) + 1) * T * Hkv * 4
+        per_layer.append(k_bytes + q_bytes + ring + gather + idx)
+    return {"k": k_bytes, "q": q_bytes, "layer_mean": float(np.mean(per_layer)),
+            "layers": per_layer}
+
+
+def kernel_bytes(name, wl, persist_m=4):
+    """Algorithmic bytes of one launch of a kernel of the fused pass (mean over layers)."""
+    ab = algorithmic_bytes(wl, persist_m)
+    T, Hkv = wl.total_tokens, wl.num_kv_heads
+    if name == "window_lse":
+        return ab["k"] + ab["q"]
+    if name == "window_score_calib":
+        ring = np.mean([(min(persist_m, l) + 1) * T * Hkv * 4 for l in range(wl.num_layers)])
+        return ab["k"] + ab["q"] + ring + 2 * T * Hkv * 4
+    if name == "select_fused":
+        kept_rows = sum(b + wl.window for b in wl.budgets)
+        return 3 * T * Hkv * 4 + 4 * kept_rows * Hkv * wl.head_dim * wl.elem_size
+    return 0.0
+
+
+def source_sha():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_14782_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except Exception:
+        return None
+    if rec.get("source_sha") != source_sha():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    return None if k is None else float(k["bytes_per_launch"])
+
+
+def cpu_baseline(wl, budget_s, gpu_idx=None):
+    """The fp64 oracle on this host, on layers 0.. of the same workload until
+    about budget_s seconds have been spent (layers run in order)."""
+    from oracle import ref
+    from paper_2606_14782_amd import inputs
+    ref.build(force=False)
+    threads = min(os.cpu_count() or 1, 16)
+    ref.set_threads(threads)
+    used = min(threads, wl.batch * wl.num_kv_heads)
+    p = ref.Prompt.for_workload(wl)
+    spent, layers, agree = 0.0, 0, True
+    while layers < wl.num_layers and spent < budget_s:
+        x = inputs.layer_inputs(wl, layers)
+        t0 = time.perf_counter()
+        r = p.layer(layers, x["q_win"], x["k"])
+        spent += time.perf_counter() - t0
+        if gpu_idx is not None and layers < len(gpu_idx):
+            agree = agree and bool(np.array_equal(r["idx"], gpu_idx[layers]))
+        layers += 1
+    keys = wl.total_tokens * wl.num_kv_heads * layers
+    return {"value": keys / spent, "unit": "keys/s", "cores": used, "kind": "oracle",
+            "sample": f"layers 0-{layers - 1} of the {wl.num_layers}-layer workload "
+                      f"({spent:.1f} s, OpenMP over (sequence, KV head))",
+            "ms_per_layer": 1e3 * spent / layers,
+            "kept_sets_identical_to_gpu": agree if gpu_idx is not None else None}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=3, help="workload index (default: 32K video)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the pass shards "
+              f"by KV head with no exchange, so N GPUs each run this one-GPU workload on "
+              f"H_kv/N heads.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_14782_amd import bacon, inputs
+
+    wl = inputs.workload(args.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload {wl.name}: generating {wl.num_layers} layers")
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    qs, ks, vs = [], [], []
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    for l in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, l)
+        qs.append(torch.from_numpy(x["q_win"]).to(dev).to(tdt))
+        ks.append(torch.from_numpy(x["k"]).to(dev).to(tdt))
+        vs.append(torch.from_numpy(x["v"]).to(dev).to(tdt))
+    params = bacon.default_params(pool_kernel=wl.pool_kernel)
+    ctx = bacon.Context(wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window,
+                        wl.batch, wl.total_tokens, wl.dtype, params)
+    n_idx = batch.idx_count(wl.num_kv_heads)
+    rows = batch.kept_rows(wl.window)
+    outs = [(torch.empty(n_idx, dtype=torch.int32, device=dev),
+             torch.empty((rows, wl.num_kv_heads, wl.head_dim), dtype=tdt, device=dev),
+             torch.empty((rows, wl.num_kv_heads, wl.head_dim), dtype=tdt, device=dev))
+            for _ in range(wl.num_layers)]
+
+    def step():
+        ctx.bacon_begin_prompt(batch)
+        for l in range(wl.num_layers):
+            ctx.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l], out=outs[l])
+
+    log("warmup")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    gpu_idx = [o[0].cpu().numpy() for o in outs[:8]]
+
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = 1e3 * wall / args.steps
+
+    # Same region again with HIP events around every launch (on the pass's stream).
+    ctx.bacon_profile_enable(True)
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kt = ctx.bacon_profile_read()
+    ctx.bacon_profile_enable(False)
+    per_kernel = {k: {"launches": n, "avg_us": 1e3 * ms / n} for k, (n, ms) in kt.items()}
+    dom = max((k for k in per_kernel if kernel_bytes(k, wl) > 0),
+              key=lambda k: per_kernel[k]["avg_us"])
+    kbytes = kernel_bytes(dom, wl)
+    achieved = kbytes / (per_kernel[dom]["avg_us"] * 1e-6) / 1e9
+    traffic = measured_traffic(dom)
+
+    ab = algorithmic_bytes(wl)
+    ms_layer = ms_step / wl.num_layers
+    keys_step = wl.total_tokens * wl.num_kv_heads * wl.num_layers
+    pass_gbs = ab["layer_mean"] / (ms_layer * 1e-3) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": keys_step / (ms_step * 1e-3),
+        "unit": "keys/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "ms_per_layer": ms_layer,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded N(0,1) Q/K/V with frame-periodic low-rank K), random",
+        "config": {"workload": f"{wl.name}: {wl.num_layers} layers, {wl.num_q_heads}/"
+                               f"{wl.num_kv_heads} heads, d={wl.head_dim}, N="
+                               f"{wl.seq_lens[0] if wl.batch == 1 else list(wl.seq_lens)}, "
+                               f"W={wl.window}, pool {wl.pool_kernel}, budget "
+                               f"{list(set(wl.budgets))}",
+                   "batch": wl.batch, "tokens": wl.total_tokens, "layers": wl.num_layers},
+        "pass_hbm": {"bytes_per_layer": ab["layer_mean"], "achieved_GBs": pass_gbs,
+                     "frac_of_peak": pass_gbs / HBM_PEAK_GBS},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": dom,
+                     "bytes_per_launch": kbytes, "avg_us": per_kernel[dom]["avg_us"]},
+        "kernels": per_kernel,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, gpu_idx)
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

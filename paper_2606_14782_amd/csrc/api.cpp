@@ -36,8 +36,8 @@ bacon_status hip_fail(hipError_t e, const char *what) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ring, vec_b, vec_ept, partials, lse2, counters, lambda, total;
-  int rpad, slots;
+  size_t ring, vec_b, vec_vp, partials, lambda, total;
+  int rpad, slots, ring_mp;
   int64_t chunks_cap;
 };
 
@@ -87,16 +87,15 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   const int G = s->num_q_heads / s->num_kv_heads;
   L.rpad = ((G * s->window + 31) / 32) * 32;
   L.slots = p->persist_m > 0 ? p->persist_m : 1;
+  L.ring_mp = 4 * ((L.slots + 3) / 4);
   const int tk = 32 * std::min(L.rpad / 32, 4);
   L.chunks_cap = (s->max_total_tokens + tk - 1) / tk + s->max_batch;
   const size_t vec = (size_t)s->num_kv_heads * (size_t)s->max_total_tokens * sizeof(float);
   size_t off = 0;
-  L.ring = off;     off += align256((size_t)L.slots * vec);
+  L.ring = off;     off += align256((size_t)L.ring_mp * vec);
   L.vec_b = off;    off += align256(vec);
-  L.vec_ept = off;  off += align256(vec);
+  L.vec_vp = off;   off += align256(vec);
   L.partials = off; off += align256((size_t)s->num_kv_heads * L.chunks_cap * L.rpad * sizeof(float2));
-  L.lse2 = off;     off += align256((size_t)s->max_batch * s->num_kv_heads * L.rpad * sizeof(float));
-  L.counters = off; off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(unsigned));
   L.lambda = off;   off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(float));
   L.total = off;
   return L;
@@ -104,9 +103,9 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
 
 const char *kKernelNames[] = {"window_lse", "window_score", "window_score_calib",
                               "select_fused", "select_calib", "select_topk", "calib_elem",
-                              "compact", "clear"};
+                              "compact"};
 enum KernelId { KI_LSE, KI_SCORE, KI_FUSED, KI_SEL_FUSED, KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM,
-                KI_COMPACT, KI_CLEAR, KI_COUNT };
+                KI_COMPACT, KI_COUNT };
 
 }  // namespace
 
@@ -120,7 +119,6 @@ struct bacon_ctx {
   int next_layer = 0;
   std::vector<int32_t> cu, budgets;
   int chunk_stages_override = 0;
-  bool counters_clean = false;
   // profiling
   bool prof = false;
   std::vector<hipEvent_t> ev_pool;
@@ -199,19 +197,22 @@ SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out) {
   SeqTable st{};
   st.batch = bt->batch;
   const bool bf16 = c->shape.dtype == BACON_BF16;
-  const PassGeom g = pass_geom(PASS_FUSED, bf16, c->shape.head_dim, c->L.rpad);
+  const int nw = c->L.rpad / 32, tk = stage_keys(nw);
   int64_t stages = 0;
   for (int b = 0; b < bt->batch; ++b) {
     const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
-    stages += (n + g.tk - 1) / g.tk;
+    stages += (n + tk - 1) / tk;
   }
   stages *= c->shape.num_kv_heads;
-  const int by_lds = std::max(1, (160 * 1024) / std::max(1, g.lds));
-  const int by_waves = std::max(1, 16 / g.nw);
+  // one round of workgroups over the 256 CUs at the occupancy LDS and waves allow
+  const int lds = pass_lds_bytes(PASS_FUSED, bf16, c->shape.head_dim, c->L.rpad, 4 * tk);
+  const int by_lds = std::max(1, (160 * 1024) / std::max(1, lds));
+  const int by_waves = std::max(1, 16 / nw);
   const int64_t slots = 256LL * std::min(by_lds, by_waves);
   int per_wg = (int)std::max<int64_t>(1, (stages + slots - 1) / slots);
   if (c->chunk_stages_override > 0) per_wg = c->chunk_stages_override;
-  const int chunk = g.tk * per_wg;
+  per_wg = std::min(per_wg, kMaxChunk / tk);
+  const int chunk = tk * per_wg;
   int cb = 0, ib = 0, kb = 0;
   for (int b = 0; b < bt->batch; ++b) {
     const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
@@ -246,23 +247,20 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   a.T = s.max_total_tokens;
   a.c2 = (float)(1.4426950408889634 / std::sqrt((double)s.head_dim));
   a.partials = reinterpret_cast<float2 *>(c->ws + c->L.partials);
-  a.lse2 = reinterpret_cast<float *>(c->ws + c->L.lse2);
-  a.counters = reinterpret_cast<unsigned *>(c->ws + c->L.counters);
   a.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
   a.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
-  a.vec_EpT = reinterpret_cast<float *>(c->ws + c->L.vec_ept);
+  a.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
+  a.radius = c->params.radius;
   a.terms = c->params.terms;
   (void)st;
   return a;
 }
 
-// Ring slots for layer `layer`: write slot and the slots of the previous
-// min(m, layer) layers, oldest first.
-void ring_slots(const bacon_ctx *c, int layer, int *wr, int *cnt, int *rd) {
-  const int m = c->params.persist_m, S = c->L.slots;
-  *cnt = std::min(m, layer);
-  for (int j = 0; j < *cnt; ++j) rd[j] = (layer - *cnt + j) % S;
-  *wr = layer % S;
+// History slots for layer `layer`: E of layer j lives in slot j % max(m, 1),
+// so the previous min(m, layer) layers occupy slots 0 .. cnt-1.
+void ring_slots(const bacon_ctx *c, int layer, int *wr, int *cnt) {
+  *cnt = std::min(c->params.persist_m, layer);
+  *wr = layer % c->L.slots;
 }
 
 SelArgs sel_args(const bacon_ctx *c) {
@@ -280,22 +278,11 @@ SelArgs sel_args(const bacon_ctx *c) {
   a.use_last_query = p.use_last_query;
   a.terms = p.terms;
   a.vec_B = reinterpret_cast<const float *>(c->ws + c->L.vec_b);
-  a.vec_EpT = reinterpret_cast<const float *>(c->ws + c->L.vec_ept);
+  a.vec_VP = reinterpret_cast<const float *>(c->ws + c->L.vec_vp);
+  a.vp_chunk = 1 << 30;
   a.lambda_ws = reinterpret_cast<float *>(c->ws + c->L.lambda);
   a.row_bytes = s.head_dim * (s.dtype == BACON_BF16 ? 2 : 4);
   return a;
-}
-
-// The pass-1 arrival counters must start at zero; they reset themselves
-// after every pass, so one clear per context suffices.
-bacon_status ensure_counters(bacon_ctx *c, hipStream_t s) {
-  if (c->counters_clean) return BACON_OK;
-  const int64_t ncnt = (int64_t)c->shape.max_batch * c->shape.num_kv_heads;
-  TRY(timed(c, KI_CLEAR, s, [&] {
-    return launch_clear_u32(reinterpret_cast<unsigned *>(c->ws + c->L.counters), ncnt, s);
-  }));
-  c->counters_clean = true;
-  return BACON_OK;
 }
 
 int max_len(const bacon_batch *bt) {
@@ -348,7 +335,6 @@ bacon_status bacon_init(bacon_ctx **ctx, const bacon_shape *shape, const bacon_p
   c->ws_bytes = ws_bytes;
   c->L = L;
   if (const char *e = std::getenv("BACON_CHUNK_STAGES")) c->chunk_stages_override = std::atoi(e);
-  c->counters_clean = false;   // cleared by the first enqueue on a stream
   *ctx = c;
   return BACON_OK;
 }
@@ -367,8 +353,8 @@ bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *strea
   c->budgets.assign(bt->budgets, bt->budgets + bt->batch);
   c->prompt = true;
   c->next_layer = 0;
-  c->counters_clean = false;
-  return ensure_counters(c, static_cast<hipStream_t>(stream));
+  (void)stream;   // nothing to enqueue: layer 0 reads no history
+  return BACON_OK;
 }
 
 bacon_status bacon_score(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
@@ -392,7 +378,6 @@ bacon_status bacon_score(bacon_ctx *c, int32_t layer, const bacon_batch *bt, con
   a.out_Q = d_Q;
   const bool bf16 = c->shape.dtype == BACON_BF16;
   const bool w32 = c->shape.window == 32;
-  TRY(ensure_counters(c, s));
   TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
   return timed(c, KI_SCORE, s, [&] { return launch_pass(PASS_SCORE, bf16, c->shape.head_dim, w32, a, st, s); });
 }
@@ -421,17 +406,23 @@ bacon_status bacon_calibrate(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
   e.in_B = d_B;
   e.in_Q = d_Q;
   e.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
-  ring_slots(c, layer, &e.ring_write, &e.ring_cnt, e.ring_read);
-  e.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
-  e.vec_EpT = reinterpret_cast<float *>(c->ws + c->L.vec_ept);
+  ring_slots(c, layer, &e.ring_write, &e.ring_cnt);
+  e.ring_mp = c->L.ring_mp;
+  e.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
   e.Hkv = c->shape.num_kv_heads;
+  e.radius = c->params.radius;
+  e.chunk = chunk;
   e.T = T;
   e.terms = c->params.terms;
   // the [Hkv, T] vectors of the split path use the batch's T as row length
-  TRY(timed(c, KI_ELEM, s, [&] { return launch_elem(e, s); }));
+  TRY(timed(c, KI_ELEM, s, [&] { return launch_elem(e, st, s); }));
   SelArgs a = sel_args(c);
   a.T = T;
-  a.ring_E = e.ring + (int64_t)e.ring_write * c->shape.num_kv_heads * T;
+  a.vec_B = d_B;
+  a.vp_chunk = chunk;   // same chunking as the fused pass
+  a.ring = e.ring;
+  a.ring_mp = c->L.ring_mp;
+  a.ring_slot = e.ring_write;
   a.out_S = d_S;
   a.out_V = d_V;
   a.out_E = d_E;
@@ -503,15 +494,18 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   const int64_t T = bt->cu_seqlens[bt->batch];
   PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
   a.T = T;
-  ring_slots(c, layer, &a.ring_write, &a.ring_cnt, a.ring_read);
+  ring_slots(c, layer, &a.ring_write, &a.ring_cnt);
+  a.ring_mp = c->L.ring_mp;
   const bool bf16 = c->shape.dtype == BACON_BF16;
   const bool w32 = c->shape.window == 32;
-  TRY(ensure_counters(c, s));
   TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
   TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
   SelArgs sa = sel_args(c);
   sa.T = T;
-  sa.ring_E = a.ring + (int64_t)a.ring_write * c->shape.num_kv_heads * T;
+  sa.ring = a.ring;
+  sa.ring_mp = c->L.ring_mp;
+  sa.ring_slot = a.ring_write;
+  sa.vp_chunk = chunk;
   sa.idx = d_idx;
   sa.k = d_k;
   sa.v = d_v;

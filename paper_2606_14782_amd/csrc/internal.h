@@ -10,7 +10,9 @@ constexpr int kMaxBatch = 64;       // sequences per batch (kernel-argument tabl
 constexpr int kMaxSeqLen = 32768;   // positions per sequence held by the select kernel
 constexpr int kMaxRows = 256;       // G*W window rows per KV head (8 row tiles of 32)
 constexpr int kMaxRing = 16;        // persistence depth m
-constexpr int kSelThreads = 512;
+constexpr int kMaxChunk = 4096;     // keys per pass workgroup
+constexpr int kSelThreads = 1024;
+constexpr int kSelPer = kMaxSeqLen / kSelThreads;   // positions per select thread
 constexpr int kHistBins = 2048;     // 11-bit digits of the block select
 
 // Per-sequence layout, passed by value to every kernel.
@@ -34,18 +36,18 @@ struct PassArgs {
   int chunk;            // keys per chunk (multiple of the stage size)
   int64_t T;            // row length of the [Hkv, T] vectors
   float c2;             // log2(e) / sqrt(d)
-  // pass 1
-  float2 *partials;     // [Hkv, total_chunks, Rpad]  (max, sum) in log2 units
-  float *lse2;          // [B, Hkv, Rpad]  log2-domain normaliser, +inf for pad rows
+  float2 *partials;     // [Hkv, total_chunks, Rpad]  (max, sum) per chunk, log2 units
   float *lse_user;      // optional [B, Hq, W] natural-log normaliser
-  unsigned *counters;   // [B, Hkv] arrival counters of the chunk WGs
-  // pass 2
-  float *out_B, *out_Q; // PASS_SCORE: [Hkv, T]
-  float *ring;          // [slots, Hkv, T] E history
+  // PASS_SCORE
+  float *out_B, *out_Q; // [Hkv, T]
+  // PASS_FUSED
+  float *ring;          // [Hkv, T, ring_mp] E history, slot l % max(m,1) holds layer l
+  int ring_mp;          // slots per position, padded to a multiple of 4
   int ring_write;       // slot receiving this layer's E
-  int ring_cnt;         // number of earlier layers averaged into T
-  int ring_read[kMaxRing];
-  float *vec_B, *vec_EpT;  // PASS_FUSED: B and E+T (per the terms mask) [Hkv, T]
+  int ring_cnt;         // earlier layers averaged into T (they occupy slots 0..cnt-1)
+  float *vec_B;         // [Hkv, T] window score
+  float *vec_VP;        // [Hkv, T] E + T + in-chunk part of L (per the terms mask)
+  int radius;
   uint32_t terms;
 };
 
@@ -55,12 +57,14 @@ struct SelArgs {
   int Hkv, W;
   int64_t T;
   int radius, pool_half;
+  int vp_chunk;            // chunk size of the in-chunk L partial in vec_VP
   float rho, gamma, eps;
   int use_last_query;
   uint32_t terms;
   const float *vec_B;      // [Hkv, T]
-  const float *vec_EpT;    // [Hkv, T]
-  const float *ring_E;     // this layer's E slot [Hkv, T]
+  const float *vec_VP;     // [Hkv, T]
+  const float *ring;       // [Hkv, T, ring_mp] E history
+  int ring_mp, ring_slot;  // slot of this layer's E
   const float *in_S;       // SEL_TOPK: user S [Hkv, T]
   float *out_S, *out_V, *out_E;  // SEL_CALIB optional outputs [Hkv, T]
   float *out_lambda;       // optional [B, Hkv]
@@ -73,14 +77,12 @@ struct SelArgs {
   int do_gather;
 };
 
-struct ElemArgs {           // split calibrate: E, T, ring update
+struct ElemArgs {           // split calibrate: E, T, L, ring update
   const float *in_B, *in_Q;
   float *ring;
-  int ring_write, ring_cnt;
-  int ring_read[kMaxRing];
-  float *vec_B, *vec_EpT;
-  float *out_E;
-  int Hkv;
+  int ring_mp, ring_write, ring_cnt;
+  float *vec_VP;
+  int Hkv, radius, chunk;
   int64_t T;
   uint32_t terms;
 };
@@ -92,20 +94,16 @@ struct CompactArgs {
   int Hkv, W, row_bytes;
 };
 
-// Launch geometry of the K-streaming passes for a given shape.
-struct PassGeom {
-  int nw;       // waves per workgroup = row tiles
-  int tk;       // keys per pipeline stage
-  int lds;      // dynamic LDS bytes
-};
-PassGeom pass_geom(int mode, bool bf16, int head_dim, int rpad);
+// Keys per pipeline stage of the passes for a given number of row tiles.
+__host__ __device__ inline int stage_keys(int nw) { return 32 * (nw < 4 ? nw : 4); }
+// Dynamic LDS of a pass workgroup.
+int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk);
 
 hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
                        const SeqTable &st, hipStream_t s);
 hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,
                          hipStream_t s);
-hipError_t launch_elem(const ElemArgs &a, hipStream_t s);
+hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
-hipError_t launch_clear_u32(unsigned *p, int64_t n, hipStream_t s);
 
 }  // namespace bacon

@@ -1,26 +1,29 @@
 // gfx950 kernels of the BACON prefill KV-compression pass.
 //
-// Pass 1 (PASS_LSE) and pass 2 (PASS_SCORE / PASS_FUSED) stream the layer's
-// keys once each.  A workgroup owns one (KV head, key chunk); its waves own
+// Pass 1 (PASS_LSE) and pass 2 (PASS_SCORE / PASS_FUSED) each stream the
+// layer's keys once.  A workgroup owns one (KV head, key chunk); its waves own
 // the 32-row tiles of the G*W window queries of that KV head.  Key tiles are
 // staged through LDS with coalesced 16-byte loads and consumed by 32x32 MFMA
 // (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32).
 //
 //  * Pass 1 computes D = K Q^T so each lane holds one query row: the running
-//    row max and sum of exp2 stay in-lane; per-chunk partials are merged by
-//    the last workgroup of each (sequence, KV head) into the row normaliser.
-//  * Pass 2 computes D = Q K^T so each lane holds one key: the window mean B
-//    and last-query score Q are in-lane sums over the lane's rows, reduced
-//    across row tiles through LDS in a fixed order (deterministic).  The fused
-//    variant then forms E = [Q-B]_+ (Eq. boundary_residual), reads the E of
-//    the previous layers for T (Eq. inter_layer_persistence) and appends E to
-//    the history ring.
+//    row max and sum of exp2 stay in-lane; each chunk writes one (max, sum)
+//    partial per row.
+//  * Pass 2 merges the partials of its KV head into the row normalisers while
+//    its first key stage is in flight, then computes D = Q K^T so each lane
+//    holds one key: the window mean B and the last-query score Q are in-lane
+//    sums over the lane's rows, reduced across row tiles through LDS in a
+//    fixed order (deterministic).  The fused variant forms E = [Q-B]_+
+//    (Eq. boundary_residual), T from the E history (Eq. inter_layer_persistence),
+//    appends E to the history, and adds the part of L = P_r E
+//    (Eq. intra_layer_coherence) whose neighbours lie inside the chunk.
 //
-// The select kernel (one workgroup per (sequence, KV head)) computes
-// L = P_r E (Eq. intra_layer_coherence), V (Eq. structurally_calibrated_evidence),
-// the scale-matching set and lambda (Eqs. scale_matching_set, lambda_solution),
-// S (Eq. bacon_score), the pooled score, the top-K (Eq. topk_selection) and
-// optionally gathers the compacted cache.
+// The select kernel (one workgroup per (sequence, KV head)) completes L at
+// chunk boundaries, forms V (Eq. structurally_calibrated_evidence), selects the
+// scale-matching set and computes lambda (Eqs. scale_matching_set,
+// lambda_solution), S (Eq. bacon_score), the pooled score and the top-K
+// (Eq. topk_selection), emits the kept positions in ascending order and
+// gathers the compacted cache.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -65,6 +68,17 @@ __device__ __forceinline__ int find_seq(const SeqTable &st, int chunk) {
   return b;
 }
 
+// Dynamic LDS above 64 KiB has to be allowed per kernel before launch.
+template <typename Kern>
+static void allow_lds(Kern kernel, size_t bytes) {
+  static size_t granted = 0;
+  if (bytes > 64 * 1024 && bytes > granted) {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    granted = bytes;
+  }
+}
+
 // ---------------------------------------------------------------- passes
 template <bool BF16, int D>
 struct PassCfg {
@@ -76,7 +90,20 @@ struct PassCfg {
   static constexpr int MAXL = PIECES / 2;      // max staged loads per thread
 };
 
-__host__ __device__ inline int stage_keys(int nw) { return 32 * (nw < 4 ? nw : 4); }
+// LDS map of a pass workgroup (bytes):
+//   kbuf  2 * tk * STRIDE         double-buffered key stages
+//   red   2 * 2 * nw * tk floats  per-stage B/Q partials of each row tile  (pass 2)
+//   lse   Rpad floats             row normalisers                          (pass 2)
+//   mrg   2 * Rpad float2         partial-merge scratch                    (pass 2)
+//   ce    chunk floats            E of the chunk                           (fused)
+//   cv    chunk floats            E + T of the chunk                       (fused)
+int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk) {
+  const int nw = rpad / 32, tk = stage_keys(nw);
+  int bytes = 2 * tk * (head_dim * (bf16 ? 2 : 4) + 16);
+  if (mode != PASS_LSE) bytes += 16 * nw * tk + 4 * rpad + 16 * rpad;
+  if (mode == PASS_FUSED) bytes += 8 * chunk;
+  return bytes;
+}
 
 template <int MODE, bool BF16, int D, bool W32>
 __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
@@ -97,7 +124,40 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   const int wfirst = n - W;                      // position of window row 0
 
   unsigned char *kbuf = smem;
-  float *red = reinterpret_cast<float *>(smem + 2 * tk * C::STRIDE);  // [2][2][nw][tk]
+  float *red = reinterpret_cast<float *>(smem + 2 * tk * C::STRIDE);   // [2][2][nw][tk]
+  float *lse_s = red + 4 * nw * tk;                                    // [Rpad]
+  float2 *mrg = reinterpret_cast<float2 *>(lse_s + a.Rpad);            // [2][Rpad]
+  float *ce = reinterpret_cast<float *>(mrg + 2 * a.Rpad);             // [chunk]
+  float *cv = ce + a.chunk;                                            // [chunk]
+
+  // Stage loader: thread t moves pieces q = t + j*nt of the stage.
+  const unsigned char *kb = static_cast<const unsigned char *>(a.k) +
+                            ((int64_t)st.cu[b] * a.Hkv + h) * C::ROWB;
+  const int64_t kstride = (int64_t)a.Hkv * C::ROWB;
+  const int stage_pieces = tk * C::PIECES;
+  u32x4 pre[C::MAXL];
+  // Straight-line, unconditional loads: pieces past the stage and keys past
+  // the chunk are clamped to valid addresses (duplicates are masked or
+  // rewritten with identical data), so all loads stay in flight together.
+  auto fetch = [&](int s) {
+    const int key0 = k0 + s * tk;
+#pragma unroll
+    for (int j = 0; j < C::MAXL; ++j) {
+      const int q = min(t + j * nt, stage_pieces - 1);
+      const int key = min(key0 + q / C::PIECES, k1 - 1);
+      pre[j] = *reinterpret_cast<const u32x4 *>(kb + (int64_t)key * kstride + 16 * (q % C::PIECES));
+    }
+  };
+  auto commit = [&](int buf) {
+    unsigned char *dst = kbuf + buf * tk * C::STRIDE;
+#pragma unroll
+    for (int j = 0; j < C::MAXL; ++j) {
+      const int q = min(t + j * nt, stage_pieces - 1);
+      *reinterpret_cast<u32x4 *>(dst + (q / C::PIECES) * C::STRIDE + 16 * (q % C::PIECES)) = pre[j];
+    }
+  };
+
+  fetch(0);   // first key stage in flight while the prologue runs
 
   // Query fragments of this wave's row tile.
   u32x4 qf[C::NU];
@@ -115,42 +175,6 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
     }
   }
 
-  // Stage loader: thread t moves pieces q = t + j*nt of the stage.
-  const unsigned char *kb = static_cast<const unsigned char *>(a.k) +
-                            ((int64_t)st.cu[b] * a.Hkv + h) * C::ROWB;
-  const int64_t kstride = (int64_t)a.Hkv * C::ROWB;
-  const int stage_pieces = tk * C::PIECES;
-  const int loads = (stage_pieces + nt - 1) / nt;
-  u32x4 pre[C::MAXL];
-  auto fetch = [&](int s) {
-    const int key0 = k0 + s * tk;
-    const int nvalid = min(tk, k1 - key0);
-#pragma unroll
-    for (int j = 0; j < C::MAXL; ++j) {
-      if (j < loads) {
-        const int q = t + j * nt;
-        const int key = q / C::PIECES, piece = q % C::PIECES;
-        if (q < stage_pieces && key < nvalid)
-          pre[j] = *reinterpret_cast<const u32x4 *>(kb + (int64_t)(key0 + key) * kstride + 16 * piece);
-        else
-          pre[j] = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  };
-  auto commit = [&](int buf) {
-    unsigned char *dst = kbuf + buf * tk * C::STRIDE;
-#pragma unroll
-    for (int j = 0; j < C::MAXL; ++j) {
-      if (j < loads) {
-        const int q = t + j * nt;
-        if (q < stage_pieces) {
-          const int key = q / C::PIECES, piece = q % C::PIECES;
-          *reinterpret_cast<u32x4 *>(dst + key * C::STRIDE + 16 * piece) = pre[j];
-        }
-      }
-    }
-  };
-
   const int nstages = (k1 - k0 + tk - 1) / tk;
 
   // ---- pass-1 state: running max (raw logit units) and sum of exp2
@@ -165,24 +189,78 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   int wrow[16];                    // window index of each row (W for pad rows)
   uint32_t lastmask = 0;           // rows that are the last query of their head
   if constexpr (MODE != PASS_LSE) {
-    const float *l2 = a.lse2 + ((int64_t)b * a.Hkv + h) * a.Rpad;
+    // Merge the pass-1 partials of this (sequence, KV head): thread t takes
+    // row t % Rpad and every other chunk; 16 independent loads per batch.
+    const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
+    const float2 *pp = a.partials + ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad;
+    const int row = t % a.Rpad, part = t / a.Rpad;
+    float mm = -INFINITY, ll = 0.f;
+    for (int c0 = part; c0 < nch; c0 += 32) {
+      float2 v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int cc = c0 + 2 * j;
+        v[j] = pp[(int64_t)min(cc, nch - 1) * a.Rpad + row];
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        if (c0 + 2 * j >= nch) v[j] = make_float2(-INFINITY, 0.f);
+      float mb = mm;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mb = fmaxf(mb, v[j].x);
+      if (mb != -INFINITY) {
+        float acc = (mm == -INFINITY) ? 0.f : ll * __builtin_amdgcn_exp2f(mm - mb);
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (v[j].x != -INFINITY) acc += v[j].y * __builtin_amdgcn_exp2f(v[j].x - mb);
+        ll = acc;
+        mm = mb;
+      }
+    }
+    mrg[part * a.Rpad + row] = make_float2(mm, ll);
+    __syncthreads();
+    if (t < a.Rpad) {
+      const float2 p0 = mrg[t], p1 = mrg[a.Rpad + t];
+      const float m = fmaxf(p0.x, p1.x);
+      float l = 0.f;
+      if (m != -INFINITY) {
+        if (p0.x != -INFINITY) l += p0.y * __builtin_amdgcn_exp2f(p0.x - m);
+        if (p1.x != -INFINITY) l += p1.y * __builtin_amdgcn_exp2f(p1.x - m);
+      }
+      const float lse2 = (t < a.R) ? m + log2f(l) : INFINITY;
+      lse_s[t] = lse2;
+      if (a.lse_user && c == 0 && t < a.R) {
+        const int g = t / W, w = t - g * W;
+        a.lse_user[((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w] = lse2 * kLn2;
+      }
+    }
+    __syncthreads();
 #pragma unroll
     for (int reg = 0; reg < 16; ++reg) {
       const int r = wave * 32 + acc_row(reg, half);
-      nl[reg] = -l2[r];
+      nl[reg] = -lse_s[r];
       wrow[reg] = (r < a.R) ? r % W : W;
       if (!W32 && r < a.R && (r % W) == W - 1) lastmask |= 1u << reg;
     }
   }
 
-  fetch(0);
   commit(0);
   __syncthreads();
   for (int s = 0; s < nstages; ++s) {
     const int buf = s & 1;
+    const int ntile = min(tk, k1 - (k0 + s * tk));
+    // E history of this stage's keys (slots 0..ring_mp-1 of the position),
+    // consumed by the stage epilogue; clamped so the loads are unconditional.
+    float4 rv[kMaxRing / 4];
+    if constexpr (MODE == PASS_FUSED) {
+      const int64_t pos = (int64_t)h * a.T + st.cu[b] + k0 + s * tk + min(t, ntile - 1);
+      const float4 *rp = reinterpret_cast<const float4 *>(a.ring + pos * a.ring_mp);
+      const int nq = a.ring_mp >> 2;
+#pragma unroll
+      for (int q = 0; q < kMaxRing / 4; ++q) rv[q] = rp[min(q, nq - 1)];
+    }
     if (s + 1 < nstages) fetch(s + 1);
     const unsigned char *kl = kbuf + buf * tk * C::STRIDE;
-    const int ntile = min(tk, k1 - (k0 + s * tk));
 #pragma unroll 1
     for (int kt = 0; kt * 32 < ntile; ++kt) {
       const int kbase = k0 + s * tk + kt * 32;   // first key of the tile (sequence-relative)
@@ -242,17 +320,15 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
         bs += __shfl_xor(bs, 32);
         qs += __shfl_xor(qs, 32);
         if (half == 0) {
-          float *rb = red + ((buf * 2 + 0) * nw + wave) * tk;
-          float *rq = red + ((buf * 2 + 1) * nw + wave) * tk;
-          rb[kt * 32 + l32] = bs;
-          rq[kt * 32 + l32] = qs;
+          red[((buf * 2 + 0) * nw + wave) * tk + kt * 32 + l32] = bs;
+          red[((buf * 2 + 1) * nw + wave) * tk + kt * 32 + l32] = qs;
         }
       }
     }
     if (s + 1 < nstages) commit(buf ^ 1);
     __syncthreads();
     if constexpr (MODE != PASS_LSE) {
-      // Epilogue of stage s: fixed-order reduction over row tiles.
+      // Stage epilogue: fixed-order reduction over row tiles, one key per thread.
       if (t < ntile) {
         const float *rb = red + (buf * 2 + 0) * nw * tk;
         const float *rq = red + (buf * 2 + 1) * nw * tk;
@@ -269,94 +345,65 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           a.out_Q[pos] = Qv;
         } else {
           const float E = (Qv > Bv) ? (Qv - Bv) : 0.f;
-          const int64_t slot = (int64_t)a.Hkv * a.T;
           float ts = 0.f;
-          for (int j = 0; j < a.ring_cnt; ++j) ts += a.ring[a.ring_read[j] * slot + pos];
+#pragma unroll
+          for (int q = 0; q < kMaxRing / 4; ++q) {
+            ts += (4 * q + 0 < a.ring_cnt) ? rv[q].x : 0.f;
+            ts += (4 * q + 1 < a.ring_cnt) ? rv[q].y : 0.f;
+            ts += (4 * q + 2 < a.ring_cnt) ? rv[q].z : 0.f;
+            ts += (4 * q + 3 < a.ring_cnt) ? rv[q].w : 0.f;
+          }
           const float Tv = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
-          a.ring[a.ring_write * slot + pos] = E;
+          a.ring[pos * a.ring_mp + a.ring_write] = E;
           a.vec_B[pos] = Bv;
-          a.vec_EpT[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
+          ce[s * tk + t] = E;
+          cv[s * tk + t] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
         }
       }
     }
   }
 
+  if constexpr (MODE == PASS_FUSED) {
+    // In-chunk part of L = P_r E: neighbours inside [k0, k1), divided by the
+    // full neighbourhood size; the select kernel adds the neighbours outside.
+    __syncthreads();
+    const int r = a.radius;
+    const bool use_l = (a.terms & 2u) != 0;
+    for (int p = t; p < k1 - k0; p += nt) {
+      const int i = k0 + p;
+      const int lo = max(0, i - r), hi = min(n - 1, i + r);
+      float sum = 0.f;
+      if (use_l) {
+        const int clo = max(lo, k0), chi = min(hi, k1 - 1);
+        for (int u = clo; u <= chi; ++u) sum += ce[u - k0];
+      }
+      const float vp = cv[p] + (use_l ? sum / (float)(hi - lo + 1) : 0.f);
+      a.vec_VP[(int64_t)h * a.T + st.cu[b] + i] = vp;
+    }
+  }
+
   if constexpr (MODE == PASS_LSE) {
-    // merge the two lane halves (same row, different keys)
+    // merge the two lane halves (same row, different keys) and store the partial
     const float mo = __shfl_xor(m_run, 32), lo = __shfl_xor(l_run, 32);
     const float m = fmaxf(m_run, mo);
     float l = 0.f;
     if (m != -INFINITY)
-      l = l_run * exp2f((m_run - m) * a.c2) + lo * exp2f((mo - m) * a.c2);
+      l = l_run * __builtin_amdgcn_exp2f((m_run - m) * a.c2) + lo * __builtin_amdgcn_exp2f((mo - m) * a.c2);
     const int r = wave * 32 + l32;
     if (half == 0) {
       a.partials[((int64_t)h * st.total_chunks + gchunk) * a.Rpad + r] =
           make_float2(m == -INFINITY ? -INFINITY : m * a.c2, l);
     }
-    // last workgroup of this (sequence, KV head) merges all chunk partials
-    __threadfence();
-    __syncthreads();
-    __shared__ int s_last;
-    if (t == 0) {
-      const unsigned nch = (unsigned)(st.chunk_base[b + 1] - st.chunk_base[b]);
-      const unsigned old = __hip_atomic_fetch_add(&a.counters[b * a.Hkv + h], 1u,
-                                                  __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      s_last = (old == nch - 1) ? 1 : 0;
-    }
-    __syncthreads();
-    if (s_last) {
-      __threadfence();
-      const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
-      const float2 *pp = a.partials + ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad;
-      for (int row = t; row < a.Rpad; row += nt) {
-        float mm = -INFINITY;
-        for (int cc = 0; cc < nch; ++cc) mm = fmaxf(mm, pp[(int64_t)cc * a.Rpad + row].x);
-        float ll = 0.f;
-        if (mm != -INFINITY) {
-          for (int cc = 0; cc < nch; ++cc) {
-            const float2 v = pp[(int64_t)cc * a.Rpad + row];
-            if (v.x != -INFINITY) ll += v.y * exp2f(v.x - mm);
-          }
-        }
-        const float lse2 = (row < a.R) ? mm + log2f(ll) : INFINITY;
-        a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + row] = lse2;
-        if (a.lse_user && row < a.R) {
-          const int g = row / W, w = row - g * W;
-          a.lse_user[((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w] = lse2 * kLn2;
-        }
-      }
-      if (t == 0) a.counters[b * a.Hkv + h] = 0u;
-    }
-  }
-}
-
-PassGeom pass_geom(int mode, bool bf16, int head_dim, int rpad) {
-  PassGeom g;
-  g.nw = rpad / 32;
-  g.tk = stage_keys(g.nw);
-  const int stride = head_dim * (bf16 ? 2 : 4) + 16;
-  g.lds = 2 * g.tk * stride;
-  if (mode != PASS_LSE) g.lds += 2 * 2 * g.nw * g.tk * (int)sizeof(float);
-  return g;
-}
-
-// Dynamic LDS above 64 KiB has to be allowed per kernel before launch.
-template <typename Kern>
-static void allow_lds(Kern kernel, size_t bytes) {
-  static size_t granted = 0;
-  if (bytes > 64 * 1024 && bytes > granted) {
-    hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    granted = bytes;
   }
 }
 
 template <int MODE, bool BF16, int D, bool W32>
 static hipError_t launch_pass_t(const PassArgs &a, const SeqTable &st, hipStream_t s) {
-  const PassGeom g = pass_geom(MODE, BF16, D, a.Rpad);
-  dim3 grid(st.total_chunks, a.Hkv), block(64 * g.nw);
-  allow_lds(k_pass<MODE, BF16, D, W32>, g.lds);
-  hipLaunchKernelGGL((k_pass<MODE, BF16, D, W32>), grid, block, g.lds, s, a, st);
+  const int nw = a.Rpad / 32;
+  const int lds = pass_lds_bytes(MODE, BF16, D, a.Rpad, a.chunk);
+  dim3 grid(st.total_chunks, a.Hkv), block(64 * nw);
+  allow_lds(k_pass<MODE, BF16, D, W32>, lds);
+  hipLaunchKernelGGL((k_pass<MODE, BF16, D, W32>), grid, block, lds, s, a, st);
   return hipGetLastError();
 }
 
@@ -383,74 +430,102 @@ hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassAr
 }
 
 // ---------------------------------------------------------------- block helpers
+constexpr int kWaves = kSelThreads / 64;
+
 struct SelShared {
   unsigned hist[kHistBins];
-  unsigned red_u[kSelThreads / 64];
-  double red_d[4][kSelThreads / 64];
+  unsigned lane_cnt[64];
+  unsigned cnt;
+  unsigned red_u[kWaves];
+  double red_d[4][kWaves];
   unsigned bc_u[4];
   double bc_d[4];
   int bc_i[4];
 };
 
+// Wave-wide reductions: xor butterflies inside each 32-lane half with
+// ds_swizzle (immediate lane pattern, no index registers), then the two
+// halves combined through readlane.  Every lane gets the result.
+template <int X>
+__device__ __forceinline__ unsigned swz(unsigned v) {
+  return (unsigned)__builtin_amdgcn_ds_swizzle((int)v, (X << 10) | 0x1f);
+}
+template <typename Op>
+__device__ __forceinline__ unsigned wave_reduce_u(unsigned v, Op op) {
+  v = op(v, swz<1>(v));
+  v = op(v, swz<2>(v));
+  v = op(v, swz<4>(v));
+  v = op(v, swz<8>(v));
+  v = op(v, swz<16>(v));
+  return op((unsigned)__builtin_amdgcn_readlane((int)v, 0), (unsigned)__builtin_amdgcn_readlane((int)v, 32));
+}
 __device__ __forceinline__ unsigned wave_min_u(unsigned v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = min(v, (unsigned)__shfl_xor((int)v, o));
-  return v;
+  return wave_reduce_u(v, [](unsigned x, unsigned y) { return min(x, y); });
 }
 __device__ __forceinline__ unsigned wave_max_u(unsigned v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = max(v, (unsigned)__shfl_xor((int)v, o));
-  return v;
+  return wave_reduce_u(v, [](unsigned x, unsigned y) { return max(x, y); });
+}
+__device__ __forceinline__ unsigned wave_sum_u(unsigned v) {
+  return wave_reduce_u(v, [](unsigned x, unsigned y) { return x + y; });
+}
+template <int X>
+__device__ __forceinline__ double swz_d(double v) {
+  const unsigned long long u = __double_as_longlong(v);
+  const unsigned lo = swz<X>((unsigned)u), hi = swz<X>((unsigned)(u >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+__device__ __forceinline__ double readlane_d(double v, int l) {
+  const unsigned long long u = __double_as_longlong(v);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)u, l);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(u >> 32), l);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 __device__ __forceinline__ double wave_sum_d(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v += swz_d<1>(v);
+  v += swz_d<2>(v);
+  v += swz_d<4>(v);
+  v += swz_d<8>(v);
+  v += swz_d<16>(v);
+  return readlane_d(v, 0) + readlane_d(v, 32);
 }
 
-__device__ unsigned block_min_u(unsigned v, SelShared &ss) {
+// Block-wide min (OP 0) / max (1) / sum (2) of unsigned values.
+template <int OP>
+__device__ __forceinline__ unsigned block_reduce_u(unsigned v, SelShared &ss) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  v = wave_min_u(v);
+  v = OP == 0 ? wave_min_u(v) : OP == 1 ? wave_max_u(v) : wave_sum_u(v);
   if (lane == 0) ss.red_u[wave] = v;
   __syncthreads();
   if (wave == 0) {
-    unsigned x = (lane < kSelThreads / 64) ? ss.red_u[lane] : 0xffffffffu;
-    x = wave_min_u(x);
+    const unsigned id = OP == 0 ? 0xffffffffu : 0u;
+    unsigned x = (lane < kWaves) ? ss.red_u[lane] : id;
+    x = OP == 0 ? wave_min_u(x) : OP == 1 ? wave_max_u(x) : wave_sum_u(x);
     if (lane == 0) ss.bc_u[0] = x;
   }
   __syncthreads();
-  return ss.bc_u[0];
-}
-__device__ unsigned block_max_u(unsigned v, SelShared &ss) {
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  v = wave_max_u(v);
-  if (lane == 0) ss.red_u[wave] = v;
+  const unsigned r = ss.bc_u[0];
   __syncthreads();
-  if (wave == 0) {
-    unsigned x = (lane < kSelThreads / 64) ? ss.red_u[lane] : 0u;
-    x = wave_max_u(x);
-    if (lane == 0) ss.bc_u[1] = x;
-  }
-  __syncthreads();
-  return ss.bc_u[1];
+  return r;
 }
-// Sum of four doubles over the block; result in out[0..3] for every thread.
-__device__ void block_sum4_d(double v0, double v1, double v2, double v3, SelShared &ss, double *out) {
+
+// Sum of four doubles over the block in a fixed order.
+__device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, double v3, SelShared &ss, double *out) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   v0 = wave_sum_d(v0); v1 = wave_sum_d(v1); v2 = wave_sum_d(v2); v3 = wave_sum_d(v3);
   if (lane == 0) { ss.red_d[0][wave] = v0; ss.red_d[1][wave] = v1; ss.red_d[2][wave] = v2; ss.red_d[3][wave] = v3; }
   __syncthreads();
   if (t < 4) {
     double s = 0.0;
-    for (int w = 0; w < kSelThreads / 64; ++w) s += ss.red_d[t][w];   // fixed order
+    for (int w = 0; w < kWaves; ++w) s += ss.red_d[t][w];
     ss.bc_d[t] = s;
   }
   __syncthreads();
   out[0] = ss.bc_d[0]; out[1] = ss.bc_d[1]; out[2] = ss.bc_d[2]; out[3] = ss.bc_d[3];
   __syncthreads();
 }
+
 // Exclusive prefix sum over threads in index order.
-__device__ unsigned block_excl_scan_u(unsigned v, SelShared &ss) {
+__device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelShared &ss) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   unsigned x = v;
 #pragma unroll
@@ -473,20 +548,53 @@ __device__ __forceinline__ unsigned float_key(float x) {
   const unsigned u = __float_as_uint(x);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
+__device__ __forceinline__ float key_float(unsigned k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// Boundary search over ss.hist (larger bin = larger keys): the bin holding
+// the need-th largest counted element and the count in the bins above it,
+// left in ss.bc_i[0] and ss.bc_i[1].  Wave 0 scans; ends with a barrier.
+__device__ __forceinline__ void hist_boundary(int need, SelShared &ss) {
+  const int t = threadIdx.x;
+  if (t < 64) {
+    const int lane = t;
+    unsigned cs = 0;
+    for (int q = 0; q < 32; ++q) cs += ss.hist[lane * 32 + ((q + lane) & 31)];   // rotated: no bank conflicts
+    ss.lane_cnt[lane] = cs;
+    __builtin_amdgcn_wave_barrier();
+    unsigned suf = 0;      // counted elements in bins of lanes >= lane
+    for (int q = 63; q >= 0; --q) suf += (q >= lane) ? ss.lane_cnt[q] : 0u;
+    const unsigned above_lane = suf - cs;
+    if (above_lane < (unsigned)need && (unsigned)need <= suf) {
+      unsigned acc = above_lane;
+      int bs = lane * 32;
+      for (int q = 31; q >= 0; --q) {
+        const unsigned hq = ss.hist[lane * 32 + q];
+        if (acc + hq >= (unsigned)need) { bs = lane * 32 + q; break; }
+        acc += hq;
+      }
+      ss.bc_i[0] = bs;
+      ss.bc_i[1] = (int)acc;
+    }
+  }
+  __syncthreads();
+}
 
 // k-th largest key among the block's non-zero keys (1 <= k <= count), by
-// MSB-first 11-bit histogram narrowing of the candidate range.  Returns the
-// key value xk and need = k - #{keys > xk} (how many ties at xk are taken).
-template <int PER>
-__device__ void block_select(const unsigned (&key)[PER], int k, unsigned &xk, int &need,
-                             SelShared &ss) {
+// MSB-first 11-bit histogram narrowing of the candidate range over all
+// elements.  Returns the key value xk and need = k - #{keys > xk}.
+template <int PER, typename KeyF>
+__device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int &need, SelShared &ss) {
   const int t = threadIdx.x;
   unsigned lo = 0xffffffffu, hi = 0u;
 #pragma unroll
-  for (int j = 0; j < PER; ++j)
-    if (key[j]) { lo = min(lo, key[j]); hi = max(hi, key[j]); }
-  lo = block_min_u(lo, ss);
-  hi = block_max_u(hi, ss);
+  for (int j = 0; j < PER; ++j) {
+    const unsigned x = key(j);
+    if (x) { lo = min(lo, x); hi = max(hi, x); }
+  }
+  lo = block_reduce_u<0>(lo, ss);
+  hi = block_reduce_u<1>(hi, ss);
   need = k;
   while (lo != hi) {
     const unsigned range = hi - lo;
@@ -495,39 +603,15 @@ __device__ void block_select(const unsigned (&key)[PER], int k, unsigned &xk, in
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-      const unsigned x = key[j];
+      const unsigned x = key(j);
       if (x >= lo && x <= hi) atomicAdd(&ss.hist[(x - lo) >> sh], 1u);
     }
     __syncthreads();
-    if (t < 64) {
-      const int lane = t;
-      unsigned cs = 0;
-      for (int q = 0; q < 32; ++q) cs += ss.hist[lane * 32 + q];
-      // suffix sums over lanes: suf = # in bins of lanes >= lane
-      unsigned suf = cs;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const unsigned y = (unsigned)__shfl_down((int)suf, o);
-        if (lane + o < 64) suf += y;
-      }
-      const unsigned above_lane = suf - cs;
-      if (above_lane < (unsigned)need && (unsigned)need <= suf) {
-        unsigned acc = above_lane;
-        int bs = lane * 32;
-        for (int q = 31; q >= 0; --q) {
-          const unsigned hq = ss.hist[lane * 32 + q];
-          if (acc + hq >= (unsigned)need) { bs = lane * 32 + q; break; }
-          acc += hq;
-        }
-        ss.bc_i[0] = bs;
-        ss.bc_i[1] = (int)acc;
-      }
-    }
-    __syncthreads();
+    hist_boundary(need, ss);
     const int bs = ss.bc_i[0];
     need -= ss.bc_i[1];
     const unsigned nlo = lo + ((unsigned)bs << sh);
-    const unsigned span = (sh >= 32) ? 0xffffffffu : ((1u << sh) - 1u);
+    const unsigned span = (1u << sh) - 1u;
     const unsigned nhi = (hi - nlo <= span) ? hi : nlo + span;
     lo = nlo;
     hi = nhi;
@@ -536,169 +620,385 @@ __device__ void block_select(const unsigned (&key)[PER], int k, unsigned &xk, in
   xk = lo;
 }
 
+constexpr int kCandCap = 1024;   // LDS list of boundary-bin candidates
+
+// Exact top-k threshold with the tie rule (key descending, then position
+// ascending) over the block's non-zero keys, 1 <= k <= count: element j is
+// kept iff key > xk, or key == xk and position <= pthr.
+// One histogram pass bins every key over [max(min, max - 8 octaves), max];
+// the boundary bin is compacted into an LDS list (ckey, cpos) and resolved
+// there; ties are split by position.  When the boundary falls below that
+// range or its bin overflows the list, full-range narrowing over all
+// elements is used instead.
+template <int PER, typename KeyF, typename PosF>
+__device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsigned &xk, int &pthr,
+                                                SelShared &ss, unsigned *ckey, int *cpos) {
+  const int t = threadIdx.x, lane = t & 63;
+  unsigned lo = 0xffffffffu, hi = 0u;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const unsigned x = key(j);
+    if (x) { lo = min(lo, x); hi = max(hi, x); }
+  }
+  lo = block_reduce_u<0>(lo, ss);
+  hi = block_reduce_u<1>(hi, ss);
+  if (hi - lo > (8u << 23)) lo = hi - (8u << 23);      // at most 8 octaves below the max
+  const int sh0 = max(0, 32 - __clz((int)(hi - lo)) - 11);
+  for (int q = t; q < kHistBins; q += kSelThreads) ss.hist[q] = 0u;
+  if (t == 0) ss.cnt = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const unsigned x = key(j);
+    if (x >= lo && hi >= lo) atomicAdd(&ss.hist[(x - lo) >> sh0], 1u);
+  }
+  __syncthreads();
+  unsigned counted = 0;
+  if (t < 64) {
+    unsigned cs = 0;
+    for (int q = 0; q < 32; ++q) cs += ss.hist[t * 32 + q];
+    counted = wave_sum_u(cs);
+    if (t == 0) ss.bc_u[2] = counted;
+  }
+  __syncthreads();
+  counted = ss.bc_u[2];
+  bool fallback = counted < (unsigned)k;                // boundary below the binned range
+  unsigned b0 = 0, C = 0;
+  int need = k;
+  if (!fallback) {
+    hist_boundary(k, ss);
+    b0 = (unsigned)ss.bc_i[0];
+    need = k - ss.bc_i[1];
+    C = ss.hist[b0];
+    fallback = C > (unsigned)kCandCap;
+  }
+  __syncthreads();
+  if (fallback) {
+    int nd;
+    block_select<PER>(key, k, xk, nd, ss);
+    unsigned eq = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) eq += key(j) == xk;
+    if (block_reduce_u<2>(eq, ss) == (unsigned)nd) {
+      pthr = 0x7fffffff;
+    } else {
+      auto pkey = [&](int j) -> unsigned { return key(j) == xk ? 0xffffffffu - (unsigned)pos(j) : 0u; };
+      unsigned xp;
+      int n2;
+      block_select<PER>(pkey, nd, xp, n2, ss);
+      pthr = (int)(0xffffffffu - xp);
+    }
+    return;
+  }
+  // compact the boundary bin: one LDS counter update per wave and element slot
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const unsigned x = key(j);
+    const bool in = x >= lo && ((x - lo) >> sh0) == b0;
+    const uint64_t m = __ballot(in);
+    if (m) {
+      unsigned basei = 0;
+      if (lane == 0) basei = atomicAdd(&ss.cnt, (unsigned)__popcll(m));
+      basei = (unsigned)__builtin_amdgcn_readfirstlane((int)basei);
+      if (in) {
+        const unsigned off = basei + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+        ckey[off] = x;
+        cpos[off] = pos(j);
+      }
+    }
+  }
+  __syncthreads();
+  // resolve the key inside the bin: 11 bits at a time from bit sh0 down
+  const unsigned blo = lo + (b0 << sh0);                // smallest key of the bin
+  unsigned pre = 0, pmask = 0;                          // known bits of (x - blo)
+  int sh = sh0;
+  unsigned E = C;                                       // candidates matching the prefix
+  while (sh > 0) {
+    const int nb = min(sh, 11);
+    sh -= nb;
+    const unsigned bm = (1u << nb) - 1u;
+    for (int q = t; q < kHistBins; q += kSelThreads) ss.hist[q] = 0u;
+    __syncthreads();
+    for (int q = t; q < (int)C; q += kSelThreads) {
+      const unsigned d = ckey[q] - blo;
+      if ((d & pmask) == pre) atomicAdd(&ss.hist[(d >> sh) & bm], 1u);
+    }
+    __syncthreads();
+    hist_boundary(need, ss);
+    const unsigned bl = (unsigned)ss.bc_i[0];
+    need -= ss.bc_i[1];
+    E = ss.hist[bl];
+    pre |= bl << sh;
+    pmask |= bm << sh;
+    __syncthreads();
+  }
+  xk = blo + pre;
+  if (E == (unsigned)need) {
+    pthr = 0x7fffffff;
+    return;
+  }
+  // the `need` lowest positions among the E ties (positions < 2^15)
+  unsigned ppre = 0, ppm = 0;
+  for (int ps = 15; ps > 0;) {
+    const int nb = min(ps, 11);
+    ps -= nb;
+    const unsigned bm = (1u << nb) - 1u;
+    for (int q = t; q < kHistBins; q += kSelThreads) ss.hist[q] = 0u;
+    __syncthreads();
+    for (int q = t; q < (int)C; q += kSelThreads) {
+      if (ckey[q] != xk) continue;
+      const unsigned d = 0x7fffu - (unsigned)cpos[q];   // larger d = lower position
+      if ((d & ppm) == ppre) atomicAdd(&ss.hist[(d >> ps) & bm], 1u);
+    }
+    __syncthreads();
+    hist_boundary(need, ss);
+    const unsigned bl = (unsigned)ss.bc_i[0];
+    need -= ss.bc_i[1];
+    ppre |= bl << ps;
+    ppm |= bm << ps;
+    __syncthreads();
+  }
+  pthr = (int)(0x7fffu - ppre);
+}
+
 // ---------------------------------------------------------------- select kernel
-template <int PER, int MODE>
+// A copy of v the compiler cannot see through: stops it from hoisting address
+// arithmetic of one phase and keeping it live through the next.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// LDS: S padded by one word per kSelPer (thread-contiguous reads hit distinct
+// banks), reused as the slot table.
+__device__ __forceinline__ int pad32(int i) { return i + i / kSelPer; }
+
+template <int MODE>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) {
-  extern __shared__ __align__(16) float arr[];     // [n] E, then V, then S, then slot table
+  constexpr int PER = kSelPer;
+  extern __shared__ __align__(16) float arr[];
   __shared__ SelShared ss;
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;                           // candidate set [0, nc)
   const int K = st.budget[b];
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  const int i0 = t * PER;
-
-  float Bv[PER], Vv[PER];
-  float lam = 0.f;
+  // LDS: arr [pad32 extent of n], candidate list, then per-mode tables
+  unsigned *ckey = reinterpret_cast<unsigned *>(arr + (n + n / PER + 64));
+  int *cpos = reinterpret_cast<int *>(ckey + kCandCap);
 
   if constexpr (MODE != SEL_TOPK) {
-    // E of this layer into LDS; own B and E+T into registers.
-    for (int i = t; i < n; i += kSelThreads) arr[i] = a.ring_E[base + i];
+    // E of this layer next to the chunk boundaries of vec_VP, staged in LDS:
+    // for boundary c*CH (c >= 1) the 2r positions [c*CH - r, c*CH + r).
+    const int r = a.radius, CH = a.vp_chunk;
+    const bool use_l = (a.terms & 2u) != 0;
+    const int nbnd = (use_l && CH < n) ? (n - 1) / CH : 0;      // boundaries inside the sequence
+    float *edge = reinterpret_cast<float *>(cpos + kCandCap);     // [nbnd][2r]
+    const float *re = a.ring + base * a.ring_mp + a.ring_slot;
+    for (int q = t; q < nbnd * 2 * r; q += kSelThreads) {
+      const int c = q / (2 * r) + 1, o = q - (c - 1) * 2 * r;
+      const int u = c * CH - r + o;
+      const float e = re[(int64_t)min(max(u, 0), n - 1) * a.ring_mp];
+      edge[q] = (u >= 0 && u < n) ? e : 0.f;
+    }
+    auto eat = [&](int u) -> float {       // E at a position next to a boundary
+      const int c = (u + r) / CH;          // boundary c*CH with |u - c*CH| <= r
+      return edge[(c - 1) * 2 * r + (u - (c * CH - r))];
+    };
+    // V_i = vec_VP_i + the L neighbours outside the chunk that produced it.
+    auto vfix = [&](int i) -> float {
+      if (!use_l) return 0.f;
+      const int k0 = (i / CH) * CH, k1 = min(n, k0 + CH);
+      const int lo = max(0, i - r), hi = min(n - 1, i + r);
+      if (lo >= k0 && hi < k1) return 0.f;
+      float sum = 0.f;
+      for (int u = lo; u < k0; ++u) sum += eat(u);
+      for (int u = k1; u <= hi; ++u) sum += eat(u);
+      return sum / (float)(hi - lo + 1);
+    };
+    // B into LDS (strided: element j of thread t is position t + j*kSelThreads);
+    // all loads of the phase are issued before any is used.
+    {
+      const int tt = opaque(t);   // keeps the phase's address arithmetic local
+      const float *pb = a.vec_B + base;
+      float bv[PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int i = i0 + j;
-      Bv[j] = (i < n) ? a.vec_B[base + i] : 0.f;
-      Vv[j] = (i < n) ? a.vec_EpT[base + i] : 0.f;
+      for (int j = 0; j < PER; ++j) bv[j] = pb[min(tt + j * kSelThreads, n - 1)];
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        if (tt + j * kSelThreads < n) arr[pad32(tt + j * kSelThreads)] = bv[j];
     }
     __syncthreads();
-    // L = P_r E: truncated box mean, sliding sum in double (Eq. intra_layer_coherence)
-    if (i0 < n) {
-      const int r = a.radius;
-      int lo = max(0, i0 - r), hi = min(n - 1, i0 + r);
-      double acc = 0.0;
-      for (int u = lo; u <= hi; ++u) acc += (double)arr[u];
-      const double inv_full = 1.0 / (double)(2 * r + 1);
-#pragma unroll
-      for (int j = 0; j < PER; ++j) {
-        const int i = i0 + j;
-        if (i < n) {
-          const int cnt = hi - lo + 1;
-          const double L = acc * ((cnt == 2 * r + 1) ? inv_full : 1.0 / (double)cnt);
-          if (a.terms & 2u) Vv[j] += (float)(L > 0.0 ? L : 0.0);
-          if constexpr (MODE == SEL_CALIB) {
-            if (a.out_E) a.out_E[base + i] = arr[i];
-          }
-          // slide the window to i+1
-          if (i + 1 + r <= n - 1) acc += (double)arr[i + 1 + r];
-          if (i - r >= 0) acc -= (double)arr[i - r];
-          lo = max(0, i + 1 - r);
-          hi = min(n - 1, i + 1 + r);
-        }
-      }
-    }
-
     // Scale-matching set: top M = min(rho K, |I|) of B over I (Eq. scale_matching_set).
     int M = (int)floorf(a.rho * (float)K);
     if (M > nc) M = nc;
     if (M < 0) M = 0;
-    double sums[4] = {0.0, 0.0, 0.0, 0.0};
-    unsigned xm = 0;
+    float lam = 0.f;
     if (M > 0 && a.use_last_query) {
-      unsigned key[PER];
+      auto keyB = [&](int j) -> unsigned {
+        const int i = t + j * kSelThreads;
+        return i < nc ? float_key(arr[pad32(min(i, n - 1))]) : 0u;
+      };
+      auto posf = [&](int j) -> int { return t + j * kSelThreads; };
+      uint64_t msk = 0;
+      if (M >= nc) {
 #pragma unroll
-      for (int j = 0; j < PER; ++j) key[j] = (i0 + j < nc) ? float_key(Bv[j]) : 0u;
-      int need = 0;
-      block_select<PER>(key, M, xm, need, ss);
-      unsigned eq_own = 0;
+        for (int j = 0; j < PER; ++j) msk |= (uint64_t)(t + j * kSelThreads < nc ? 1u : 0u) << j;
+      } else {
+        unsigned xm;
+        int pm;
+        block_threshold<PER>(keyB, posf, M, xm, pm, ss, ckey, cpos);
 #pragma unroll
-      for (int j = 0; j < PER; ++j) eq_own += (key[j] == xm) ? 1u : 0u;
-      unsigned e = block_excl_scan_u(eq_own, ss);
-      // moments of B (shifted by the M-th value) and V over the set, in double
-      const float bref = __uint_as_float(xm & 0x80000000u ? (xm & 0x7fffffffu) : ~xm);
-      double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-#pragma unroll
-      for (int j = 0; j < PER; ++j) {
-        bool sel = false;
-        if (key[j] > xm) sel = true;
-        else if (key[j] == xm) { sel = e < (unsigned)need; ++e; }
-        if (sel) {
-          const double db = (double)Bv[j] - (double)bref, dv = (double)Vv[j];
-          s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
+        for (int j = 0; j < PER; ++j) {
+          const unsigned kj = keyB(j);
+          msk |= (uint64_t)(kj > xm || (kj == xm && posf(j) <= pm) ? 1u : 0u) << j;
         }
       }
+      // list of the set's positions in LDS (after the staged boundary E)
+      int *mlist = reinterpret_cast<int *>(edge + nbnd * 2 * r);
+      unsigned off = block_excl_scan_u((unsigned)__popcll(msk), ss);
+      {
+        uint64_t m2 = msk;
+        while (m2) {
+          const int j = __builtin_ctzll(m2);
+          m2 &= m2 - 1;
+          mlist[off++] = t + j * kSelThreads;
+        }
+      }
+      __syncthreads();
+      // population moments over the set in double; B shifted by the set minimum
+      unsigned kmin = 0xffffffffu;
+      for (int q = t; q < M; q += kSelThreads) kmin = min(kmin, float_key(arr[pad32(mlist[q])]));
+      kmin = block_reduce_u<0>(kmin, ss);
+      const double bref = (double)key_float(kmin);
+      double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+      for (int q = t; q < M; q += kSelThreads) {
+        const int i = mlist[q];
+        const double db = (double)arr[pad32(i)] - bref;
+        const double dv = (double)(a.vec_VP[base + i] + vfix(i));
+        s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
+      }
+      double sums[4];
       block_sum4_d(s0, s1, s2, s3, ss, sums);
       const double mb = sums[0] / M, mv = sums[2] / M;
       double vb = sums[1] / M - mb * mb, vv = sums[3] / M - mv * mv;
       vb = vb > 0.0 ? vb : 0.0;
       vv = vv > 0.0 ? vv : 0.0;
-      const double sb = sqrt(vb), sv = sqrt(vv);
-      lam = (float)((double)a.gamma * sb / (sv + (double)a.eps));   // Eq. lambda_solution
+      lam = (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));   // Eq. lambda_solution
     }
     if (t == 0) {
       a.lambda_ws[b * a.Hkv + h] = lam;
       if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = lam;
     }
-    __syncthreads();   // all reads of E in LDS are done
-
-    // S = B + lambda V (Eq. bacon_score)
+    // S = B + lambda V (Eq. bacon_score), in place of B; each thread touches
+    // only its own positions.  V = vec_VP here; positions next to a chunk
+    // boundary are recomputed below with their outside neighbours.
+    {
+      const int tt = opaque(t);
+      const float *pv = a.vec_VP + base;
+      float vp[PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int i = i0 + j;
-      if (i < n) {
-        const float S = fmaf(lam, Vv[j], Bv[j]);
+      for (int j = 0; j < PER; ++j) vp[j] = pv[min(tt + j * kSelThreads, n - 1)];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const int i = tt + j * kSelThreads;
+        if (i < n) {
+          const float S = fmaf(lam, vp[j], arr[pad32(i)]);
+          if constexpr (MODE == SEL_CALIB) {
+            a.out_S[base + i] = S;
+            if (a.out_V) a.out_V[base + i] = vp[j];
+            if (a.out_E) a.out_E[base + i] = re[(int64_t)i * a.ring_mp];
+          } else {
+            arr[pad32(i)] = S;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    for (int q = t; q < nbnd * 2 * r; q += kSelThreads) {
+      const int c = q / (2 * r) + 1, o = q - (c - 1) * 2 * r;
+      const int i = c * CH - r + o;
+      if (i >= 0 && i < n) {
+        const float V = a.vec_VP[base + i] + vfix(i);
+        const float S = fmaf(lam, V, a.vec_B[base + i]);
         if constexpr (MODE == SEL_CALIB) {
           a.out_S[base + i] = S;
-          if (a.out_V) a.out_V[base + i] = Vv[j];
+          if (a.out_V) a.out_V[base + i] = V;
         } else {
-          arr[i] = S;
+          arr[pad32(i)] = S;
         }
       }
     }
     if constexpr (MODE == SEL_CALIB) return;
   } else {
-    for (int i = t; i < nc; i += kSelThreads) arr[i] = a.in_S[base + i];
+    float sv[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) sv[j] = a.in_S[base + min(t + j * kSelThreads, n - 1)];
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      if (t + j * kSelThreads < nc) arr[pad32(t + j * kSelThreads)] = sv[j];
   }
   __syncthreads();
 
-  // Pooled score over I and its keys.
+  // Pooled score over I and its keys, contiguous ownership: positions
+  // [t*PER, t*PER + PER).  Sliding window sums in double.
+  const int i0 = t * PER;
   unsigned key[PER];
   {
     const int hp = a.pool_half;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) key[j] = 0u;
     if (i0 < nc) {
       int lo = max(0, i0 - hp), hi = min(nc - 1, i0 + hp);
       double acc = 0.0;
-      for (int u = lo; u <= hi; ++u) acc += (double)arr[u];
+      for (int u = lo; u <= hi; ++u) acc += (double)arr[pad32(u)];
+      const double inv_full = 1.0 / (double)(2 * hp + 1);
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         const int i = i0 + j;
-        key[j] = 0u;
         if (i < nc) {
-          const double P = acc / (double)(hi - lo + 1);
-          key[j] = float_key((float)P);
-          if (i + 1 + hp <= nc - 1) acc += (double)arr[i + 1 + hp];
-          if (i - hp >= 0) acc -= (double)arr[i - hp];
+          const int cnt = hi - lo + 1;
+          double inv = inv_full;
+          if (cnt != 2 * hp + 1) inv = 1.0 / (double)cnt;
+          key[j] = float_key((float)(acc * inv));
+          if (i + 1 + hp <= nc - 1) acc += (double)arr[pad32(i + 1 + hp)];
+          if (i - hp >= 0) acc -= (double)arr[pad32(i - hp)];
           lo = max(0, i + 1 - hp);
           hi = min(nc - 1, i + 1 + hp);
         }
       }
-    } else {
-#pragma unroll
-      for (int j = 0; j < PER; ++j) key[j] = 0u;
     }
   }
   __syncthreads();   // pooled values read; arr is reused as the slot table
 
   // Top-K over I (Eq. topk_selection), emitted in ascending position.
   const int kept = min(K, nc);
+  uint64_t msk = 0;
+  if (kept == nc) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) msk |= (uint64_t)(i0 + j < nc ? 1u : 0u) << j;
+  } else if (kept > 0) {
+    auto keyS = [&](int j) -> unsigned { return key[j]; };
+    auto posf = [&](int j) -> int { return i0 + j; };
+    unsigned xk;
+    int pk;
+    block_threshold<PER>(keyS, posf, kept, xk, pk, ss, ckey, cpos);
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      msk |= (uint64_t)(key[j] > xk || (key[j] == xk && i0 + j <= pk) ? 1u : 0u) << j;
+  }
   int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
   int *tbl = reinterpret_cast<int *>(arr);
-  if (kept == nc) {
-    for (int i = t; i < nc; i += kSelThreads) { idx[i] = i; tbl[i] = i; }
-  } else if (kept > 0) {
-    unsigned xk = 0;
-    int need = 0;
-    block_select<PER>(key, kept, xk, need, ss);
-    unsigned gt_own = 0, eq_own = 0;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) { gt_own += key[j] > xk; eq_own += key[j] == xk; }
-    const unsigned packed = block_excl_scan_u((gt_own << 16) | eq_own, ss);
-    unsigned g = packed >> 16, e = packed & 0xffffu;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      int slot = -1;
-      if (key[j] > xk) { slot = (int)(g + min(e, (unsigned)need)); ++g; }
-      else if (key[j] == xk) { if (e < (unsigned)need) slot = (int)(g + e); ++e; }
-      if (slot >= 0) { idx[slot] = i0 + j; tbl[slot] = i0 + j; }
+  unsigned slot = block_excl_scan_u((unsigned)__popcll(msk), ss);
+  {
+    uint64_t m2 = msk;
+    while (m2) {
+      const int j = __builtin_ctzll(m2);
+      m2 &= m2 - 1;
+      idx[slot] = i0 + j;
+      tbl[slot] = i0 + j;
+      ++slot;
     }
   }
   for (int j = kept + t; j < K; j += kSelThreads) idx[j] = -1;
@@ -708,75 +1008,102 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     for (int w = t; w < a.W; w += kSelThreads) tbl[kept + w] = nc + w;
     __syncthreads();
     const int pieces = a.row_bytes / 16;
-    const int rows = K + a.W;
-    const int total = rows * pieces;
+    const int total = (K + a.W) * pieces;
     const unsigned char *ks = static_cast<const unsigned char *>(a.k);
     const unsigned char *vs = static_cast<const unsigned char *>(a.v);
     unsigned char *ko = static_cast<unsigned char *>(a.k_out);
     unsigned char *vo = static_cast<unsigned char *>(a.v_out);
-    const int64_t rs = (int64_t)a.Hkv * a.row_bytes;
-    for (int q = t; q < total; q += kSelThreads) {
-      const int r = q / pieces, p = q - r * pieces;
-      const int src = (r < kept + a.W) ? tbl[r] : -1;
-      const int64_t dst = ((int64_t)(st.kept_base[b] + r) * a.Hkv + h) * a.row_bytes + 16 * p;
-      u32x4 kv = u32x4{0u, 0u, 0u, 0u}, vv = u32x4{0u, 0u, 0u, 0u};
-      if (src >= 0) {
-        const int64_t so = ((int64_t)(st.cu[b] + src) * a.Hkv + h) * a.row_bytes + 16 * p;
-        kv = *reinterpret_cast<const u32x4 *>(ks + so);
-        vv = *reinterpret_cast<const u32x4 *>(vs + so);
+    constexpr int BATCH = 5;
+    for (int q0 = t; q0 < total; q0 += BATCH * kSelThreads) {
+      u32x4 kv[BATCH], vv[BATCH];
+      int64_t dst[BATCH];
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const int q = min(q0 + u * kSelThreads, total - 1);
+        const int r = q / pieces, p = q - r * pieces;
+        const int src = (r < kept + a.W) ? tbl[r] : -1;
+        dst[u] = ((int64_t)(st.kept_base[b] + r) * a.Hkv + h) * a.row_bytes + 16 * p;
+        const int64_t so = ((int64_t)(st.cu[b] + max(src, 0)) * a.Hkv + h) * a.row_bytes + 16 * p;
+        kv[u] = *reinterpret_cast<const u32x4 *>(ks + so);
+        vv[u] = *reinterpret_cast<const u32x4 *>(vs + so);
+        if (src < 0) { kv[u] = u32x4{0u, 0u, 0u, 0u}; vv[u] = u32x4{0u, 0u, 0u, 0u}; }
       }
-      *reinterpret_cast<u32x4 *>(ko + dst) = kv;
-      *reinterpret_cast<u32x4 *>(vo + dst) = vv;
-      (void)rs;
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        if (q0 + u * kSelThreads < total) {
+          *reinterpret_cast<u32x4 *>(ko + dst[u]) = kv[u];
+          *reinterpret_cast<u32x4 *>(vo + dst[u]) = vv[u];
+        }
+      }
     }
   }
 }
 
-template <int PER>
-static hipError_t launch_select_p(int mode, int max_len, const SelArgs &a, const SeqTable &st,
-                                  hipStream_t s) {
+hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,
+                         hipStream_t s) {
   dim3 grid(st.batch, a.Hkv), block(kSelThreads);
-  const size_t lds = (size_t)max_len * sizeof(float);
+  size_t extra_lds = 0;
+  if (mode != SEL_TOPK) {
+    const int nbnd = (a.vp_chunk < max_len) ? (max_len - 1) / a.vp_chunk : 0;
+    int mmax = 0;
+    for (int b = 0; b < st.batch; ++b) mmax = max(mmax, (int)floorf(a.rho * (float)st.budget[b]));
+    mmax = min(mmax, max_len);
+    extra_lds = ((size_t)nbnd * 2 * a.radius + (size_t)mmax + 16) * sizeof(float);
+  }
+    // arr (padded), candidate list, boundary E table, scale-matching set list
+  const size_t lds = (size_t)(max_len + max_len / kSelPer + 64) * sizeof(float) +
+                     2 * kCandCap * sizeof(unsigned) + extra_lds;
   if (mode == SEL_FUSED) {
-    allow_lds(k_select<PER, SEL_FUSED>, lds);
-    hipLaunchKernelGGL((k_select<PER, SEL_FUSED>), grid, block, lds, s, a, st);
+    allow_lds(k_select<SEL_FUSED>, lds);
+    hipLaunchKernelGGL((k_select<SEL_FUSED>), grid, block, lds, s, a, st);
   } else if (mode == SEL_CALIB) {
-    allow_lds(k_select<PER, SEL_CALIB>, lds);
-    hipLaunchKernelGGL((k_select<PER, SEL_CALIB>), grid, block, lds, s, a, st);
+    allow_lds(k_select<SEL_CALIB>, lds);
+    hipLaunchKernelGGL((k_select<SEL_CALIB>), grid, block, lds, s, a, st);
   } else {
-    allow_lds(k_select<PER, SEL_TOPK>, lds);
-    hipLaunchKernelGGL((k_select<PER, SEL_TOPK>), grid, block, lds, s, a, st);
+    allow_lds(k_select<SEL_TOPK>, lds);
+    hipLaunchKernelGGL((k_select<SEL_TOPK>), grid, block, lds, s, a, st);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,
-                         hipStream_t s) {
-  if (max_len <= 16 * kSelThreads) return launch_select_p<16>(mode, max_len, a, st, s);
-  if (max_len <= 32 * kSelThreads) return launch_select_p<32>(mode, max_len, a, st, s);
-  return launch_select_p<64>(mode, max_len, a, st, s);
-}
-
 // ---------------------------------------------------------------- split calibrate
-__global__ __launch_bounds__(256) void k_elem(ElemArgs a) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// One position per thread: E from B and Q (Eq. boundary_residual), T from the
+// history, the full L over the sequence-truncated neighbourhood, history update.
+__global__ __launch_bounds__(256) void k_elem(ElemArgs a, SeqTable st) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int h = blockIdx.y;
-  if (i >= a.T) return;
-  const int64_t pos = (int64_t)h * a.T + i;
-  const float Bv = a.in_B[pos], Qv = a.in_Q[pos];
-  const float E = (Qv > Bv) ? (Qv - Bv) : 0.f;
-  const int64_t slot = (int64_t)a.Hkv * a.T;
+  if (g >= a.T) return;
+  int b = 0;
+  while (b + 1 < st.batch && st.cu[b + 1] <= g) ++b;
+  const int s0 = st.cu[b], n = st.cu[b + 1] - s0;
+  const int i = (int)(g - s0);
+  const int64_t row = (int64_t)h * a.T;
+  const int64_t pos = row + g;
+  auto resid = [&](int64_t p) {
+    const float Bv = a.in_B[p], Qv = a.in_Q[p];
+    return (Qv > Bv) ? (Qv - Bv) : 0.f;
+  };
+  const float E = resid(pos);
   float ts = 0.f;
-  for (int j = 0; j < a.ring_cnt; ++j) ts += a.ring[a.ring_read[j] * slot + pos];
+  for (int j = 0; j < a.ring_cnt; ++j) ts += a.ring[pos * a.ring_mp + j];
   const float Tv = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
-  a.ring[a.ring_write * slot + pos] = E;
-  a.vec_B[pos] = Bv;
-  a.vec_EpT[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
+  // part of L with neighbours inside the position's chunk, as the fused pass
+  // forms it (the select kernel adds the neighbours across chunk boundaries)
+  float L = 0.f;
+  if (a.terms & 2u) {
+    const int k0 = (i / a.chunk) * a.chunk, k1 = min(n, k0 + a.chunk);
+    const int lo = max(0, i - a.radius), hi = min(n - 1, i + a.radius);
+    float s = 0.f;
+    for (int u = max(lo, k0); u <= min(hi, k1 - 1); ++u) s += resid(row + s0 + u);
+    L = s / (float)(hi - lo + 1);
+  }
+  a.ring[pos * a.ring_mp + a.ring_write] = E;
+  a.vec_VP[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f) + L;
 }
 
-hipError_t launch_elem(const ElemArgs &a, hipStream_t s) {
+hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s) {
   dim3 grid((unsigned)((a.T + 255) / 256), a.Hkv), block(256);
-  hipLaunchKernelGGL(k_elem, grid, block, 0, s, a);
+  hipLaunchKernelGGL(k_elem, grid, block, 0, s, a, st);
   return hipGetLastError();
 }
 
@@ -818,17 +1145,6 @@ __global__ __launch_bounds__(256) void k_compact(CompactArgs a, SeqTable st) {
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s) {
   dim3 grid(st.batch, a.Hkv, 4), block(256);
   hipLaunchKernelGGL(k_compact, grid, block, 0, s, a, st);
-  return hipGetLastError();
-}
-
-__global__ void k_clear_u32(unsigned *p, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0u;
-}
-
-hipError_t launch_clear_u32(unsigned *p, int64_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_clear_u32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p, n);
   return hipGetLastError();
 }
 

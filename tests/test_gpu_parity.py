@@ -47,7 +47,7 @@ CASES = {
 }
 
 
-def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True):
+def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=None):
     import torch
     from paper_2606_14782_amd import bacon
     rtol = P.RTOL[wl.dtype]
@@ -64,7 +64,7 @@ def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True):
     worst = {}
     stats = {"pairs": 0, "strict": 0, "swaps": 0}
     for layer in range(wl.num_layers):
-        x = inputs.layer_inputs(wl, layer)
+        x = make(layer) if make else inputs.layer_inputs(wl, layer)
         r = orc.layer(layer, x["q_win"], x["k"])
         q, k, v = P.to_dev(x["q_win"], wl), P.to_dev(x["k"], wl), P.to_dev(x["v"], wl)
         kb, vb = P.as_bytes(x["k"], wl), P.as_bytes(x["v"], wl)
@@ -231,3 +231,28 @@ def test_ragged_batch_equals_single_sequences(monkeypatch):
             assert np.array_equal(got, want), f"sequence {b} layer {layer}"
         base += K
     torch.cuda.synchronize()
+
+
+def _tied_inputs(wl, distinct):
+    """Keys drawn from `distinct` fixed vectors: the window scores of the
+    candidates take only a few values, so every selection meets exact ties."""
+    def make(layer):
+        rng = np.random.default_rng(1000 + layer)
+        T, Hkv, d = wl.total_tokens, wl.num_kv_heads, wl.head_dim
+        q = inputs.round_bf16(rng.standard_normal((wl.batch * wl.window, wl.num_q_heads, d),
+                                                  dtype=np.float32))
+        base = inputs.round_bf16(rng.standard_normal((distinct, Hkv, d), dtype=np.float32))
+        which = rng.integers(0, distinct, T) if distinct > 1 else np.zeros(T, np.int64)
+        k = np.ascontiguousarray(base[which])
+        v = inputs.round_bf16(rng.standard_normal((T, Hkv, d), dtype=np.float32))
+        return {"q_win": q, "k": k, "v": v}
+    return make
+
+
+@pytest.mark.parametrize("n,K,distinct", [(600, 40, 1), (3000, 100, 1), (3000, 100, 3),
+                                          (20000, 256, 2)])
+def test_exact_ties_resolve_by_lowest_position(n, K, distinct):
+    """Identical or few distinct keys: equal scores everywhere; the kept set must
+    follow (score desc, position asc) exactly (list path and fallback path)."""
+    wl = inputs.Workload("ties", 3, 4, 2, 64, 8, 5, "bf16", (n,), (K,), ((0, 0),), 0, 21)
+    run_case(f"ties-n{n}-d{distinct}", wl, make=_tied_inputs(wl, distinct))
