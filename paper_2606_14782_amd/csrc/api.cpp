@@ -36,7 +36,9 @@ bacon_status hip_fail(hipError_t e, const char *what) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ring, vec_b, vec_vp, partials, lambda, total;
+  size_t ring, vec_b, vec_vp, vec_pb, vec_pv, cand_key, cand_pos, cand_v, partials, lambda, counter,
+      total;
+  int64_t cand_stride;
   int rpad, slots, ring_mp;
   int64_t chunks_cap;
 };
@@ -95,17 +97,29 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.ring = off;     off += align256((size_t)L.ring_mp * vec);
   L.vec_b = off;    off += align256(vec);
   L.vec_vp = off;   off += align256(vec);
+  // per head: segments * kSegLen pooled values, and candidate slots
+  // sum over sequences of segments * min(M or K, kSegLen); both are at most
+  // T + max_batch * kSegLen
+  L.cand_stride = s->max_total_tokens + (int64_t)s->max_batch * kSegLen;
+  const size_t cand = (size_t)s->num_kv_heads * (size_t)L.cand_stride * 4;
+  L.vec_pb = off;   off += align256(cand);
+  L.vec_pv = off;   off += align256(cand);
+  L.cand_key = off; off += align256(cand);
+  L.cand_pos = off; off += align256(cand);
+  L.cand_v = off;   off += align256(cand);
   L.partials = off; off += align256((size_t)s->num_kv_heads * L.chunks_cap * L.rpad * sizeof(float2));
   L.lambda = off;   off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(float));
+  L.counter = off;  off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(unsigned));
   L.total = off;
   return L;
 }
 
-const char *kKernelNames[] = {"window_lse", "window_score", "window_score_calib",
-                              "select_fused", "select_calib", "select_topk", "calib_elem",
-                              "compact"};
-enum KernelId { KI_LSE, KI_SCORE, KI_FUSED, KI_SEL_FUSED, KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM,
-                KI_COMPACT, KI_COUNT };
+const char *kKernelNames[] = {"window_lse",     "window_score",   "window_score_calib",
+                              "segment_lambda", "segment_topk",   "select_fused",
+                              "select_calib",   "select_topk",    "calib_elem",
+                              "compact",        "zero"};
+enum KernelId { KI_LSE, KI_SCORE, KI_FUSED, KI_SEGA, KI_SEGB, KI_SEL_FUSED, KI_SEL_CALIB,
+                KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_ZERO, KI_COUNT };
 
 }  // namespace
 
@@ -211,23 +225,42 @@ SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out) {
   const int64_t slots = 256LL * std::min(by_lds, by_waves);
   int per_wg = (int)std::max<int64_t>(1, (stages + slots - 1) / slots);
   if (c->chunk_stages_override > 0) per_wg = c->chunk_stages_override;
+  // the select kernel stages 2r positions around every chunk boundary
+  int nmax = 0;
+  for (int b = 0; b < bt->batch; ++b) nmax = std::max(nmax, bt->cu_seqlens[b + 1] - bt->cu_seqlens[b]);
+  if (c->params.radius > 0) {
+    const int min_chunk = (int)(((int64_t)nmax * 2 * c->params.radius + kEdgeEntries - 1) / kEdgeEntries);
+    per_wg = std::max(per_wg, (min_chunk + tk - 1) / tk);
+  }
   per_wg = std::min(per_wg, kMaxChunk / tk);
   const int chunk = tk * per_wg;
-  int cb = 0, ib = 0, kb = 0;
+  int cb = 0, ib = 0, kb = 0, sb = 0, cnb = 0;
   for (int b = 0; b < bt->batch; ++b) {
     const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
+    const int nc = n - c->shape.window;
+    int M = (int)floorf(c->params.rho * (float)bt->budgets[b]);
+    M = std::max(0, std::min(M, nc));
+    const int nseg = (n + kSegLen - 1) / kSegLen;
     st.cu[b] = bt->cu_seqlens[b];
     st.chunk_base[b] = cb;
     st.budget[b] = bt->budgets[b];
     st.idx_base[b] = ib;
     st.kept_base[b] = kb;
+    st.seg_base[b] = sb;
+    st.cand_base[b] = cnb;
+    st.mc[b] = std::min(M, kSegLen);
     cb += (n + chunk - 1) / chunk;
     ib += bt->budgets[b];
     kb += bt->budgets[b] + c->shape.window;
+    sb += nseg;
+    cnb += nseg * st.mc[b];
   }
   st.cu[bt->batch] = bt->cu_seqlens[bt->batch];
   st.chunk_base[bt->batch] = cb;
+  st.seg_base[bt->batch] = sb;
+  st.cand_base[bt->batch] = cnb;
   st.total_chunks = cb;
+  st.total_segs = sb;
   *chunk_out = chunk;
   return st;
 }
@@ -283,6 +316,42 @@ SelArgs sel_args(const bacon_ctx *c) {
   a.lambda_ws = reinterpret_cast<float *>(c->ws + c->L.lambda);
   a.row_bytes = s.head_dim * (s.dtype == BACON_BF16 ? 2 : 4);
   return a;
+}
+
+int max_len(const bacon_batch *bt);
+
+// The segmented select (one workgroup per kSegLen positions) applies when the
+// union of the segments' candidates of a (sequence, KV head), for both the
+// scale-matching set and the top-K, fits one closing workgroup.
+bool segmented_select(const bacon_ctx *c, const bacon_batch *bt) {
+  for (int b = 0; b < bt->batch; ++b) {
+    const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
+    const int nc = n - c->shape.window;
+    const int nseg = (n + kSegLen - 1) / kSegLen;
+    int M = (int)floorf(c->params.rho * (float)bt->budgets[b]);
+    M = std::max(0, std::min(M, nc));
+    if ((int64_t)nseg * std::min(M, kSegLen) > kUnionCap) return false;
+    if ((int64_t)nseg * std::min(bt->budgets[b], kSegLen) > kUnionCap) return false;
+  }
+  return true;
+}
+
+// Every workgroup of the pass must fit the LDS of one CU; checked before
+// anything is enqueued.
+bacon_status check_lds(const bacon_ctx *c, const bacon_batch *bt, int chunk, bool passes,
+                       int sel_mode) {
+  const bool bf16 = c->shape.dtype == BACON_BF16;
+  if (passes && pass_lds_bytes(PASS_FUSED, bf16, c->shape.head_dim, c->L.rpad, chunk) > kLdsBytes)
+    return fail(BACON_ERR_UNSUPPORTED, "pass workgroup needs more LDS than a CU has");
+  if (sel_mode >= 0 && sel_mode != SEL_SEGMENTED &&
+      select_lds_bytes(sel_mode, max_len(bt)) > (size_t)kLdsBytes)
+    return fail(BACON_ERR_UNSUPPORTED, "select workgroup needs more LDS than a CU has");
+  if (sel_mode == SEL_FUSED || sel_mode == SEL_CALIB || sel_mode == SEL_SEGMENTED) {
+    const int n = max_len(bt);
+    if (chunk < n && (int64_t)((n - 1) / chunk) * 2 * c->params.radius > kEdgeEntries)
+      return fail(BACON_ERR_UNSUPPORTED, "too many chunk boundaries for radius %d", c->params.radius);
+  }
+  return BACON_OK;
 }
 
 int max_len(const bacon_batch *bt) {
@@ -353,8 +422,12 @@ bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *strea
   c->budgets.assign(bt->budgets, bt->budgets + bt->batch);
   c->prompt = true;
   c->next_layer = 0;
-  (void)stream;   // nothing to enqueue: layer 0 reads no history
-  return BACON_OK;
+  // arrival counters of the segment kernels start at zero (layer 0 reads no history)
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned *cnt = reinterpret_cast<unsigned *>(c->ws + c->L.counter);
+  return timed(c, KI_ZERO, s, [&] {
+    return launch_zero_u32(cnt, c->shape.max_batch * c->shape.num_kv_heads, s);
+  });
 }
 
 bacon_status bacon_score(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
@@ -371,6 +444,7 @@ bacon_status bacon_score(bacon_ctx *c, int32_t layer, const bacon_batch *bt, con
   hipStream_t s = static_cast<hipStream_t>(stream);
   int chunk = 0;
   const SeqTable st = make_table(c, bt, &chunk);
+  TRY(check_lds(c, bt, chunk, true, -1));
   PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
   a.T = bt->cu_seqlens[bt->batch];
   a.lse_user = d_lse;
@@ -401,6 +475,7 @@ bacon_status bacon_calibrate(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
   hipStream_t s = static_cast<hipStream_t>(stream);
   int chunk = 0;
   const SeqTable st = make_table(c, bt, &chunk);
+  TRY(check_lds(c, bt, chunk, false, SEL_CALIB));
   const int64_t T = bt->cu_seqlens[bt->batch];
   ElemArgs e{};
   e.in_B = d_B;
@@ -441,6 +516,7 @@ bacon_status bacon_select_topk(bacon_ctx *c, const bacon_batch *bt, const float 
   hipStream_t s = static_cast<hipStream_t>(stream);
   int chunk = 0;
   const SeqTable st = make_table(c, bt, &chunk);
+  TRY(check_lds(c, bt, chunk, false, SEL_TOPK));
   SelArgs a = sel_args(c);
   a.T = bt->cu_seqlens[bt->batch];
   a.in_S = d_S;
@@ -491,6 +567,7 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   hipStream_t s = static_cast<hipStream_t>(stream);
   int chunk = 0;
   const SeqTable st = make_table(c, bt, &chunk);
+  TRY(check_lds(c, bt, chunk, true, segmented_select(c, bt) ? SEL_SEGMENTED : SEL_FUSED));
   const int64_t T = bt->cu_seqlens[bt->batch];
   PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
   a.T = T;
@@ -500,19 +577,63 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   const bool w32 = c->shape.window == 32;
   TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
   TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
-  SelArgs sa = sel_args(c);
-  sa.T = T;
-  sa.ring = a.ring;
-  sa.ring_mp = c->L.ring_mp;
-  sa.ring_slot = a.ring_write;
-  sa.vp_chunk = chunk;
-  sa.idx = d_idx;
-  sa.k = d_k;
-  sa.v = d_v;
-  sa.k_out = d_k_out;
-  sa.v_out = d_v_out;
-  sa.do_gather = 1;
-  TRY(timed(c, KI_SEL_FUSED, s, [&] { return launch_select(SEL_FUSED, max_len(bt), sa, st, s); }));
+  if (!segmented_select(c, bt)) {
+    // a union of segment candidates would not fit one workgroup: one
+    // workgroup per (sequence, KV head) selects over the whole sequence
+    SelArgs sa = sel_args(c);
+    sa.T = T;
+    sa.ring = a.ring;
+    sa.ring_mp = c->L.ring_mp;
+    sa.ring_slot = a.ring_write;
+    sa.vp_chunk = chunk;
+    sa.idx = d_idx;
+    sa.k = d_k;
+    sa.v = d_v;
+    sa.k_out = d_k_out;
+    sa.v_out = d_v_out;
+    sa.do_gather = 1;
+    TRY(timed(c, KI_SEL_FUSED, s, [&] { return launch_select(SEL_FUSED, max_len(bt), sa, st, s); }));
+    c->next_layer = layer + 1;
+    return BACON_OK;
+  }
+  SegArgs g{};
+  g.Hkv = c->shape.num_kv_heads;
+  g.W = c->shape.window;
+  g.T = T;
+  g.radius = c->params.radius;
+  g.pool_half = c->params.pool_kernel / 2;
+  g.vp_chunk = chunk;
+  g.rho = c->params.rho;
+  g.gamma = c->params.gamma;
+  g.eps = c->params.eps;
+  g.use_last_query = c->params.use_last_query;
+  g.terms = c->params.terms;
+  g.vec_B = a.vec_B;
+  g.vec_VP = a.vec_VP;
+  g.ring = a.ring;
+  g.ring_mp = c->L.ring_mp;
+  g.ring_slot = a.ring_write;
+  g.vec_pB = reinterpret_cast<float *>(c->ws + c->L.vec_pb);
+  g.vec_pV = reinterpret_cast<float *>(c->ws + c->L.vec_pv);
+  g.cand_key = reinterpret_cast<unsigned *>(c->ws + c->L.cand_key);
+  g.cand_pos = reinterpret_cast<int *>(c->ws + c->L.cand_pos);
+  g.cand_v = reinterpret_cast<float *>(c->ws + c->L.cand_v);
+  g.cand_stride = c->L.cand_stride;
+  g.lambda_ws = reinterpret_cast<float *>(c->ws + c->L.lambda);
+  g.counter = reinterpret_cast<unsigned *>(c->ws + c->L.counter);
+  g.idx = d_idx;
+  TRY(timed(c, KI_SEGA, s, [&] { return launch_sega(g, st, s); }));
+  TRY(timed(c, KI_SEGB, s, [&] { return launch_segb(g, st, s); }));
+  CompactArgs ca{};
+  ca.idx = d_idx;
+  ca.k = d_k;
+  ca.v = d_v;
+  ca.k_out = d_k_out;
+  ca.v_out = d_v_out;
+  ca.Hkv = c->shape.num_kv_heads;
+  ca.W = c->shape.window;
+  ca.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
+  TRY(timed(c, KI_COMPACT, s, [&] { return launch_compact(ca, st, s); }));
   c->next_layer = layer + 1;
   return BACON_OK;
 }

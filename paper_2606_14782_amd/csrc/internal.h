@@ -14,11 +14,21 @@ constexpr int kMaxChunk = 4096;     // keys per pass workgroup
 constexpr int kSelThreads = 1024;
 constexpr int kSelPer = kMaxSeqLen / kSelThreads;   // positions per select thread
 constexpr int kHistBins = 2048;     // 11-bit digits of the block select
+constexpr int kSegLen = 2048;       // positions per segment of the distributed select
+constexpr int kSegThreads = 1024;
+constexpr int kPoolHalo = 16;       // largest pool half-width
+constexpr int kUnionCap = 8192;     // candidate slots a closing segment workgroup holds
+constexpr int kLdsBytes = 160 * 1024;   // LDS per CU (and per workgroup) on gfx950
+constexpr int kEdgeEntries = 1024;      // positions next to chunk boundaries the select stages
 
 // Per-sequence layout, passed by value to every kernel.
 struct SeqTable {
   int32_t batch;
   int32_t total_chunks;                 // key chunks per KV head over the batch
+  int32_t total_segs;                   // select segments per KV head over the batch
+  int32_t seg_base[kMaxBatch + 1];      // first select segment of each sequence
+  int32_t cand_base[kMaxBatch + 1];     // first scale-matching candidate slot of each sequence
+  int32_t mc[kMaxBatch];                // candidate slots per segment: min(M, kSegLen)
   int32_t cu[kMaxBatch + 1];            // token offsets
   int32_t chunk_base[kMaxBatch + 1];    // first chunk of each sequence
   int32_t budget[kMaxBatch];            // kept keys per KV head
@@ -51,7 +61,7 @@ struct PassArgs {
   uint32_t terms;
 };
 
-enum SelMode { SEL_FUSED = 0, SEL_CALIB = 1, SEL_TOPK = 2 };
+enum SelMode { SEL_FUSED = 0, SEL_CALIB = 1, SEL_TOPK = 2, SEL_SEGMENTED = 3 };
 
 struct SelArgs {
   int Hkv, W;
@@ -75,6 +85,27 @@ struct SelArgs {
   void *k_out, *v_out;
   int row_bytes;
   int do_gather;
+};
+
+// Distributed select of the fused pass (segment kernel, then final kernel).
+struct SegArgs {
+  int Hkv, W;
+  int64_t T;
+  int radius, pool_half, vp_chunk;
+  float rho, gamma, eps;
+  int use_last_query;
+  uint32_t terms;
+  const float *vec_B, *vec_VP;   // [Hkv, T]
+  const float *ring;             // [Hkv, T, ring_mp]
+  int ring_mp, ring_slot;
+  float *vec_pB, *vec_pV;        // [Hkv, total_segs, kSegLen] pooled B and V over I
+  unsigned *cand_key;            // [Hkv, cand_stride] scale-matching candidates
+  int *cand_pos;
+  float *cand_v;
+  int64_t cand_stride;
+  float *lambda_ws, *out_lambda; // [B, Hkv]
+  unsigned *counter;             // [B, Hkv] arrival counters, zero between launches
+  int32_t *idx;
 };
 
 struct ElemArgs {           // split calibrate: E, T, L, ring update
@@ -101,9 +132,14 @@ int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk);
 
 hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
                        const SeqTable &st, hipStream_t s);
+// LDS a select workgroup needs (static + dynamic) for sequences up to max_len.
+size_t select_lds_bytes(int mode, int max_len);
 hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,
                          hipStream_t s);
 hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_sega(const SegArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_segb(const SegArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_zero_u32(unsigned *p, int count, hipStream_t s);
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
 
 }  // namespace bacon

@@ -401,6 +401,7 @@ template <int MODE, bool BF16, int D, bool W32>
 static hipError_t launch_pass_t(const PassArgs &a, const SeqTable &st, hipStream_t s) {
   const int nw = a.Rpad / 32;
   const int lds = pass_lds_bytes(MODE, BF16, D, a.Rpad, a.chunk);
+  if (lds > kLdsBytes) return hipErrorInvalidValue;
   dim3 grid(st.total_chunks, a.Hkv), block(64 * nw);
   allow_lds(k_pass<MODE, BF16, D, W32>, lds);
   hipLaunchKernelGGL((k_pass<MODE, BF16, D, W32>), grid, block, lds, s, a, st);
@@ -430,14 +431,12 @@ hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassAr
 }
 
 // ---------------------------------------------------------------- block helpers
-constexpr int kWaves = kSelThreads / 64;
-
-struct SelShared {
+// Shared scratch of the block-wide primitives for NT threads.
+template <int NT>
+struct SelSharedT {
   unsigned hist[kHistBins];
-  unsigned lane_cnt[64];
-  unsigned cnt;
-  unsigned red_u[kWaves];
-  double red_d[4][kWaves];
+  unsigned red_u[NT / 64], red_u2[NT / 64];
+  double red_d[4][NT / 64];
   unsigned bc_u[4];
   double bc_d[4];
   int bc_i[4];
@@ -490,15 +489,15 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 }
 
 // Block-wide min (OP 0) / max (1) / sum (2) of unsigned values.
-template <int OP>
-__device__ __forceinline__ unsigned block_reduce_u(unsigned v, SelShared &ss) {
+template <int OP, int NT>
+__device__ __forceinline__ unsigned block_reduce_u(unsigned v, SelSharedT<NT> &ss) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   v = OP == 0 ? wave_min_u(v) : OP == 1 ? wave_max_u(v) : wave_sum_u(v);
   if (lane == 0) ss.red_u[wave] = v;
   __syncthreads();
   if (wave == 0) {
     const unsigned id = OP == 0 ? 0xffffffffu : 0u;
-    unsigned x = (lane < kWaves) ? ss.red_u[lane] : id;
+    unsigned x = (lane < NT / 64) ? ss.red_u[lane] : id;
     x = OP == 0 ? wave_min_u(x) : OP == 1 ? wave_max_u(x) : wave_sum_u(x);
     if (lane == 0) ss.bc_u[0] = x;
   }
@@ -509,14 +508,15 @@ __device__ __forceinline__ unsigned block_reduce_u(unsigned v, SelShared &ss) {
 }
 
 // Sum of four doubles over the block in a fixed order.
-__device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, double v3, SelShared &ss, double *out) {
+template <int NT>
+__device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, double v3, SelSharedT<NT> &ss, double *out) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   v0 = wave_sum_d(v0); v1 = wave_sum_d(v1); v2 = wave_sum_d(v2); v3 = wave_sum_d(v3);
   if (lane == 0) { ss.red_d[0][wave] = v0; ss.red_d[1][wave] = v1; ss.red_d[2][wave] = v2; ss.red_d[3][wave] = v3; }
   __syncthreads();
   if (t < 4) {
     double s = 0.0;
-    for (int w = 0; w < kWaves; ++w) s += ss.red_d[t][w];
+    for (int w = 0; w < NT / 64; ++w) s += ss.red_d[t][w];
     ss.bc_d[t] = s;
   }
   __syncthreads();
@@ -525,7 +525,8 @@ __device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, do
 }
 
 // Exclusive prefix sum over threads in index order.
-__device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelShared &ss) {
+template <int NT>
+__device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelSharedT<NT> &ss) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   unsigned x = v;
 #pragma unroll
@@ -552,40 +553,52 @@ __device__ __forceinline__ float key_float(unsigned k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
 
-// Boundary search over ss.hist (larger bin = larger keys): the bin holding
-// the need-th largest counted element and the count in the bins above it,
-// left in ss.bc_i[0] and ss.bc_i[1].  Wave 0 scans; ends with a barrier.
-__device__ __forceinline__ void hist_boundary(int need, SelShared &ss) {
-  const int t = threadIdx.x;
-  if (t < 64) {
-    const int lane = t;
-    unsigned cs = 0;
-    for (int q = 0; q < 32; ++q) cs += ss.hist[lane * 32 + ((q + lane) & 31)];   // rotated: no bank conflicts
-    ss.lane_cnt[lane] = cs;
-    __builtin_amdgcn_wave_barrier();
-    unsigned suf = 0;      // counted elements in bins of lanes >= lane
-    for (int q = 63; q >= 0; --q) suf += (q >= lane) ? ss.lane_cnt[q] : 0u;
-    const unsigned above_lane = suf - cs;
-    if (above_lane < (unsigned)need && (unsigned)need <= suf) {
-      unsigned acc = above_lane;
-      int bs = lane * 32;
-      for (int q = 31; q >= 0; --q) {
-        const unsigned hq = ss.hist[lane * 32 + q];
-        if (acc + hq >= (unsigned)need) { bs = lane * 32 + q; break; }
-        acc += hq;
-      }
-      ss.bc_i[0] = bs;
-      ss.bc_i[1] = (int)acc;
-    }
+// Boundary search over ss.hist (larger bin = larger keys), block-parallel:
+// thread t owns the kHistBins/NT consecutive bins starting at t*kHistBins/NT;
+// suffix sums over threads give, for the need-th largest counted element, its
+// bin (ss.bc_i[0]) and the count in the bins above it (ss.bc_i[1]);
+// ss.bc_u[3] gets the total count.  Ends with a barrier.
+template <int NT>
+__device__ __forceinline__ void hist_boundary(int need, SelSharedT<NT> &ss) {
+  constexpr int BPT = kHistBins / NT;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  unsigned cb[BPT];
+  unsigned c = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) { cb[q] = ss.hist[BPT * t + q]; c += cb[q]; }
+  unsigned suf = c;                    // inclusive suffix sum within the wave
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned y = (unsigned)__shfl_down((int)suf, o);
+    if (lane + o < 64) suf += y;
   }
+  if (lane == 0) ss.red_u[wave] = suf;   // wave total
+  __syncthreads();
+  unsigned higher = 0;                 // counted elements in later waves
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) higher += (w > wave) ? ss.red_u[w] : 0u;
+  suf += higher;
+  const unsigned above = suf - c;
+  if (above < (unsigned)need && (unsigned)need <= suf) {
+    unsigned acc = above;
+    int bs = BPT * t;
+#pragma unroll
+    for (int q = BPT - 1; q >= 0; --q) {
+      if (acc + cb[q] >= (unsigned)need) { bs = BPT * t + q; break; }
+      acc += cb[q];
+    }
+    ss.bc_i[0] = bs;
+    ss.bc_i[1] = (int)acc;
+  }
+  if (t == 0) ss.bc_u[3] = suf;
   __syncthreads();
 }
 
 // k-th largest key among the block's non-zero keys (1 <= k <= count), by
 // MSB-first 11-bit histogram narrowing of the candidate range over all
 // elements.  Returns the key value xk and need = k - #{keys > xk}.
-template <int PER, typename KeyF>
-__device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int &need, SelShared &ss) {
+template <int PER, typename KeyF, int NT>
+__device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int &need, SelSharedT<NT> &ss) {
   const int t = threadIdx.x;
   unsigned lo = 0xffffffffu, hi = 0u;
 #pragma unroll
@@ -599,7 +612,7 @@ __device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int 
   while (lo != hi) {
     const unsigned range = hi - lo;
     const int sh = max(0, 32 - __clz((int)range) - 11);
-    for (int q = t; q < kHistBins; q += kSelThreads) ss.hist[q] = 0u;
+    for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -621,52 +634,53 @@ __device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int 
 }
 
 constexpr int kCandCap = 1024;   // LDS list of boundary-bin candidates
+constexpr int kEdgeCap = kEdgeEntries;   // LDS tables of E and L corrections next to chunk boundaries
 
 // Exact top-k threshold with the tie rule (key descending, then position
 // ascending) over the block's non-zero keys, 1 <= k <= count: element j is
 // kept iff key > xk, or key == xk and position <= pthr.
 // One histogram pass bins every key over [max(min, max - 8 octaves), max];
-// the boundary bin is compacted into an LDS list (ckey, cpos) and resolved
-// there; ties are split by position.  When the boundary falls below that
-// range or its bin overflows the list, full-range narrowing over all
-// elements is used instead.
-template <int PER, typename KeyF, typename PosF>
+// the boundary bin is compacted into an LDS list (ckey, cpos) in a fixed
+// order (ballots, no atomics).  A list of at most NT entries is resolved by
+// ranking every entry against all others under the tie rule; a longer one by
+// 11-bit histogram rounds.  When the boundary falls below the binned range or
+// its bin overflows the list, full-range narrowing over all elements is used.
+// Ends with a barrier.
+template <int PER, typename KeyF, typename PosF, int NT>
 __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsigned &xk, int &pthr,
-                                                SelShared &ss, unsigned *ckey, int *cpos) {
-  const int t = threadIdx.x, lane = t & 63;
+                                                SelSharedT<NT> &ss, unsigned *ckey, int *cpos) {
+  constexpr int NW = NT / 64;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  // the range reduction's barrier also orders this clear before the binning
+  for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
   unsigned lo = 0xffffffffu, hi = 0u;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const unsigned x = key(j);
     if (x) { lo = min(lo, x); hi = max(hi, x); }
   }
-  lo = block_reduce_u<0>(lo, ss);
-  hi = block_reduce_u<1>(hi, ss);
+  lo = wave_min_u(lo);
+  hi = wave_max_u(hi);
+  if (lane == 0) { ss.red_u[wave] = lo; ss.red_u2[wave] = hi; }
+  __syncthreads();
+  lo = 0xffffffffu;
+  hi = 0u;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) { lo = min(lo, ss.red_u[w]); hi = max(hi, ss.red_u2[w]); }
   if (hi - lo > (8u << 23)) lo = hi - (8u << 23);      // at most 8 octaves below the max
   const int sh0 = max(0, 32 - __clz((int)(hi - lo)) - 11);
-  for (int q = t; q < kHistBins; q += kSelThreads) ss.hist[q] = 0u;
-  if (t == 0) ss.cnt = 0u;
-  __syncthreads();
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const unsigned x = key(j);
     if (x >= lo && hi >= lo) atomicAdd(&ss.hist[(x - lo) >> sh0], 1u);
   }
   __syncthreads();
-  unsigned counted = 0;
-  if (t < 64) {
-    unsigned cs = 0;
-    for (int q = 0; q < 32; ++q) cs += ss.hist[t * 32 + q];
-    counted = wave_sum_u(cs);
-    if (t == 0) ss.bc_u[2] = counted;
-  }
-  __syncthreads();
-  counted = ss.bc_u[2];
+  hist_boundary(k, ss);
+  const unsigned counted = ss.bc_u[3];
   bool fallback = counted < (unsigned)k;                // boundary below the binned range
   unsigned b0 = 0, C = 0;
   int need = k;
   if (!fallback) {
-    hist_boundary(k, ss);
     b0 = (unsigned)ss.bc_i[0];
     need = k - ss.bc_i[1];
     C = ss.hist[b0];
@@ -690,25 +704,63 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     }
     return;
   }
-  // compact the boundary bin: one LDS counter update per wave and element slot
+  // compact the boundary bin in (wave, element slot, lane) order
+  {
+    auto inbin = [&](unsigned x) { return x >= lo && ((x - lo) >> sh0) == b0; };
+    unsigned wc = 0;
 #pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const unsigned x = key(j);
-    const bool in = x >= lo && ((x - lo) >> sh0) == b0;
-    const uint64_t m = __ballot(in);
-    if (m) {
-      unsigned basei = 0;
-      if (lane == 0) basei = atomicAdd(&ss.cnt, (unsigned)__popcll(m));
-      basei = (unsigned)__builtin_amdgcn_readfirstlane((int)basei);
+    for (int j = 0; j < PER; ++j) wc += (unsigned)__popcll(__ballot(inbin(key(j))));
+    if (lane == 0) ss.red_u[wave] = wc;
+    __syncthreads();
+    unsigned off = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) off += (w < wave) ? ss.red_u[w] : 0u;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const unsigned x = key(j);
+      const bool in = inbin(x);
+      const uint64_t m = __ballot(in);
       if (in) {
-        const unsigned off = basei + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
-                                                               __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
-        ckey[off] = x;
-        cpos[off] = pos(j);
+        const unsigned o = off + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+        ckey[o] = x;
+        cpos[o] = pos(j);
+      }
+      off += (unsigned)__popcll(m);
+    }
+    __syncthreads();
+  }
+  if (C <= (unsigned)NT) {
+    // rank of each entry under the tie rule, tpe consecutive lanes per entry
+    int tpe = 1;
+    while (tpe < 32 && 2 * tpe * (int)C <= NT) tpe *= 2;
+    const int q = t / tpe, sub = t & (tpe - 1);
+    unsigned rk = 0, kq = 0;
+    int pq = 0;
+    if (q < (int)C) {
+      kq = ckey[q];
+      pq = cpos[q];
+      for (int p = sub; p < (int)C; p += tpe) {
+        const unsigned kp = ckey[p];
+        const int pp = cpos[p];
+        rk += (kp > kq || (kp == kq && pp < pq)) ? 1u : 0u;
       }
     }
+    if (tpe > 1) rk += swz<1>(rk);
+    if (tpe > 2) rk += swz<2>(rk);
+    if (tpe > 4) rk += swz<4>(rk);
+    if (tpe > 8) rk += swz<8>(rk);
+    if (tpe > 16) rk += swz<16>(rk);
+    if (q < (int)C && sub == 0 && rk == (unsigned)(need - 1)) {
+      ss.bc_u[1] = kq;
+      ss.bc_i[2] = pq;
+    }
+    __syncthreads();
+    xk = ss.bc_u[1];
+    pthr = ss.bc_i[2];
+    __syncthreads();
+    return;
   }
-  __syncthreads();
   // resolve the key inside the bin: 11 bits at a time from bit sh0 down
   const unsigned blo = lo + (b0 << sh0);                // smallest key of the bin
   unsigned pre = 0, pmask = 0;                          // known bits of (x - blo)
@@ -718,9 +770,9 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     const int nb = min(sh, 11);
     sh -= nb;
     const unsigned bm = (1u << nb) - 1u;
-    for (int q = t; q < kHistBins; q += kSelThreads) ss.hist[q] = 0u;
+    for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
     __syncthreads();
-    for (int q = t; q < (int)C; q += kSelThreads) {
+    for (int q = t; q < (int)C; q += NT) {
       const unsigned d = ckey[q] - blo;
       if ((d & pmask) == pre) atomicAdd(&ss.hist[(d >> sh) & bm], 1u);
     }
@@ -744,9 +796,9 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     const int nb = min(ps, 11);
     ps -= nb;
     const unsigned bm = (1u << nb) - 1u;
-    for (int q = t; q < kHistBins; q += kSelThreads) ss.hist[q] = 0u;
+    for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
     __syncthreads();
-    for (int q = t; q < (int)C; q += kSelThreads) {
+    for (int q = t; q < (int)C; q += NT) {
       if (ckey[q] != xk) continue;
       const unsigned d = 0x7fffu - (unsigned)cpos[q];   // larger d = lower position
       if ((d & ppm) == ppre) atomicAdd(&ss.hist[(d >> ps) & bm], 1u);
@@ -762,6 +814,8 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
   pthr = (int)(0x7fffu - ppre);
 }
 
+using SelShared = SelSharedT<kSelThreads>;
+
 // ---------------------------------------------------------------- select kernel
 // A copy of v the compiler cannot see through: stops it from hoisting address
 // arithmetic of one phase and keeping it live through the next.
@@ -773,6 +827,7 @@ __device__ __forceinline__ int opaque(int v) {
 // LDS: S padded by one word per kSelPer (thread-contiguous reads hit distinct
 // banks), reused as the slot table.
 __device__ __forceinline__ int pad32(int i) { return i + i / kSelPer; }
+constexpr int kArrWords = kMaxSeqLen + kMaxSeqLen / kSelPer + 64;
 
 template <int MODE>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) {
@@ -784,38 +839,46 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
   const int nc = n - a.W;                           // candidate set [0, nc)
   const int K = st.budget[b];
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  // LDS: arr [pad32 extent of n], candidate list, then per-mode tables
-  unsigned *ckey = reinterpret_cast<unsigned *>(arr + (n + n / PER + 64));
+  // LDS: arr [pad32 extent of kMaxSeqLen], candidate list, then per-mode tables
+  unsigned *ckey = reinterpret_cast<unsigned *>(arr + kArrWords);
   int *cpos = reinterpret_cast<int *>(ckey + kCandCap);
 
   if constexpr (MODE != SEL_TOPK) {
-    // E of this layer next to the chunk boundaries of vec_VP, staged in LDS:
-    // for boundary c*CH (c >= 1) the 2r positions [c*CH - r, c*CH + r).
+    // The L neighbours of positions next to a chunk boundary of vec_VP that lie
+    // in the neighbouring chunk.  Boundary c*CH (c >= 1) covers the 2r
+    // positions [c*CH - r, c*CH + r); the host keeps nbnd*2r <= kEdgeCap.
     const int r = a.radius, CH = a.vp_chunk;
     const bool use_l = (a.terms & 2u) != 0;
     const int nbnd = (use_l && CH < n) ? (n - 1) / CH : 0;      // boundaries inside the sequence
-    float *edge = reinterpret_cast<float *>(cpos + kCandCap);     // [nbnd][2r]
+    const int nedge = nbnd * 2 * r;
+    float *edge = reinterpret_cast<float *>(cpos + kCandCap);     // E at those positions
+    float *fixt = edge + kEdgeCap;                                // their L correction
     const float *re = a.ring + base * a.ring_mp + a.ring_slot;
-    for (int q = t; q < nbnd * 2 * r; q += kSelThreads) {
+    for (int q = t; q < nedge; q += kSelThreads) {
       const int c = q / (2 * r) + 1, o = q - (c - 1) * 2 * r;
       const int u = c * CH - r + o;
       const float e = re[(int64_t)min(max(u, 0), n - 1) * a.ring_mp];
       edge[q] = (u >= 0 && u < n) ? e : 0.f;
     }
-    auto eat = [&](int u) -> float {       // E at a position next to a boundary
-      const int c = (u + r) / CH;          // boundary c*CH with |u - c*CH| <= r
-      return edge[(c - 1) * 2 * r + (u - (c * CH - r))];
-    };
-    // V_i = vec_VP_i + the L neighbours outside the chunk that produced it.
-    auto vfix = [&](int i) -> float {
-      if (!use_l) return 0.f;
-      const int k0 = (i / CH) * CH, k1 = min(n, k0 + CH);
+    __syncthreads();
+    for (int q = t; q < nedge; q += kSelThreads) {
+      const int c = q / (2 * r) + 1, o = q - (c - 1) * 2 * r;
+      const int i = c * CH - r + o;                 // position next to boundary c*CH
       const int lo = max(0, i - r), hi = min(n - 1, i + r);
-      if (lo >= k0 && hi < k1) return 0.f;
       float sum = 0.f;
-      for (int u = lo; u < k0; ++u) sum += eat(u);
-      for (int u = k1; u <= hi; ++u) sum += eat(u);
-      return sum / (float)(hi - lo + 1);
+      if (i < c * CH) {                             // left of the boundary: right neighbours
+        for (int u = c * CH; u <= hi; ++u) sum += edge[(c - 1) * 2 * r + (u - (c * CH - r))];
+      } else {                                      // right of it: left neighbours
+        for (int u = lo; u < c * CH; ++u) sum += edge[(c - 1) * 2 * r + (u - (c * CH - r))];
+      }
+      fixt[q] = (i >= 0 && i < n) ? sum / (float)(hi - lo + 1) : 0.f;
+    }
+    // correction of position i (0 when i is not next to a boundary)
+    auto vfix = [&](int i) -> float {
+      if (nbnd == 0) return 0.f;
+      const int c = (i + r) / CH;
+      const int o = i - (c * CH - r);
+      return (c >= 1 && c <= nbnd && o < 2 * r) ? fixt[(c - 1) * 2 * r + o] : 0.f;
     };
     // B into LDS (strided: element j of thread t is position t + j*kSelThreads);
     // all loads of the phase are issued before any is used.
@@ -834,14 +897,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     int M = (int)floorf(a.rho * (float)K);
     if (M > nc) M = nc;
     if (M < 0) M = 0;
-    float lam = 0.f;
-    if (M > 0 && a.use_last_query) {
+    const bool calib = M > 0 && a.use_last_query;
+    uint64_t msk = 0;
+    if (calib) {
       auto keyB = [&](int j) -> unsigned {
         const int i = t + j * kSelThreads;
-        return i < nc ? float_key(arr[pad32(min(i, n - 1))]) : 0u;
+        const unsigned kx = float_key(arr[pad32(i)]);   // i < kMaxSeqLen: inside arr
+        return i < nc ? kx : 0u;
       };
       auto posf = [&](int j) -> int { return t + j * kSelThreads; };
-      uint64_t msk = 0;
       if (M >= nc) {
 #pragma unroll
         for (int j = 0; j < PER; ++j) msk |= (uint64_t)(t + j * kSelThreads < nc ? 1u : 0u) << j;
@@ -855,28 +919,34 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
           msk |= (uint64_t)(kj > xm || (kj == xm && posf(j) <= pm) ? 1u : 0u) << j;
         }
       }
-      // list of the set's positions in LDS (after the staged boundary E)
-      int *mlist = reinterpret_cast<int *>(edge + nbnd * 2 * r);
-      unsigned off = block_excl_scan_u((unsigned)__popcll(msk), ss);
-      {
-        uint64_t m2 = msk;
-        while (m2) {
-          const int j = __builtin_ctzll(m2);
-          m2 &= m2 - 1;
-          mlist[off++] = t + j * kSelThreads;
-        }
-      }
-      __syncthreads();
+    }
+    // V for the thread's positions: vec_VP, completed next to chunk boundaries.
+    const int tt = opaque(t);
+    float vp[PER];
+    {
+      const float *pv = a.vec_VP + base;
+#pragma unroll
+      for (int j = 0; j < PER; ++j) vp[j] = pv[min(tt + j * kSelThreads, n - 1)];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) vp[j] += vfix(tt + j * kSelThreads);
+    }
+    float lam = 0.f;
+    if (calib) {
       // population moments over the set in double; B shifted by the set minimum
+      float bv[PER];
+#pragma unroll
+      for (int j = 0; j < PER; ++j) bv[j] = arr[pad32(tt + j * kSelThreads)];
       unsigned kmin = 0xffffffffu;
-      for (int q = t; q < M; q += kSelThreads) kmin = min(kmin, float_key(arr[pad32(mlist[q])]));
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        kmin = ((msk >> j) & 1ull) ? min(kmin, float_key(bv[j])) : kmin;
       kmin = block_reduce_u<0>(kmin, ss);
       const double bref = (double)key_float(kmin);
       double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-      for (int q = t; q < M; q += kSelThreads) {
-        const int i = mlist[q];
-        const double db = (double)arr[pad32(i)] - bref;
-        const double dv = (double)(a.vec_VP[base + i] + vfix(i));
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const bool in = (msk >> j) & 1ull;
+        const double db = in ? (double)bv[j] - bref : 0.0, dv = in ? (double)vp[j] : 0.0;
         s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
       }
       double sums[4];
@@ -892,39 +962,16 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
       if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = lam;
     }
     // S = B + lambda V (Eq. bacon_score), in place of B; each thread touches
-    // only its own positions.  V = vec_VP here; positions next to a chunk
-    // boundary are recomputed below with their outside neighbours.
-    {
-      const int tt = opaque(t);
-      const float *pv = a.vec_VP + base;
-      float vp[PER];
+    // only its own positions.
 #pragma unroll
-      for (int j = 0; j < PER; ++j) vp[j] = pv[min(tt + j * kSelThreads, n - 1)];
-#pragma unroll
-      for (int j = 0; j < PER; ++j) {
-        const int i = tt + j * kSelThreads;
-        if (i < n) {
-          const float S = fmaf(lam, vp[j], arr[pad32(i)]);
-          if constexpr (MODE == SEL_CALIB) {
-            a.out_S[base + i] = S;
-            if (a.out_V) a.out_V[base + i] = vp[j];
-            if (a.out_E) a.out_E[base + i] = re[(int64_t)i * a.ring_mp];
-          } else {
-            arr[pad32(i)] = S;
-          }
-        }
-      }
-    }
-    __syncthreads();
-    for (int q = t; q < nbnd * 2 * r; q += kSelThreads) {
-      const int c = q / (2 * r) + 1, o = q - (c - 1) * 2 * r;
-      const int i = c * CH - r + o;
-      if (i >= 0 && i < n) {
-        const float V = a.vec_VP[base + i] + vfix(i);
-        const float S = fmaf(lam, V, a.vec_B[base + i]);
+    for (int j = 0; j < PER; ++j) {
+      const int i = tt + j * kSelThreads;
+      if (i < n) {
+        const float S = fmaf(lam, vp[j], arr[pad32(i)]);
         if constexpr (MODE == SEL_CALIB) {
           a.out_S[base + i] = S;
-          if (a.out_V) a.out_V[base + i] = V;
+          if (a.out_V) a.out_V[base + i] = vp[j];
+          if (a.out_E) a.out_E[base + i] = re[(int64_t)i * a.ring_mp];
         } else {
           arr[pad32(i)] = S;
         }
@@ -957,13 +1004,16 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         const int i = i0 + j;
+        // both reads are unconditional (clamped) so they never wait on a branch
+        const float in_v = arr[pad32(min(i + 1 + hp, nc - 1))];
+        const float out_v = arr[pad32(max(i - hp, 0))];
         if (i < nc) {
           const int cnt = hi - lo + 1;
           double inv = inv_full;
           if (cnt != 2 * hp + 1) inv = 1.0 / (double)cnt;
           key[j] = float_key((float)(acc * inv));
-          if (i + 1 + hp <= nc - 1) acc += (double)arr[pad32(i + 1 + hp)];
-          if (i - hp >= 0) acc -= (double)arr[pad32(i - hp)];
+          acc += (i + 1 + hp <= nc - 1) ? (double)in_v : 0.0;
+          acc -= (i - hp >= 0) ? (double)out_v : 0.0;
           lo = max(0, i + 1 - hp);
           hi = min(nc - 1, i + 1 + hp);
         }
@@ -1039,20 +1089,19 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
   }
 }
 
+size_t select_lds_bytes(int mode, int max_len) {
+  (void)max_len;   // arr always spans kMaxSeqLen so strided reads need no clamping
+  size_t bytes = (size_t)kArrWords * sizeof(float) +                              // arr (padded)
+                 2 * kCandCap * sizeof(unsigned);                                // candidate list
+  if (mode != SEL_TOPK) bytes += 2 * kEdgeCap * sizeof(float);                   // boundary tables
+  return bytes + sizeof(SelShared);
+}
+
 hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,
                          hipStream_t s) {
   dim3 grid(st.batch, a.Hkv), block(kSelThreads);
-  size_t extra_lds = 0;
-  if (mode != SEL_TOPK) {
-    const int nbnd = (a.vp_chunk < max_len) ? (max_len - 1) / a.vp_chunk : 0;
-    int mmax = 0;
-    for (int b = 0; b < st.batch; ++b) mmax = max(mmax, (int)floorf(a.rho * (float)st.budget[b]));
-    mmax = min(mmax, max_len);
-    extra_lds = ((size_t)nbnd * 2 * a.radius + (size_t)mmax + 16) * sizeof(float);
-  }
-    // arr (padded), candidate list, boundary E table, scale-matching set list
-  const size_t lds = (size_t)(max_len + max_len / kSelPer + 64) * sizeof(float) +
-                     2 * kCandCap * sizeof(unsigned) + extra_lds;
+  const size_t lds = select_lds_bytes(mode, max_len) - sizeof(SelShared);
+  if (lds + sizeof(SelShared) > kLdsBytes) return hipErrorInvalidValue;
   if (mode == SEL_FUSED) {
     allow_lds(k_select<SEL_FUSED>, lds);
     hipLaunchKernelGGL((k_select<SEL_FUSED>), grid, block, lds, s, a, st);
@@ -1063,6 +1112,432 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
     allow_lds(k_select<SEL_TOPK>, lds);
     hipLaunchKernelGGL((k_select<SEL_TOPK>), grid, block, lds, s, a, st);
   }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- distributed select
+// Two kernels of one workgroup per (segment of kSegLen positions, KV head).
+// In each, the workgroup of a (sequence, KV head) that finishes last reduces
+// what all its segments wrote: the first computes lambda from the union of
+// the segments' local scale-matching candidates (the global top-M of B lies in
+// the union of the segments' local top-M), the second the top-K from the union
+// of the segments' local top-K of the pooled score.
+constexpr int kSegPer = kSegLen / kSegThreads;             // positions per thread (strided)
+constexpr int kSegWin = kSegLen + 2 * kPoolHalo;           // segment plus pool halo
+constexpr int kSegWinJ = (kSegWin + kSegThreads - 1) / kSegThreads;
+constexpr int kUnionPer = kUnionCap / kSegThreads;         // union slots per thread
+static_assert(kEdgeEntries % kSegThreads == 0 || kSegThreads % kEdgeEntries == 0, "edge table load");
+constexpr int kEdgeJ = (kEdgeEntries + kSegThreads - 1) / kSegThreads;
+
+__device__ __forceinline__ int find_seg(const SeqTable &st, int seg) {
+  int b = 0;
+  while (b + 1 < st.batch && st.seg_base[b + 1] <= seg) ++b;
+  return b;
+}
+
+// Arrival of a workgroup at the per-(sequence, KV head) counter after its
+// global writes.  True in the workgroup that arrives last (expected-th), which
+// then sees every other workgroup's writes; that workgroup re-arms the counter.
+// No workgroup waits for another.  The barrier makes the workgroup's writes
+// visible to thread 0, whose device-scope release fence and counter update
+// publish them (one cache write-back per workgroup); the last workgroup's
+// thread 0 acquires before the barrier that releases the other threads.
+template <int NT>
+__device__ __forceinline__ bool last_arrival(unsigned *counter, unsigned expected, SelSharedT<NT> &ss) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    const unsigned prev = atomicAdd(counter, 1u);
+    const int last = prev + 1u == expected;
+    if (last) {
+      atomicExch(counter, 0u);
+      __threadfence();
+    }
+    ss.bc_i[3] = last;
+  }
+  __syncthreads();
+  return ss.bc_i[3] != 0;
+}
+
+// Slots of the set elements of a strided layout (element j of thread t is
+// item t + j*NT) in item order: pre[j*NW + wave] receives the number of set
+// elements before (j, wave); an element's slot is that plus its lane rank in
+// the ballot.  Ends with a barrier.
+template <int PER, int NT>
+__device__ __forceinline__ void ordered_bases(uint32_t msk, unsigned *pre) {
+  constexpr int NW = NT / 64, NE = PER * NW, E = (NE + 63) / 64;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const uint64_t m = __ballot((msk >> j) & 1u);
+    if (lane == 0) pre[j * NW + wave] = (unsigned)__popcll(m);
+  }
+  __syncthreads();
+  if (wave == 0) {
+    unsigned x[E], s = 0;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      x[e] = (lane * E + e < NE) ? pre[lane * E + e] : 0u;
+      s += x[e];
+    }
+    unsigned inc = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const unsigned y = (unsigned)__shfl_up((int)inc, o);
+      if (lane >= o) inc += y;
+    }
+    unsigned ex = inc - s;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      if (lane * E + e < NE) pre[lane * E + e] = ex;
+      ex += x[e];
+    }
+  }
+  __syncthreads();
+}
+__device__ __forceinline__ unsigned lane_rank(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+}
+
+// Calibration kernel.  Completes V = E + L + T next to chunk boundaries (the
+// L neighbours in another chunk, from this layer's E in the history), writes
+// the pooled window score pB and pooled evidence pV over I for the segment
+// (Eq. bacon_score is pooled as pool(B + lambda V) = pB + lambda pV), and the
+// segment's top-min(M, kSegLen) of B with their V.  The last workgroup of a
+// (sequence, KV head) takes the exact top-M of B over the union
+// (Eq. scale_matching_set) and solves lambda (Eq. lambda_solution).
+__global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
+  constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
+  __shared__ float Bs[kSegWin], Vs[kSegWin];
+  __shared__ float ed[kEdgeEntries];
+  __shared__ unsigned ckey[kCandCap];
+  __shared__ int cpos[kCandCap];
+  __shared__ SelSharedT<NT> ss;
+  __shared__ unsigned pre[kUnionPer * NW];
+  const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
+  const int wave = t >> 6;
+  const int b = find_seg(st, gs);
+  const int sg = gs - st.seg_base[b];
+  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
+  const int n = st.cu[b + 1] - st.cu[b];
+  const int nc = n - a.W;
+  const int i0 = sg * kSegLen;
+  const int w0 = i0 - kPoolHalo;                    // position of Bs[0]
+  const int64_t base = (int64_t)h * a.T + st.cu[b];
+  const int r = a.radius, CH = a.vp_chunk, tr = max(2 * r, 1);
+  const bool use_l = (a.terms & 2u) != 0 && r > 0 && CH < n;
+  // chunk boundaries m*CH (1 <= m <= (n-1)/CH) whose positions [m*CH - r,
+  // m*CH + r) meet the window; the host keeps their count times 2r within
+  // kEdgeEntries for the whole sequence
+  int m0 = 1, nedge = 0;
+  if (use_l) {
+    const int x = w0 - r + 1;
+    m0 = x <= 0 ? 1 : max(1, (x + CH - 1) / CH);
+    const int m1 = min((n - 1) / CH, (w0 + kSegWin - 1 + r) / CH);
+    nedge = max(0, m1 - m0 + 1) * 2 * r;
+  }
+  const float *re = a.ring + base * a.ring_mp + a.ring_slot;
+
+  // one round of loads: B and VP over the window, E next to the boundaries
+  {
+    const int tt = opaque(t);
+    float bv[kSegWinJ], vv[kSegWinJ], ev[kEdgeJ];
+#pragma unroll
+    for (int j = 0; j < kSegWinJ; ++j) {
+      const int u = min(max(w0 + tt + j * NT, 0), n - 1);
+      bv[j] = a.vec_B[base + u];
+      vv[j] = a.vec_VP[base + u];
+    }
+#pragma unroll
+    for (int j = 0; j < kEdgeJ; ++j) {
+      const int e = min(tt + j * NT, max(nedge - 1, 0));
+      const int m = e / tr;
+      const int x = (m0 + m) * CH - r + (e - m * tr);
+      ev[j] = re[(int64_t)min(max(x, 0), n - 1) * a.ring_mp];
+    }
+#pragma unroll
+    for (int j = 0; j < kEdgeJ; ++j)
+      if (tt + j * NT < nedge) ed[tt + j * NT] = ev[j];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kSegWinJ; ++j) {
+      const int q = tt + j * NT;
+      if (q < kSegWin) {
+        const int u = w0 + q;
+        float v = vv[j];
+        if (use_l && u >= 0 && u < n) {
+          const int k0 = (u / CH) * CH, k1 = min(n, k0 + CH);
+          const int lo = max(0, u - r), hi = min(n - 1, u + r);
+          if (lo < k0 || hi >= k1) {
+            // neighbours before k0 sit at offsets [0, r) of boundary k0's
+            // entries, those from k1 on at offsets [r, 2r) of boundary k1's
+            float sum = 0.f;
+            const int o0 = (k0 / CH - m0) * 2 * r + r - k0;
+            for (int x = lo; x < k0; ++x) sum += ed[o0 + x];
+            const int o1 = (k1 / CH - m0) * 2 * r + r - k1;
+            for (int x = k1; x <= hi; ++x) sum += ed[o1 + x];
+            v += sum / (float)(hi - lo + 1);
+          }
+        }
+        Bs[q] = bv[j];
+        Vs[q] = v;
+      }
+    }
+  }
+  __syncthreads();
+
+  // pooled B and V of the segment's positions over I (truncated windows)
+  const int hp = a.pool_half;
+  const int ncand = max(0, min(i0 + kSegLen, nc) - i0);    // candidates in the segment
+  float xb[PER], xv[PER];                                  // B, V at the thread's positions
+  {
+    const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int q = t + j * NT, i = i0 + q;
+      xb[j] = Bs[kPoolHalo + q];
+      xv[j] = Vs[kPoolHalo + q];
+      if (q < ncand) {
+        const int lo = max(0, i - hp), hi = min(nc - 1, i + hp);
+        float sb = 0.f, sv = 0.f;
+        for (int u = lo - w0; u <= hi - w0; ++u) { sb += Bs[u]; sv += Vs[u]; }
+        const float cnt = (float)(hi - lo + 1);
+        a.vec_pB[tile + q] = sb / cnt;
+        a.vec_pV[tile + q] = sv / cnt;
+      }
+    }
+  }
+
+  int M = (int)floorf(a.rho * (float)st.budget[b]);
+  M = max(0, min(M, nc));
+  if (M == 0 || !a.use_last_query) {                  // no calibration: lambda = 0
+    if (sg == 0 && t == 0) {
+      a.lambda_ws[b * a.Hkv + h] = 0.f;
+      if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = 0.f;
+    }
+    return;
+  }
+  // the segment's top-Mc of B, in ascending position
+  const int Mc = st.mc[b];
+  const int64_t slot0 = (int64_t)h * a.cand_stride + st.cand_base[b] + (int64_t)sg * Mc;
+  {
+    auto keyB = [&](int j) -> unsigned { return t + j * NT < ncand ? float_key(xb[j]) : 0u; };
+    auto posf = [&](int j) -> int { return i0 + t + j * NT; };
+    uint32_t msk = 0;
+    if (ncand <= Mc) {
+#pragma unroll
+      for (int j = 0; j < PER; ++j) msk |= (t + j * NT < ncand ? 1u : 0u) << j;
+    } else {
+      unsigned xm;
+      int pm;
+      block_threshold<PER>(keyB, posf, Mc, xm, pm, ss, ckey, cpos);
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const unsigned kj = keyB(j);
+        msk |= (kj > xm || (kj == xm && posf(j) <= pm) ? 1u : 0u) << j;
+      }
+    }
+    ordered_bases<PER, NT>(msk, pre);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const bool in = (msk >> j) & 1u;
+      const uint64_t m = __ballot(in);
+      if (in) {
+        const int64_t o = slot0 + pre[j * NW + wave] + lane_rank(m);
+        a.cand_key[o] = float_key(xb[j]);
+        a.cand_pos[o] = posf(j);
+        a.cand_v[o] = xv[j];
+      }
+    }
+    for (int q = min(ncand, Mc) + t; q < Mc; q += NT) a.cand_key[slot0 + q] = 0u;   // empty slots
+  }
+  if (!last_arrival(a.counter + b * a.Hkv + h, (unsigned)nseg, ss)) return;
+
+  // last workgroup: top-M of B over the union, moments, lambda
+  const int U = nseg * Mc;                          // <= kUnionCap (host check)
+  const int64_t c0 = (int64_t)h * a.cand_stride + st.cand_base[b];
+  unsigned ck[kUnionPer];
+  int cp[kUnionPer];
+  float cv[kUnionPer];
+  {
+    const int tt = opaque(t);
+#pragma unroll
+    for (int j = 0; j < kUnionPer; ++j) {
+      const int q = min(tt + j * NT, U - 1);
+      ck[j] = a.cand_key[c0 + q];
+      cp[j] = a.cand_pos[c0 + q];
+      cv[j] = a.cand_v[c0 + q];
+    }
+#pragma unroll
+    for (int j = 0; j < kUnionPer; ++j) if (tt + j * NT >= U) ck[j] = 0u;
+  }
+  auto keyU = [&](int j) -> unsigned { return ck[j]; };
+  auto posU = [&](int j) -> int { return cp[j]; };
+  unsigned xm;
+  int pm;
+  block_threshold<kUnionPer>(keyU, posU, M, xm, pm, ss, ckey, cpos);
+  uint32_t inm = 0;
+#pragma unroll
+  for (int j = 0; j < kUnionPer; ++j)
+    inm |= (ck[j] > xm || (ck[j] == xm && ck[j] != 0u && cp[j] <= pm) ? 1u : 0u) << j;
+  // population moments over the set in double; B shifted by the set minimum
+  unsigned kmin = 0xffffffffu;
+#pragma unroll
+  for (int j = 0; j < kUnionPer; ++j) kmin = ((inm >> j) & 1u) ? min(kmin, ck[j]) : kmin;
+  kmin = block_reduce_u<0>(kmin, ss);
+  const double bref = (double)key_float(kmin);
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+#pragma unroll
+  for (int j = 0; j < kUnionPer; ++j) {
+    const bool in = (inm >> j) & 1u;
+    const double db = in ? (double)key_float(ck[j]) - bref : 0.0, dv = in ? (double)cv[j] : 0.0;
+    s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
+  }
+  double sums[4];
+  block_sum4_d(s0, s1, s2, s3, ss, sums);
+  const double mb = sums[0] / M, mv = sums[2] / M;
+  double vb = sums[1] / M - mb * mb, vv = sums[3] / M - mv * mv;
+  vb = vb > 0.0 ? vb : 0.0;
+  vv = vv > 0.0 ? vv : 0.0;
+  const float lam = (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));
+  if (t == 0) {
+    a.lambda_ws[b * a.Hkv + h] = lam;
+    if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = lam;
+  }
+}
+
+// Top-K kernel.  Each segment takes its top-min(K, kSegLen) of the pooled
+// score pB + lambda pV over I; the last workgroup of a (sequence, KV head)
+// takes the exact top-K over the union (Eq. topk_selection, ties to the lower
+// position) and writes the indices in ascending position, -1 beyond |I|.
+__global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
+  constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
+  __shared__ unsigned ckey[kCandCap];
+  __shared__ int cpos[kCandCap];
+  __shared__ SelSharedT<NT> ss;
+  __shared__ unsigned pre[kUnionPer * NW];
+  const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
+  const int wave = t >> 6;
+  const int b = find_seg(st, gs);
+  const int sg = gs - st.seg_base[b];
+  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
+  const int n = st.cu[b + 1] - st.cu[b];
+  const int nc = n - a.W;
+  const int i0 = sg * kSegLen;
+  const int K = st.budget[b];
+  const int kept = min(K, nc);
+  const int Kc = min(K, kSegLen);
+  const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
+  int cb = 0;                                        // first slot of the sequence
+  for (int x = 0; x < b; ++x) cb += (st.seg_base[x + 1] - st.seg_base[x]) * min(st.budget[x], kSegLen);
+  const int64_t c0 = (int64_t)h * a.cand_stride + cb;
+  const float lam = a.lambda_ws[b * a.Hkv + h];
+
+  {
+    const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
+    float pb[PER], pv[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      pb[j] = a.vec_pB[tile + t + j * NT];
+      pv[j] = a.vec_pV[tile + t + j * NT];
+    }
+    unsigned key[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      key[j] = t + j * NT < ncand ? float_key(fmaf(lam, pv[j], pb[j])) : 0u;
+    auto keyS = [&](int j) -> unsigned { return key[j]; };
+    auto posf = [&](int j) -> int { return i0 + t + j * NT; };
+    uint32_t msk = 0;
+    if (ncand <= Kc) {
+#pragma unroll
+      for (int j = 0; j < PER; ++j) msk |= (t + j * NT < ncand ? 1u : 0u) << j;
+    } else {
+      unsigned xk;
+      int pk;
+      block_threshold<PER>(keyS, posf, Kc, xk, pk, ss, ckey, cpos);
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        msk |= (key[j] > xk || (key[j] == xk && posf(j) <= pk) ? 1u : 0u) << j;
+    }
+    const int64_t slot0 = c0 + (int64_t)sg * Kc;
+    ordered_bases<PER, NT>(msk, pre);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const bool in = (msk >> j) & 1u;
+      const uint64_t m = __ballot(in);
+      if (in) {
+        const int64_t o = slot0 + pre[j * NW + wave] + lane_rank(m);
+        a.cand_key[o] = key[j];
+        a.cand_pos[o] = posf(j);
+      }
+    }
+    for (int q = min(ncand, Kc) + t; q < Kc; q += NT) a.cand_key[slot0 + q] = 0u;
+  }
+  if (!last_arrival(a.counter + b * a.Hkv + h, (unsigned)nseg, ss)) return;
+
+  // last workgroup: exact top-K over the union (held in ascending position)
+  int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
+  if (kept > 0) {
+    const int U = nseg * Kc;                        // <= kUnionCap (host check)
+    unsigned ck[kUnionPer];
+    int cp[kUnionPer];
+    {
+      const int tt = opaque(t);
+#pragma unroll
+      for (int j = 0; j < kUnionPer; ++j) {
+        const int q = min(tt + j * NT, U - 1);
+        ck[j] = a.cand_key[c0 + q];
+        cp[j] = a.cand_pos[c0 + q];
+      }
+#pragma unroll
+      for (int j = 0; j < kUnionPer; ++j) if (tt + j * NT >= U) ck[j] = 0u;
+    }
+    uint32_t msk = 0;
+    if (kept == nc) {
+#pragma unroll
+      for (int j = 0; j < kUnionPer; ++j) msk |= (ck[j] != 0u ? 1u : 0u) << j;
+    } else {
+      auto keyU = [&](int j) -> unsigned { return ck[j]; };
+      auto posU = [&](int j) -> int { return cp[j]; };
+      unsigned xk;
+      int pk;
+      block_threshold<kUnionPer>(keyU, posU, kept, xk, pk, ss, ckey, cpos);
+#pragma unroll
+      for (int j = 0; j < kUnionPer; ++j)
+        msk |= (ck[j] > xk || (ck[j] == xk && ck[j] != 0u && cp[j] <= pk) ? 1u : 0u) << j;
+    }
+    // emission in slot order, which is ascending position
+    ordered_bases<kUnionPer, NT>(msk, pre);
+#pragma unroll
+    for (int j = 0; j < kUnionPer; ++j) {
+      const bool in = (msk >> j) & 1u;
+      const uint64_t m = __ballot(in);
+      if (in) idx[pre[j * NW + wave] + lane_rank(m)] = cp[j];
+    }
+  }
+  for (int j = max(kept, 0) + t; j < K; j += NT) idx[j] = -1;
+}
+
+hipError_t launch_sega(const SegArgs &a, const SeqTable &st, hipStream_t s) {
+  dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
+  hipLaunchKernelGGL(k_sega, grid, block, 0, s, a, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_segb(const SegArgs &a, const SeqTable &st, hipStream_t s) {
+  dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
+  hipLaunchKernelGGL(k_segb, grid, block, 0, s, a, st);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void k_zero_u32(unsigned *p, int count) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) p[i] = 0u;
+}
+
+hipError_t launch_zero_u32(unsigned *p, int count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero_u32, dim3((count + 255) / 256), dim3(256), 0, s, p, count);
   return hipGetLastError();
 }
 
@@ -1108,6 +1583,11 @@ hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------- compaction
+// Rows of the compacted cache of a (sequence, KV head): the kept positions of
+// idx, the W window rows, then zero rows up to K + W.  Each thread moves
+// kCompactPer 16-byte pieces of K and V, all loads issued before the stores.
+constexpr int kCompactPer = 2;
+
 __global__ __launch_bounds__(256) void k_compact(CompactArgs a, SeqTable st) {
   const int b = blockIdx.x, h = blockIdx.y;
   const int n = st.cu[b + 1] - st.cu[b];
@@ -1117,33 +1597,49 @@ __global__ __launch_bounds__(256) void k_compact(CompactArgs a, SeqTable st) {
   const int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
   const int pieces = a.row_bytes / 16;
   const int total = (K + a.W) * pieces;
+  const int q0 = blockIdx.z * (256 * kCompactPer) + threadIdx.x;
+  if (q0 >= total) return;
   const unsigned char *ks = static_cast<const unsigned char *>(a.k);
   const unsigned char *vs = static_cast<const unsigned char *>(a.v);
   unsigned char *ko = static_cast<unsigned char *>(a.k_out);
   unsigned char *vo = static_cast<unsigned char *>(a.v_out);
-  for (int q = blockIdx.z * blockDim.x + threadIdx.x; q < total; q += gridDim.z * blockDim.x) {
-    const int r = q / pieces, p = q - r * pieces;
-    int src = -1;
-    if (r < kept) {
-      src = idx[r];
-      if (src < 0 || src >= n) src = -1;
-    } else if (r < kept + a.W) {
-      src = nc + (r - kept);
+  int src[kCompactPer];
+#pragma unroll
+  for (int u = 0; u < kCompactPer; ++u) {
+    const int q = min(q0 + 256 * u, total - 1);
+    const int r = q / pieces;
+    const int s = idx[min(r, max(kept - 1, 0))];
+    src[u] = r < kept ? ((s >= 0 && s < n) ? s : -1) : (r < kept + a.W ? nc + (r - kept) : -1);
+  }
+  u32x4 kv[kCompactPer], vv[kCompactPer];
+#pragma unroll
+  for (int u = 0; u < kCompactPer; ++u) {
+    const int q = min(q0 + 256 * u, total - 1);
+    const int p = q - (q / pieces) * pieces;
+    const int64_t so = ((int64_t)(st.cu[b] + max(src[u], 0)) * a.Hkv + h) * a.row_bytes + 16 * p;
+    kv[u] = *reinterpret_cast<const u32x4 *>(ks + so);
+    vv[u] = *reinterpret_cast<const u32x4 *>(vs + so);
+  }
+#pragma unroll
+  for (int u = 0; u < kCompactPer; ++u) {
+    const int q = q0 + 256 * u;
+    if (q < total) {
+      const int r = q / pieces, p = q - r * pieces;
+      const int64_t dst = ((int64_t)(st.kept_base[b] + r) * a.Hkv + h) * a.row_bytes + 16 * p;
+      const u32x4 z = u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4 *>(ko + dst) = src[u] >= 0 ? kv[u] : z;
+      *reinterpret_cast<u32x4 *>(vo + dst) = src[u] >= 0 ? vv[u] : z;
     }
-    const int64_t dst = ((int64_t)(st.kept_base[b] + r) * a.Hkv + h) * a.row_bytes + 16 * p;
-    u32x4 kv = u32x4{0u, 0u, 0u, 0u}, vv = u32x4{0u, 0u, 0u, 0u};
-    if (src >= 0) {
-      const int64_t so = ((int64_t)(st.cu[b] + src) * a.Hkv + h) * a.row_bytes + 16 * p;
-      kv = *reinterpret_cast<const u32x4 *>(ks + so);
-      vv = *reinterpret_cast<const u32x4 *>(vs + so);
-    }
-    *reinterpret_cast<u32x4 *>(ko + dst) = kv;
-    *reinterpret_cast<u32x4 *>(vo + dst) = vv;
   }
 }
 
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s) {
-  dim3 grid(st.batch, a.Hkv, 4), block(256);
+  int kmax = 0;
+  for (int b = 0; b < st.batch; ++b) kmax = max(kmax, st.budget[b]);
+  const int64_t total = (int64_t)(kmax + a.W) * (a.row_bytes / 16);
+  const int z = (int)((total + 256 * kCompactPer - 1) / (256 * kCompactPer));
+  if (z <= 0) return hipSuccess;
+  dim3 grid(st.batch, a.Hkv, z), block(256);
   hipLaunchKernelGGL(k_compact, grid, block, 0, s, a, st);
   return hipGetLastError();
 }

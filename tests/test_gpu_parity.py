@@ -89,15 +89,20 @@ def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=No
             torch.cuda.synchronize()
             gi = idx.cpu().numpy()
             s = P.check_idx(f"{name} L{layer} fused", gi, r, wl, rtol)
-            for key in stats:
+            for key in ("pairs", "strict", "swaps"):
                 stats[key] += s[key]
             assert np.array_equal(P.tensor_bytes(ko), P.gather_rows(kb, gi, wl)), "K gather"
             assert np.array_equal(P.tensor_bytes(vo), P.gather_rows(vb, gi, wl)), "V gather"
             if idx_split is not None:
-                assert np.array_equal(gi, idx_split), "fused and split paths disagree"
+                # both paths are checked against the oracle above; they round
+                # pooling differently (pool(S) against pool(B) + lambda pool(V)),
+                # so they may swap keys whose scores tie within the tolerance
+                stats["fused_split_diff"] = stats.get("fused_split_diff", 0) + int(
+                    np.count_nonzero(gi != idx_split))
         del q, k, v
     P.log(f"[{name}] ok; worst rel err {worst}; kept sets strict {stats['strict']}/"
-          f"{stats['pairs']}, swaps {stats['swaps']}")
+          f"{stats['pairs']}, swaps {stats['swaps']}, fused/split index differences "
+          f"{stats.get('fused_split_diff', 0)}")
     return worst, stats
 
 
@@ -138,6 +143,21 @@ EDGE = {
     "gamma-rho": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 7, "bf16", (1000, 700),
                                          (64, 300), ((30, 800), (30, 600)), 3, 16),
                       gpu=dict(gamma=0.5, rho=3.0), orc=dict(gamma=0.5, rho=3.0)),
+    # widest pool (33) and coherence radius (16) over several select segments,
+    # sequence ends inside a segment and inside the pool halo
+    "pool33-r16-segments": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 33, "bf16",
+                                                   (5000, 2070, 4111), (100, 40, 700),
+                                                   ((30, 4000), (0, 2000), (100, 4000)), 4, 17),
+                                gpu=dict(radius=16), orc=dict(radius=16)),
+    # scale-matching set larger than a segment (every segment position is a
+    # candidate) and a budget above half the candidate set
+    "M-over-segment": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 7, "bf16", (8000,),
+                                              (1500,), ((30, 7000),), 4, 18)),
+    # candidate unions beyond one workgroup: one select workgroup per
+    # (sequence, KV head) over the whole sequence
+    "large-budget-whole-sequence": dict(wl=inputs.Workload("edge", 2, 8, 2, 128, 32, 7, "bf16",
+                                                           (20000, 3000), (3000, 200),
+                                                           ((30, 19000), (10, 2500)), 4, 19)),
 }
 
 
