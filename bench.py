@@ -15,7 +15,6 @@ sample of the same workload.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -27,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+COPY_BYTES = 1 << 30          # plain copy of the counter calibration (read once, written once)
 METRIC = "KV compression pass ms/layer + keys scored/sec; HBM GB/s vs peak at N=32K"
 
 
@@ -53,26 +53,24 @@ def algorithmic_bytes(wl, persist_m=4):
 
 
 def kernel_bytes(name, wl, persist_m=4):
-    """Algorithmic bytes of one launch of a kernel of the fused pass (mean over layers)."""
+    """Algorithmic bytes of one launch of a kernel of the fused pass (mean over
+    layers): what the kernel must read and write at minimum in this design."""
     ab = algorithmic_bytes(wl, persist_m)
     T, Hkv = wl.total_tokens, wl.num_kv_heads
-    if name == "window_lse":
+    vec = T * Hkv * 4                                   # one fp32 value per (position, KV head)
+    ring = float(np.mean([(min(persist_m, l) + 1) * vec for l in range(wl.num_layers)]))
+    kept_rows = sum(b + wl.window for b in wl.budgets)
+    if name == "window_lse":                            # K, Q_win
         return ab["k"] + ab["q"]
-    if name == "window_score_calib":
-        ring = np.mean([(min(persist_m, l) + 1) * T * Hkv * 4 for l in range(wl.num_layers)])
-        return ab["k"] + ab["q"] + ring + 2 * T * Hkv * 4
-    if name == "select_fused":
-        kept_rows = sum(b + wl.window for b in wl.budgets)
-        return 3 * T * Hkv * 4 + 4 * kept_rows * Hkv * wl.head_dim * wl.elem_size
+    if name == "window_score_calib":                    # K, Q_win, E history, B and E+T+L out
+        return ab["k"] + ab["q"] + ring + 2 * vec
+    if name == "segment_lambda":                        # B, E+T+L in; pooled B, V out
+        return 4 * vec
+    if name == "segment_topk":                          # pooled B, V in; indices out
+        return 2 * vec + 4 * sum(wl.budgets) * Hkv
+    if name == "compact":                               # kept + window rows of K and V, in and out
+        return 2 * 2 * kept_rows * Hkv * wl.head_dim * wl.elem_size + 4 * sum(wl.budgets) * Hkv
     return 0.0
-
-
-def source_sha():
-    h = hashlib.sha256()
-    for f in ("kernels.hip", "internal.h"):
-        with open(os.path.join(ROOT, "paper_2606_14782_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel):
@@ -85,6 +83,7 @@ def measured_traffic(kernel):
         rec = json.load(open(path))
     except Exception:
         return None
+    from paper_2606_14782_amd.counters import source_sha
     if rec.get("source_sha") != source_sha():
         return None
     k = rec.get("kernels", {}).get(kernel)
@@ -126,6 +125,9 @@ def main():
     ap.add_argument("--workload", type=int, default=3, help="workload index (default: 32K video)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain fp32 copy of COPY_BYTES (read and written once) whose "
+                         "HBM counters scale the kernels' counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the pass shards "
@@ -145,6 +147,8 @@ def main():
     tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     for l in range(wl.num_layers):
         x = inputs.layer_inputs(wl, l)
+        if l % 8 == 7:
+            log(f"  layer {l + 1}/{wl.num_layers} generated")
         qs.append(torch.from_numpy(x["q_win"]).to(dev).to(tdt))
         ks.append(torch.from_numpy(x["k"]).to(dev).to(tdt))
         vs.append(torch.from_numpy(x["v"]).to(dev).to(tdt))
@@ -162,6 +166,16 @@ def main():
         ctx.bacon_begin_prompt(batch)
         for l in range(wl.num_layers):
             ctx.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l], out=outs[l])
+
+    if args.copy_calibration:
+        n = COPY_BYTES // 4
+        src = torch.randn(n, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"copy calibration: {COPY_BYTES} bytes read and written, 3 launches")
 
     log("warmup")
     for _ in range(args.warmup):
@@ -211,7 +225,8 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl.dtype,
-        "data": "synthetic (seeded N(0,1) Q/K/V with frame-periodic low-rank K), random",
+        "data": "synthetic: seeded N(0,1) Q/K/V, frame-periodic low-rank K component, "
+                "planted query-aligned evidence keys (no checkpoint or dataset)",
         "config": {"workload": f"{wl.name}: {wl.num_layers} layers, {wl.num_q_heads}/"
                                f"{wl.num_kv_heads} heads, d={wl.head_dim}, N="
                                f"{wl.seq_lens[0] if wl.batch == 1 else list(wl.seq_lens)}, "

@@ -1,0 +1,135 @@
+"""HBM traffic per kernel launch from rocprofv3 counter runs.
+
+Reads the counter-collection CSVs of two `rocprofv3 --pmc FETCH_SIZE` and
+`rocprofv3 --pmc WRITE_SIZE` runs of `bench.py --copy-calibration`, scales
+each kernel's mean counter (KiB per dispatch) by what the same counter reads
+for the plain copy of a known size in the same run, and writes the result
+(with the hash of the kernel sources it was taken on) for bench.py:
+
+    python -m paper_2606_14782_amd.counters --fetch DIR --write DIR \
+        --out profiles/traffic.json --md profiles/traffic_<workload>.md
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import re
+from collections import defaultdict
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+COPY_BYTES = 1 << 30
+
+# demangled kernel name -> name used by the library's own timing
+_NAMES = [
+    (r"bacon::k_pass<0,", "window_lse"),
+    (r"bacon::k_pass<1,", "window_score"),
+    (r"bacon::k_pass<2,", "window_score_calib"),
+    (r"bacon::k_sega\b", "segment_lambda"),
+    (r"bacon::k_segb\b", "segment_topk"),
+    (r"bacon::k_compact\b", "compact"),
+    (r"bacon::k_zero_u32\b", "zero"),
+    (r"bacon::k_select<0>", "select_fused"),
+    (r"bacon::k_select<1>", "select_calib"),
+    (r"bacon::k_select<2>", "select_topk"),
+    (r"bacon::k_elem\b", "calib_elem"),
+]
+
+
+def source_sha() -> str:
+    """Hash of the kernel sources; counters taken on other sources are stale."""
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "internal.h"):
+        with open(os.path.join(HERE, "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def library_name(kernel: str) -> str | None:
+    for pat, name in _NAMES:
+        if re.search(pat, kernel):
+            return name
+    return None
+
+
+def _rows(d: str):
+    files = sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True))
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    for f in files:
+        with open(f, newline="") as fh:
+            yield from csv.DictReader(fh)
+
+
+def per_kernel(d: str, counter: str):
+    """Mean counter value per dispatch (KiB) for each kernel name."""
+    acc = defaultdict(list)
+    for r in _rows(d):
+        if r.get("Counter_Name") != counter:
+            continue
+        acc[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
+
+
+def copy_kib(stats) -> float:
+    """Counter of the calibration copy: torch's elementwise multiply by 1."""
+    cands = [(v, k) for k, (v, n) in stats.items() if "Mul" in k and library_name(k) is None]
+    if not cands:
+        raise SystemExit("calibration copy kernel not found (run bench.py --copy-calibration)")
+    return max(cands)[0]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--md", required=True)
+    ap.add_argument("--command", default="")
+    args = ap.parse_args()
+    fs, ws = per_kernel(args.fetch, "FETCH_SIZE"), per_kernel(args.write, "WRITE_SIZE")
+    ffac = COPY_BYTES / (copy_kib(fs) * 1024.0)
+    wfac = COPY_BYTES / (copy_kib(ws) * 1024.0)
+    kernels = {}
+    for k in sorted(set(fs) | set(ws)):
+        name = library_name(k)
+        if name is None:
+            continue
+        fb = fs.get(k, (0.0, 0))[0] * 1024.0 * ffac
+        wb = ws.get(k, (0.0, 0))[0] * 1024.0 * wfac
+        e = kernels.setdefault(name, {"fetch_bytes": 0.0, "write_bytes": 0.0, "dispatches": 0,
+                                      "variants": []})
+        n = fs.get(k, (0, 0))[1]
+        # several template instances of one library name: dispatch-weighted mean
+        tot = e["dispatches"] + n
+        if tot:
+            e["fetch_bytes"] = (e["fetch_bytes"] * e["dispatches"] + fb * n) / tot
+            e["write_bytes"] = (e["write_bytes"] * e["dispatches"] + wb * n) / tot
+        e["dispatches"] = tot
+        e["variants"].append(k)
+    for e in kernels.values():
+        e["bytes_per_launch"] = e["fetch_bytes"] + e["write_bytes"]
+    rec = {"source_sha": source_sha(), "copy_bytes": COPY_BYTES,
+           "copy_factor": {"fetch": ffac, "write": wfac}, "command": args.command,
+           "kernels": kernels}
+    with open(args.out, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    lines = [f"# HBM traffic per launch (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
+             f"kernel sources: {rec['source_sha']}", "",
+             f"command: `{args.command}`", "",
+             f"copy calibration: {COPY_BYTES} B read + written; counter scale factors "
+             f"fetch {ffac:.4f}, write {wfac:.4f}", "",
+             "| kernel | dispatches | fetch MB | write MB | total MB |", "|---|---|---|---|---|"]
+    for name, e in sorted(kernels.items()):
+        lines.append(f"| {name} | {e['dispatches']} | {e['fetch_bytes'] / 1e6:.2f} | "
+                     f"{e['write_bytes'] / 1e6:.2f} | {e['bytes_per_launch'] / 1e6:.2f} |")
+    with open(args.md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+if __name__ == "__main__":
+    main()

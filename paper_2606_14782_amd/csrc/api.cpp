@@ -657,7 +657,8 @@ bacon_status bacon_profile_enable(bacon_ctx *c, int32_t enable) {
   if (enable && c->ev_pool.empty()) {
     c->ev_pool.resize(16384);
     for (auto &e : c->ev_pool) {
-      const hipError_t r = hipEventCreate(&e);
+      // timing-only events: no system-scope cache write-back when recorded
+      const hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
       if (r != hipSuccess) return hip_fail(r, "hipEventCreate");
     }
   }

@@ -18,12 +18,18 @@
 //    appends E to the history, and adds the part of L = P_r E
 //    (Eq. intra_layer_coherence) whose neighbours lie inside the chunk.
 //
-// The select kernel (one workgroup per (sequence, KV head)) completes L at
-// chunk boundaries, forms V (Eq. structurally_calibrated_evidence), selects the
-// scale-matching set and computes lambda (Eqs. scale_matching_set,
-// lambda_solution), S (Eq. bacon_score), the pooled score and the top-K
-// (Eq. topk_selection), emits the kept positions in ascending order and
-// gathers the compacted cache.
+// The fused pass selects in two segment kernels (one workgroup per kSegLen
+// positions and KV head).  The first completes L at chunk boundaries, forms V
+// (Eq. structurally_calibrated_evidence), pools B and V, and keeps each
+// segment's top of B; the workgroup that finishes last for a (sequence, KV
+// head) selects the scale-matching set over the union and computes lambda
+// (Eqs. scale_matching_set, lambda_solution).  The second keeps each segment's
+// top of the pooled S = B + lambda V (Eq. bacon_score); its last workgroup
+// takes the top-K over the union (Eq. topk_selection) and writes the kept
+// positions in ascending order; the compaction kernel gathers the cache.
+// One workgroup per (sequence, KV head) runs the same steps over the whole
+// sequence for the split calls and for budgets whose candidate unions exceed
+// one workgroup.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
