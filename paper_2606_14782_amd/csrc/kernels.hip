@@ -448,36 +448,52 @@ struct SelSharedT {
   int bc_i[4];
 };
 
-// Wave-wide reductions: xor butterflies inside each 32-lane half with
-// ds_swizzle (immediate lane pattern, no index registers), then the two
-// halves combined through readlane.  Every lane gets the result.
+// Xor lane exchange inside each 32-lane half through ds_swizzle (immediate
+// pattern, no index registers).
 template <int X>
 __device__ __forceinline__ unsigned swz(unsigned v) {
   return (unsigned)__builtin_amdgcn_ds_swizzle((int)v, (X << 10) | 0x1f);
 }
+
+// Wave-wide scans and reductions through DPP lane moves (GFX9 encodings):
+// row_shr:n (0x110 + n) shifts lanes by n inside each 16-lane row,
+// row_bcast:15 (0x142) copies lane 15 of a row into the next row and
+// row_bcast:31 (0x143) lane 31 into rows 2 and 3.  Lanes with no source, or
+// outside the row mask, receive `id`.  After the six steps lane i holds the
+// inclusive scan over lanes 0..i; lane 63 the whole wave.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ unsigned dpp_u(unsigned id, unsigned v) {
+  return (unsigned)__builtin_amdgcn_update_dpp((int)id, (int)v, CTRL, ROWS, 0xf, false);
+}
 template <typename Op>
-__device__ __forceinline__ unsigned wave_reduce_u(unsigned v, Op op) {
-  v = op(v, swz<1>(v));
-  v = op(v, swz<2>(v));
-  v = op(v, swz<4>(v));
-  v = op(v, swz<8>(v));
-  v = op(v, swz<16>(v));
-  return op((unsigned)__builtin_amdgcn_readlane((int)v, 0), (unsigned)__builtin_amdgcn_readlane((int)v, 32));
+__device__ __forceinline__ unsigned wave_scan_u(unsigned v, unsigned id, Op op) {
+  v = op(v, dpp_u<0x111, 0xf>(id, v));
+  v = op(v, dpp_u<0x112, 0xf>(id, v));
+  v = op(v, dpp_u<0x114, 0xf>(id, v));
+  v = op(v, dpp_u<0x118, 0xf>(id, v));
+  v = op(v, dpp_u<0x142, 0xa>(id, v));
+  v = op(v, dpp_u<0x143, 0xc>(id, v));
+  return v;
+}
+__device__ __forceinline__ unsigned lane63_u(unsigned v) {
+  return (unsigned)__builtin_amdgcn_readlane((int)v, 63);
+}
+// inclusive prefix sum over the lanes of the wave
+__device__ __forceinline__ unsigned wave_incl_sum_u(unsigned v) {
+  return wave_scan_u(v, 0u, [](unsigned x, unsigned y) { return x + y; });
 }
 __device__ __forceinline__ unsigned wave_min_u(unsigned v) {
-  return wave_reduce_u(v, [](unsigned x, unsigned y) { return min(x, y); });
+  return lane63_u(wave_scan_u(v, 0xffffffffu, [](unsigned x, unsigned y) { return min(x, y); }));
 }
 __device__ __forceinline__ unsigned wave_max_u(unsigned v) {
-  return wave_reduce_u(v, [](unsigned x, unsigned y) { return max(x, y); });
+  return lane63_u(wave_scan_u(v, 0u, [](unsigned x, unsigned y) { return max(x, y); }));
 }
-__device__ __forceinline__ unsigned wave_sum_u(unsigned v) {
-  return wave_reduce_u(v, [](unsigned x, unsigned y) { return x + y; });
-}
-template <int X>
-__device__ __forceinline__ double swz_d(double v) {
+__device__ __forceinline__ unsigned wave_sum_u(unsigned v) { return lane63_u(wave_incl_sum_u(v)); }
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_d(double v) {
   const unsigned long long u = __double_as_longlong(v);
-  const unsigned lo = swz<X>((unsigned)u), hi = swz<X>((unsigned)(u >> 32));
-  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+  const unsigned lo = dpp_u<CTRL, ROWS>(0u, (unsigned)u), hi = dpp_u<CTRL, ROWS>(0u, (unsigned)(u >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));   // 0 bits = +0.0
 }
 __device__ __forceinline__ double readlane_d(double v, int l) {
   const unsigned long long u = __double_as_longlong(v);
@@ -485,13 +501,15 @@ __device__ __forceinline__ double readlane_d(double v, int l) {
   const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(u >> 32), l);
   return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
+// sum over the wave in a fixed order
 __device__ __forceinline__ double wave_sum_d(double v) {
-  v += swz_d<1>(v);
-  v += swz_d<2>(v);
-  v += swz_d<4>(v);
-  v += swz_d<8>(v);
-  v += swz_d<16>(v);
-  return readlane_d(v, 0) + readlane_d(v, 32);
+  v += dpp_d<0x111, 0xf>(v);
+  v += dpp_d<0x112, 0xf>(v);
+  v += dpp_d<0x114, 0xf>(v);
+  v += dpp_d<0x118, 0xf>(v);
+  v += dpp_d<0x142, 0xa>(v);
+  v += dpp_d<0x143, 0xc>(v);
+  return readlane_d(v, 63);
 }
 
 // Block-wide min (OP 0) / max (1) / sum (2) of unsigned values.
@@ -534,12 +552,7 @@ __device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, do
 template <int NT>
 __device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelSharedT<NT> &ss) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  unsigned x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const unsigned y = (unsigned)__shfl_up((int)x, o);
-    if (lane >= o) x += y;
-  }
+  const unsigned x = wave_incl_sum_u(v);
   if (lane == 63) ss.red_u[wave] = x;
   __syncthreads();
   unsigned before = 0;
@@ -572,13 +585,10 @@ __device__ __forceinline__ void hist_boundary(int need, SelSharedT<NT> &ss) {
   unsigned c = 0;
 #pragma unroll
   for (int q = 0; q < BPT; ++q) { cb[q] = ss.hist[BPT * t + q]; c += cb[q]; }
-  unsigned suf = c;                    // inclusive suffix sum within the wave
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const unsigned y = (unsigned)__shfl_down((int)suf, o);
-    if (lane + o < 64) suf += y;
-  }
-  if (lane == 0) ss.red_u[wave] = suf;   // wave total
+  const unsigned pre = wave_incl_sum_u(c);
+  const unsigned tot = lane63_u(pre);
+  unsigned suf = tot - pre + c;        // inclusive suffix sum within the wave
+  if (lane == 0) ss.red_u[wave] = tot;
   __syncthreads();
   unsigned higher = 0;                 // counted elements in later waves
 #pragma unroll
@@ -1186,13 +1196,7 @@ __device__ __forceinline__ void ordered_bases(uint32_t msk, unsigned *pre) {
       x[e] = (lane * E + e < NE) ? pre[lane * E + e] : 0u;
       s += x[e];
     }
-    unsigned inc = s;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const unsigned y = (unsigned)__shfl_up((int)inc, o);
-      if (lane >= o) inc += y;
-    }
-    unsigned ex = inc - s;
+    unsigned ex = wave_incl_sum_u(s) - s;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       if (lane * E + e < NE) pre[lane * E + e] = ex;
