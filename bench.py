@@ -64,11 +64,14 @@ def kernel_bytes(name, wl, persist_m=4):
         return ab["k"] + ab["q"]
     if name == "window_score_calib":                    # K, Q_win, E history, B and E+T+L out
         return ab["k"] + ab["q"] + ring + 2 * vec
-    if name == "segment_lambda":                        # B, E+T+L in; pooled B, V out
+    if name == "lse_merge":                             # per-chunk (max, sum) partials
+        chunks = T / 512 + wl.batch
+        return Hkv * chunks * wl.group * wl.window * 8
+    if name == "segment_calib":                         # B, E+T+L in; pooled B, V out
         return 4 * vec
-    if name == "segment_topk":                          # pooled B, V in; indices out
-        return 2 * vec + 4 * sum(wl.budgets) * Hkv
-    if name == "compact":                               # kept + window rows of K and V, in and out
+    if name == "segment_topk":                          # pooled B, V in
+        return 2 * vec
+    if name == "final_topk":                            # kept + window rows of K and V, in and out
         return 2 * 2 * kept_rows * Hkv * wl.head_dim * wl.elem_size + 4 * sum(wl.budgets) * Hkv
     return 0.0
 

@@ -36,8 +36,8 @@ bacon_status hip_fail(hipError_t e, const char *what) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ring, vec_b, vec_vp, vec_pb, vec_pv, cand_key, cand_pos, cand_v, partials, lambda, counter,
-      total;
+  size_t ring, vec_b, vec_vp, vec_pb, vec_pv, cand_key, cand_pos, cand_v, cand2_key, cand2_pos,
+      partials, lse2, lambda, total;
   int64_t cand_stride;
   int rpad, slots, ring_mp;
   int64_t chunks_cap;
@@ -107,19 +107,20 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.cand_key = off; off += align256(cand);
   L.cand_pos = off; off += align256(cand);
   L.cand_v = off;   off += align256(cand);
+  L.cand2_key = off; off += align256(cand);
+  L.cand2_pos = off; off += align256(cand);
   L.partials = off; off += align256((size_t)s->num_kv_heads * L.chunks_cap * L.rpad * sizeof(float2));
+  L.lse2 = off;     off += align256((size_t)s->max_batch * s->num_kv_heads * L.rpad * sizeof(float));
   L.lambda = off;   off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(float));
-  L.counter = off;  off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(unsigned));
   L.total = off;
   return L;
 }
 
-const char *kKernelNames[] = {"window_lse",     "window_score",   "window_score_calib",
-                              "segment_lambda", "segment_topk",   "select_fused",
-                              "select_calib",   "select_topk",    "calib_elem",
-                              "compact",        "zero"};
-enum KernelId { KI_LSE, KI_SCORE, KI_FUSED, KI_SEGA, KI_SEGB, KI_SEL_FUSED, KI_SEL_CALIB,
-                KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_ZERO, KI_COUNT };
+const char *kKernelNames[] = {"window_lse",    "lse_merge",   "window_score", "window_score_calib",
+                              "segment_calib", "segment_topk", "final_topk",  "select_fused",
+                              "select_calib",  "select_topk",  "calib_elem",  "compact"};
+enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGA, KI_SEGB, KI_FINAL, KI_SEL_FUSED,
+                KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_COUNT };
 
 }  // namespace
 
@@ -280,6 +281,7 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   a.T = s.max_total_tokens;
   a.c2 = (float)(1.4426950408889634 / std::sqrt((double)s.head_dim));
   a.partials = reinterpret_cast<float2 *>(c->ws + c->L.partials);
+  a.lse2 = reinterpret_cast<float *>(c->ws + c->L.lse2);
   a.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
   a.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
   a.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
@@ -332,6 +334,7 @@ bool segmented_select(const bacon_ctx *c, const bacon_batch *bt) {
     M = std::max(0, std::min(M, nc));
     if ((int64_t)nseg * std::min(M, kSegLen) > kUnionCap) return false;
     if ((int64_t)nseg * std::min(bt->budgets[b], kSegLen) > kUnionCap) return false;
+    if (final_lds_bytes(bt->budgets[b], c->shape.window) > (size_t)kLdsBytes) return false;
   }
   return true;
 }
@@ -422,12 +425,8 @@ bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *strea
   c->budgets.assign(bt->budgets, bt->budgets + bt->batch);
   c->prompt = true;
   c->next_layer = 0;
-  // arrival counters of the segment kernels start at zero (layer 0 reads no history)
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  unsigned *cnt = reinterpret_cast<unsigned *>(c->ws + c->L.counter);
-  return timed(c, KI_ZERO, s, [&] {
-    return launch_zero_u32(cnt, c->shape.max_batch * c->shape.num_kv_heads, s);
-  });
+  (void)stream;   // nothing to enqueue: layer 0 reads no history
+  return BACON_OK;
 }
 
 bacon_status bacon_score(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
@@ -453,6 +452,7 @@ bacon_status bacon_score(bacon_ctx *c, int32_t layer, const bacon_batch *bt, con
   const bool bf16 = c->shape.dtype == BACON_BF16;
   const bool w32 = c->shape.window == 32;
   TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+  TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
   return timed(c, KI_SCORE, s, [&] { return launch_pass(PASS_SCORE, bf16, c->shape.head_dim, w32, a, st, s); });
 }
 
@@ -576,6 +576,7 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   const bool bf16 = c->shape.dtype == BACON_BF16;
   const bool w32 = c->shape.window == 32;
   TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+  TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
   TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
   if (!segmented_select(c, bt)) {
     // a union of segment candidates would not fit one workgroup: one
@@ -620,20 +621,19 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   g.cand_v = reinterpret_cast<float *>(c->ws + c->L.cand_v);
   g.cand_stride = c->L.cand_stride;
   g.lambda_ws = reinterpret_cast<float *>(c->ws + c->L.lambda);
-  g.counter = reinterpret_cast<unsigned *>(c->ws + c->L.counter);
+  g.cand2_key = reinterpret_cast<unsigned *>(c->ws + c->L.cand2_key);
+  g.cand2_pos = reinterpret_cast<int *>(c->ws + c->L.cand2_pos);
   g.idx = d_idx;
+  g.k = d_k;
+  g.v = d_v;
+  g.k_out = d_k_out;
+  g.v_out = d_v_out;
+  g.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
+  int kmax = 0;
+  for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, bt->budgets[b]);
   TRY(timed(c, KI_SEGA, s, [&] { return launch_sega(g, st, s); }));
   TRY(timed(c, KI_SEGB, s, [&] { return launch_segb(g, st, s); }));
-  CompactArgs ca{};
-  ca.idx = d_idx;
-  ca.k = d_k;
-  ca.v = d_v;
-  ca.k_out = d_k_out;
-  ca.v_out = d_v_out;
-  ca.Hkv = c->shape.num_kv_heads;
-  ca.W = c->shape.window;
-  ca.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
-  TRY(timed(c, KI_COMPACT, s, [&] { return launch_compact(ca, st, s); }));
+  TRY(timed(c, KI_FINAL, s, [&] { return launch_final(g, st, kmax, s); }));
   c->next_layer = layer + 1;
   return BACON_OK;
 }

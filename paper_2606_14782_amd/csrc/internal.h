@@ -47,6 +47,7 @@ struct PassArgs {
   int64_t T;            // row length of the [Hkv, T] vectors
   float c2;             // log2(e) / sqrt(d)
   float2 *partials;     // [Hkv, total_chunks, Rpad]  (max, sum) per chunk, log2 units
+  float *lse2;          // [B, Hkv, Rpad] row normalisers, log2 units (merge kernel writes)
   float *lse_user;      // optional [B, Hq, W] natural-log normaliser
   // PASS_SCORE
   float *out_B, *out_Q; // [Hkv, T]
@@ -102,10 +103,14 @@ struct SegArgs {
   unsigned *cand_key;            // [Hkv, cand_stride] scale-matching candidates
   int *cand_pos;
   float *cand_v;
+  unsigned *cand2_key;           // [Hkv, cand_stride] top-K candidates
+  int *cand2_pos;
   int64_t cand_stride;
   float *lambda_ws, *out_lambda; // [B, Hkv]
-  unsigned *counter;             // [B, Hkv] arrival counters, zero between launches
   int32_t *idx;
+  const void *k, *v;             // gather of the final kernel
+  void *k_out, *v_out;
+  int row_bytes;
 };
 
 struct ElemArgs {           // split calibrate: E, T, L, ring update
@@ -137,9 +142,12 @@ size_t select_lds_bytes(int mode, int max_len);
 hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,
                          hipStream_t s);
 hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_lse_merge(const PassArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_sega(const SegArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_segb(const SegArgs &a, const SeqTable &st, hipStream_t s);
-hipError_t launch_zero_u32(unsigned *p, int count, hipStream_t s);
+// LDS of the final workgroup for budgets up to max_budget.
+size_t final_lds_bytes(int max_budget, int window);
+hipError_t launch_final(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s);
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
 
 }  // namespace bacon

@@ -92,21 +92,23 @@ struct PassCfg {
   static constexpr int ROWB = D * ES;          // bytes per key / query row
   static constexpr int NU = ROWB / 32;         // 16-byte units per lane
   static constexpr int PIECES = ROWB / 16;     // 16-byte pieces per row
-  static constexpr int STRIDE = ROWB + 16;     // padded LDS row (bank spread)
+  // LDS rows are unpadded; the 16-byte piece p of key k sits in slot
+  // p ^ (k & SWM), so the 32 keys one MFMA operand read touches fall on
+  // different banks.
+  static constexpr int SWM = (PIECES < 16 ? PIECES : 16) - 1;
   static constexpr int MAXL = PIECES / 2;      // max staged loads per thread
 };
 
 // LDS map of a pass workgroup (bytes):
-//   kbuf  2 * tk * STRIDE         double-buffered key stages
+//   kbuf  2 * tk * ROWB           double-buffered key stages (swizzled pieces)
 //   red   2 * 2 * nw * tk floats  per-stage B/Q partials of each row tile  (pass 2)
 //   lse   Rpad floats             row normalisers                          (pass 2)
-//   mrg   2 * Rpad float2         partial-merge scratch                    (pass 2)
 //   ce    chunk floats            E of the chunk                           (fused)
 //   cv    chunk floats            E + T of the chunk                       (fused)
 int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk) {
   const int nw = rpad / 32, tk = stage_keys(nw);
-  int bytes = 2 * tk * (head_dim * (bf16 ? 2 : 4) + 16);
-  if (mode != PASS_LSE) bytes += 16 * nw * tk + 4 * rpad + 16 * rpad;
+  int bytes = 2 * tk * head_dim * (bf16 ? 2 : 4);
+  if (mode != PASS_LSE) bytes += 16 * nw * tk + 4 * rpad;
   if (mode == PASS_FUSED) bytes += 8 * chunk;
   return bytes;
 }
@@ -128,12 +130,12 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   const int k1 = min(n, k0 + a.chunk);
   const int W = a.W;
   const int wfirst = n - W;                      // position of window row 0
+  const int nstages = (k1 - k0 + tk - 1) / tk;
 
   unsigned char *kbuf = smem;
-  float *red = reinterpret_cast<float *>(smem + 2 * tk * C::STRIDE);   // [2][2][nw][tk]
+  float *red = reinterpret_cast<float *>(smem + 2 * tk * C::ROWB);     // [2][2][nw][tk]
   float *lse_s = red + 4 * nw * tk;                                    // [Rpad]
-  float2 *mrg = reinterpret_cast<float2 *>(lse_s + a.Rpad);            // [2][Rpad]
-  float *ce = reinterpret_cast<float *>(mrg + 2 * a.Rpad);             // [chunk]
+  float *ce = lse_s + a.Rpad;                                          // [chunk]
   float *cv = ce + a.chunk;                                            // [chunk]
 
   // Stage loader: thread t moves pieces q = t + j*nt of the stage.
@@ -141,10 +143,10 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
                             ((int64_t)st.cu[b] * a.Hkv + h) * C::ROWB;
   const int64_t kstride = (int64_t)a.Hkv * C::ROWB;
   const int stage_pieces = tk * C::PIECES;
-  u32x4 pre[C::MAXL];
   // Straight-line, unconditional loads: pieces past the stage and keys past
   // the chunk are clamped to valid addresses (duplicates are masked or
   // rewritten with identical data), so all loads stay in flight together.
+  u32x4 pre[C::MAXL];
   auto fetch = [&](int s) {
     const int key0 = k0 + s * tk;
 #pragma unroll
@@ -155,11 +157,12 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
     }
   };
   auto commit = [&](int buf) {
-    unsigned char *dst = kbuf + buf * tk * C::STRIDE;
+    unsigned char *dst = kbuf + buf * tk * C::ROWB;
 #pragma unroll
     for (int j = 0; j < C::MAXL; ++j) {
       const int q = min(t + j * nt, stage_pieces - 1);
-      *reinterpret_cast<u32x4 *>(dst + (q / C::PIECES) * C::STRIDE + 16 * (q % C::PIECES)) = pre[j];
+      const int key = q / C::PIECES, pc = q % C::PIECES;
+      *reinterpret_cast<u32x4 *>(dst + key * C::ROWB + 16 * (pc ^ (key & C::SWM))) = pre[j];
     }
   };
 
@@ -181,7 +184,10 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
     }
   }
 
-  const int nstages = (k1 - k0 + tk - 1) / tk;
+  // byte offsets of this lane's operand pieces 2u + half within its key row
+  int koff[C::NU];
+#pragma unroll
+  for (int u = 0; u < C::NU; ++u) koff[u] = 16 * ((2 * u + half) ^ (l32 & C::SWM));
 
   // ---- pass-1 state: running max (raw logit units) and sum of exp2
   float m_run = -INFINITY, l_run = 0.f;
@@ -195,51 +201,8 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   int wrow[16];                    // window index of each row (W for pad rows)
   uint32_t lastmask = 0;           // rows that are the last query of their head
   if constexpr (MODE != PASS_LSE) {
-    // Merge the pass-1 partials of this (sequence, KV head): thread t takes
-    // row t % Rpad and every other chunk; 16 independent loads per batch.
-    const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
-    const float2 *pp = a.partials + ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad;
-    const int row = t % a.Rpad, part = t / a.Rpad;
-    float mm = -INFINITY, ll = 0.f;
-    for (int c0 = part; c0 < nch; c0 += 32) {
-      float2 v[16];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int cc = c0 + 2 * j;
-        v[j] = pp[(int64_t)min(cc, nch - 1) * a.Rpad + row];
-      }
-#pragma unroll
-      for (int j = 0; j < 16; ++j)
-        if (c0 + 2 * j >= nch) v[j] = make_float2(-INFINITY, 0.f);
-      float mb = mm;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) mb = fmaxf(mb, v[j].x);
-      if (mb != -INFINITY) {
-        float acc = (mm == -INFINITY) ? 0.f : ll * __builtin_amdgcn_exp2f(mm - mb);
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (v[j].x != -INFINITY) acc += v[j].y * __builtin_amdgcn_exp2f(v[j].x - mb);
-        ll = acc;
-        mm = mb;
-      }
-    }
-    mrg[part * a.Rpad + row] = make_float2(mm, ll);
-    __syncthreads();
-    if (t < a.Rpad) {
-      const float2 p0 = mrg[t], p1 = mrg[a.Rpad + t];
-      const float m = fmaxf(p0.x, p1.x);
-      float l = 0.f;
-      if (m != -INFINITY) {
-        if (p0.x != -INFINITY) l += p0.y * __builtin_amdgcn_exp2f(p0.x - m);
-        if (p1.x != -INFINITY) l += p1.y * __builtin_amdgcn_exp2f(p1.x - m);
-      }
-      const float lse2 = (t < a.R) ? m + log2f(l) : INFINITY;
-      lse_s[t] = lse2;
-      if (a.lse_user && c == 0 && t < a.R) {
-        const int g = t / W, w = t - g * W;
-        a.lse_user[((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w] = lse2 * kLn2;
-      }
-    }
+    // row normalisers of this (sequence, KV head), merged by pass 1
+    for (int r = t; r < a.Rpad; r += nt) lse_s[r] = a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + r];
     __syncthreads();
 #pragma unroll
     for (int reg = 0; reg < 16; ++reg) {
@@ -266,16 +229,16 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
       for (int q = 0; q < kMaxRing / 4; ++q) rv[q] = rp[min(q, nq - 1)];
     }
     if (s + 1 < nstages) fetch(s + 1);
-    const unsigned char *kl = kbuf + buf * tk * C::STRIDE;
+    const unsigned char *kl = kbuf + buf * tk * C::ROWB;
 #pragma unroll 1
     for (int kt = 0; kt * 32 < ntile; ++kt) {
       const int kbase = k0 + s * tk + kt * 32;   // first key of the tile (sequence-relative)
-      const unsigned char *kr = kl + (kt * 32 + l32) * C::STRIDE + 16 * half;
+      const unsigned char *kr = kl + (kt * 32 + l32) * C::ROWB;
       f32x16 acc = {};
       if constexpr (MODE == PASS_LSE) {
 #pragma unroll
         for (int u = 0; u < C::NU; ++u)
-          acc = mfma_unit<BF16>(*reinterpret_cast<const u32x4 *>(kr + 32 * u), qf[u], acc);
+          acc = mfma_unit<BF16>(*reinterpret_cast<const u32x4 *>(kr + koff[u]), qf[u], acc);
         // acc[reg]: key kbase + acc_row(reg, half), row = wave*32 + l32
         const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
         if (edge) {
@@ -302,7 +265,7 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
       } else {
 #pragma unroll
         for (int u = 0; u < C::NU; ++u)
-          acc = mfma_unit<BF16>(qf[u], *reinterpret_cast<const u32x4 *>(kr + 32 * u), acc);
+          acc = mfma_unit<BF16>(qf[u], *reinterpret_cast<const u32x4 *>(kr + koff[u]), acc);
         // acc[reg]: row wave*32 + acc_row(reg, half), key kbase + l32
         float p[16];
 #pragma unroll
@@ -427,6 +390,66 @@ static hipError_t launch_pass_m(bool bf16, int d, bool w32, const PassArgs &a, c
                            : launch_pass_t<MODE, false, 128, false>(a, st, s);
   return w32 ? launch_pass_t<MODE, false, 64, true>(a, st, s)
              : launch_pass_t<MODE, false, 64, false>(a, st, s);
+}
+
+// Row normalisers of each (sequence, KV head) from the per-chunk (max, sum)
+// partials of pass 1: thread t takes row t % Rpad and the chunks congruent to
+// t / Rpad, 16 independent loads per batch; the parts are combined in LDS in
+// a fixed order.
+constexpr int kMergeThreads = 512;
+__global__ __launch_bounds__(kMergeThreads) void k_lse_merge(PassArgs a, SeqTable st) {
+  __shared__ float2 mrg[kMergeThreads];
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
+  const float2 *pp = a.partials + ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad;
+  const int parts = max(1, kMergeThreads / a.Rpad);
+  const int row = t % a.Rpad, part = t / a.Rpad;
+  float mm = -INFINITY, ll = 0.f;
+  if (part < parts) {
+    for (int c0 = part; c0 < nch; c0 += 16 * parts) {
+      float2 v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v[j] = pp[(int64_t)min(c0 + parts * j, nch - 1) * a.Rpad + row];
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        if (c0 + parts * j >= nch) v[j] = make_float2(-INFINITY, 0.f);
+      float mb = mm;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) mb = fmaxf(mb, v[j].x);
+      if (mb != -INFINITY) {
+        float acc = (mm == -INFINITY) ? 0.f : ll * __builtin_amdgcn_exp2f(mm - mb);
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (v[j].x != -INFINITY) acc += v[j].y * __builtin_amdgcn_exp2f(v[j].x - mb);
+        ll = acc;
+        mm = mb;
+      }
+    }
+    mrg[t] = make_float2(mm, ll);
+  }
+  __syncthreads();
+  if (t < a.Rpad) {
+    float mx = -INFINITY;
+    for (int q = 0; q < parts; ++q) mx = fmaxf(mx, mrg[q * a.Rpad + t].x);
+    float sx = 0.f;
+    if (mx != -INFINITY)
+      for (int q = 0; q < parts; ++q) {
+        const float2 pq = mrg[q * a.Rpad + t];
+        if (pq.x != -INFINITY) sx += pq.y * __builtin_amdgcn_exp2f(pq.x - mx);
+      }
+    const float lse2 = (t < a.R) ? mx + log2f(sx) : INFINITY;
+    a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + t] = lse2;
+    if (a.lse_user && t < a.R) {
+      const int W = a.W, g = t / W, w = t - g * W;
+      a.lse_user[((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w] = lse2 * kLn2;
+    }
+  }
+}
+
+hipError_t launch_lse_merge(const PassArgs &a, const SeqTable &st, hipStream_t s) {
+  if (a.Rpad > 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_lse_merge, dim3(st.batch, a.Hkv), dim3(kMergeThreads), 0, s, a, st);
+  return hipGetLastError();
 }
 
 hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
@@ -1151,30 +1174,6 @@ __device__ __forceinline__ int find_seg(const SeqTable &st, int seg) {
   return b;
 }
 
-// Arrival of a workgroup at the per-(sequence, KV head) counter after its
-// global writes.  True in the workgroup that arrives last (expected-th), which
-// then sees every other workgroup's writes; that workgroup re-arms the counter.
-// No workgroup waits for another.  The barrier makes the workgroup's writes
-// visible to thread 0, whose device-scope release fence and counter update
-// publish them (one cache write-back per workgroup); the last workgroup's
-// thread 0 acquires before the barrier that releases the other threads.
-template <int NT>
-__device__ __forceinline__ bool last_arrival(unsigned *counter, unsigned expected, SelSharedT<NT> &ss) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    const unsigned prev = atomicAdd(counter, 1u);
-    const int last = prev + 1u == expected;
-    if (last) {
-      atomicExch(counter, 0u);
-      __threadfence();
-    }
-    ss.bc_i[3] = last;
-  }
-  __syncthreads();
-  return ss.bc_i[3] != 0;
-}
-
 // Slots of the set elements of a strided layout (element j of thread t is
 // item t + j*NT) in item order: pre[j*NW + wave] receives the number of set
 // elements before (j, wave); an element's slot is that plus its lane rank in
@@ -1213,9 +1212,7 @@ __device__ __forceinline__ unsigned lane_rank(uint64_t m) {
 // L neighbours in another chunk, from this layer's E in the history), writes
 // the pooled window score pB and pooled evidence pV over I for the segment
 // (Eq. bacon_score is pooled as pool(B + lambda V) = pB + lambda pV), and the
-// segment's top-min(M, kSegLen) of B with their V.  The last workgroup of a
-// (sequence, KV head) takes the exact top-M of B over the union
-// (Eq. scale_matching_set) and solves lambda (Eq. lambda_solution).
+// segment's top-min(M, kSegLen) of B with their V (Eq. scale_matching_set).
 __global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ float Bs[kSegWin], Vs[kSegWin];
@@ -1320,13 +1317,7 @@ __global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
 
   int M = (int)floorf(a.rho * (float)st.budget[b]);
   M = max(0, min(M, nc));
-  if (M == 0 || !a.use_last_query) {                  // no calibration: lambda = 0
-    if (sg == 0 && t == 0) {
-      a.lambda_ws[b * a.Hkv + h] = 0.f;
-      if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = 0.f;
-    }
-    return;
-  }
+  if (M == 0 || !a.use_last_query) return;            // no calibration: lambda = 0
   // the segment's top-Mc of B, in ascending position
   const int Mc = st.mc[b];
   const int64_t slot0 = (int64_t)h * a.cand_stride + st.cand_base[b] + (int64_t)sg * Mc;
@@ -1361,11 +1352,20 @@ __global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
     }
     for (int q = min(ncand, Mc) + t; q < Mc; q += NT) a.cand_key[slot0 + q] = 0u;   // empty slots
   }
-  if (!last_arrival(a.counter + b * a.Hkv + h, (unsigned)nseg, ss)) return;
+}
 
-  // last workgroup: top-M of B over the union, moments, lambda
-  const int U = nseg * Mc;                          // <= kUnionCap (host check)
+// Top M of B over the union of the segments' candidates of a (sequence, KV
+// head) (Eq. scale_matching_set) and lambda = gamma Std(B) / (Std(V) + eps)
+// over it (Eq. lambda_solution); population moments in double, B shifted by
+// the set minimum.  Every thread returns lambda.
+__device__ __forceinline__ float segment_lambda(const SegArgs &a, const SeqTable &st, int b, int h,
+                                                int M, SelSharedT<kSegThreads> &ss, unsigned *ckey,
+                                                int *cpos) {
+  constexpr int NT = kSegThreads;
+  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
+  const int U = nseg * st.mc[b];                    // <= kUnionCap (host check)
   const int64_t c0 = (int64_t)h * a.cand_stride + st.cand_base[b];
+  const int t = threadIdx.x;
   unsigned ck[kUnionPer];
   int cp[kUnionPer];
   float cv[kUnionPer];
@@ -1390,7 +1390,6 @@ __global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
 #pragma unroll
   for (int j = 0; j < kUnionPer; ++j)
     inm |= (ck[j] > xm || (ck[j] == xm && ck[j] != 0u && cp[j] <= pm) ? 1u : 0u) << j;
-  // population moments over the set in double; B shifted by the set minimum
   unsigned kmin = 0xffffffffu;
 #pragma unroll
   for (int j = 0; j < kUnionPer; ++j) kmin = ((inm >> j) & 1u) ? min(kmin, ck[j]) : kmin;
@@ -1409,17 +1408,13 @@ __global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
   double vb = sums[1] / M - mb * mb, vv = sums[3] / M - mv * mv;
   vb = vb > 0.0 ? vb : 0.0;
   vv = vv > 0.0 ? vv : 0.0;
-  const float lam = (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));
-  if (t == 0) {
-    a.lambda_ws[b * a.Hkv + h] = lam;
-    if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = lam;
-  }
+  return (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));
 }
 
-// Top-K kernel.  Each segment takes its top-min(K, kSegLen) of the pooled
-// score pB + lambda pV over I; the last workgroup of a (sequence, KV head)
-// takes the exact top-K over the union (Eq. topk_selection, ties to the lower
-// position) and writes the indices in ascending position, -1 beyond |I|.
+// Top-K kernel.  Every segment workgroup first solves lambda from the union of
+// the calibration kernel's candidates (the same exact computation in each
+// workgroup of a (sequence, KV head), so no workgroup waits for another), then
+// takes its top-min(K, kSegLen) of the pooled score pB + lambda pV over I.
 __global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ unsigned ckey[kCandCap];
@@ -1430,62 +1425,89 @@ __global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
-  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
   const int i0 = sg * kSegLen;
   const int K = st.budget[b];
-  const int kept = min(K, nc);
   const int Kc = min(K, kSegLen);
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
+
+  int M = (int)floorf(a.rho * (float)K);
+  M = max(0, min(M, nc));
+  float lam = 0.f;
+  if (M > 0 && a.use_last_query) lam = segment_lambda(a, st, b, h, M, ss, ckey, cpos);
+  if (sg == 0 && t == 0) {
+    a.lambda_ws[b * a.Hkv + h] = lam;
+    if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = lam;
+  }
+
   int cb = 0;                                        // first slot of the sequence
   for (int x = 0; x < b; ++x) cb += (st.seg_base[x + 1] - st.seg_base[x]) * min(st.budget[x], kSegLen);
-  const int64_t c0 = (int64_t)h * a.cand_stride + cb;
-  const float lam = a.lambda_ws[b * a.Hkv + h];
-
+  const int64_t slot0 = (int64_t)h * a.cand_stride + cb + (int64_t)sg * Kc;
+  const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
+  float pb[PER], pv[PER];
   {
-    const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
-    float pb[PER], pv[PER];
+    const int tt = opaque(t);
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-      pb[j] = a.vec_pB[tile + t + j * NT];
-      pv[j] = a.vec_pV[tile + t + j * NT];
+      pb[j] = a.vec_pB[tile + tt + j * NT];
+      pv[j] = a.vec_pV[tile + tt + j * NT];
     }
-    unsigned key[PER];
+  }
+  unsigned key[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    key[j] = t + j * NT < ncand ? float_key(fmaf(lam, pv[j], pb[j])) : 0u;
+  auto keyS = [&](int j) -> unsigned { return key[j]; };
+  auto posf = [&](int j) -> int { return i0 + t + j * NT; };
+  uint32_t msk = 0;
+  if (ncand <= Kc) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) msk |= (t + j * NT < ncand ? 1u : 0u) << j;
+  } else {
+    unsigned xk;
+    int pk;
+    block_threshold<PER>(keyS, posf, Kc, xk, pk, ss, ckey, cpos);
 #pragma unroll
     for (int j = 0; j < PER; ++j)
-      key[j] = t + j * NT < ncand ? float_key(fmaf(lam, pv[j], pb[j])) : 0u;
-    auto keyS = [&](int j) -> unsigned { return key[j]; };
-    auto posf = [&](int j) -> int { return i0 + t + j * NT; };
-    uint32_t msk = 0;
-    if (ncand <= Kc) {
-#pragma unroll
-      for (int j = 0; j < PER; ++j) msk |= (t + j * NT < ncand ? 1u : 0u) << j;
-    } else {
-      unsigned xk;
-      int pk;
-      block_threshold<PER>(keyS, posf, Kc, xk, pk, ss, ckey, cpos);
-#pragma unroll
-      for (int j = 0; j < PER; ++j)
-        msk |= (key[j] > xk || (key[j] == xk && posf(j) <= pk) ? 1u : 0u) << j;
-    }
-    const int64_t slot0 = c0 + (int64_t)sg * Kc;
-    ordered_bases<PER, NT>(msk, pre);
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const bool in = (msk >> j) & 1u;
-      const uint64_t m = __ballot(in);
-      if (in) {
-        const int64_t o = slot0 + pre[j * NW + wave] + lane_rank(m);
-        a.cand_key[o] = key[j];
-        a.cand_pos[o] = posf(j);
-      }
-    }
-    for (int q = min(ncand, Kc) + t; q < Kc; q += NT) a.cand_key[slot0 + q] = 0u;
+      msk |= (key[j] > xk || (key[j] == xk && posf(j) <= pk) ? 1u : 0u) << j;
   }
-  if (!last_arrival(a.counter + b * a.Hkv + h, (unsigned)nseg, ss)) return;
+  ordered_bases<PER, NT>(msk, pre);
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const bool in = (msk >> j) & 1u;
+    const uint64_t m = __ballot(in);
+    if (in) {
+      const int64_t o = slot0 + pre[j * NW + wave] + lane_rank(m);
+      a.cand2_key[o] = key[j];
+      a.cand2_pos[o] = posf(j);
+    }
+  }
+  for (int q = min(ncand, Kc) + t; q < Kc; q += NT) a.cand2_key[slot0 + q] = 0u;
+}
 
-  // last workgroup: exact top-K over the union (held in ascending position)
+// Final kernel, one workgroup per (sequence, KV head): the exact top-K over
+// the union of the segments' candidates (Eq. topk_selection, ties to the lower
+// position), indices in ascending position (-1 beyond |I|), then the
+// compacted cache: kept rows, the W window rows, zero rows up to K + W.
+__global__ __launch_bounds__(kSegThreads) void k_final(SegArgs a, SeqTable st) {
+  constexpr int NT = kSegThreads, NW = NT / 64;
+  extern __shared__ __align__(16) int tbl[];         // [K + W] source position of each row
+  __shared__ unsigned ckey[kCandCap];
+  __shared__ int cpos[kCandCap];
+  __shared__ SelSharedT<NT> ss;
+  __shared__ unsigned pre[kUnionPer * NW];
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  const int wave = t >> 6;
+  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
+  const int n = st.cu[b + 1] - st.cu[b];
+  const int nc = n - a.W;
+  const int K = st.budget[b];
+  const int kept = min(K, nc);
+  const int Kc = min(K, kSegLen);
+  int cb = 0;
+  for (int x = 0; x < b; ++x) cb += (st.seg_base[x + 1] - st.seg_base[x]) * min(st.budget[x], kSegLen);
+  const int64_t c0 = (int64_t)h * a.cand_stride + cb;
   int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
   if (kept > 0) {
     const int U = nseg * Kc;                        // <= kUnionCap (host check)
@@ -1496,8 +1518,8 @@ __global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
 #pragma unroll
       for (int j = 0; j < kUnionPer; ++j) {
         const int q = min(tt + j * NT, U - 1);
-        ck[j] = a.cand_key[c0 + q];
-        cp[j] = a.cand_pos[c0 + q];
+        ck[j] = a.cand2_key[c0 + q];
+        cp[j] = a.cand2_pos[c0 + q];
       }
 #pragma unroll
       for (int j = 0; j < kUnionPer; ++j) if (tt + j * NT >= U) ck[j] = 0u;
@@ -1516,16 +1538,69 @@ __global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
       for (int j = 0; j < kUnionPer; ++j)
         msk |= (ck[j] > xk || (ck[j] == xk && ck[j] != 0u && cp[j] <= pk) ? 1u : 0u) << j;
     }
-    // emission in slot order, which is ascending position
+    // the union is held in ascending position, so slot order is position order
     ordered_bases<kUnionPer, NT>(msk, pre);
 #pragma unroll
     for (int j = 0; j < kUnionPer; ++j) {
       const bool in = (msk >> j) & 1u;
       const uint64_t m = __ballot(in);
-      if (in) idx[pre[j * NW + wave] + lane_rank(m)] = cp[j];
+      if (in) {
+        const unsigned o = pre[j * NW + wave] + lane_rank(m);
+        idx[o] = cp[j];
+        tbl[o] = cp[j];
+      }
     }
   }
+  // output rows: kept positions, the W window rows, then zero rows up to K + W
   for (int j = max(kept, 0) + t; j < K; j += NT) idx[j] = -1;
+  for (int w = t; w < a.W; w += NT) tbl[kept + w] = nc + w;
+  for (int j = kept + a.W + t; j < K + a.W; j += NT) tbl[j] = -1;
+  __syncthreads();
+
+  const int pieces = a.row_bytes / 16;
+  const int total = (K + a.W) * pieces;
+  const unsigned char *ks = static_cast<const unsigned char *>(a.k);
+  const unsigned char *vs = static_cast<const unsigned char *>(a.v);
+  unsigned char *ko = static_cast<unsigned char *>(a.k_out);
+  unsigned char *vo = static_cast<unsigned char *>(a.v_out);
+  constexpr int BATCH = 5;
+  for (int q0 = t; q0 < total; q0 += BATCH * NT) {
+    u32x4 kv[BATCH], vv[BATCH];
+    int srcs[BATCH];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int q = min(q0 + u * NT, total - 1);
+      const int rr = q / pieces, p = q - rr * pieces;
+      srcs[u] = tbl[rr];
+      const int64_t so = ((int64_t)(st.cu[b] + max(srcs[u], 0)) * a.Hkv + h) * a.row_bytes + 16 * p;
+      kv[u] = *reinterpret_cast<const u32x4 *>(ks + so);
+      vv[u] = *reinterpret_cast<const u32x4 *>(vs + so);
+    }
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int q = q0 + u * NT;
+      if (q < total) {
+        const int rr = q / pieces, p = q - rr * pieces;
+        const int64_t dst = ((int64_t)(st.kept_base[b] + rr) * a.Hkv + h) * a.row_bytes + 16 * p;
+        const u32x4 z = u32x4{0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4 *>(ko + dst) = srcs[u] >= 0 ? kv[u] : z;
+        *reinterpret_cast<u32x4 *>(vo + dst) = srcs[u] >= 0 ? vv[u] : z;
+      }
+    }
+  }
+}
+
+size_t final_lds_bytes(int max_budget, int window) {
+  return (size_t)(max_budget + window) * sizeof(int) + 2 * kCandCap * sizeof(unsigned) +
+         sizeof(SelSharedT<kSegThreads>) + kUnionPer * (kSegThreads / 64) * sizeof(unsigned);
+}
+
+hipError_t launch_final(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s) {
+  const size_t lds = (size_t)(max_budget + a.W) * sizeof(int);
+  if (final_lds_bytes(max_budget, a.W) > (size_t)kLdsBytes) return hipErrorInvalidValue;
+  allow_lds(k_final, lds);
+  hipLaunchKernelGGL(k_final, dim3(st.batch, a.Hkv), dim3(kSegThreads), lds, s, a, st);
+  return hipGetLastError();
 }
 
 hipError_t launch_sega(const SegArgs &a, const SeqTable &st, hipStream_t s) {
@@ -1537,17 +1612,6 @@ hipError_t launch_sega(const SegArgs &a, const SeqTable &st, hipStream_t s) {
 hipError_t launch_segb(const SegArgs &a, const SeqTable &st, hipStream_t s) {
   dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
   hipLaunchKernelGGL(k_segb, grid, block, 0, s, a, st);
-  return hipGetLastError();
-}
-
-__global__ __launch_bounds__(256) void k_zero_u32(unsigned *p, int count) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < count) p[i] = 0u;
-}
-
-hipError_t launch_zero_u32(unsigned *p, int count, hipStream_t s) {
-  if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_zero_u32, dim3((count + 255) / 256), dim3(256), 0, s, p, count);
   return hipGetLastError();
 }
 
