@@ -146,24 +146,36 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   // Straight-line, unconditional loads: pieces past the stage and keys past
   // the chunk are clamped to valid addresses (duplicates are masked or
   // rewritten with identical data), so all loads stay in flight together.
+  // The thread's piece offsets are the same in every stage: a full stage is
+  // one uniform base plus them.
   u32x4 pre[C::MAXL];
+  int goff[C::MAXL], loff[C::MAXL];
+#pragma unroll
+  for (int j = 0; j < C::MAXL; ++j) {
+    const int q = min(t + j * nt, stage_pieces - 1);
+    const int key = q / C::PIECES, pc = q % C::PIECES;
+    goff[j] = key * (int)kstride + 16 * pc;
+    loff[j] = key * C::ROWB + 16 * (pc ^ (key & C::SWM));
+  }
   auto fetch = [&](int s) {
     const int key0 = k0 + s * tk;
+    if (key0 + tk <= k1) {
+      const unsigned char *base = kb + (int64_t)key0 * kstride;
 #pragma unroll
-    for (int j = 0; j < C::MAXL; ++j) {
-      const int q = min(t + j * nt, stage_pieces - 1);
-      const int key = min(key0 + q / C::PIECES, k1 - 1);
-      pre[j] = *reinterpret_cast<const u32x4 *>(kb + (int64_t)key * kstride + 16 * (q % C::PIECES));
+      for (int j = 0; j < C::MAXL; ++j) pre[j] = *reinterpret_cast<const u32x4 *>(base + goff[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < C::MAXL; ++j) {
+        const int q = min(t + j * nt, stage_pieces - 1);
+        const int key = min(key0 + q / C::PIECES, k1 - 1);
+        pre[j] = *reinterpret_cast<const u32x4 *>(kb + (int64_t)key * kstride + 16 * (q % C::PIECES));
+      }
     }
   };
   auto commit = [&](int buf) {
     unsigned char *dst = kbuf + buf * tk * C::ROWB;
 #pragma unroll
-    for (int j = 0; j < C::MAXL; ++j) {
-      const int q = min(t + j * nt, stage_pieces - 1);
-      const int key = q / C::PIECES, pc = q % C::PIECES;
-      *reinterpret_cast<u32x4 *>(dst + key * C::ROWB + 16 * (pc ^ (key & C::SWM))) = pre[j];
-    }
+    for (int j = 0; j < C::MAXL; ++j) *reinterpret_cast<u32x4 *>(dst + loff[j]) = pre[j];
   };
 
   fetch(0);   // first key stage in flight while the prologue runs
