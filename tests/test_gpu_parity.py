@@ -111,6 +111,14 @@ def test_workload_parity(name):
     run_case(name, CASES[name]())
 
 
+def _batch64():
+    rng = np.random.default_rng(64)
+    lens = tuple(int(x) for x in rng.integers(40, 401, size=64))
+    budgets = tuple(int(x) for x in rng.choice([1, 8, 64, 300], size=64))
+    visual = tuple((2, n - 12) for n in lens)
+    return inputs.Workload("edge", 2, 4, 2, 64, 8, 5, "bf16", lens, budgets, visual, 1, 22)
+
+
 EDGE = {
     # generic row layout (G*W = 24, pad rows), d = 64, budget > |I|, budget = |I|
     "gqa3-w8-d64": dict(wl=inputs.Workload("edge", 3, 6, 2, 64, 8, 5, "bf16", (40, 300, 77),
@@ -153,6 +161,14 @@ EDGE = {
     # candidate) and a budget above half the candidate set
     "M-over-segment": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 7, "bf16", (8000,),
                                               (1500,), ((30, 7000),), 4, 18)),
+    # the largest window-row block: G*W = 256 rows (eight row tiles)
+    "rows256-g8-w32": dict(wl=inputs.Workload("edge", 3, 16, 2, 128, 32, 7, "bf16", (3000, 1500),
+                                              (100, 40), ((30, 2500), (0, 1200)), 4, 20)),
+    # a 256-query window with one head per group
+    "w256-mha": dict(wl=inputs.Workload("edge", 2, 2, 2, 64, 256, 5, "bf16", (1200,), (50,),
+                                        ((10, 800),), 3, 21)),
+    # the largest batch: 64 sequences of ragged lengths and budgets
+    "batch64": dict(wl=_batch64()),
     # candidate unions beyond one workgroup: one select workgroup per
     # (sequence, KV head) over the whole sequence
     "large-budget-whole-sequence": dict(wl=inputs.Workload("edge", 2, 8, 2, 128, 32, 7, "bf16",
