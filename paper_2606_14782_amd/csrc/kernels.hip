@@ -63,6 +63,27 @@ __device__ __forceinline__ f32x16 mfma_unit(u32x4 a, u32x4 b, f32x16 c) {
   }
 }
 
+// The value of lane l ^ 32 (the other half of the wave), through a VALU lane
+// swap rather than an LDS permute.
+__device__ __forceinline__ float xor32(float v, int half) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(half ? r[0] : r[1]);
+}
+
+// Pairwise (tree) sum and max of 16 values: depth 4 instead of a 16-long chain.
+__device__ __forceinline__ float tree_sum16(const float *x) {
+  const float a0 = (x[0] + x[1]) + (x[2] + x[3]), a1 = (x[4] + x[5]) + (x[6] + x[7]);
+  const float a2 = (x[8] + x[9]) + (x[10] + x[11]), a3 = (x[12] + x[13]) + (x[14] + x[15]);
+  return (a0 + a1) + (a2 + a3);
+}
+__device__ __forceinline__ float tree_max16(const float *x) {
+  const float a0 = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+  const float a1 = fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7]));
+  const float a2 = fmaxf(fmaxf(x[8], x[9]), fmaxf(x[10], x[11]));
+  const float a3 = fmaxf(fmaxf(x[12], x[13]), fmaxf(x[14], x[15]));
+  return fmaxf(fmaxf(a0, a1), fmaxf(a2, a3));
+}
+
 // Row (or column) of accumulator register `reg` in the 32x32 output layout.
 __device__ __forceinline__ int acc_row(int reg, int half) {
   return 8 * (reg >> 2) + 4 * half + (reg & 3);
@@ -260,19 +281,20 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
             if (!(key < k1 && key <= tpos_row)) acc[reg] = -INFINITY;
           }
         }
-        float mt = acc[0];
+        float av[16];
 #pragma unroll
-        for (int reg = 1; reg < 16; ++reg) mt = fmaxf(mt, acc[reg]);
+        for (int reg = 0; reg < 16; ++reg) av[reg] = acc[reg];
+        const float mt = tree_max16(av);
         if (mt > m_run) {
           l_run *= __builtin_amdgcn_exp2f((m_run - mt) * a.c2);
           m_run = mt;
         }
         if (m_run != -INFINITY) {
           const float off = -m_run * a.c2;
-          float sum = 0.f;
+          float ev[16];
 #pragma unroll
-          for (int reg = 0; reg < 16; ++reg) sum += __builtin_amdgcn_exp2f(fmaf(acc[reg], a.c2, off));
-          l_run += sum;
+          for (int reg = 0; reg < 16; ++reg) ev[reg] = __builtin_amdgcn_exp2f(fmaf(av[reg], a.c2, off));
+          l_run += tree_sum16(ev);
         }
       } else {
 #pragma unroll
@@ -289,17 +311,15 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           for (int reg = 0; reg < 16; ++reg)
             if (!(key < k1 && key - wfirst <= wrow[reg])) p[reg] = 0.f;
         }
-        float bs = 0.f, qs = 0.f;
-#pragma unroll
-        for (int reg = 0; reg < 16; ++reg) bs += p[reg];
+        float bs = tree_sum16(p), qs = 0.f;
         if constexpr (W32) {
           qs = half ? p[15] : 0.f;
         } else {
 #pragma unroll
           for (int reg = 0; reg < 16; ++reg) qs += ((lastmask >> reg) & 1u) ? p[reg] : 0.f;
         }
-        bs += __shfl_xor(bs, 32);
-        qs += __shfl_xor(qs, 32);
+        bs += xor32(bs, half);
+        qs += xor32(qs, half);
         if (half == 0) {
           red[((buf * 2 + 0) * nw + wave) * tk + kt * 32 + l32] = bs;
           red[((buf * 2 + 1) * nw + wave) * tk + kt * 32 + l32] = qs;
@@ -365,7 +385,7 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
 
   if constexpr (MODE == PASS_LSE) {
     // merge the two lane halves (same row, different keys) and store the partial
-    const float mo = __shfl_xor(m_run, 32), lo = __shfl_xor(l_run, 32);
+    const float mo = xor32(m_run, half), lo = xor32(l_run, half);
     const float m = fmaxf(m_run, mo);
     float l = 0.f;
     if (m != -INFINITY)
