@@ -1464,6 +1464,15 @@ __global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
   const int Kc = min(K, kSegLen);
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
 
+  // the segment's pooled B and V do not depend on lambda: in flight first
+  const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
+  float pb[PER], pv[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    pb[j] = a.vec_pB[tile + t + j * NT];
+    pv[j] = a.vec_pV[tile + t + j * NT];
+  }
+
   int M = (int)floorf(a.rho * (float)K);
   M = max(0, min(M, nc));
   float lam = 0.f;
@@ -1476,16 +1485,6 @@ __global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
   int cb = 0;                                        // first slot of the sequence
   for (int x = 0; x < b; ++x) cb += (st.seg_base[x + 1] - st.seg_base[x]) * min(st.budget[x], kSegLen);
   const int64_t slot0 = (int64_t)h * a.cand_stride + cb + (int64_t)sg * Kc;
-  const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
-  float pb[PER], pv[PER];
-  {
-    const int tt = opaque(t);
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      pb[j] = a.vec_pB[tile + tt + j * NT];
-      pv[j] = a.vec_pV[tile + tt + j * NT];
-    }
-  }
   unsigned key[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j)
