@@ -67,11 +67,13 @@ def kernel_bytes(name, wl, persist_m=4):
     if name == "lse_merge":                             # per-chunk (max, sum) partials
         chunks = T / 512 + wl.batch
         return Hkv * chunks * wl.group * wl.window * 8
-    if name == "segment_calib":                         # B, E+T+L in; pooled B, V out
-        return 4 * vec
-    if name == "segment_topk":                          # pooled B, V in
-        return 2 * vec
-    if name == "final_topk":                            # kept + window rows of K and V, in and out
+    if name == "segment_calib":                         # B, E+T+L in; V, pooled B and V out
+        return 5 * vec
+    if name == "segment_score":                         # pooled B and V in; score keys out
+        return 3 * vec
+    if name == "segment_cand":                          # score keys in
+        return vec
+    if name == "final_topk":                            # kept + window rows of K and V in and out
         return 2 * 2 * kept_rows * Hkv * wl.head_dim * wl.elem_size + 4 * sum(wl.budgets) * Hkv
     return 0.0
 

@@ -29,11 +29,11 @@ _NAMES = [
     (r"bacon::k_pass<1,", "window_score"),
     (r"bacon::k_pass<2,", "window_score_calib"),
     (r"bacon::k_lse_merge\b", "lse_merge"),
-    (r"bacon::k_sega\b", "segment_calib"),
-    (r"bacon::k_segb\b", "segment_topk"),
-    (r"bacon::k_final\b", "final_topk"),
+    (r"bacon::k_segcal\b", "segment_calib"),
+    (r"bacon::k_segscore\b", "segment_score"),
+    (r"bacon::k_segcand\b", "segment_cand"),
+    (r"bacon::k_segfinal\b", "final_topk"),
     (r"bacon::k_compact\b", "compact"),
-    (r"bacon::k_select<0>", "select_fused"),
     (r"bacon::k_select<1>", "select_calib"),
     (r"bacon::k_select<2>", "select_topk"),
     (r"bacon::k_elem\b", "calib_elem"),

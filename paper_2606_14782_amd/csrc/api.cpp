@@ -36,9 +36,8 @@ bacon_status hip_fail(hipError_t e, const char *what) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t ring, vec_b, vec_vp, vec_pb, vec_pv, cand_key, cand_pos, cand_v, cand2_key, cand2_pos,
-      partials, lse2, lambda, total;
-  int64_t cand_stride;
+  size_t ring, vec_b, vec_vp, vec_v, vec_pb, vec_pv, vec_s, hist_b, hist_s, list_bk, list_bp, list_bv,
+      list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, total;
   int rpad, slots, ring_mp;
   int64_t chunks_cap;
 };
@@ -97,18 +96,23 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.ring = off;     off += align256((size_t)L.ring_mp * vec);
   L.vec_b = off;    off += align256(vec);
   L.vec_vp = off;   off += align256(vec);
-  // per head: segments * kSegLen pooled values, and candidate slots
-  // sum over sequences of segments * min(M or K, kSegLen); both are at most
-  // T + max_batch * kSegLen
-  L.cand_stride = s->max_total_tokens + (int64_t)s->max_batch * kSegLen;
-  const size_t cand = (size_t)s->num_kv_heads * (size_t)L.cand_stride * 4;
-  L.vec_pb = off;   off += align256(cand);
-  L.vec_pv = off;   off += align256(cand);
-  L.cand_key = off; off += align256(cand);
-  L.cand_pos = off; off += align256(cand);
-  L.cand_v = off;   off += align256(cand);
-  L.cand2_key = off; off += align256(cand);
-  L.cand2_pos = off; off += align256(cand);
+  L.vec_v = off;    off += align256(vec);
+  L.vec_pb = off;   off += align256(vec);
+  L.vec_pv = off;   off += align256(vec);
+  L.vec_s = off;    off += align256(vec);
+  const size_t hist = (size_t)s->max_batch * s->num_kv_heads * kHBins * sizeof(unsigned);
+  L.hist_b = off;   off += align256(hist);
+  L.hist_s = off;   off += align256(hist);
+  L.list_bk = off;  off += align256(vec);
+  L.list_bp = off;  off += align256(vec);
+  L.list_bv = off;  off += align256(vec);
+  L.list_sk = off;  off += align256(vec);
+  L.list_sp = off;  off += align256(vec);
+  const int64_t segs_cap = (s->max_total_tokens + kSegLen - 1) / kSegLen + s->max_batch;
+  L.cnt_b = off;    off += align256((size_t)s->num_kv_heads * segs_cap * sizeof(int));
+  L.cnt_s = off;    off += align256((size_t)s->num_kv_heads * segs_cap * sizeof(int));
+  L.rec_b = off;    off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(int4));
+  L.rec_s = off;    off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(int4));
   L.partials = off; off += align256((size_t)s->num_kv_heads * L.chunks_cap * L.rpad * sizeof(float2));
   L.lse2 = off;     off += align256((size_t)s->max_batch * s->num_kv_heads * L.rpad * sizeof(float));
   L.lambda = off;   off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(float));
@@ -116,10 +120,11 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   return L;
 }
 
-const char *kKernelNames[] = {"window_lse",    "lse_merge",   "window_score", "window_score_calib",
-                              "segment_calib", "segment_topk", "final_topk",  "select_fused",
-                              "select_calib",  "select_topk",  "calib_elem",  "compact"};
-enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGA, KI_SEGB, KI_FINAL, KI_SEL_FUSED,
+const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", "window_score_calib",
+                              "segment_calib", "segment_score", "segment_cand",
+                              "final_topk",    "select_calib",  "select_topk",
+                              "calib_elem",    "compact"};
+enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
                 KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_COUNT };
 
 }  // namespace
@@ -235,12 +240,9 @@ SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out) {
   }
   per_wg = std::min(per_wg, kMaxChunk / tk);
   const int chunk = tk * per_wg;
-  int cb = 0, ib = 0, kb = 0, sb = 0, cnb = 0;
+  int cb = 0, ib = 0, kb = 0, sb = 0;
   for (int b = 0; b < bt->batch; ++b) {
     const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
-    const int nc = n - c->shape.window;
-    int M = (int)floorf(c->params.rho * (float)bt->budgets[b]);
-    M = std::max(0, std::min(M, nc));
     const int nseg = (n + kSegLen - 1) / kSegLen;
     st.cu[b] = bt->cu_seqlens[b];
     st.chunk_base[b] = cb;
@@ -248,18 +250,14 @@ SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out) {
     st.idx_base[b] = ib;
     st.kept_base[b] = kb;
     st.seg_base[b] = sb;
-    st.cand_base[b] = cnb;
-    st.mc[b] = std::min(M, kSegLen);
     cb += (n + chunk - 1) / chunk;
     ib += bt->budgets[b];
     kb += bt->budgets[b] + c->shape.window;
     sb += nseg;
-    cnb += nseg * st.mc[b];
   }
   st.cu[bt->batch] = bt->cu_seqlens[bt->batch];
   st.chunk_base[bt->batch] = cb;
   st.seg_base[bt->batch] = sb;
-  st.cand_base[bt->batch] = cnb;
   st.total_chunks = cb;
   st.total_segs = sb;
   *chunk_out = chunk;
@@ -282,6 +280,8 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   a.c2 = (float)(1.4426950408889634 / std::sqrt((double)s.head_dim));
   a.partials = reinterpret_cast<float2 *>(c->ws + c->L.partials);
   a.lse2 = reinterpret_cast<float *>(c->ws + c->L.lse2);
+  a.hist_B = reinterpret_cast<unsigned *>(c->ws + c->L.hist_b);
+  a.hist_S = reinterpret_cast<unsigned *>(c->ws + c->L.hist_s);
   a.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
   a.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
   a.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
@@ -322,23 +322,6 @@ SelArgs sel_args(const bacon_ctx *c) {
 
 int max_len(const bacon_batch *bt);
 
-// The segmented select (one workgroup per kSegLen positions) applies when the
-// union of the segments' candidates of a (sequence, KV head), for both the
-// scale-matching set and the top-K, fits one closing workgroup.
-bool segmented_select(const bacon_ctx *c, const bacon_batch *bt) {
-  for (int b = 0; b < bt->batch; ++b) {
-    const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
-    const int nc = n - c->shape.window;
-    const int nseg = (n + kSegLen - 1) / kSegLen;
-    int M = (int)floorf(c->params.rho * (float)bt->budgets[b]);
-    M = std::max(0, std::min(M, nc));
-    if ((int64_t)nseg * std::min(M, kSegLen) > kUnionCap) return false;
-    if ((int64_t)nseg * std::min(bt->budgets[b], kSegLen) > kUnionCap) return false;
-    if (final_lds_bytes(bt->budgets[b], c->shape.window) > (size_t)kLdsBytes) return false;
-  }
-  return true;
-}
-
 // Every workgroup of the pass must fit the LDS of one CU; checked before
 // anything is enqueued.
 bacon_status check_lds(const bacon_ctx *c, const bacon_batch *bt, int chunk, bool passes,
@@ -346,10 +329,9 @@ bacon_status check_lds(const bacon_ctx *c, const bacon_batch *bt, int chunk, boo
   const bool bf16 = c->shape.dtype == BACON_BF16;
   if (passes && pass_lds_bytes(PASS_FUSED, bf16, c->shape.head_dim, c->L.rpad, chunk) > kLdsBytes)
     return fail(BACON_ERR_UNSUPPORTED, "pass workgroup needs more LDS than a CU has");
-  if (sel_mode >= 0 && sel_mode != SEL_SEGMENTED &&
-      select_lds_bytes(sel_mode, max_len(bt)) > (size_t)kLdsBytes)
+  if (sel_mode >= 0 && select_lds_bytes(sel_mode, max_len(bt)) > (size_t)kLdsBytes)
     return fail(BACON_ERR_UNSUPPORTED, "select workgroup needs more LDS than a CU has");
-  if (sel_mode == SEL_FUSED || sel_mode == SEL_CALIB || sel_mode == SEL_SEGMENTED) {
+  if (sel_mode == SEL_FUSED || sel_mode == SEL_CALIB) {
     const int n = max_len(bt);
     if (chunk < n && (int64_t)((n - 1) / chunk) * 2 * c->params.radius > kEdgeEntries)
       return fail(BACON_ERR_UNSUPPORTED, "too many chunk boundaries for radius %d", c->params.radius);
@@ -567,7 +549,11 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   hipStream_t s = static_cast<hipStream_t>(stream);
   int chunk = 0;
   const SeqTable st = make_table(c, bt, &chunk);
-  TRY(check_lds(c, bt, chunk, true, segmented_select(c, bt) ? SEL_SEGMENTED : SEL_FUSED));
+  TRY(check_lds(c, bt, chunk, true, SEL_FUSED));
+  int kmax = 0;
+  for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, bt->budgets[b]);
+  if (final_lds_bytes(kmax, c->shape.window) > (size_t)kLdsBytes)
+    return fail(BACON_ERR_UNSUPPORTED, "budget %d needs more LDS than a CU has", kmax);
   const int64_t T = bt->cu_seqlens[bt->batch];
   PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
   a.T = T;
@@ -575,28 +561,6 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   a.ring_mp = c->L.ring_mp;
   const bool bf16 = c->shape.dtype == BACON_BF16;
   const bool w32 = c->shape.window == 32;
-  TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
-  TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
-  TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
-  if (!segmented_select(c, bt)) {
-    // a union of segment candidates would not fit one workgroup: one
-    // workgroup per (sequence, KV head) selects over the whole sequence
-    SelArgs sa = sel_args(c);
-    sa.T = T;
-    sa.ring = a.ring;
-    sa.ring_mp = c->L.ring_mp;
-    sa.ring_slot = a.ring_write;
-    sa.vp_chunk = chunk;
-    sa.idx = d_idx;
-    sa.k = d_k;
-    sa.v = d_v;
-    sa.k_out = d_k_out;
-    sa.v_out = d_v_out;
-    sa.do_gather = 1;
-    TRY(timed(c, KI_SEL_FUSED, s, [&] { return launch_select(SEL_FUSED, max_len(bt), sa, st, s); }));
-    c->next_layer = layer + 1;
-    return BACON_OK;
-  }
   SegArgs g{};
   g.Hkv = c->shape.num_kv_heads;
   g.W = c->shape.window;
@@ -614,26 +578,37 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   g.ring = a.ring;
   g.ring_mp = c->L.ring_mp;
   g.ring_slot = a.ring_write;
+  g.vec_V = reinterpret_cast<float *>(c->ws + c->L.vec_v);
   g.vec_pB = reinterpret_cast<float *>(c->ws + c->L.vec_pb);
   g.vec_pV = reinterpret_cast<float *>(c->ws + c->L.vec_pv);
-  g.cand_key = reinterpret_cast<unsigned *>(c->ws + c->L.cand_key);
-  g.cand_pos = reinterpret_cast<int *>(c->ws + c->L.cand_pos);
-  g.cand_v = reinterpret_cast<float *>(c->ws + c->L.cand_v);
-  g.cand_stride = c->L.cand_stride;
+  g.vec_S = reinterpret_cast<unsigned *>(c->ws + c->L.vec_s);
+  g.hist_B = a.hist_B;
+  g.hist_S = a.hist_S;
+  g.listB_key = reinterpret_cast<unsigned *>(c->ws + c->L.list_bk);
+  g.listB_pos = reinterpret_cast<int *>(c->ws + c->L.list_bp);
+  g.listB_v = reinterpret_cast<float *>(c->ws + c->L.list_bv);
+  g.listS_key = reinterpret_cast<unsigned *>(c->ws + c->L.list_sk);
+  g.listS_pos = reinterpret_cast<int *>(c->ws + c->L.list_sp);
+  g.cntB = reinterpret_cast<int *>(c->ws + c->L.cnt_b);
+  g.cntS = reinterpret_cast<int *>(c->ws + c->L.cnt_s);
+  g.recB = reinterpret_cast<int4 *>(c->ws + c->L.rec_b);
+  g.recS = reinterpret_cast<int4 *>(c->ws + c->L.rec_s);
   g.lambda_ws = reinterpret_cast<float *>(c->ws + c->L.lambda);
-  g.cand2_key = reinterpret_cast<unsigned *>(c->ws + c->L.cand2_key);
-  g.cand2_pos = reinterpret_cast<int *>(c->ws + c->L.cand2_pos);
   g.idx = d_idx;
   g.k = d_k;
   g.v = d_v;
   g.k_out = d_k_out;
   g.v_out = d_v_out;
   g.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
-  int kmax = 0;
-  for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, bt->budgets[b]);
-  TRY(timed(c, KI_SEGA, s, [&] { return launch_sega(g, st, s); }));
-  TRY(timed(c, KI_SEGB, s, [&] { return launch_segb(g, st, s); }));
-  TRY(timed(c, KI_FINAL, s, [&] { return launch_final(g, st, kmax, s); }));
+  // final workgroups per (sequence, KV head): about one round over the CUs
+  g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
+  TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+  TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+  TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
+  TRY(timed(c, KI_SEGCAL, s, [&] { return launch_segcal(g, st, s); }));
+  TRY(timed(c, KI_SEGSCORE, s, [&] { return launch_segscore(g, st, s); }));
+  TRY(timed(c, KI_SEGCAND, s, [&] { return launch_segcand(g, st, s); }));
+  TRY(timed(c, KI_FINAL, s, [&] { return launch_segfinal(g, st, kmax, s); }));
   c->next_layer = layer + 1;
   return BACON_OK;
 }

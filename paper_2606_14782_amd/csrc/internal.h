@@ -14,10 +14,10 @@ constexpr int kMaxChunk = 4096;     // keys per pass workgroup
 constexpr int kSelThreads = 1024;
 constexpr int kSelPer = kMaxSeqLen / kSelThreads;   // positions per select thread
 constexpr int kHistBins = 2048;     // 11-bit digits of the block select
-constexpr int kSegLen = 2048;       // positions per segment of the distributed select
+constexpr int kSegLen = 2048;       // positions per segment of the histogram select
 constexpr int kSegThreads = 1024;
 constexpr int kPoolHalo = 16;       // largest pool half-width
-constexpr int kUnionCap = 8192;     // candidate slots a closing segment workgroup holds
+constexpr int kHBins = 8192;        // bins of the select histograms (32 per octave of a float)
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU (and per workgroup) on gfx950
 constexpr int kEdgeEntries = 1024;      // positions next to chunk boundaries the select stages
 
@@ -27,8 +27,6 @@ struct SeqTable {
   int32_t total_chunks;                 // key chunks per KV head over the batch
   int32_t total_segs;                   // select segments per KV head over the batch
   int32_t seg_base[kMaxBatch + 1];      // first select segment of each sequence
-  int32_t cand_base[kMaxBatch + 1];     // first scale-matching candidate slot of each sequence
-  int32_t mc[kMaxBatch];                // candidate slots per segment: min(M, kSegLen)
   int32_t cu[kMaxBatch + 1];            // token offsets
   int32_t chunk_base[kMaxBatch + 1];    // first chunk of each sequence
   int32_t budget[kMaxBatch];            // kept keys per KV head
@@ -48,7 +46,8 @@ struct PassArgs {
   float c2;             // log2(e) / sqrt(d)
   float2 *partials;     // [Hkv, total_chunks, Rpad]  (max, sum) per chunk, log2 units
   float *lse2;          // [B, Hkv, Rpad] row normalisers, log2 units (merge kernel writes)
-  float *lse_user;      // optional [B, Hq, W] natural-log normaliser
+  float *lse_user;      // optional [B, Hq, W] natural-log normaliser (merge kernel writes)
+  unsigned *hist_B, *hist_S;   // optional [B, Hkv, kHBins] select histograms pass 1 clears
   // PASS_SCORE
   float *out_B, *out_Q; // [Hkv, T]
   // PASS_FUSED
@@ -62,7 +61,7 @@ struct PassArgs {
   uint32_t terms;
 };
 
-enum SelMode { SEL_FUSED = 0, SEL_CALIB = 1, SEL_TOPK = 2, SEL_SEGMENTED = 3 };
+enum SelMode { SEL_FUSED = 0, SEL_CALIB = 1, SEL_TOPK = 2 };
 
 struct SelArgs {
   int Hkv, W;
@@ -88,7 +87,7 @@ struct SelArgs {
   int do_gather;
 };
 
-// Distributed select of the fused pass (segment kernel, then final kernel).
+// Histogram select of the fused pass (calibration, score and final kernels).
 struct SegArgs {
   int Hkv, W;
   int64_t T;
@@ -99,18 +98,23 @@ struct SegArgs {
   const float *vec_B, *vec_VP;   // [Hkv, T]
   const float *ring;             // [Hkv, T, ring_mp]
   int ring_mp, ring_slot;
-  float *vec_pB, *vec_pV;        // [Hkv, total_segs, kSegLen] pooled B and V over I
-  unsigned *cand_key;            // [Hkv, cand_stride] scale-matching candidates
-  int *cand_pos;
-  float *cand_v;
-  unsigned *cand2_key;           // [Hkv, cand_stride] top-K candidates
-  int *cand2_pos;
-  int64_t cand_stride;
+  float *vec_V;                  // [Hkv, T] V = E + L + T over I
+  float *vec_pB, *vec_pV;        // [Hkv, T] pooled B and V over I
+  unsigned *vec_S;               // [Hkv, T] keys of the pooled score over I
+  unsigned *hist_B, *hist_S;     // [B, Hkv, kHBins] key histograms of B and of the pooled score
+  // per-segment lists at or above a boundary bin: segment s of a sequence
+  // writes slots [s*kSegLen, ...) of the [Hkv, T] arrays, its count to cnt
+  unsigned *listB_key, *listS_key;
+  int *listB_pos, *listS_pos;
+  float *listB_v;
+  int *cntB, *cntS;              // [Hkv, total_segs]
+  int4 *recB, *recS;             // [B, Hkv] boundary bin, count above, rank in it, its count
   float *lambda_ws, *out_lambda; // [B, Hkv]
   int32_t *idx;
   const void *k, *v;             // gather of the final kernel
   void *k_out, *v_out;
   int row_bytes;
+  int parts;                     // final-kernel workgroups per (sequence, KV head)
 };
 
 struct ElemArgs {           // split calibrate: E, T, L, ring update
@@ -143,11 +147,12 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
                          hipStream_t s);
 hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_lse_merge(const PassArgs &a, const SeqTable &st, hipStream_t s);
-hipError_t launch_sega(const SegArgs &a, const SeqTable &st, hipStream_t s);
-hipError_t launch_segb(const SegArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_segcal(const SegArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_segscore(const SegArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_segcand(const SegArgs &a, const SeqTable &st, hipStream_t s);
 // LDS of the final workgroup for budgets up to max_budget.
 size_t final_lds_bytes(int max_budget, int window);
-hipError_t launch_final(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s);
+hipError_t launch_segfinal(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s);
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
 
 }  // namespace bacon

@@ -84,6 +84,24 @@ __device__ __forceinline__ float tree_max16(const float *x) {
   return fmaxf(fmaxf(a0, a1), fmaxf(a2, a3));
 }
 
+// Order-preserving map of a float to uint32 (larger float -> larger key);
+// -0 is folded to +0.  0 is reserved for "not a candidate".
+__device__ __forceinline__ unsigned float_key(float x) {
+  x = x + 0.0f;
+  const unsigned u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_float(unsigned k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// Bin of a key in the select histograms: bits 30..18 of a non-negative float
+// (32 bins per octave); keys of negative values, which the method does not
+// produce, share bin 0, so the bins stay monotone in the key.
+__device__ __forceinline__ int hbin(unsigned key) {
+  return key >= 0x80000000u ? (int)((key >> 18) & (unsigned)(kHBins - 1)) : 0;
+}
+
 // Row (or column) of accumulator register `reg` in the 32x32 output layout.
 __device__ __forceinline__ int acc_row(int reg, int half) {
   return 8 * (reg >> 2) + 4 * half + (reg & 3);
@@ -126,11 +144,14 @@ struct PassCfg {
 //   lse   Rpad floats             row normalisers                          (pass 2)
 //   ce    chunk floats            E of the chunk                           (fused)
 //   cv    chunk floats            E + T of the chunk                       (fused)
+//   cb    chunk floats            B of the chunk                           (fused)
+// After the stages the fused pass reuses kbuf for its B histogram.
 int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk) {
   const int nw = rpad / 32, tk = stage_keys(nw);
   int bytes = 2 * tk * head_dim * (bf16 ? 2 : 4);
+  if (mode == PASS_FUSED && bytes < 4 * kHBins) bytes = 4 * kHBins;   // room for the B histogram
   if (mode != PASS_LSE) bytes += 16 * nw * tk + 4 * rpad;
-  if (mode == PASS_FUSED) bytes += 8 * chunk;
+  if (mode == PASS_FUSED) bytes += 12 * chunk;
   return bytes;
 }
 
@@ -154,10 +175,12 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   const int nstages = (k1 - k0 + tk - 1) / tk;
 
   unsigned char *kbuf = smem;
-  float *red = reinterpret_cast<float *>(smem + 2 * tk * C::ROWB);     // [2][2][nw][tk]
+  const int kbytes = (MODE == PASS_FUSED) ? max(2 * tk * C::ROWB, 4 * kHBins) : 2 * tk * C::ROWB;
+  float *red = reinterpret_cast<float *>(smem + kbytes);               // [2][2][nw][tk]
   float *lse_s = red + 4 * nw * tk;                                    // [Rpad]
   float *ce = lse_s + a.Rpad;                                          // [chunk]
   float *cv = ce + a.chunk;                                            // [chunk]
+  float *cb = cv + a.chunk;                                            // [chunk]
 
   // Stage loader: thread t moves pieces q = t + j*nt of the stage.
   const unsigned char *kb = static_cast<const unsigned char *>(a.k) +
@@ -234,7 +257,8 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   int wrow[16];                    // window index of each row (W for pad rows)
   uint32_t lastmask = 0;           // rows that are the last query of their head
   if constexpr (MODE != PASS_LSE) {
-    // row normalisers of this (sequence, KV head), merged by pass 1
+    // row normalisers of this (sequence, KV head), merged from pass 1's
+    // per-chunk partials by the merge kernel
     for (int r = t; r < a.Rpad; r += nt) lse_s[r] = a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + r];
     __syncthreads();
 #pragma unroll
@@ -243,6 +267,19 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
       nl[reg] = -lse_s[r];
       wrow[reg] = (r < a.R) ? r % W : W;
       if (!W32 && r < a.R && (r % W) == W - 1) lastmask |= 1u << reg;
+    }
+  }
+  if constexpr (MODE == PASS_LSE) {
+    // pass 1 clears the select histograms of its (sequence, KV head) that the
+    // later kernels of the pass accumulate: chunk c takes an equal slice
+    if (a.hist_B) {
+      const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
+      const int sl = 4 * ((kHBins / 4 + nch - 1) / nch);
+      const int64_t row = ((int64_t)b * a.Hkv + h) * kHBins;
+      for (int q = c * sl + 4 * t; q < min(kHBins, (c + 1) * sl); q += 4 * nt) {
+        *reinterpret_cast<u32x4 *>(a.hist_B + row + q) = u32x4{0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4 *>(a.hist_S + row + q) = u32x4{0u, 0u, 0u, 0u};
+      }
     }
   }
 
@@ -357,6 +394,7 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           const float Tv = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
           a.ring[pos * a.ring_mp + a.ring_write] = E;
           a.vec_B[pos] = Bv;
+          cb[s * tk + t] = Bv;
           ce[s * tk + t] = E;
           cv[s * tk + t] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
         }
@@ -380,6 +418,19 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
       }
       const float vp = cv[p] + (use_l ? sum / (float)(hi - lo + 1) : 0.f);
       a.vec_VP[(int64_t)h * a.T + st.cu[b] + i] = vp;
+    }
+    // B histogram of the chunk's candidates (positions before the window) in
+    // the key-stage buffers, added to the (sequence, KV head) histogram of the
+    // select bin by bin: a hot bin takes one global atomic per workgroup.
+    unsigned *hist = reinterpret_cast<unsigned *>(kbuf);
+    for (int q = t; q < kHBins; q += nt) hist[q] = 0u;
+    __syncthreads();
+    for (int p = t; p < min(k1, wfirst) - k0; p += nt) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
+    __syncthreads();
+    unsigned *gh = a.hist_B + ((int64_t)b * a.Hkv + h) * kHBins;
+    for (int q = t; q < kHBins; q += nt) {
+      const unsigned c = hist[q];
+      if (c) atomicAdd(&gh[q], c);
     }
   }
 
@@ -425,62 +476,60 @@ static hipError_t launch_pass_m(bool bf16, int d, bool w32, const PassArgs &a, c
 }
 
 // Row normalisers of each (sequence, KV head) from the per-chunk (max, sum)
-// partials of pass 1: thread t takes row t % Rpad and the chunks congruent to
-// t / Rpad, 16 independent loads per batch; the parts are combined in LDS in
-// a fixed order.
-constexpr int kMergeThreads = 512;
-__global__ __launch_bounds__(kMergeThreads) void k_lse_merge(PassArgs a, SeqTable st) {
-  __shared__ float2 mrg[kMergeThreads];
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+// partials of pass 1.  A workgroup takes 16 rows: thread t merges row t % 16
+// over the chunks congruent to t / 16 (mod 16), kMergeBatch loads in flight
+// per batch; the 16 parts of a row are combined through LDS in a fixed order.
+constexpr int kMergeRows = 16, kMergeParts = 16, kMergeBatch = 8;
+__global__ __launch_bounds__(kMergeRows * kMergeParts) void k_lse_merge(PassArgs a, SeqTable st) {
+  __shared__ float2 mrg[kMergeParts][kMergeRows];
+  const int rg = blockIdx.x, b = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
+  const int row = rg * kMergeRows + (t % kMergeRows), part = t / kMergeRows;
   const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
-  const float2 *pp = a.partials + ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad;
-  const int parts = max(1, kMergeThreads / a.Rpad);
-  const int row = t % a.Rpad, part = t / a.Rpad;
+  const float2 *pp = a.partials + ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad + row;
   float mm = -INFINITY, ll = 0.f;
-  if (part < parts) {
-    for (int c0 = part; c0 < nch; c0 += 16 * parts) {
-      float2 v[16];
+  for (int c0 = part; c0 < nch; c0 += kMergeParts * kMergeBatch) {
+    float2 v[kMergeBatch];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) v[j] = pp[(int64_t)min(c0 + parts * j, nch - 1) * a.Rpad + row];
+    for (int j = 0; j < kMergeBatch; ++j) v[j] = pp[(int64_t)min(c0 + kMergeParts * j, nch - 1) * a.Rpad];
 #pragma unroll
-      for (int j = 0; j < 16; ++j)
-        if (c0 + parts * j >= nch) v[j] = make_float2(-INFINITY, 0.f);
-      float mb = mm;
+    for (int j = 0; j < kMergeBatch; ++j)
+      if (c0 + kMergeParts * j >= nch) v[j] = make_float2(-INFINITY, 0.f);
+    float mb = mm;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) mb = fmaxf(mb, v[j].x);
-      if (mb != -INFINITY) {
-        float acc = (mm == -INFINITY) ? 0.f : ll * __builtin_amdgcn_exp2f(mm - mb);
+    for (int j = 0; j < kMergeBatch; ++j) mb = fmaxf(mb, v[j].x);
+    if (mb != -INFINITY) {
+      float acc = (mm == -INFINITY) ? 0.f : ll * __builtin_amdgcn_exp2f(mm - mb);
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (v[j].x != -INFINITY) acc += v[j].y * __builtin_amdgcn_exp2f(v[j].x - mb);
-        ll = acc;
-        mm = mb;
-      }
+      for (int j = 0; j < kMergeBatch; ++j)
+        if (v[j].x != -INFINITY) acc += v[j].y * __builtin_amdgcn_exp2f(v[j].x - mb);
+      ll = acc;
+      mm = mb;
     }
-    mrg[t] = make_float2(mm, ll);
   }
+  mrg[part][t % kMergeRows] = make_float2(mm, ll);
   __syncthreads();
-  if (t < a.Rpad) {
+  if (t < kMergeRows) {
     float mx = -INFINITY;
-    for (int q = 0; q < parts; ++q) mx = fmaxf(mx, mrg[q * a.Rpad + t].x);
+    for (int q = 0; q < kMergeParts; ++q) mx = fmaxf(mx, mrg[q][t].x);
     float sx = 0.f;
     if (mx != -INFINITY)
-      for (int q = 0; q < parts; ++q) {
-        const float2 pq = mrg[q * a.Rpad + t];
+      for (int q = 0; q < kMergeParts; ++q) {
+        const float2 pq = mrg[q][t];
         if (pq.x != -INFINITY) sx += pq.y * __builtin_amdgcn_exp2f(pq.x - mx);
       }
-    const float lse2 = (t < a.R) ? mx + log2f(sx) : INFINITY;
-    a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + t] = lse2;
-    if (a.lse_user && t < a.R) {
-      const int W = a.W, g = t / W, w = t - g * W;
+    const float lse2 = (row < a.R) ? mx + log2f(sx) : INFINITY;
+    a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + row] = lse2;
+    if (a.lse_user && row < a.R) {
+      const int W = a.W, g = row / W, w = row - g * W;
       a.lse_user[((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w] = lse2 * kLn2;
     }
   }
 }
 
 hipError_t launch_lse_merge(const PassArgs &a, const SeqTable &st, hipStream_t s) {
-  if (a.Rpad > 256) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_lse_merge, dim3(st.batch, a.Hkv), dim3(kMergeThreads), 0, s, a, st);
+  if (a.Rpad % kMergeRows) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_lse_merge, dim3(a.Rpad / kMergeRows, st.batch, a.Hkv),
+                     dim3(kMergeRows * kMergeParts), 0, s, a, st);
   return hipGetLastError();
 }
 
@@ -616,30 +665,19 @@ __device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelSharedT<NT>
   return before + x - v;
 }
 
-// Order-preserving map of a float to uint32 (larger float -> larger key);
-// -0 is folded to +0.  0 is reserved for "not a candidate".
-__device__ __forceinline__ unsigned float_key(float x) {
-  x = x + 0.0f;
-  const unsigned u = __float_as_uint(x);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key_float(unsigned k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
-}
+constexpr int kCandCap = 1024;   // LDS list of boundary-bin candidates
 
-// Boundary search over ss.hist (larger bin = larger keys), block-parallel:
-// thread t owns the kHistBins/NT consecutive bins starting at t*kHistBins/NT;
-// suffix sums over threads give, for the need-th largest counted element, its
-// bin (ss.bc_i[0]) and the count in the bins above it (ss.bc_i[1]);
+// Boundary search over bin counts held in registers (larger bin = larger
+// keys): thread t holds the BPT consecutive bins starting at BPT*t.  For the
+// need-th largest counted element, ss.bc_i[0] receives its bin, ss.bc_i[1]
+// the count in the bins above it and ss.bc_u[2] the count of its bin;
 // ss.bc_u[3] gets the total count.  Ends with a barrier.
-template <int NT>
-__device__ __forceinline__ void hist_boundary(int need, SelSharedT<NT> &ss) {
-  constexpr int BPT = kHistBins / NT;
+template <int BPT, int NT>
+__device__ __forceinline__ void bins_boundary(const unsigned *cb, int need, SelSharedT<NT> &ss) {
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-  unsigned cb[BPT];
   unsigned c = 0;
 #pragma unroll
-  for (int q = 0; q < BPT; ++q) { cb[q] = ss.hist[BPT * t + q]; c += cb[q]; }
+  for (int q = 0; q < BPT; ++q) c += cb[q];
   const unsigned pre = wave_incl_sum_u(c);
   const unsigned tot = lane63_u(pre);
   unsigned suf = tot - pre + c;        // inclusive suffix sum within the wave
@@ -651,17 +689,99 @@ __device__ __forceinline__ void hist_boundary(int need, SelSharedT<NT> &ss) {
   suf += higher;
   const unsigned above = suf - c;
   if (above < (unsigned)need && (unsigned)need <= suf) {
-    unsigned acc = above;
+    unsigned acc = above, bc = 0;
     int bs = BPT * t;
 #pragma unroll
     for (int q = BPT - 1; q >= 0; --q) {
-      if (acc + cb[q] >= (unsigned)need) { bs = BPT * t + q; break; }
+      if (acc + cb[q] >= (unsigned)need) { bs = BPT * t + q; bc = cb[q]; break; }
       acc += cb[q];
     }
     ss.bc_i[0] = bs;
     ss.bc_i[1] = (int)acc;
+    ss.bc_u[2] = bc;
   }
   if (t == 0) ss.bc_u[3] = suf;
+  __syncthreads();
+}
+
+// The same over ss.hist (kHistBins bins).
+template <int NT>
+__device__ __forceinline__ void hist_boundary(int need, SelSharedT<NT> &ss) {
+  constexpr int BPT = kHistBins / NT;
+  unsigned cb[BPT];
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) cb[q] = ss.hist[BPT * threadIdx.x + q];
+  bins_boundary<BPT, NT>(cb, need, ss);
+}
+
+// Compacts the elements j with in(j) into the LDS list (ckey, cpos) in
+// (wave, element slot, lane) order, through ballots (no atomics); returns
+// nothing, the list length is the caller's count (entries beyond the
+// kCandCap slots of the list are dropped).  Ends with a barrier.
+template <int PER, int NT, typename InF, typename KeyF, typename PosF>
+__device__ __forceinline__ void compact_ballot(InF in, KeyF key, PosF pos, unsigned *ckey, int *cpos,
+                                               SelSharedT<NT> &ss) {
+  constexpr unsigned CAP = kCandCap;
+  constexpr int NW = NT / 64;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  unsigned wc = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) wc += (unsigned)__popcll(__ballot(in(j)));
+  if (lane == 0) ss.red_u[wave] = wc;
+  __syncthreads();
+  unsigned off = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) off += (w < wave) ? ss.red_u[w] : 0u;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const bool i = in(j);
+    const uint64_t m = __ballot(i);
+    if (i) {
+      const unsigned o = off + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+      if (o < CAP) {
+        ckey[o] = key(j);
+        cpos[o] = pos(j);
+      }
+    }
+    off += (unsigned)__popcll(m);
+  }
+  __syncthreads();
+}
+
+// The need-th entry (1-based) of C <= NT listed entries under the tie rule
+// (key descending, position ascending): xk = its key, pthr = its position.
+// Every entry is ranked against all others by tpe consecutive lanes.
+template <int NT>
+__device__ __forceinline__ void rank_pick(int C, int need, const unsigned *ckey, const int *cpos,
+                                          SelSharedT<NT> &ss, unsigned &xk, int &pthr) {
+  const int t = threadIdx.x;
+  int tpe = 1;
+  while (tpe < 32 && 2 * tpe * C <= NT) tpe *= 2;
+  const int q = t / tpe, sub = t & (tpe - 1);
+  unsigned rk = 0, kq = 0;
+  int pq = 0;
+  if (q < C) {
+    kq = ckey[q];
+    pq = cpos[q];
+    for (int p = sub; p < C; p += tpe) {
+      const unsigned kp = ckey[p];
+      const int pp = cpos[p];
+      rk += (kp > kq || (kp == kq && pp < pq)) ? 1u : 0u;
+    }
+  }
+  if (tpe > 1) rk += swz<1>(rk);
+  if (tpe > 2) rk += swz<2>(rk);
+  if (tpe > 4) rk += swz<4>(rk);
+  if (tpe > 8) rk += swz<8>(rk);
+  if (tpe > 16) rk += swz<16>(rk);
+  if (q < C && sub == 0 && rk == (unsigned)(need - 1)) {
+    ss.bc_u[1] = kq;
+    ss.bc_i[2] = pq;
+  }
+  __syncthreads();
+  xk = ss.bc_u[1];
+  pthr = ss.bc_i[2];
   __syncthreads();
 }
 
@@ -704,7 +824,6 @@ __device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int 
   xk = lo;
 }
 
-constexpr int kCandCap = 1024;   // LDS list of boundary-bin candidates
 constexpr int kEdgeCap = kEdgeEntries;   // LDS tables of E and L corrections next to chunk boundaries
 
 // Exact top-k threshold with the tie rule (key descending, then position
@@ -776,60 +895,10 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     return;
   }
   // compact the boundary bin in (wave, element slot, lane) order
-  {
-    auto inbin = [&](unsigned x) { return x >= lo && ((x - lo) >> sh0) == b0; };
-    unsigned wc = 0;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) wc += (unsigned)__popcll(__ballot(inbin(key(j))));
-    if (lane == 0) ss.red_u[wave] = wc;
-    __syncthreads();
-    unsigned off = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) off += (w < wave) ? ss.red_u[w] : 0u;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const unsigned x = key(j);
-      const bool in = inbin(x);
-      const uint64_t m = __ballot(in);
-      if (in) {
-        const unsigned o = off + __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
-                                                           __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
-        ckey[o] = x;
-        cpos[o] = pos(j);
-      }
-      off += (unsigned)__popcll(m);
-    }
-    __syncthreads();
-  }
+  compact_ballot<PER, NT>([&](int j) { const unsigned x = key(j); return x >= lo && ((x - lo) >> sh0) == b0; },
+                          key, pos, ckey, cpos, ss);
   if (C <= (unsigned)NT) {
-    // rank of each entry under the tie rule, tpe consecutive lanes per entry
-    int tpe = 1;
-    while (tpe < 32 && 2 * tpe * (int)C <= NT) tpe *= 2;
-    const int q = t / tpe, sub = t & (tpe - 1);
-    unsigned rk = 0, kq = 0;
-    int pq = 0;
-    if (q < (int)C) {
-      kq = ckey[q];
-      pq = cpos[q];
-      for (int p = sub; p < (int)C; p += tpe) {
-        const unsigned kp = ckey[p];
-        const int pp = cpos[p];
-        rk += (kp > kq || (kp == kq && pp < pq)) ? 1u : 0u;
-      }
-    }
-    if (tpe > 1) rk += swz<1>(rk);
-    if (tpe > 2) rk += swz<2>(rk);
-    if (tpe > 4) rk += swz<4>(rk);
-    if (tpe > 8) rk += swz<8>(rk);
-    if (tpe > 16) rk += swz<16>(rk);
-    if (q < (int)C && sub == 0 && rk == (unsigned)(need - 1)) {
-      ss.bc_u[1] = kq;
-      ss.bc_i[2] = pq;
-    }
-    __syncthreads();
-    xk = ss.bc_u[1];
-    pthr = ss.bc_i[2];
-    __syncthreads();
+    rank_pick<NT>((int)C, need, ckey, cpos, ss, xk, pthr);
     return;
   }
   // resolve the key inside the bin: 11 bits at a time from bit sh0 down
@@ -1186,19 +1255,46 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- distributed select
-// Two kernels of one workgroup per (segment of kSegLen positions, KV head).
-// In each, the workgroup of a (sequence, KV head) that finishes last reduces
-// what all its segments wrote: the first computes lambda from the union of
-// the segments' local scale-matching candidates (the global top-M of B lies in
-// the union of the segments' local top-M), the second the top-K from the union
-// of the segments' local top-K of the pooled score.
+// ---------------------------------------------------------------- histogram select
+// Four kernels after the fused pass; none waits on another workgroup.  The
+// selections use per-(sequence, KV head) histograms of the order-preserving
+// keys of the scores (kHBins bins, 32 per octave of a float): one kernel
+// accumulates a histogram, the next finds the boundary bin of its top-k in
+// one scan of the bins.  Work on positions stays spread over the segments of
+// kSegLen positions (two positions per thread); the segments exchange only
+// their lists of entries at or above the boundary bin, and the exact order
+// inside the boundary bin (ties to the lower position) is resolved on those
+// short lists.  Lists longer than one workgroup holds fall back to the exact
+// block select over the whole sequence.
+//
+//  * segment_calib (one workgroup per segment and KV head): completes
+//    V = E + L + T next to chunk boundaries (Eq. structurally_calibrated_evidence),
+//    writes the pooled B and V over I, finds the boundary bin of the top-M of
+//    B in the B histogram the fused pass accumulated (Eqs. scale_matching_size,
+//    scale_matching_set), and lists its candidates at or above it with their V.
+//  * segment_score (same grid): every workgroup of a (sequence, KV head)
+//    resolves the scale-matching set from the segments' lists and solves
+//    lambda (Eq. lambda_solution) -- the same exact computation in each, so no
+//    workgroup waits for another -- then forms the pooled score
+//    pB + lambda pV of its segment (Eq. bacon_score, pooled) and adds its keys
+//    to the S histogram.
+//  * segment_cand (same grid): the boundary bin of the top-K of the pooled
+//    score (Eq. topk_selection) and the segment's list of entries at or above it.
+//  * final_topk (`parts` workgroups per (sequence, KV head)): the top-K from
+//    the lists, the kept positions in ascending order, and each workgroup's
+//    share of the compacted cache rows.
 constexpr int kSegPer = kSegLen / kSegThreads;             // positions per thread (strided)
 constexpr int kSegWin = kSegLen + 2 * kPoolHalo;           // segment plus pool halo
 constexpr int kSegWinJ = (kSegWin + kSegThreads - 1) / kSegThreads;
-constexpr int kUnionPer = kUnionCap / kSegThreads;         // union slots per thread
 static_assert(kEdgeEntries % kSegThreads == 0 || kSegThreads % kEdgeEntries == 0, "edge table load");
 constexpr int kEdgeJ = (kEdgeEntries + kSegThreads - 1) / kSegThreads;
+constexpr int kAllPer = kMaxSeqLen / kSegThreads;          // positions of a sequence per thread
+constexpr int kHPer = kHBins / kSegThreads;                // histogram bins per thread
+constexpr int kListPer = 8;                                // list entries per thread
+constexpr int kListCap = kListPer * kSegThreads;           // list entries of a (sequence, KV head)
+constexpr int kMaxSegs = kMaxSeqLen / kSegLen;             // segments of a sequence
+constexpr int kMomChunk = 4096;                            // scale-matching entries per LDS round
+static_assert(kAllPer <= 32 && kHPer % 4 == 0 && kMaxSegs <= kSegThreads / 64, "select layout");
 
 __device__ __forceinline__ int find_seg(const SeqTable &st, int seg) {
   int b = 0;
@@ -1208,8 +1304,8 @@ __device__ __forceinline__ int find_seg(const SeqTable &st, int seg) {
 
 // Slots of the set elements of a strided layout (element j of thread t is
 // item t + j*NT) in item order: pre[j*NW + wave] receives the number of set
-// elements before (j, wave); an element's slot is that plus its lane rank in
-// the ballot.  Ends with a barrier.
+// elements before (j, wave), and pre[PER*NW] the total; an element's slot is
+// pre[j*NW + wave] plus its lane rank in the ballot.  Ends with a barrier.
 template <int PER, int NT>
 __device__ __forceinline__ void ordered_bases(uint32_t msk, unsigned *pre) {
   constexpr int NW = NT / 64, NE = PER * NW, E = (NE + 63) / 64;
@@ -1227,12 +1323,14 @@ __device__ __forceinline__ void ordered_bases(uint32_t msk, unsigned *pre) {
       x[e] = (lane * E + e < NE) ? pre[lane * E + e] : 0u;
       s += x[e];
     }
-    unsigned ex = wave_incl_sum_u(s) - s;
+    const unsigned incl = wave_incl_sum_u(s);
+    unsigned ex = incl - s;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       if (lane * E + e < NE) pre[lane * E + e] = ex;
       ex += x[e];
     }
+    if (lane == 63) pre[NE] = incl;
   }
   __syncthreads();
 }
@@ -1240,24 +1338,61 @@ __device__ __forceinline__ unsigned lane_rank(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
 }
 
-// Calibration kernel.  Completes V = E + L + T next to chunk boundaries (the
-// L neighbours in another chunk, from this layer's E in the history), writes
-// the pooled window score pB and pooled evidence pV over I for the segment
-// (Eq. bacon_score is pooled as pool(B + lambda V) = pB + lambda pV), and the
-// segment's top-min(M, kSegLen) of B with their V (Eq. scale_matching_set).
-__global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
+// The thread's kHPer consecutive bins of a histogram row.
+__device__ __forceinline__ void load_bins(const unsigned *gh, unsigned *cb) {
+  const u32x4 *hp = reinterpret_cast<const u32x4 *>(gh + kHPer * threadIdx.x);
+#pragma unroll
+  for (int q = 0; q < kHPer / 4; ++q) {
+    const u32x4 v = hp[q];
+    cb[4 * q + 0] = v.x; cb[4 * q + 1] = v.y; cb[4 * q + 2] = v.z; cb[4 * q + 3] = v.w;
+  }
+}
+
+// Exact top-k threshold (xk, pthr) of the keys key(j), j < PER, of the block
+// (0 = not a candidate) from the histogram gh of those keys: element j is
+// kept iff key > xk, or key == xk and position <= pthr.  1 <= k <= count.
+// Ends with a barrier.
+template <int PER, typename KeyF, typename PosF>
+__device__ __forceinline__ void hist_threshold(const unsigned *gh, KeyF key, PosF pos, int k,
+                                               unsigned &xk, int &pthr,
+                                               SelSharedT<kSegThreads> &ss, unsigned *ckey,
+                                               int *cpos) {
+  constexpr int NT = kSegThreads;
+  unsigned cb[kHPer];
+  load_bins(gh, cb);
+  bins_boundary<kHPer, NT>(cb, k, ss);
+  const int beta = ss.bc_i[0];
+  const int need = k - ss.bc_i[1];
+  const unsigned C = ss.bc_u[2];
+  __syncthreads();
+  if (C <= (unsigned)kCandCap) {
+    compact_ballot<PER, NT>([&](int j) { const unsigned x = key(j); return x != 0u && hbin(x) == beta; },
+                            key, pos, ckey, cpos, ss);
+    rank_pick<NT>((int)C, need, ckey, cpos, ss, xk, pthr);
+  } else {
+    block_threshold<PER>(key, pos, k, xk, pthr, ss, ckey, cpos);
+  }
+}
+
+// The lists of the nseg segments of a (sequence, KV head) as one sequence of
+// entries e = t + j*NT: segment e / cap, slot e % cap.  `fits` is false when
+// a segment's count exceeds cap.
+struct ListView {
+  int nseg, cap;
+  bool fits;
+};
+
+// Calibration kernel (segment_calib).
+__global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ float Bs[kSegWin], Vs[kSegWin];
   __shared__ float ed[kEdgeEntries];
-  __shared__ unsigned ckey[kCandCap];
-  __shared__ int cpos[kCandCap];
   __shared__ SelSharedT<NT> ss;
-  __shared__ unsigned pre[kUnionPer * NW];
+  __shared__ unsigned pre[PER * NW + 1];
   const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
-  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
   const int i0 = sg * kSegLen;
@@ -1265,6 +1400,13 @@ __global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
   const int64_t base = (int64_t)h * a.T + st.cu[b];
   const int r = a.radius, CH = a.vp_chunk, tr = max(2 * r, 1);
   const bool use_l = (a.terms & 2u) != 0 && r > 0 && CH < n;
+  int M = (int)floorf(a.rho * (float)st.budget[b]);
+  M = max(0, min(M, nc));
+  const bool calib = M > 0 && a.use_last_query;
+  // the bins of the B histogram (accumulated by the fused pass), in flight
+  // with the loads below
+  unsigned cb[kHPer];
+  if (calib) load_bins(a.hist_B + ((int64_t)b * a.Hkv + h) * kHBins, cb);
   // chunk boundaries m*CH (1 <= m <= (n-1)/CH) whose positions [m*CH - r,
   // m*CH + r) meet the window; the host keeps their count times 2r within
   // kEdgeEntries for the whole sequence
@@ -1325,134 +1467,150 @@ __global__ __launch_bounds__(kSegThreads) void k_sega(SegArgs a, SeqTable st) {
   }
   __syncthreads();
 
-  // pooled B and V of the segment's positions over I (truncated windows)
+  // V, and the pooled B and V over I (truncated windows), of the segment's candidates
   const int hp = a.pool_half;
-  const int ncand = max(0, min(i0 + kSegLen, nc) - i0);    // candidates in the segment
-  float xb[PER], xv[PER];                                  // B, V at the thread's positions
-  {
-    const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
+  const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
+  float xb[PER], xv[PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int q = t + j * NT, i = i0 + q;
-      xb[j] = Bs[kPoolHalo + q];
-      xv[j] = Vs[kPoolHalo + q];
-      if (q < ncand) {
-        const int lo = max(0, i - hp), hi = min(nc - 1, i + hp);
-        float sb = 0.f, sv = 0.f;
-        for (int u = lo - w0; u <= hi - w0; ++u) { sb += Bs[u]; sv += Vs[u]; }
-        const float cnt = (float)(hi - lo + 1);
-        a.vec_pB[tile + q] = sb / cnt;
-        a.vec_pV[tile + q] = sv / cnt;
-      }
+  for (int j = 0; j < PER; ++j) {
+    const int q = t + j * NT, i = i0 + q;
+    xb[j] = Bs[kPoolHalo + q];
+    xv[j] = Vs[kPoolHalo + q];
+    if (q < ncand) {
+      const int lo = max(0, i - hp), hi = min(nc - 1, i + hp);
+      float sb = 0.f, sv = 0.f;
+      for (int u = lo - w0; u <= hi - w0; ++u) { sb += Bs[u]; sv += Vs[u]; }
+      const float cnt = (float)(hi - lo + 1);
+      a.vec_pB[base + i] = sb / cnt;
+      a.vec_pV[base + i] = sv / cnt;
+      a.vec_V[base + i] = xv[j];
     }
   }
+  if (!calib) return;
 
-  int M = (int)floorf(a.rho * (float)st.budget[b]);
-  M = max(0, min(M, nc));
-  if (M == 0 || !a.use_last_query) return;            // no calibration: lambda = 0
-  // the segment's top-Mc of B, in ascending position
-  const int Mc = st.mc[b];
-  const int64_t slot0 = (int64_t)h * a.cand_stride + st.cand_base[b] + (int64_t)sg * Mc;
-  {
-    auto keyB = [&](int j) -> unsigned { return t + j * NT < ncand ? float_key(xb[j]) : 0u; };
-    auto posf = [&](int j) -> int { return i0 + t + j * NT; };
-    uint32_t msk = 0;
-    if (ncand <= Mc) {
+  // boundary bin of the top-M of B, and the segment's list of candidates at
+  // or above it (key, position, V) in position order
+  bins_boundary<kHPer, NT>(cb, M, ss);
+  const int beta = ss.bc_i[0], above = ss.bc_i[1];
+  const unsigned cntb = ss.bc_u[2];
+  uint32_t msk = 0;
 #pragma unroll
-      for (int j = 0; j < PER; ++j) msk |= (t + j * NT < ncand ? 1u : 0u) << j;
-    } else {
-      unsigned xm;
-      int pm;
-      block_threshold<PER>(keyB, posf, Mc, xm, pm, ss, ckey, cpos);
+  for (int j = 0; j < PER; ++j)
+    msk |= (t + j * NT < ncand && hbin(float_key(xb[j])) >= beta ? 1u : 0u) << j;
+  ordered_bases<PER, NT>(msk, pre);
 #pragma unroll
-      for (int j = 0; j < PER; ++j) {
-        const unsigned kj = keyB(j);
-        msk |= (kj > xm || (kj == xm && posf(j) <= pm) ? 1u : 0u) << j;
-      }
+  for (int j = 0; j < PER; ++j) {
+    const bool in = (msk >> j) & 1u;
+    const uint64_t m = __ballot(in);
+    if (in) {
+      const int64_t o = base + i0 + pre[j * NW + wave] + lane_rank(m);
+      a.listB_key[o] = float_key(xb[j]);
+      a.listB_pos[o] = i0 + t + j * NT;
+      a.listB_v[o] = xv[j];
     }
-    ordered_bases<PER, NT>(msk, pre);
+  }
+  if (t == 0) a.cntB[(int64_t)h * st.total_segs + gs] = (int)pre[PER * NW];
+  if (sg == 0 && t == 0) a.recB[b * a.Hkv + h] = make_int4(beta, above, M - above, (int)cntb);
+}
+
+// Loads the selection record and the segments' lists of a (sequence, KV
+// head) into registers (entry e = t + j*NT), every slot a segment may hold,
+// with the counts in flight alongside; entries beyond their segment's count
+// get key 0.  scnt is LDS for the kMaxSegs counts.  Ends with a barrier.
+template <bool WITH_V>
+__device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t base, int n, int h,
+                                           const int4 *recp, const unsigned *lkey, const int *lpos,
+                                           const float *lv, const int *cnts, int *scnt, ListView &L,
+                                           int4 &rec, unsigned *k, int *p, float *v) {
+  constexpr int NT = kSegThreads;
+  const int t = threadIdx.x;
+  L.nseg = st.seg_base[b + 1] - st.seg_base[b];
+  L.cap = ((kListCap / L.nseg) / 64) * 64;
+  const int tt = opaque(t);
+  rec = *recp;                                   // first: it heads the longest chain
+  int c = 0;
+  if (tt < L.nseg) c = cnts[(int64_t)h * st.total_segs + st.seg_base[b] + tt];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const bool in = (msk >> j) & 1u;
-      const uint64_t m = __ballot(in);
-      if (in) {
-        const int64_t o = slot0 + pre[j * NW + wave] + lane_rank(m);
-        a.cand_key[o] = float_key(xb[j]);
-        a.cand_pos[o] = posf(j);
-        a.cand_v[o] = xv[j];
-      }
-    }
-    for (int q = min(ncand, Mc) + t; q < Mc; q += NT) a.cand_key[slot0 + q] = 0u;   // empty slots
+  for (int j = 0; j < kListPer; ++j) {
+    const int e = tt + j * NT, s = min(e / L.cap, L.nseg - 1);
+    const int64_t o = base + min(s * kSegLen + (e - s * L.cap), n - 1);
+    k[j] = lkey[o];
+    p[j] = lpos[o];
+    if constexpr (WITH_V) v[j] = lv[o];
+  }
+  if (t < kMaxSegs) scnt[t] = t < L.nseg ? c : 0;
+  __syncthreads();
+  const int over = (t < kMaxSegs && scnt[t] > L.cap) ? 1 : 0;
+  L.fits = __syncthreads_or(over) == 0;
+#pragma unroll
+  for (int j = 0; j < kListPer; ++j) {
+    const int e = t + j * NT, s = e / L.cap;
+    if (s >= L.nseg || e - s * L.cap >= scnt[s]) k[j] = 0u;   // 0: not an entry
   }
 }
 
-// Top M of B over the union of the segments' candidates of a (sequence, KV
-// head) (Eq. scale_matching_set) and lambda = gamma Std(B) / (Std(V) + eps)
-// over it (Eq. lambda_solution); population moments in double, B shifted by
-// the set minimum.  Every thread returns lambda.
-__device__ __forceinline__ float segment_lambda(const SegArgs &a, const SeqTable &st, int b, int h,
-                                                int M, SelSharedT<kSegThreads> &ss, unsigned *ckey,
-                                                int *cpos) {
-  constexpr int NT = kSegThreads;
-  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
-  const int U = nseg * st.mc[b];                    // <= kUnionCap (host check)
-  const int64_t c0 = (int64_t)h * a.cand_stride + st.cand_base[b];
-  const int t = threadIdx.x;
-  unsigned ck[kUnionPer];
-  int cp[kUnionPer];
-  float cv[kUnionPer];
+// Scale-matching set and the thread's part of its moments over every
+// candidate of a sequence, for lists beyond one workgroup: the B of all
+// candidates in registers, the exact threshold over them; V is read for the
+// members only.  Kept out of line so that its registers do not weigh on the
+// list path of the calling kernel.
+__device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_t base, int nc, int M,
+                                                         const unsigned *gh, SelSharedT<kSegThreads> &ss,
+                                                         unsigned *ckey, int *cpos, unsigned *pre,
+                                                         float2 *mom, double *part) {
+  constexpr int NT = kSegThreads, NW = NT / 64;
+  const int t = threadIdx.x, wave = t >> 6;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  float xb[kAllPer];
   {
     const int tt = opaque(t);
 #pragma unroll
-    for (int j = 0; j < kUnionPer; ++j) {
-      const int q = min(tt + j * NT, U - 1);
-      ck[j] = a.cand_key[c0 + q];
-      cp[j] = a.cand_pos[c0 + q];
-      cv[j] = a.cand_v[c0 + q];
-    }
-#pragma unroll
-    for (int j = 0; j < kUnionPer; ++j) if (tt + j * NT >= U) ck[j] = 0u;
+    for (int j = 0; j < kAllPer; ++j) xb[j] = a.vec_B[base + min(tt + j * NT, nc - 1)];
   }
-  auto keyU = [&](int j) -> unsigned { return ck[j]; };
-  auto posU = [&](int j) -> int { return cp[j]; };
+  auto keyB = [&](int j) -> unsigned { return t + j * NT < nc ? float_key(xb[j]) : 0u; };
+  auto posf = [&](int j) -> int { return t + j * NT; };
   unsigned xm;
   int pm;
-  block_threshold<kUnionPer>(keyU, posU, M, xm, pm, ss, ckey, cpos);
-  uint32_t inm = 0;
+  hist_threshold<kAllPer>(gh, keyB, posf, M, xm, pm, ss, ckey, cpos);
+  uint32_t msk = 0;
 #pragma unroll
-  for (int j = 0; j < kUnionPer; ++j)
-    inm |= (ck[j] > xm || (ck[j] == xm && ck[j] != 0u && cp[j] <= pm) ? 1u : 0u) << j;
-  unsigned kmin = 0xffffffffu;
-#pragma unroll
-  for (int j = 0; j < kUnionPer; ++j) kmin = ((inm >> j) & 1u) ? min(kmin, ck[j]) : kmin;
-  kmin = block_reduce_u<0>(kmin, ss);
-  const double bref = (double)key_float(kmin);
-  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-#pragma unroll
-  for (int j = 0; j < kUnionPer; ++j) {
-    const bool in = (inm >> j) & 1u;
-    const double db = in ? (double)key_float(ck[j]) - bref : 0.0, dv = in ? (double)cv[j] : 0.0;
-    s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
+  for (int j = 0; j < kAllPer; ++j) {
+    const unsigned kj = keyB(j);
+    msk |= (kj != 0u && (kj > xm || (kj == xm && posf(j) <= pm)) ? 1u : 0u) << j;
   }
-  double sums[4];
-  block_sum4_d(s0, s1, s2, s3, ss, sums);
-  const double mb = sums[0] / M, mv = sums[2] / M;
-  double vb = sums[1] / M - mb * mb, vv = sums[3] / M - mv * mv;
-  vb = vb > 0.0 ? vb : 0.0;
-  vv = vv > 0.0 ? vv : 0.0;
-  return (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));
+  ordered_bases<kAllPer, NT>(msk, pre);
+  const double bref = (double)key_float(xm);
+  for (int r0 = 0; r0 < M; r0 += kMomChunk) {
+#pragma unroll
+    for (int j = 0; j < kAllPer; ++j) {
+      const bool in = (msk >> j) & 1u;
+      const uint64_t m = __ballot(in);
+      if (in) {
+        const int o = (int)(pre[j * NW + wave] + lane_rank(m)) - r0;
+        if (o >= 0 && o < kMomChunk) mom[o] = make_float2(xb[j], a.vec_V[base + t + j * NT]);
+      }
+    }
+    __syncthreads();
+    const int cnt = min(kMomChunk, M - r0);
+    for (int e = t; e < cnt; e += NT) {
+      const double db = (double)mom[e].x - bref, dv = (double)mom[e].y;
+      s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
+    }
+    __syncthreads();
+  }
+  part[0] = s0; part[1] = s1; part[2] = s2; part[3] = s3;
 }
 
-// Top-K kernel.  Every segment workgroup first solves lambda from the union of
-// the calibration kernel's candidates (the same exact computation in each
-// workgroup of a (sequence, KV head), so no workgroup waits for another), then
-// takes its top-min(K, kSegLen) of the pooled score pB + lambda pV over I.
-__global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
+// Score kernel (segment_score).
+__global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
+  __shared__ unsigned hist[kHBins];
   __shared__ unsigned ckey[kCandCap];
   __shared__ int cpos[kCandCap];
   __shared__ SelSharedT<NT> ss;
-  __shared__ unsigned pre[kUnionPer * NW];
+  __shared__ unsigned pre[kAllPer * NW + 1];
+  __shared__ float2 mom[kMomChunk];
+  __shared__ int scnt[kMaxSegs];
   const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
@@ -1460,148 +1618,257 @@ __global__ __launch_bounds__(kSegThreads) void k_segb(SegArgs a, SeqTable st) {
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
   const int i0 = sg * kSegLen;
-  const int K = st.budget[b];
-  const int Kc = min(K, kSegLen);
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
+  const int64_t base = (int64_t)h * a.T + st.cu[b];
+  const int64_t hrow = ((int64_t)b * a.Hkv + h) * kHBins;
+  for (int q = t; q < kHBins; q += NT) hist[q] = 0u;
 
   // the segment's pooled B and V do not depend on lambda: in flight first
-  const int64_t tile = ((int64_t)h * st.total_segs + gs) * kSegLen;
   float pb[PER], pv[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    pb[j] = a.vec_pB[tile + t + j * NT];
-    pv[j] = a.vec_pV[tile + t + j * NT];
+    const int q = min(t + j * NT, max(ncand - 1, 0));
+    pb[j] = a.vec_pB[base + i0 + q];
+    pv[j] = a.vec_pV[base + i0 + q];
   }
 
-  int M = (int)floorf(a.rho * (float)K);
+  int M = (int)floorf(a.rho * (float)st.budget[b]);
   M = max(0, min(M, nc));
   float lam = 0.f;
-  if (M > 0 && a.use_last_query) lam = segment_lambda(a, st, b, h, M, ss, ckey, cpos);
+  if (M > 0 && a.use_last_query) {
+    int4 rec;                                          // boundary bin, above, need, its count
+    unsigned lk[kListPer];
+    int lp[kListPer];
+    float lv[kListPer];
+    ListView L;
+    load_lists<true>(st, b, base, n, h, a.recB + b * a.Hkv + h, a.listB_key, a.listB_pos, a.listB_v,
+                     a.cntB, scnt, L, rec, lk, lp, lv);
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    if (L.fits && rec.w <= kCandCap) {
+      // the boundary bin's entries, ranked under the tie rule
+      compact_ballot<kListPer, NT>([&](int j) { return lk[j] != 0u && hbin(lk[j]) == rec.x; },
+                                   [&](int j) { return lk[j]; }, [&](int j) { return lp[j]; },
+                                   ckey, cpos, ss);
+      unsigned xm;
+      int pm;
+      rank_pick<NT>(rec.w, rec.z, ckey, cpos, ss, xm, pm);
+      // population moments over the set, B shifted by its smallest member
+      // (the boundary key), in double
+      const double bref = (double)key_float(xm);
+#pragma unroll
+      for (int j = 0; j < kListPer; ++j) {
+        if (lk[j] != 0u && (lk[j] > xm || (lk[j] == xm && lp[j] <= pm))) {
+          const double db = (double)key_float(lk[j]) - bref, dv = (double)lv[j];
+          s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
+        }
+      }
+    } else {
+      double part[4];
+      whole_moments(a, base, nc, M, a.hist_B + hrow, ss, ckey, cpos, pre, mom, part);
+      s0 = part[0]; s1 = part[1]; s2 = part[2]; s3 = part[3];
+    }
+    double sums[4];
+    block_sum4_d(s0, s1, s2, s3, ss, sums);
+    const double mb = sums[0] / M, mv = sums[2] / M;
+    double vb = sums[1] / M - mb * mb, vv = sums[3] / M - mv * mv;
+    vb = vb > 0.0 ? vb : 0.0;
+    vv = vv > 0.0 ? vv : 0.0;
+    lam = (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));
+  }
   if (sg == 0 && t == 0) {
     a.lambda_ws[b * a.Hkv + h] = lam;
     if (a.out_lambda) a.out_lambda[b * a.Hkv + h] = lam;
   }
 
-  int cb = 0;                                        // first slot of the sequence
-  for (int x = 0; x < b; ++x) cb += (st.seg_base[x + 1] - st.seg_base[x]) * min(st.budget[x], kSegLen);
-  const int64_t slot0 = (int64_t)h * a.cand_stride + cb + (int64_t)sg * Kc;
+  // pooled score keys of the segment, and their histogram
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int q = t + j * NT;
+    if (q < ncand) {
+      const unsigned key = float_key(fmaf(lam, pv[j], pb[j]));
+      a.vec_S[base + i0 + q] = key;
+      atomicAdd(&hist[hbin(key)], 1u);
+    }
+  }
+  __syncthreads();
+  unsigned *gh = a.hist_S + hrow;
+  for (int q = t; q < kHBins; q += NT) {
+    const unsigned c = hist[q];
+    if (c) atomicAdd(&gh[q], c);
+  }
+}
+
+// Candidate kernel (segment_cand): the boundary bin of the top-K of the
+// pooled score and the segment's list of entries at or above it.
+__global__ __launch_bounds__(kSegThreads) void k_segcand(SegArgs a, SeqTable st) {
+  constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
+  __shared__ SelSharedT<NT> ss;
+  __shared__ unsigned pre[PER * NW + 1];
+  const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
+  const int wave = t >> 6;
+  const int b = find_seg(st, gs);
+  const int sg = gs - st.seg_base[b];
+  const int n = st.cu[b + 1] - st.cu[b];
+  const int nc = n - a.W;
+  const int i0 = sg * kSegLen;
+  const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
+  const int64_t base = (int64_t)h * a.T + st.cu[b];
+  const int kept = min(st.budget[b], nc);
+  if (kept <= 0 || kept == nc) return;               // none or all kept: no list needed
+  unsigned cb[kHPer];
+  load_bins(a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, cb);
   unsigned key[PER];
 #pragma unroll
-  for (int j = 0; j < PER; ++j)
-    key[j] = t + j * NT < ncand ? float_key(fmaf(lam, pv[j], pb[j])) : 0u;
-  auto keyS = [&](int j) -> unsigned { return key[j]; };
-  auto posf = [&](int j) -> int { return i0 + t + j * NT; };
+  for (int j = 0; j < PER; ++j) key[j] = a.vec_S[base + i0 + min(t + j * NT, max(ncand - 1, 0))];
+  bins_boundary<kHPer, NT>(cb, kept, ss);
+  const int beta = ss.bc_i[0], above = ss.bc_i[1];
+  const unsigned cntb = ss.bc_u[2];
   uint32_t msk = 0;
-  if (ncand <= Kc) {
 #pragma unroll
-    for (int j = 0; j < PER; ++j) msk |= (t + j * NT < ncand ? 1u : 0u) << j;
-  } else {
-    unsigned xk;
-    int pk;
-    block_threshold<PER>(keyS, posf, Kc, xk, pk, ss, ckey, cpos);
-#pragma unroll
-    for (int j = 0; j < PER; ++j)
-      msk |= (key[j] > xk || (key[j] == xk && posf(j) <= pk) ? 1u : 0u) << j;
-  }
+  for (int j = 0; j < PER; ++j) msk |= (t + j * NT < ncand && hbin(key[j]) >= beta ? 1u : 0u) << j;
   ordered_bases<PER, NT>(msk, pre);
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const bool in = (msk >> j) & 1u;
     const uint64_t m = __ballot(in);
     if (in) {
-      const int64_t o = slot0 + pre[j * NW + wave] + lane_rank(m);
-      a.cand2_key[o] = key[j];
-      a.cand2_pos[o] = posf(j);
+      const int64_t o = base + i0 + pre[j * NW + wave] + lane_rank(m);
+      a.listS_key[o] = key[j];
+      a.listS_pos[o] = i0 + t + j * NT;
     }
   }
-  for (int q = min(ncand, Kc) + t; q < Kc; q += NT) a.cand2_key[slot0 + q] = 0u;
+  if (t == 0) a.cntS[(int64_t)h * st.total_segs + gs] = (int)pre[PER * NW];
+  if (sg == 0 && t == 0) a.recS[b * a.Hkv + h] = make_int4(beta, above, kept - above, (int)cntb);
 }
 
-// Final kernel, one workgroup per (sequence, KV head): the exact top-K over
-// the union of the segments' candidates (Eq. topk_selection, ties to the lower
-// position), indices in ascending position (-1 beyond |I|), then the
-// compacted cache: kept rows, the W window rows, zero rows up to K + W.
-__global__ __launch_bounds__(kSegThreads) void k_final(SegArgs a, SeqTable st) {
+// Top-K over every candidate of a sequence for lists beyond one workgroup:
+// the pooled score keys of all candidates in registers, the exact threshold
+// over them, the kept positions in ascending order into tbl (and idx unless
+// it is null).  Kept out of line like whole_moments.
+__device__ __attribute__((noinline)) void whole_topk(const SegArgs &a, int64_t base, int nc, int kept,
+                                                      const unsigned *gh, int32_t *idx, int *tbl,
+                                                      SelSharedT<kSegThreads> &ss, unsigned *ckey,
+                                                      int *cpos, unsigned *pre) {
+  constexpr int NT = kSegThreads, NW = NT / 64;
+  const int t = threadIdx.x, wave = t >> 6;
+  unsigned key[kAllPer];
+  {
+    const int tt = opaque(t);
+#pragma unroll
+    for (int j = 0; j < kAllPer; ++j) key[j] = a.vec_S[base + min(tt + j * NT, nc - 1)];
+#pragma unroll
+    for (int j = 0; j < kAllPer; ++j) if (tt + j * NT >= nc) key[j] = 0u;
+  }
+  auto keyS = [&](int j) -> unsigned { return key[j]; };
+  auto posf = [&](int j) -> int { return t + j * NT; };
+  unsigned xk;
+  int pk;
+  hist_threshold<kAllPer>(gh, keyS, posf, kept, xk, pk,
+                          ss, ckey, cpos);
+  uint32_t msk = 0;
+#pragma unroll
+  for (int j = 0; j < kAllPer; ++j)
+    msk |= (key[j] != 0u && (key[j] > xk || (key[j] == xk && posf(j) <= pk)) ? 1u : 0u) << j;
+  // element j of thread t is position t + j*NT, so slot order is position order
+  ordered_bases<kAllPer, NT>(msk, pre);
+#pragma unroll
+  for (int j = 0; j < kAllPer; ++j) {
+    const bool in = (msk >> j) & 1u;
+    const uint64_t m = __ballot(in);
+    if (in) {
+      const unsigned o = pre[j * NW + wave] + lane_rank(m);
+      if (idx) idx[o] = posf(j);
+      tbl[o] = posf(j);
+    }
+  }
+}
+
+// Final kernel (final_topk): `parts` workgroups per (sequence, KV head)
+// select the same top-K; part 0 writes the indices, each part gathers its
+// share of the compacted rows (kept positions, the W window rows, zero rows
+// up to K + W).
+__global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st) {
   constexpr int NT = kSegThreads, NW = NT / 64;
   extern __shared__ __align__(16) int tbl[];         // [K + W] source position of each row
   __shared__ unsigned ckey[kCandCap];
   __shared__ int cpos[kCandCap];
   __shared__ SelSharedT<NT> ss;
-  __shared__ unsigned pre[kUnionPer * NW];
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  __shared__ unsigned pre[kAllPer * NW + 1];
+  __shared__ int scnt[kMaxSegs];
+  const int part = blockIdx.x, b = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
   const int wave = t >> 6;
-  const int nseg = st.seg_base[b + 1] - st.seg_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
   const int K = st.budget[b];
   const int kept = min(K, nc);
-  const int Kc = min(K, kSegLen);
-  int cb = 0;
-  for (int x = 0; x < b; ++x) cb += (st.seg_base[x + 1] - st.seg_base[x]) * min(st.budget[x], kSegLen);
-  const int64_t c0 = (int64_t)h * a.cand_stride + cb;
+  const int64_t base = (int64_t)h * a.T + st.cu[b];
   int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
-  if (kept > 0) {
-    const int U = nseg * Kc;                        // <= kUnionCap (host check)
-    unsigned ck[kUnionPer];
-    int cp[kUnionPer];
-    {
-      const int tt = opaque(t);
-#pragma unroll
-      for (int j = 0; j < kUnionPer; ++j) {
-        const int q = min(tt + j * NT, U - 1);
-        ck[j] = a.cand2_key[c0 + q];
-        cp[j] = a.cand2_pos[c0 + q];
-      }
-#pragma unroll
-      for (int j = 0; j < kUnionPer; ++j) if (tt + j * NT >= U) ck[j] = 0u;
+  if (kept > 0 && kept == nc) {
+    // every candidate is kept
+    for (int j = t; j < nc; j += NT) {
+      if (part == 0) idx[j] = j;
+      tbl[j] = j;
     }
-    uint32_t msk = 0;
-    if (kept == nc) {
-#pragma unroll
-      for (int j = 0; j < kUnionPer; ++j) msk |= (ck[j] != 0u ? 1u : 0u) << j;
-    } else {
-      auto keyU = [&](int j) -> unsigned { return ck[j]; };
-      auto posU = [&](int j) -> int { return cp[j]; };
+  } else if (kept > 0) {
+    int4 rec;
+    unsigned lk[kListPer];
+    int lp[kListPer];
+    ListView L;
+    load_lists<false>(st, b, base, n, h, a.recS + b * a.Hkv + h, a.listS_key, a.listS_pos, nullptr,
+                      a.cntS, scnt, L, rec, lk, lp, nullptr);
+    if (L.fits && rec.w <= kCandCap) {
+      compact_ballot<kListPer, NT>([&](int j) { return lk[j] != 0u && hbin(lk[j]) == rec.x; },
+                                   [&](int j) { return lk[j]; }, [&](int j) { return lp[j]; },
+                                   ckey, cpos, ss);
       unsigned xk;
       int pk;
-      block_threshold<kUnionPer>(keyU, posU, kept, xk, pk, ss, ckey, cpos);
+      rank_pick<NT>(rec.w, rec.z, ckey, cpos, ss, xk, pk);
+      uint32_t msk = 0;
 #pragma unroll
-      for (int j = 0; j < kUnionPer; ++j)
-        msk |= (ck[j] > xk || (ck[j] == xk && ck[j] != 0u && cp[j] <= pk) ? 1u : 0u) << j;
-    }
-    // the union is held in ascending position, so slot order is position order
-    ordered_bases<kUnionPer, NT>(msk, pre);
+      for (int j = 0; j < kListPer; ++j)
+        msk |= (lk[j] != 0u && (lk[j] > xk || (lk[j] == xk && lp[j] <= pk)) ? 1u : 0u) << j;
+      // entries are in (segment, slot) = position order
+      ordered_bases<kListPer, NT>(msk, pre);
 #pragma unroll
-    for (int j = 0; j < kUnionPer; ++j) {
-      const bool in = (msk >> j) & 1u;
-      const uint64_t m = __ballot(in);
-      if (in) {
-        const unsigned o = pre[j * NW + wave] + lane_rank(m);
-        idx[o] = cp[j];
-        tbl[o] = cp[j];
+      for (int j = 0; j < kListPer; ++j) {
+        const bool in = (msk >> j) & 1u;
+        const uint64_t m = __ballot(in);
+        if (in) {
+          const unsigned o = pre[j * NW + wave] + lane_rank(m);
+          if (part == 0) idx[o] = lp[j];
+          tbl[o] = lp[j];
+        }
       }
+    } else {
+      whole_topk(a, base, nc, kept, a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, part == 0 ? idx : nullptr,
+                 tbl, ss, ckey, cpos, pre);
     }
   }
-  // output rows: kept positions, the W window rows, then zero rows up to K + W
-  for (int j = max(kept, 0) + t; j < K; j += NT) idx[j] = -1;
+  if (part == 0)
+    for (int j = max(kept, 0) + t; j < K; j += NT) idx[j] = -1;
   for (int w = t; w < a.W; w += NT) tbl[kept + w] = nc + w;
   for (int j = kept + a.W + t; j < K + a.W; j += NT) tbl[j] = -1;
   __syncthreads();
 
+  // this part's rows of the compacted cache
+  const int rows = K + a.W;
+  const int per = (rows + a.parts - 1) / a.parts;
+  const int r0 = part * per, r1 = min(rows, r0 + per);
   const int pieces = a.row_bytes / 16;
-  const int total = (K + a.W) * pieces;
+  const int total = max(0, r1 - r0) * pieces;
   const unsigned char *ks = static_cast<const unsigned char *>(a.k);
   const unsigned char *vs = static_cast<const unsigned char *>(a.v);
   unsigned char *ko = static_cast<unsigned char *>(a.k_out);
   unsigned char *vo = static_cast<unsigned char *>(a.v_out);
-  constexpr int BATCH = 5;
+  constexpr int BATCH = 4;
   for (int q0 = t; q0 < total; q0 += BATCH * NT) {
     u32x4 kv[BATCH], vv[BATCH];
     int srcs[BATCH];
 #pragma unroll
     for (int u = 0; u < BATCH; ++u) {
       const int q = min(q0 + u * NT, total - 1);
-      const int rr = q / pieces, p = q - rr * pieces;
+      const int rr = r0 + q / pieces, p = q % pieces;
       srcs[u] = tbl[rr];
       const int64_t so = ((int64_t)(st.cu[b] + max(srcs[u], 0)) * a.Hkv + h) * a.row_bytes + 16 * p;
       kv[u] = *reinterpret_cast<const u32x4 *>(ks + so);
@@ -1611,7 +1878,7 @@ __global__ __launch_bounds__(kSegThreads) void k_final(SegArgs a, SeqTable st) {
     for (int u = 0; u < BATCH; ++u) {
       const int q = q0 + u * NT;
       if (q < total) {
-        const int rr = q / pieces, p = q - rr * pieces;
+        const int rr = r0 + q / pieces, p = q % pieces;
         const int64_t dst = ((int64_t)(st.kept_base[b] + rr) * a.Hkv + h) * a.row_bytes + 16 * p;
         const u32x4 z = u32x4{0u, 0u, 0u, 0u};
         *reinterpret_cast<u32x4 *>(ko + dst) = srcs[u] >= 0 ? kv[u] : z;
@@ -1623,26 +1890,33 @@ __global__ __launch_bounds__(kSegThreads) void k_final(SegArgs a, SeqTable st) {
 
 size_t final_lds_bytes(int max_budget, int window) {
   return (size_t)(max_budget + window) * sizeof(int) + 2 * kCandCap * sizeof(unsigned) +
-         sizeof(SelSharedT<kSegThreads>) + kUnionPer * (kSegThreads / 64) * sizeof(unsigned);
+         sizeof(SelSharedT<kSegThreads>) + (kAllPer * (kSegThreads / 64) + 1) * sizeof(unsigned) +
+         kMaxSegs * sizeof(int);
 }
 
-hipError_t launch_final(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s) {
+hipError_t launch_segcal(const SegArgs &a, const SeqTable &st, hipStream_t s) {
+  dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
+  hipLaunchKernelGGL(k_segcal, grid, block, 0, s, a, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_segscore(const SegArgs &a, const SeqTable &st, hipStream_t s) {
+  dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
+  hipLaunchKernelGGL(k_segscore, grid, block, 0, s, a, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_segcand(const SegArgs &a, const SeqTable &st, hipStream_t s) {
+  dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
+  hipLaunchKernelGGL(k_segcand, grid, block, 0, s, a, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_segfinal(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s) {
   const size_t lds = (size_t)(max_budget + a.W) * sizeof(int);
-  if (final_lds_bytes(max_budget, a.W) > (size_t)kLdsBytes) return hipErrorInvalidValue;
-  allow_lds(k_final, lds);
-  hipLaunchKernelGGL(k_final, dim3(st.batch, a.Hkv), dim3(kSegThreads), lds, s, a, st);
-  return hipGetLastError();
-}
-
-hipError_t launch_sega(const SegArgs &a, const SeqTable &st, hipStream_t s) {
-  dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
-  hipLaunchKernelGGL(k_sega, grid, block, 0, s, a, st);
-  return hipGetLastError();
-}
-
-hipError_t launch_segb(const SegArgs &a, const SeqTable &st, hipStream_t s) {
-  dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
-  hipLaunchKernelGGL(k_segb, grid, block, 0, s, a, st);
+  if (final_lds_bytes(max_budget, a.W) > (size_t)kLdsBytes || a.parts < 1) return hipErrorInvalidValue;
+  allow_lds(k_segfinal, lds);
+  hipLaunchKernelGGL(k_segfinal, dim3(a.parts, st.batch, a.Hkv), dim3(kSegThreads), lds, s, a, st);
   return hipGetLastError();
 }
 

@@ -169,8 +169,7 @@ EDGE = {
                                         ((10, 800),), 3, 21)),
     # the largest batch: 64 sequences of ragged lengths and budgets
     "batch64": dict(wl=_batch64()),
-    # candidate unions beyond one workgroup: one select workgroup per
-    # (sequence, KV head) over the whole sequence
+    # large budgets: scale-matching set and kept set of thousands of positions
     "large-budget-whole-sequence": dict(wl=inputs.Workload("edge", 2, 8, 2, 128, 32, 7, "bf16",
                                                            (20000, 3000), (3000, 200),
                                                            ((30, 19000), (10, 2500)), 4, 19)),
