@@ -101,7 +101,7 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.vec_pv = off;   off += align256(vec);
   L.vec_s = off;    off += align256(vec);
   const size_t hist = (size_t)s->max_batch * s->num_kv_heads * kHBins * sizeof(unsigned);
-  L.hist_b = off;   off += align256(hist);
+  L.hist_b = off;   off += align256(hist * kHCopies);
   L.hist_s = off;   off += align256(hist);
   L.list_bk = off;  off += align256(vec);
   L.list_bp = off;  off += align256(vec);

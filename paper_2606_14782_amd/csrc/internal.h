@@ -18,6 +18,7 @@ constexpr int kSegLen = 2048;       // positions per segment of the histogram se
 constexpr int kSegThreads = 1024;
 constexpr int kPoolHalo = 16;       // largest pool half-width
 constexpr int kHBins = 8192;        // bins of the select histograms (32 per octave of a float)
+constexpr int kHCopies = 2;         // copies of the B histogram the fused pass spreads its atomics over
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU (and per workgroup) on gfx950
 constexpr int kEdgeEntries = 1024;      // positions next to chunk boundaries the select stages
 
@@ -47,7 +48,8 @@ struct PassArgs {
   float2 *partials;     // [Hkv, total_chunks, Rpad]  (max, sum) per chunk, log2 units
   float *lse2;          // [B, Hkv, Rpad] row normalisers, log2 units (merge kernel writes)
   float *lse_user;      // optional [B, Hq, W] natural-log normaliser (merge kernel writes)
-  unsigned *hist_B, *hist_S;   // optional [B, Hkv, kHBins] select histograms pass 1 clears
+  unsigned *hist_B, *hist_S;   // optional select histograms pass 1 clears: [B, Hkv, kHCopies, kHBins]
+                               // and [B, Hkv, kHBins]
   // PASS_SCORE
   float *out_B, *out_Q; // [Hkv, T]
   // PASS_FUSED
@@ -101,7 +103,8 @@ struct SegArgs {
   float *vec_V;                  // [Hkv, T] V = E + L + T over I
   float *vec_pB, *vec_pV;        // [Hkv, T] pooled B and V over I
   unsigned *vec_S;               // [Hkv, T] keys of the pooled score over I
-  unsigned *hist_B, *hist_S;     // [B, Hkv, kHBins] key histograms of B and of the pooled score
+  unsigned *hist_B, *hist_S;     // key histograms of B [B, Hkv, kHCopies, kHBins] (the bin count is
+                                 // the sum of the copies) and of the pooled score [B, Hkv, kHBins]
   // per-segment lists at or above a boundary bin: segment s of a sequence
   // writes slots [s*kSegLen, ...) of the [Hkv, T] arrays, its count to cnt
   unsigned *listB_key, *listS_key;

@@ -41,6 +41,12 @@ namespace bacon {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void g_void;
+
+// s_waitcnt immediate (gfx9 encoding) waiting for vmcnt = 0 only:
+// vmcnt bits [3:0] and [15:14] zero, expcnt [6:4] and lgkmcnt [11:8] at max.
+constexpr int kWaitVm0 = 0x0F70;
 
 constexpr float kLn2 = 0.69314718055994531f;
 
@@ -182,45 +188,53 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   float *cv = ce + a.chunk;                                            // [chunk]
   float *cb = cv + a.chunk;                                            // [chunk]
 
-  // Stage loader: thread t moves pieces q = t + j*nt of the stage.
+  // Stage loader: direct-to-LDS 16-byte loads (no register staging).  LDS
+  // slot s of a stage holds piece (s % PIECES) ^ (key & SWM) of key
+  // s / PIECES; load instruction i fills the 64 slots [64 i, 64 i + 64),
+  // lane l slot 64 i + l, and wave w issues instructions w, w + nw, ...
+  // Loads are unconditional: keys past the chunk are clamped to valid
+  // addresses (their data is masked).  The thread's global offsets are the
+  // same in every full stage: one uniform base plus them.
   const unsigned char *kb = static_cast<const unsigned char *>(a.k) +
                             ((int64_t)st.cu[b] * a.Hkv + h) * C::ROWB;
   const int64_t kstride = (int64_t)a.Hkv * C::ROWB;
-  const int stage_pieces = tk * C::PIECES;
-  // Straight-line, unconditional loads: pieces past the stage and keys past
-  // the chunk are clamped to valid addresses (duplicates are masked or
-  // rewritten with identical data), so all loads stay in flight together.
-  // The thread's piece offsets are the same in every stage: a full stage is
-  // one uniform base plus them.
-  u32x4 pre[C::MAXL];
-  int goff[C::MAXL], loff[C::MAXL];
+  const int nins = tk * C::PIECES / 64;           // load instructions per stage
+  int goff[C::MAXL];
 #pragma unroll
   for (int j = 0; j < C::MAXL; ++j) {
-    const int q = min(t + j * nt, stage_pieces - 1);
-    const int key = q / C::PIECES, pc = q % C::PIECES;
+    const int sl = min(wave + nw * j, nins - 1) * 64 + lane;
+    const int key = sl / C::PIECES, pc = (sl % C::PIECES) ^ (key & C::SWM);
     goff[j] = key * (int)kstride + 16 * pc;
-    loff[j] = key * C::ROWB + 16 * (pc ^ (key & C::SWM));
   }
   auto fetch = [&](int s) {
     const int key0 = k0 + s * tk;
+    unsigned char *dst = kbuf + (s & 1) * tk * C::ROWB;
     if (key0 + tk <= k1) {
       const unsigned char *base = kb + (int64_t)key0 * kstride;
 #pragma unroll
-      for (int j = 0; j < C::MAXL; ++j) pre[j] = *reinterpret_cast<const u32x4 *>(base + goff[j]);
+      for (int j = 0; j < C::MAXL; ++j) {
+        const int i = wave + nw * j;
+        if (i < nins)
+          __builtin_amdgcn_global_load_lds((const g_void *)(base + goff[j]), (lds_void *)(dst + i * 1024),
+                                           16, 0, 0);
+      }
     } else {
 #pragma unroll
       for (int j = 0; j < C::MAXL; ++j) {
-        const int q = min(t + j * nt, stage_pieces - 1);
-        const int key = min(key0 + q / C::PIECES, k1 - 1);
-        pre[j] = *reinterpret_cast<const u32x4 *>(kb + (int64_t)key * kstride + 16 * (q % C::PIECES));
+        const int i = wave + nw * j;
+        if (i < nins) {
+          const int sl = i * 64 + lane;
+          const int kk = sl / C::PIECES, pc = (sl % C::PIECES) ^ (kk & C::SWM);
+          const int key = min(key0 + kk, k1 - 1);
+          __builtin_amdgcn_global_load_lds((const g_void *)(kb + (int64_t)key * kstride + 16 * pc),
+                                           (lds_void *)(dst + i * 1024), 16, 0, 0);
+        }
       }
     }
   };
-  auto commit = [&](int buf) {
-    unsigned char *dst = kbuf + buf * tk * C::ROWB;
-#pragma unroll
-    for (int j = 0; j < C::MAXL; ++j) *reinterpret_cast<u32x4 *>(dst + loff[j]) = pre[j];
-  };
+  // the direct loads count in vmcnt: wait for all of them before the barrier
+  // that publishes a stage
+  auto stage_wait = [] { __builtin_amdgcn_s_waitcnt(kWaitVm0); };
 
   fetch(0);   // first key stage in flight while the prologue runs
 
@@ -240,10 +254,11 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
     }
   }
 
-  // byte offsets of this lane's operand pieces 2u + half within its key row
+  // byte offsets of this lane's operand pieces 2u + half of key l32 of a
+  // tile, from the tile's first key row
   int koff[C::NU];
 #pragma unroll
-  for (int u = 0; u < C::NU; ++u) koff[u] = 16 * ((2 * u + half) ^ (l32 & C::SWM));
+  for (int u = 0; u < C::NU; ++u) koff[u] = l32 * C::ROWB + 16 * ((2 * u + half) ^ (l32 & C::SWM));
 
   // ---- pass-1 state: running max (raw logit units) and sum of exp2
   float m_run = -INFINITY, l_run = 0.f;
@@ -274,16 +289,18 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
     // later kernels of the pass accumulate: chunk c takes an equal slice
     if (a.hist_B) {
       const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
-      const int sl = 4 * ((kHBins / 4 + nch - 1) / nch);
-      const int64_t row = ((int64_t)b * a.Hkv + h) * kHBins;
-      for (int q = c * sl + 4 * t; q < min(kHBins, (c + 1) * sl); q += 4 * nt) {
-        *reinterpret_cast<u32x4 *>(a.hist_B + row + q) = u32x4{0u, 0u, 0u, 0u};
-        *reinterpret_cast<u32x4 *>(a.hist_S + row + q) = u32x4{0u, 0u, 0u, 0u};
-      }
+      const int64_t bh = (int64_t)b * a.Hkv + h;
+      int sl = 4 * ((kHBins / 4 + nch - 1) / nch);
+      for (int q = c * sl + 4 * t; q < min(kHBins, (c + 1) * sl); q += 4 * nt)
+        *reinterpret_cast<u32x4 *>(a.hist_S + bh * kHBins + q) = u32x4{0u, 0u, 0u, 0u};
+      constexpr int HB = kHCopies * kHBins;
+      sl = 4 * ((HB / 4 + nch - 1) / nch);
+      for (int q = c * sl + 4 * t; q < min(HB, (c + 1) * sl); q += 4 * nt)
+        *reinterpret_cast<u32x4 *>(a.hist_B + bh * HB + q) = u32x4{0u, 0u, 0u, 0u};
     }
   }
 
-  commit(0);
+  stage_wait();
   __syncthreads();
   for (int s = 0; s < nstages; ++s) {
     const int buf = s & 1;
@@ -300,15 +317,24 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
     }
     if (s + 1 < nstages) fetch(s + 1);
     const unsigned char *kl = kbuf + buf * tk * C::ROWB;
-#pragma unroll 1
-    for (int kt = 0; kt * 32 < ntile; ++kt) {
-      const int kbase = k0 + s * tk + kt * 32;   // first key of the tile (sequence-relative)
-      const unsigned char *kr = kl + (kt * 32 + l32) * C::ROWB;
+    // The tiles of a stage are unrolled (a tile's row offset is a constant in
+    // the LDS read instruction) and software-pipelined: the MFMA chain of
+    // tile kt + 1 is issued before the vector work on tile kt, so the matrix
+    // and vector units overlap inside one wave.
+    auto tile_mma = [&](int kt) {
+      const unsigned char *kr = kl + kt * 32 * C::ROWB;
       f32x16 acc = {};
-      if constexpr (MODE == PASS_LSE) {
 #pragma unroll
-        for (int u = 0; u < C::NU; ++u)
-          acc = mfma_unit<BF16>(*reinterpret_cast<const u32x4 *>(kr + koff[u]), qf[u], acc);
+      for (int u = 0; u < C::NU; ++u) {
+        const u32x4 kv = *reinterpret_cast<const u32x4 *>(kr + koff[u]);
+        if constexpr (MODE == PASS_LSE) acc = mfma_unit<BF16>(kv, qf[u], acc);   // D = K Q^T
+        else acc = mfma_unit<BF16>(qf[u], kv, acc);                              // D = Q K^T
+      }
+      return acc;
+    };
+    auto tile_post = [&](int kt, f32x16 acc) {
+      const int kbase = k0 + s * tk + kt * 32;   // first key of the tile (sequence-relative)
+      if constexpr (MODE == PASS_LSE) {
         // acc[reg]: key kbase + acc_row(reg, half), row = wave*32 + l32
         const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
         if (edge) {
@@ -334,9 +360,6 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           l_run += tree_sum16(ev);
         }
       } else {
-#pragma unroll
-        for (int u = 0; u < C::NU; ++u)
-          acc = mfma_unit<BF16>(qf[u], *reinterpret_cast<const u32x4 *>(kr + koff[u]), acc);
         // acc[reg]: row wave*32 + acc_row(reg, half), key kbase + l32
         float p[16];
 #pragma unroll
@@ -362,8 +385,18 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           red[((buf * 2 + 1) * nw + wave) * tk + kt * 32 + l32] = qs;
         }
       }
+    };
+    const int ntiles = (ntile + 31) / 32;        // 1..4
+    f32x16 cur = tile_mma(0);
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      if (kt >= ntiles) break;
+      f32x16 nxt = cur;
+      if (kt + 1 < ntiles) nxt = tile_mma(kt + 1);
+      tile_post(kt, cur);
+      cur = nxt;
     }
-    if (s + 1 < nstages) commit(buf ^ 1);
+    stage_wait();
     __syncthreads();
     if constexpr (MODE != PASS_LSE) {
       // Stage epilogue: fixed-order reduction over row tiles, one key per thread.
@@ -420,17 +453,39 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
       a.vec_VP[(int64_t)h * a.T + st.cu[b] + i] = vp;
     }
     // B histogram of the chunk's candidates (positions before the window) in
-    // the key-stage buffers, added to the (sequence, KV head) histogram of the
-    // select bin by bin: a hot bin takes one global atomic per workgroup.
+    // the key-stage buffers, added to one of kHCopies copies of the
+    // (sequence, KV head) histogram of the select bin by bin (workgroup w
+    // takes copy w % kHCopies: consecutive workgroups run on different XCDs,
+    // so a hot bin takes few atomics per copy); only the bins between the
+    // chunk's smallest and largest are cleared and flushed.
     unsigned *hist = reinterpret_cast<unsigned *>(kbuf);
-    for (int q = t; q < kHBins; q += nt) hist[q] = 0u;
+    const int ncnd = max(0, min(k1, wfirst) - k0);
+    int blo = kHBins, bhi = -1;
+    for (int p = t; p < ncnd; p += nt) {
+      const int q = hbin(float_key(cb[p]));
+      blo = min(blo, q);
+      bhi = max(bhi, q);
+    }
+    blo = __reduce_min_sync(~0ull, blo);
+    bhi = __reduce_max_sync(~0ull, bhi);
+    float *mm = red;                              // wave minima / maxima (red is free here)
+    if (lane == 0) { mm[wave] = __int_as_float(blo); mm[16 + wave] = __int_as_float(bhi); }
     __syncthreads();
-    for (int p = t; p < min(k1, wfirst) - k0; p += nt) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
+    blo = kHBins;
+    bhi = -1;
+    for (int w = 0; w < nw; ++w) {
+      blo = min(blo, __float_as_int(mm[w]));
+      bhi = max(bhi, __float_as_int(mm[16 + w]));
+    }
+    for (int q = blo + t; q <= bhi; q += nt) hist[q] = 0u;
     __syncthreads();
-    unsigned *gh = a.hist_B + ((int64_t)b * a.Hkv + h) * kHBins;
-    for (int q = t; q < kHBins; q += nt) {
-      const unsigned c = hist[q];
-      if (c) atomicAdd(&gh[q], c);
+    for (int p = t; p < ncnd; p += nt) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
+    __syncthreads();
+    const int copy = (blockIdx.y * gridDim.x + blockIdx.x) % kHCopies;
+    unsigned *gh = a.hist_B + (((int64_t)b * a.Hkv + h) * kHCopies + copy) * kHBins;
+    for (int q = blo + t; q <= bhi; q += nt) {
+      const unsigned cnt = hist[q];
+      if (cnt) atomicAdd(&gh[q], cnt);
     }
   }
 
@@ -1291,6 +1346,7 @@ constexpr int kEdgeJ = (kEdgeEntries + kSegThreads - 1) / kSegThreads;
 constexpr int kAllPer = kMaxSeqLen / kSegThreads;          // positions of a sequence per thread
 constexpr int kHPer = kHBins / kSegThreads;                // histogram bins per thread
 constexpr int kListPer = 8;                                // list entries per thread
+constexpr int kListSpec = 2;                               // of them loaded before the counts are known
 constexpr int kListCap = kListPer * kSegThreads;           // list entries of a (sequence, KV head)
 constexpr int kMaxSegs = kMaxSeqLen / kSegLen;             // segments of a sequence
 constexpr int kMomChunk = 4096;                            // scale-matching entries per LDS round
@@ -1338,13 +1394,23 @@ __device__ __forceinline__ unsigned lane_rank(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
 }
 
-// The thread's kHPer consecutive bins of a histogram row.
+// The thread's kHPer consecutive bins of a histogram row, summed over
+// `copies` consecutive copies of the row.
+template <int COPIES = 1>
 __device__ __forceinline__ void load_bins(const unsigned *gh, unsigned *cb) {
-  const u32x4 *hp = reinterpret_cast<const u32x4 *>(gh + kHPer * threadIdx.x);
+  u32x4 v[COPIES][kHPer / 4];
+#pragma unroll
+  for (int c = 0; c < COPIES; ++c) {
+    const u32x4 *hp = reinterpret_cast<const u32x4 *>(gh + (int64_t)c * kHBins + kHPer * threadIdx.x);
+#pragma unroll
+    for (int q = 0; q < kHPer / 4; ++q) v[c][q] = hp[q];
+  }
 #pragma unroll
   for (int q = 0; q < kHPer / 4; ++q) {
-    const u32x4 v = hp[q];
-    cb[4 * q + 0] = v.x; cb[4 * q + 1] = v.y; cb[4 * q + 2] = v.z; cb[4 * q + 3] = v.w;
+    u32x4 x = v[0][q];
+#pragma unroll
+    for (int c = 1; c < COPIES; ++c) x += v[c][q];
+    cb[4 * q + 0] = x.x; cb[4 * q + 1] = x.y; cb[4 * q + 2] = x.z; cb[4 * q + 3] = x.w;
   }
 }
 
@@ -1352,14 +1418,14 @@ __device__ __forceinline__ void load_bins(const unsigned *gh, unsigned *cb) {
 // (0 = not a candidate) from the histogram gh of those keys: element j is
 // kept iff key > xk, or key == xk and position <= pthr.  1 <= k <= count.
 // Ends with a barrier.
-template <int PER, typename KeyF, typename PosF>
+template <int PER, int COPIES, typename KeyF, typename PosF>
 __device__ __forceinline__ void hist_threshold(const unsigned *gh, KeyF key, PosF pos, int k,
                                                unsigned &xk, int &pthr,
                                                SelSharedT<kSegThreads> &ss, unsigned *ckey,
                                                int *cpos) {
   constexpr int NT = kSegThreads;
   unsigned cb[kHPer];
-  load_bins(gh, cb);
+  load_bins<COPIES>(gh, cb);
   bins_boundary<kHPer, NT>(cb, k, ss);
   const int beta = ss.bc_i[0];
   const int need = k - ss.bc_i[1];
@@ -1406,7 +1472,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   // the bins of the B histogram (accumulated by the fused pass), in flight
   // with the loads below
   unsigned cb[kHPer];
-  if (calib) load_bins(a.hist_B + ((int64_t)b * a.Hkv + h) * kHBins, cb);
+  if (calib) load_bins<kHCopies>(a.hist_B + ((int64_t)b * a.Hkv + h) * kHCopies * kHBins, cb);
   // chunk boundaries m*CH (1 <= m <= (n-1)/CH) whose positions [m*CH - r,
   // m*CH + r) meet the window; the host keeps their count times 2r within
   // kEdgeEntries for the whole sequence
@@ -1514,9 +1580,13 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
 }
 
 // Loads the selection record and the segments' lists of a (sequence, KV
-// head) into registers (entry e = t + j*NT), every slot a segment may hold,
-// with the counts in flight alongside; entries beyond their segment's count
-// get key 0.  scnt is LDS for the kMaxSegs counts.  Ends with a barrier.
+// head) into registers as one sequence of entries e = t + j*NT in (segment,
+// slot) order, which is position order.  First round: kListSpec slots per
+// thread, every slot a segment may hold up to cs = kListSpec*NT/nseg, loaded
+// with the counts in flight alongside.  When a count exceeds cs, a second
+// round loads the exact entries from the counts' prefix (up to kListCap).
+// Entries that do not exist get key 0.  `fits` is false when the lists
+// exceed kListCap.  scnt is LDS for kMaxSegs + 1 values.  Ends with a barrier.
 template <bool WITH_V>
 __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t base, int n, int h,
                                            const int4 *recp, const unsigned *lkey, const int *lpos,
@@ -1525,27 +1595,52 @@ __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t ba
   constexpr int NT = kSegThreads;
   const int t = threadIdx.x;
   L.nseg = st.seg_base[b + 1] - st.seg_base[b];
-  L.cap = ((kListCap / L.nseg) / 64) * 64;
+  const int cs = ((kListSpec * NT / L.nseg) / 64) * 64;
+  L.cap = cs;
   const int tt = opaque(t);
   rec = *recp;                                   // first: it heads the longest chain
   int c = 0;
   if (tt < L.nseg) c = cnts[(int64_t)h * st.total_segs + st.seg_base[b] + tt];
 #pragma unroll
-  for (int j = 0; j < kListPer; ++j) {
-    const int e = tt + j * NT, s = min(e / L.cap, L.nseg - 1);
-    const int64_t o = base + min(s * kSegLen + (e - s * L.cap), n - 1);
+  for (int j = 0; j < kListSpec; ++j) {
+    const int e = tt + j * NT, s = min(e / cs, L.nseg - 1);
+    const int64_t o = base + min(s * kSegLen + (e - s * cs), n - 1);
     k[j] = lkey[o];
     p[j] = lpos[o];
     if constexpr (WITH_V) v[j] = lv[o];
   }
+#pragma unroll
+  for (int j = kListSpec; j < kListPer; ++j) k[j] = 0u;
   if (t < kMaxSegs) scnt[t] = t < L.nseg ? c : 0;
   __syncthreads();
-  const int over = (t < kMaxSegs && scnt[t] > L.cap) ? 1 : 0;
-  L.fits = __syncthreads_or(over) == 0;
+  const int over = (t < kMaxSegs && scnt[t] > cs) ? 1 : 0;
+  if (__syncthreads_or(over) == 0) {
+    L.fits = true;
+#pragma unroll
+    for (int j = 0; j < kListSpec; ++j) {
+      const int e = t + j * NT, s = e / cs;
+      if (s >= L.nseg || e - s * cs >= scnt[s]) k[j] = 0u;   // 0: not an entry
+    }
+    return;
+  }
+  // second round: exact entries after the counts' prefix
+  int pre[kMaxSegs + 1];
+  pre[0] = 0;
+#pragma unroll
+  for (int s = 0; s < kMaxSegs; ++s) pre[s + 1] = pre[s] + scnt[s];
+  const int total = pre[kMaxSegs];
+  L.fits = total <= kListCap;
+  if (!L.fits) return;
 #pragma unroll
   for (int j = 0; j < kListPer; ++j) {
-    const int e = t + j * NT, s = e / L.cap;
-    if (s >= L.nseg || e - s * L.cap >= scnt[s]) k[j] = 0u;   // 0: not an entry
+    const int e = t + j * NT;
+    int s = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxSegs; ++q) s += (e >= pre[q]) ? 1 : 0;
+    const int64_t o = base + min(s * kSegLen + (e - pre[s]), n - 1);
+    k[j] = e < total ? lkey[o] : 0u;
+    p[j] = lpos[o];
+    if constexpr (WITH_V) v[j] = lv[o];
   }
 }
 
@@ -1571,7 +1666,7 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
   auto posf = [&](int j) -> int { return t + j * NT; };
   unsigned xm;
   int pm;
-  hist_threshold<kAllPer>(gh, keyB, posf, M, xm, pm, ss, ckey, cpos);
+  hist_threshold<kAllPer, kHCopies>(gh, keyB, posf, M, xm, pm, ss, ckey, cpos);
   uint32_t msk = 0;
 #pragma unroll
   for (int j = 0; j < kAllPer; ++j) {
@@ -1664,7 +1759,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
       }
     } else {
       double part[4];
-      whole_moments(a, base, nc, M, a.hist_B + hrow, ss, ckey, cpos, pre, mom, part);
+      whole_moments(a, base, nc, M, a.hist_B + hrow * kHCopies, ss, ckey, cpos, pre, mom, part);
       s0 = part[0]; s1 = part[1]; s2 = part[2]; s3 = part[3];
     }
     double sums[4];
@@ -1717,7 +1812,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segcand(SegArgs a, SeqTable st)
   const int kept = min(st.budget[b], nc);
   if (kept <= 0 || kept == nc) return;               // none or all kept: no list needed
   unsigned cb[kHPer];
-  load_bins(a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, cb);
+  load_bins<1>(a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, cb);
   unsigned key[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) key[j] = a.vec_S[base + i0 + min(t + j * NT, max(ncand - 1, 0))];
@@ -1764,7 +1859,7 @@ __device__ __attribute__((noinline)) void whole_topk(const SegArgs &a, int64_t b
   auto posf = [&](int j) -> int { return t + j * NT; };
   unsigned xk;
   int pk;
-  hist_threshold<kAllPer>(gh, keyS, posf, kept, xk, pk,
+  hist_threshold<kAllPer, 1>(gh, keyS, posf, kept, xk, pk,
                           ss, ckey, cpos);
   uint32_t msk = 0;
 #pragma unroll
@@ -1778,8 +1873,10 @@ __device__ __attribute__((noinline)) void whole_topk(const SegArgs &a, int64_t b
     const uint64_t m = __ballot(in);
     if (in) {
       const unsigned o = pre[j * NW + wave] + lane_rank(m);
-      if (idx) idx[o] = posf(j);
-      tbl[o] = posf(j);
+      if (o < (unsigned)kept) {
+        if (idx) idx[o] = posf(j);
+        tbl[o] = posf(j);
+      }
     }
   }
 }
@@ -1836,8 +1933,10 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
         const uint64_t m = __ballot(in);
         if (in) {
           const unsigned o = pre[j * NW + wave] + lane_rank(m);
-          if (part == 0) idx[o] = lp[j];
-          tbl[o] = lp[j];
+          if (o < (unsigned)kept) {              // exactly `kept` are set; the bound guards the buffers
+            if (part == 0) idx[o] = lp[j];
+            tbl[o] = lp[j];
+          }
         }
       }
     } else {
