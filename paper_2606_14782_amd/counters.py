@@ -1,4 +1,5 @@
-"""HBM traffic per kernel launch from rocprofv3 counter runs.
+"""HBM traffic per kernel launch from rocprofv3 counter runs, and kernel-time
+summaries from rocprofv3 kernel-trace statistics.
 
 Reads the counter-collection CSVs of two `rocprofv3 --pmc FETCH_SIZE` and
 `rocprofv3 --pmc WRITE_SIZE` runs of `bench.py --copy-calibration`, scales
@@ -8,6 +9,9 @@ for the plain copy of a known size in the same run, and writes the result
 
     python -m paper_2606_14782_amd.counters --fetch DIR --write DIR \
         --out profiles/traffic.json --md profiles/traffic_<workload>.md
+
+With --trace DIR it instead summarises the *kernel_stats.csv of a
+`rocprofv3 --kernel-trace --stats` run into a markdown table (--md).
 """
 from __future__ import annotations
 
@@ -83,14 +87,50 @@ def copy_kib(stats) -> float:
     return max(cands)[0]
 
 
+def trace_summary(d: str, md: str, command: str, title: str) -> None:
+    """Markdown table of the per-kernel statistics of a kernel-trace run."""
+    files = sorted(glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True))
+    if not files:
+        raise SystemExit(f"no kernel_stats.csv under {d}")
+    rows = []
+    for f in files:
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                calls = int(float(r.get("Calls", 0)))
+                tot = float(r.get("TotalDurationNs", 0.0))
+                avg = float(r.get("AverageNs", tot / max(calls, 1)))
+                rows.append((tot, r.get("Name", "?"), calls, avg, float(r.get("MinNs", 0.0)),
+                             float(r.get("MaxNs", 0.0))))
+    total = sum(x[0] for x in rows) or 1.0
+    lines = [f"# {title}", "", f"command (from /tmp with TMPDIR=/tmp): `{command}`", "",
+             f"kernel sources: {source_sha()}", "",
+             "| kernel | library name | calls | avg us | min us | max us | share |",
+             "|---|---|---|---|---|---|---|"]
+    for tot, name, calls, avg, mn, mx in sorted(rows, reverse=True):
+        short = name if len(name) <= 60 else name[:57] + "..."
+        lib = library_name(name) or "(torch / runtime)"
+        lines.append(f"| `{short}` | {lib} | {calls} | {avg / 1e3:.2f} | {mn / 1e3:.2f} | "
+                     f"{mx / 1e3:.2f} | {100 * tot / total:.1f}% |")
+    with open(md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--fetch", required=True)
-    ap.add_argument("--write", required=True)
-    ap.add_argument("--out", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--out")
+    ap.add_argument("--trace")
+    ap.add_argument("--title", default="Kernel durations")
     ap.add_argument("--md", required=True)
     ap.add_argument("--command", default="")
     args = ap.parse_args()
+    if args.trace:
+        trace_summary(args.trace, args.md, args.command, args.title)
+        return
+    if not (args.fetch and args.write and args.out):
+        raise SystemExit("--fetch, --write and --out are required without --trace")
     fs, ws = per_kernel(args.fetch, "FETCH_SIZE"), per_kernel(args.write, "WRITE_SIZE")
     ffac = COPY_BYTES / (copy_kib(fs) * 1024.0)
     wfac = COPY_BYTES / (copy_kib(ws) * 1024.0)

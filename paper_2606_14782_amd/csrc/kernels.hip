@@ -1345,7 +1345,7 @@ static_assert(kEdgeEntries % kSegThreads == 0 || kSegThreads % kEdgeEntries == 0
 constexpr int kEdgeJ = (kEdgeEntries + kSegThreads - 1) / kSegThreads;
 constexpr int kAllPer = kMaxSeqLen / kSegThreads;          // positions of a sequence per thread
 constexpr int kHPer = kHBins / kSegThreads;                // histogram bins per thread
-constexpr int kListPer = 8;                                // list entries per thread
+constexpr int kListPer = 4;                                // list entries per thread
 constexpr int kListSpec = 2;                               // of them loaded before the counts are known
 constexpr int kListCap = kListPer * kSegThreads;           // list entries of a (sequence, KV head)
 constexpr int kMaxSegs = kMaxSeqLen / kSegLen;             // segments of a sequence
