@@ -213,7 +213,10 @@ bacon_status check_ptr(const void *p, const char *name, size_t align) {
     if (_s != BACON_OK) return _s; \
   } while (0)
 
-SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out) {
+// edge_tables: the split calibrate path completes L next to chunk boundaries
+// from an LDS table of kEdgeEntries positions, which bounds the chunk count.
+SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out,
+                    bool edge_tables = true) {
   SeqTable st{};
   st.batch = bt->batch;
   const bool bf16 = c->shape.dtype == BACON_BF16;
@@ -234,7 +237,7 @@ SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out) {
   // the select kernel stages 2r positions around every chunk boundary
   int nmax = 0;
   for (int b = 0; b < bt->batch; ++b) nmax = std::max(nmax, bt->cu_seqlens[b + 1] - bt->cu_seqlens[b]);
-  if (c->params.radius > 0) {
+  if (edge_tables && c->params.radius > 0) {
     const int min_chunk = (int)(((int64_t)nmax * 2 * c->params.radius + kEdgeEntries - 1) / kEdgeEntries);
     per_wg = std::max(per_wg, (min_chunk + tk - 1) / tk);
   }
@@ -331,7 +334,7 @@ bacon_status check_lds(const bacon_ctx *c, const bacon_batch *bt, int chunk, boo
     return fail(BACON_ERR_UNSUPPORTED, "pass workgroup needs more LDS than a CU has");
   if (sel_mode >= 0 && select_lds_bytes(sel_mode, max_len(bt)) > (size_t)kLdsBytes)
     return fail(BACON_ERR_UNSUPPORTED, "select workgroup needs more LDS than a CU has");
-  if (sel_mode == SEL_FUSED || sel_mode == SEL_CALIB) {
+  if (sel_mode == SEL_CALIB) {
     const int n = max_len(bt);
     if (chunk < n && (int64_t)((n - 1) / chunk) * 2 * c->params.radius > kEdgeEntries)
       return fail(BACON_ERR_UNSUPPORTED, "too many chunk boundaries for radius %d", c->params.radius);
@@ -548,8 +551,8 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   TRY(check_ptr(d_v_out, "v_out", 16));
   hipStream_t s = static_cast<hipStream_t>(stream);
   int chunk = 0;
-  const SeqTable st = make_table(c, bt, &chunk);
-  TRY(check_lds(c, bt, chunk, true, SEL_FUSED));
+  const SeqTable st = make_table(c, bt, &chunk, false);
+  TRY(check_lds(c, bt, chunk, true, -1));
   int kmax = 0;
   for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, bt->budgets[b]);
   if (final_lds_bytes(kmax, c->shape.window) > (size_t)kLdsBytes)

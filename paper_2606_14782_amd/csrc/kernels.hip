@@ -2,34 +2,29 @@
 //
 // Pass 1 (PASS_LSE) and pass 2 (PASS_SCORE / PASS_FUSED) each stream the
 // layer's keys once.  A workgroup owns one (KV head, key chunk); its waves own
-// the 32-row tiles of the G*W window queries of that KV head.  Key tiles are
-// staged through LDS with coalesced 16-byte loads and consumed by 32x32 MFMA
-// (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32).
+// the 32-row tiles of the G*W window queries of that KV head.  Key stages go
+// straight from HBM to LDS (16-byte direct loads) and are consumed by 32x32
+// MFMA (bf16: v_mfma_f32_32x32x16_bf16, fp32: v_mfma_f32_32x32x2_f32).
 //
 //  * Pass 1 computes D = K Q^T so each lane holds one query row: the running
 //    row max and sum of exp2 stay in-lane; each chunk writes one (max, sum)
-//    partial per row.
-//  * Pass 2 merges the partials of its KV head into the row normalisers while
-//    its first key stage is in flight, then computes D = Q K^T so each lane
-//    holds one key: the window mean B and the last-query score Q are in-lane
-//    sums over the lane's rows, reduced across row tiles through LDS in a
-//    fixed order (deterministic).  The fused variant forms E = [Q-B]_+
-//    (Eq. boundary_residual), T from the E history (Eq. inter_layer_persistence),
-//    appends E to the history, and adds the part of L = P_r E
-//    (Eq. intra_layer_coherence) whose neighbours lie inside the chunk.
+//    partial per row, and a merge kernel forms the row normalisers.
+//  * Pass 2 computes D = Q K^T so each lane holds one key: the window mean B
+//    and the last-query score Q are in-lane sums over the lane's rows,
+//    reduced across row tiles through LDS in a fixed order (deterministic).
+//    The fused variant forms E = [Q-B]_+ (Eq. boundary_residual), T from the
+//    E history (Eq. inter_layer_persistence), appends E to the history, and
+//    adds the B keys of its candidates to the B histogram of the select; the
+//    select's calibration kernel forms L = P_r E (Eq. intra_layer_coherence)
+//    from the history.
 //
-// The fused pass selects in two segment kernels (one workgroup per kSegLen
-// positions and KV head).  The first completes L at chunk boundaries, forms V
-// (Eq. structurally_calibrated_evidence), pools B and V, and keeps each
-// segment's top of B; the workgroup that finishes last for a (sequence, KV
-// head) selects the scale-matching set over the union and computes lambda
-// (Eqs. scale_matching_set, lambda_solution).  The second keeps each segment's
-// top of the pooled S = B + lambda V (Eq. bacon_score); its last workgroup
-// takes the top-K over the union (Eq. topk_selection) and writes the kept
-// positions in ascending order; the compaction kernel gathers the cache.
+// The fused pass then selects in four kernels over segments of kSegLen
+// positions, exchanging histograms and short per-segment lists (see the
+// "histogram select" section): calibration (V, pooling, the candidates of
+// the scale-matching set), score (lambda and the pooled score), candidates of
+// the top-K, and the final top-K with the gather of the compacted cache.
 // One workgroup per (sequence, KV head) runs the same steps over the whole
-// sequence for the split calls and for budgets whose candidate unions exceed
-// one workgroup.
+// sequence for the split calls.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -148,8 +143,6 @@ struct PassCfg {
 //   kbuf  2 * tk * ROWB           double-buffered key stages (swizzled pieces)
 //   red   2 * 2 * nw * tk floats  per-stage B/Q partials of each row tile  (pass 2)
 //   lse   Rpad floats             row normalisers                          (pass 2)
-//   ce    chunk floats            E of the chunk                           (fused)
-//   cv    chunk floats            E + T of the chunk                       (fused)
 //   cb    chunk floats            B of the chunk                           (fused)
 // After the stages the fused pass reuses kbuf for its B histogram.
 int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk) {
@@ -157,7 +150,7 @@ int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk) {
   int bytes = 2 * tk * head_dim * (bf16 ? 2 : 4);
   if (mode == PASS_FUSED && bytes < 4 * kHBins) bytes = 4 * kHBins;   // room for the B histogram
   if (mode != PASS_LSE) bytes += 16 * nw * tk + 4 * rpad;
-  if (mode == PASS_FUSED) bytes += 12 * chunk;
+  if (mode == PASS_FUSED) bytes += 4 * chunk;
   return bytes;
 }
 
@@ -184,9 +177,7 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   const int kbytes = (MODE == PASS_FUSED) ? max(2 * tk * C::ROWB, 4 * kHBins) : 2 * tk * C::ROWB;
   float *red = reinterpret_cast<float *>(smem + kbytes);               // [2][2][nw][tk]
   float *lse_s = red + 4 * nw * tk;                                    // [Rpad]
-  float *ce = lse_s + a.Rpad;                                          // [chunk]
-  float *cv = ce + a.chunk;                                            // [chunk]
-  float *cb = cv + a.chunk;                                            // [chunk]
+  float *cb = lse_s + a.Rpad;                                          // [chunk]
 
   // Stage loader: direct-to-LDS 16-byte loads (no register staging).  LDS
   // slot s of a stage holds piece (s % PIECES) ^ (key & SWM) of key
@@ -427,31 +418,16 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           const float Tv = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
           a.ring[pos * a.ring_mp + a.ring_write] = E;
           a.vec_B[pos] = Bv;
+          // E + T; the select kernel adds L = P_r E from the history
+          a.vec_VP[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
           cb[s * tk + t] = Bv;
-          ce[s * tk + t] = E;
-          cv[s * tk + t] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
         }
       }
     }
   }
 
   if constexpr (MODE == PASS_FUSED) {
-    // In-chunk part of L = P_r E: neighbours inside [k0, k1), divided by the
-    // full neighbourhood size; the select kernel adds the neighbours outside.
     __syncthreads();
-    const int r = a.radius;
-    const bool use_l = (a.terms & 2u) != 0;
-    for (int p = t; p < k1 - k0; p += nt) {
-      const int i = k0 + p;
-      const int lo = max(0, i - r), hi = min(n - 1, i + r);
-      float sum = 0.f;
-      if (use_l) {
-        const int clo = max(lo, k0), chi = min(hi, k1 - 1);
-        for (int u = clo; u <= chi; ++u) sum += ce[u - k0];
-      }
-      const float vp = cv[p] + (use_l ? sum / (float)(hi - lo + 1) : 0.f);
-      a.vec_VP[(int64_t)h * a.T + st.cu[b] + i] = vp;
-    }
     // B histogram of the chunk's candidates (positions before the window) in
     // the key-stage buffers, added to one of kHCopies copies of the
     // (sequence, KV head) histogram of the select bin by bin (workgroup w
@@ -1322,8 +1298,8 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
 // short lists.  Lists longer than one workgroup holds fall back to the exact
 // block select over the whole sequence.
 //
-//  * segment_calib (one workgroup per segment and KV head): completes
-//    V = E + L + T next to chunk boundaries (Eq. structurally_calibrated_evidence),
+//  * segment_calib (one workgroup per segment and KV head): forms
+//    L = P_r E from the history and V = E + L + T (Eq. structurally_calibrated_evidence),
 //    writes the pooled B and V over I, finds the boundary bin of the top-M of
 //    B in the B histogram the fused pass accumulated (Eqs. scale_matching_size,
 //    scale_matching_set), and lists its candidates at or above it with their V.
@@ -1341,8 +1317,9 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
 constexpr int kSegPer = kSegLen / kSegThreads;             // positions per thread (strided)
 constexpr int kSegWin = kSegLen + 2 * kPoolHalo;           // segment plus pool halo
 constexpr int kSegWinJ = (kSegWin + kSegThreads - 1) / kSegThreads;
-static_assert(kEdgeEntries % kSegThreads == 0 || kSegThreads % kEdgeEntries == 0, "edge table load");
-constexpr int kEdgeJ = (kEdgeEntries + kSegThreads - 1) / kSegThreads;
+constexpr int kMaxRadius = 16;                             // largest coherence radius
+constexpr int kSegE = kSegWin + 2 * kMaxRadius;            // E over the window and the radius
+constexpr int kSegEJ = (kSegE + kSegThreads - 1) / kSegThreads;
 constexpr int kAllPer = kMaxSeqLen / kSegThreads;          // positions of a sequence per thread
 constexpr int kHPer = kHBins / kSegThreads;                // histogram bins per thread
 constexpr int kListPer = 4;                                // list entries per thread
@@ -1452,7 +1429,7 @@ struct ListView {
 __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ float Bs[kSegWin], Vs[kSegWin];
-  __shared__ float ed[kEdgeEntries];
+  __shared__ float Es[kSegE];
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[PER * NW + 1];
   const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
@@ -1464,8 +1441,8 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   const int i0 = sg * kSegLen;
   const int w0 = i0 - kPoolHalo;                    // position of Bs[0]
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  const int r = a.radius, CH = a.vp_chunk, tr = max(2 * r, 1);
-  const bool use_l = (a.terms & 2u) != 0 && r > 0 && CH < n;
+  const int r = a.radius;
+  const bool use_l = (a.terms & 2u) != 0;
   int M = (int)floorf(a.rho * (float)st.budget[b]);
   M = max(0, min(M, nc));
   const bool calib = M > 0 && a.use_last_query;
@@ -1473,22 +1450,13 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   // with the loads below
   unsigned cb[kHPer];
   if (calib) load_bins<kHCopies>(a.hist_B + ((int64_t)b * a.Hkv + h) * kHCopies * kHBins, cb);
-  // chunk boundaries m*CH (1 <= m <= (n-1)/CH) whose positions [m*CH - r,
-  // m*CH + r) meet the window; the host keeps their count times 2r within
-  // kEdgeEntries for the whole sequence
-  int m0 = 1, nedge = 0;
-  if (use_l) {
-    const int x = w0 - r + 1;
-    m0 = x <= 0 ? 1 : max(1, (x + CH - 1) / CH);
-    const int m1 = min((n - 1) / CH, (w0 + kSegWin - 1 + r) / CH);
-    nedge = max(0, m1 - m0 + 1) * 2 * r;
-  }
   const float *re = a.ring + base * a.ring_mp + a.ring_slot;
 
-  // one round of loads: B and VP over the window, E next to the boundaries
+  // one round of loads: B and E + T over the window, E over the window
+  // widened by the coherence radius
   {
     const int tt = opaque(t);
-    float bv[kSegWinJ], vv[kSegWinJ], ev[kEdgeJ];
+    float bv[kSegWinJ], vv[kSegWinJ], ev[kSegEJ];
 #pragma unroll
     for (int j = 0; j < kSegWinJ; ++j) {
       const int u = min(max(w0 + tt + j * NT, 0), n - 1);
@@ -1496,16 +1464,15 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
       vv[j] = a.vec_VP[base + u];
     }
 #pragma unroll
-    for (int j = 0; j < kEdgeJ; ++j) {
-      const int e = min(tt + j * NT, max(nedge - 1, 0));
-      const int m = e / tr;
-      const int x = (m0 + m) * CH - r + (e - m * tr);
-      ev[j] = re[(int64_t)min(max(x, 0), n - 1) * a.ring_mp];
+    for (int j = 0; j < kSegEJ; ++j) {
+      const int u = min(max(w0 - kMaxRadius + tt + j * NT, 0), n - 1);
+      ev[j] = re[(int64_t)u * a.ring_mp];
     }
 #pragma unroll
-    for (int j = 0; j < kEdgeJ; ++j)
-      if (tt + j * NT < nedge) ed[tt + j * NT] = ev[j];
+    for (int j = 0; j < kSegEJ; ++j)
+      if (tt + j * NT < kSegE) Es[tt + j * NT] = ev[j];
     __syncthreads();
+    // V = E + T + L, L = P_r E over the sequence-truncated neighbourhood
 #pragma unroll
     for (int j = 0; j < kSegWinJ; ++j) {
       const int q = tt + j * NT;
@@ -1513,18 +1480,10 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
         const int u = w0 + q;
         float v = vv[j];
         if (use_l && u >= 0 && u < n) {
-          const int k0 = (u / CH) * CH, k1 = min(n, k0 + CH);
           const int lo = max(0, u - r), hi = min(n - 1, u + r);
-          if (lo < k0 || hi >= k1) {
-            // neighbours before k0 sit at offsets [0, r) of boundary k0's
-            // entries, those from k1 on at offsets [r, 2r) of boundary k1's
-            float sum = 0.f;
-            const int o0 = (k0 / CH - m0) * 2 * r + r - k0;
-            for (int x = lo; x < k0; ++x) sum += ed[o0 + x];
-            const int o1 = (k1 / CH - m0) * 2 * r + r - k1;
-            for (int x = k1; x <= hi; ++x) sum += ed[o1 + x];
-            v += sum / (float)(hi - lo + 1);
-          }
+          float sum = 0.f;
+          for (int x = lo; x <= hi; ++x) sum += Es[x - w0 + kMaxRadius];
+          v += sum / (float)(hi - lo + 1);
         }
         Bs[q] = bv[j];
         Vs[q] = v;
