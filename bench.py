@@ -212,6 +212,29 @@ def main():
     achieved = kbytes / (per_kernel[dom]["avg_us"] * 1e-6) / 1e9
     traffic = measured_traffic(dom)
 
+    # The same pass with the window-row normalisers supplied, as a prefill
+    # attention that returns its softmax normalisers would (the first K pass and
+    # the merge are skipped); reported beside the headline, never as it.
+    lses = []
+    for l in range(wl.num_layers):
+        _, _, lse = ctx.bacon_score(l, batch, qs[l], ks[l], want_lse=True)
+        lses.append(lse)
+    torch.cuda.synchronize()
+
+    def step_lse():
+        ctx.bacon_begin_prompt(batch)
+        for l in range(wl.num_layers):
+            ctx.bacon_compress_layer_lse(l, batch, qs[l], ks[l], vs[l], lses[l], out=outs[l])
+
+    for _ in range(args.warmup):
+        step_lse()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step_lse()
+    torch.cuda.synchronize()
+    ms_step_lse = 1e3 * (time.perf_counter() - t0) / args.steps
+
     ab = algorithmic_bytes(wl)
     ms_layer = ms_step / wl.num_layers
     keys_step = wl.total_tokens * wl.num_kv_heads * wl.num_layers
@@ -244,6 +267,11 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": dom,
                      "bytes_per_launch": kbytes, "avg_us": per_kernel[dom]["avg_us"]},
         "kernels": per_kernel,
+        "supplied_lse": {
+            "note": "window-row softmax normalisers given by the prefill attention "
+                    "(bacon_compress_layer_lse); the first K pass and the merge are skipped",
+            "ms_per_layer": ms_step_lse / wl.num_layers,
+            "value": keys_step / (ms_step_lse * 1e-3), "unit": "keys/s"},
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")

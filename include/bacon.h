@@ -168,6 +168,20 @@ bacon_status bacon_compress_layer(bacon_ctx *ctx, int32_t layer, const bacon_bat
                                   const void *d_q_win, const void *d_k, const void *d_v,
                                   int32_t *d_idx, void *d_k_out, void *d_v_out, void *stream);
 
+/* The same pass with the window-row normalisers given by the caller: d_lse
+ * [B, Hq, W] float32 holds, for window row w of query head q of sequence b,
+ * the natural log of sum_{i <= t_w} exp(q_w . k_i / sqrt(d)) over the row's
+ * causal keys (Sec. 4.1; the softmax normaliser that a flash-attention
+ * prefill computes for every query row).  The first K pass that forms these
+ * normalisers is skipped; with the normalisers of bacon_score the results
+ * equal bacon_compress_layer's up to their rounding.  d_lse must be a
+ * 4-byte-aligned device pointer (INVALID otherwise); the caller keeps
+ * ownership.  Same ordering rule as calibrate. */
+bacon_status bacon_compress_layer_lse(bacon_ctx *ctx, int32_t layer, const bacon_batch *batch,
+                                      const void *d_q_win, const void *d_k, const void *d_v,
+                                      const float *d_lse, int32_t *d_idx, void *d_k_out,
+                                      void *d_v_out, void *stream);
+
 /* Sizes of the outputs for a batch: idx entries and compacted rows. */
 int64_t bacon_idx_count(const bacon_batch *batch, int32_t num_kv_heads);
 int64_t bacon_kept_rows(const bacon_batch *batch, int32_t window);

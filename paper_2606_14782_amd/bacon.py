@@ -21,7 +21,8 @@ TERM_E, TERM_L, TERM_T = 1, 2, 4
 ENTRY_POINTS = [
     "bacon_default_params", "bacon_workspace_bytes", "bacon_init", "bacon_free",
     "bacon_begin_prompt", "bacon_score", "bacon_calibrate", "bacon_select_topk",
-    "bacon_compact", "bacon_compress_layer", "bacon_idx_count", "bacon_kept_rows",
+    "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_idx_count",
+    "bacon_kept_rows",
     "bacon_profile_enable", "bacon_profile_read", "bacon_status_string", "bacon_last_error",
 ]
 
@@ -77,6 +78,8 @@ def lib() -> C.CDLL:
         L.bacon_compact.argtypes = [vp, C.POINTER(Batch), vp, vp, vp, vp, vp, vp]
         L.bacon_compress_layer.argtypes = [vp, C.c_int32, C.POINTER(Batch), vp, vp, vp, vp, vp,
                                            vp, vp]
+        L.bacon_compress_layer_lse.argtypes = [vp, C.c_int32, C.POINTER(Batch), vp, vp, vp, vp,
+                                               vp, vp, vp, vp]
         L.bacon_idx_count.argtypes = [C.POINTER(Batch), C.c_int32]
         L.bacon_idx_count.restype = C.c_int64
         L.bacon_kept_rows.argtypes = [C.POINTER(Batch), C.c_int32]
@@ -89,7 +92,7 @@ def lib() -> C.CDLL:
         L.bacon_last_error.restype = C.c_char_p
         for name in ("bacon_init", "bacon_free", "bacon_begin_prompt", "bacon_score",
                      "bacon_calibrate", "bacon_select_topk", "bacon_compact",
-                     "bacon_compress_layer", "bacon_profile_enable"):
+                     "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_profile_enable"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -223,6 +226,21 @@ class Context:
                                           _stream()))
         return idx, k_out, v_out
 
+    def bacon_compress_layer_lse(self, layer, batch: BatchLayout, q_win, k, v, lse, out=None):
+        """The fused pass with the window-row normalisers lse [B, Hq, W] (natural
+        log) given, e.g. by the prefill attention."""
+        import torch
+        if out is None:
+            idx = torch.empty(batch.idx_count(self.shape.num_kv_heads), dtype=torch.int32,
+                              device=k.device)
+            k_out, v_out = self._kv_out(batch, k)
+        else:
+            idx, k_out, v_out = out
+        _check(lib().bacon_compress_layer_lse(self._h, layer, C.byref(batch.c), _ptr(q_win),
+                                              _ptr(k), _ptr(v), _ptr(lse), _ptr(idx),
+                                              _ptr(k_out), _ptr(v_out), _stream()))
+        return idx, k_out, v_out
+
     def bacon_profile_enable(self, enable=True):
         _check(lib().bacon_profile_enable(self._h, 1 if enable else 0))
 
@@ -256,3 +274,7 @@ def bacon_compact(ctx: Context, batch, k, v, idx):
 
 def bacon_compress_layer(ctx: Context, layer, batch, q_win, k, v, out=None):
     return ctx.bacon_compress_layer(layer, batch, q_win, k, v, out)
+
+
+def bacon_compress_layer_lse(ctx: Context, layer, batch, q_win, k, v, lse, out=None):
+    return ctx.bacon_compress_layer_lse(layer, batch, q_win, k, v, lse, out)

@@ -284,7 +284,6 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   a.partials = reinterpret_cast<float2 *>(c->ws + c->L.partials);
   a.lse2 = reinterpret_cast<float *>(c->ws + c->L.lse2);
   a.hist_B = reinterpret_cast<unsigned *>(c->ws + c->L.hist_b);
-  a.hist_S = reinterpret_cast<unsigned *>(c->ws + c->L.hist_s);
   a.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
   a.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
   a.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
@@ -408,9 +407,14 @@ bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *strea
   TRY(check_batch(c, bt));
   c->cu.assign(bt->cu_seqlens, bt->cu_seqlens + bt->batch + 1);
   c->budgets.assign(bt->budgets, bt->budgets + bt->batch);
+  // layer 0 reads no history; the B histogram of the select starts at zero
+  // (each layer's final kernel clears it for the next)
+  const hipError_t e = launch_zero(reinterpret_cast<unsigned *>(c->ws + c->L.hist_b),
+                                   (int64_t)bt->batch * c->shape.num_kv_heads * kHCopies * kHBins,
+                                   static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "clear");
   c->prompt = true;
   c->next_layer = 0;
-  (void)stream;   // nothing to enqueue: layer 0 reads no history
   return BACON_OK;
 }
 
@@ -533,9 +537,14 @@ bacon_status bacon_compact(bacon_ctx *c, const bacon_batch *bt, const void *d_k,
   return timed(c, KI_COMPACT, s, [&] { return launch_compact(a, st, s); });
 }
 
-bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
-                                  const void *d_q_win, const void *d_k, const void *d_v,
-                                  int32_t *d_idx, void *d_k_out, void *d_v_out, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The fused pass of one layer; d_lse (caller normalisers) skips pass 1.
+bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
+                      const void *d_k, const void *d_v, const float *d_lse, int32_t *d_idx,
+                      void *d_k_out, void *d_v_out, void *stream) {
   if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
   TRY(check_batch(c, bt));
   TRY(check_prompt_batch(c, bt));
@@ -560,6 +569,7 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   const int64_t T = bt->cu_seqlens[bt->batch];
   PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
   a.T = T;
+  a.lse_in = d_lse;
   ring_slots(c, layer, &a.ring_write, &a.ring_cnt);
   a.ring_mp = c->L.ring_mp;
   const bool bf16 = c->shape.dtype == BACON_BF16;
@@ -586,7 +596,7 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   g.vec_pV = reinterpret_cast<float *>(c->ws + c->L.vec_pv);
   g.vec_S = reinterpret_cast<unsigned *>(c->ws + c->L.vec_s);
   g.hist_B = a.hist_B;
-  g.hist_S = a.hist_S;
+  g.hist_S = reinterpret_cast<unsigned *>(c->ws + c->L.hist_s);
   g.listB_key = reinterpret_cast<unsigned *>(c->ws + c->L.list_bk);
   g.listB_pos = reinterpret_cast<int *>(c->ws + c->L.list_bp);
   g.listB_v = reinterpret_cast<float *>(c->ws + c->L.list_bv);
@@ -605,8 +615,10 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   g.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
   // final workgroups per (sequence, KV head): about one round over the CUs
   g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
-  TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
-  TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+  if (!d_lse) {
+    TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+    TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+  }
   TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
   TRY(timed(c, KI_SEGCAL, s, [&] { return launch_segcal(g, st, s); }));
   TRY(timed(c, KI_SEGSCORE, s, [&] { return launch_segscore(g, st, s); }));
@@ -614,6 +626,25 @@ bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch
   TRY(timed(c, KI_FINAL, s, [&] { return launch_segfinal(g, st, kmax, s); }));
   c->next_layer = layer + 1;
   return BACON_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+bacon_status bacon_compress_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
+                                  const void *d_q_win, const void *d_k, const void *d_v,
+                                  int32_t *d_idx, void *d_k_out, void *d_v_out, void *stream) {
+  return compress(c, layer, bt, d_q_win, d_k, d_v, nullptr, d_idx, d_k_out, d_v_out, stream);
+}
+
+bacon_status bacon_compress_layer_lse(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
+                                      const void *d_q_win, const void *d_k, const void *d_v,
+                                      const float *d_lse, int32_t *d_idx, void *d_k_out,
+                                      void *d_v_out, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_ptr(d_lse, "lse", 4));
+  return compress(c, layer, bt, d_q_win, d_k, d_v, d_lse, d_idx, d_k_out, d_v_out, stream);
 }
 
 int64_t bacon_idx_count(const bacon_batch *bt, int32_t num_kv_heads) {

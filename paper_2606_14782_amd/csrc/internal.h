@@ -48,8 +48,8 @@ struct PassArgs {
   float2 *partials;     // [Hkv, total_chunks, Rpad]  (max, sum) per chunk, log2 units
   float *lse2;          // [B, Hkv, Rpad] row normalisers, log2 units (merge kernel writes)
   float *lse_user;      // optional [B, Hq, W] natural-log normaliser (merge kernel writes)
-  unsigned *hist_B, *hist_S;   // optional select histograms pass 1 clears: [B, Hkv, kHCopies, kHBins]
-                               // and [B, Hkv, kHBins]
+  const float *lse_in;  // optional [B, Hq, W] natural-log normalisers given by the caller (pass 2 reads)
+  unsigned *hist_B;     // [B, Hkv, kHCopies, kHBins] B histogram of the select (fused pass adds)
   // PASS_SCORE
   float *out_B, *out_Q; // [Hkv, T]
   // PASS_FUSED
@@ -104,7 +104,9 @@ struct SegArgs {
   float *vec_pB, *vec_pV;        // [Hkv, T] pooled B and V over I
   unsigned *vec_S;               // [Hkv, T] keys of the pooled score over I
   unsigned *hist_B, *hist_S;     // key histograms of B [B, Hkv, kHCopies, kHBins] (the bin count is
-                                 // the sum of the copies) and of the pooled score [B, Hkv, kHBins]
+                                 // the sum of the copies) and of the pooled score [B, Hkv, kHBins];
+                                 // the final kernel clears hist_B for the next layer, the
+                                 // calibration kernel clears hist_S
   // per-segment lists at or above a boundary bin: segment s of a sequence
   // writes slots [s*kSegLen, ...) of the [Hkv, T] arrays, its count to cnt
   unsigned *listB_key, *listS_key;
@@ -157,5 +159,6 @@ hipError_t launch_segcand(const SegArgs &a, const SeqTable &st, hipStream_t s);
 size_t final_lds_bytes(int max_budget, int window);
 hipError_t launch_segfinal(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s);
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
+hipError_t launch_zero(unsigned *p, int64_t n, hipStream_t s);
 
 }  // namespace bacon

@@ -44,6 +44,7 @@ typedef __attribute__((address_space(1))) void g_void;
 constexpr int kWaitVm0 = 0x0F70;
 
 constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kLog2e = 1.44269504088896341f;
 
 // ---------------------------------------------------------------- MFMA units
 // A "unit" is 16 bytes per lane: 8 bf16 (one 32x32x16 step) or 4 fp32 (four
@@ -263,9 +264,18 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   int wrow[16];                    // window index of each row (W for pad rows)
   uint32_t lastmask = 0;           // rows that are the last query of their head
   if constexpr (MODE != PASS_LSE) {
-    // row normalisers of this (sequence, KV head), merged from pass 1's
-    // per-chunk partials by the merge kernel
-    for (int r = t; r < a.Rpad; r += nt) lse_s[r] = a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + r];
+    // row normalisers of this (sequence, KV head): merged from pass 1's
+    // per-chunk partials by the merge kernel, or given by the caller as the
+    // natural-log normalisers of the window rows [B, Hq, W]
+    for (int r = t; r < a.Rpad; r += nt) {
+      if (a.lse_in) {
+        const int g = r / W, w = r - g * W;
+        lse_s[r] = r < a.R ? a.lse_in[((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w] * kLog2e
+                           : INFINITY;
+      } else {
+        lse_s[r] = a.lse2[((int64_t)b * a.Hkv + h) * a.Rpad + r];
+      }
+    }
     __syncthreads();
 #pragma unroll
     for (int reg = 0; reg < 16; ++reg) {
@@ -275,22 +285,6 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
       if (!W32 && r < a.R && (r % W) == W - 1) lastmask |= 1u << reg;
     }
   }
-  if constexpr (MODE == PASS_LSE) {
-    // pass 1 clears the select histograms of its (sequence, KV head) that the
-    // later kernels of the pass accumulate: chunk c takes an equal slice
-    if (a.hist_B) {
-      const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
-      const int64_t bh = (int64_t)b * a.Hkv + h;
-      int sl = 4 * ((kHBins / 4 + nch - 1) / nch);
-      for (int q = c * sl + 4 * t; q < min(kHBins, (c + 1) * sl); q += 4 * nt)
-        *reinterpret_cast<u32x4 *>(a.hist_S + bh * kHBins + q) = u32x4{0u, 0u, 0u, 0u};
-      constexpr int HB = kHCopies * kHBins;
-      sl = 4 * ((HB / 4 + nch - 1) / nch);
-      for (int q = c * sl + 4 * t; q < min(HB, (c + 1) * sl); q += 4 * nt)
-        *reinterpret_cast<u32x4 *>(a.hist_B + bh * HB + q) = u32x4{0u, 0u, 0u, 0u};
-    }
-  }
-
   stage_wait();
   __syncthreads();
   for (int s = 0; s < nstages; ++s) {
@@ -1451,6 +1445,15 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   unsigned cb[kHPer];
   if (calib) load_bins<kHCopies>(a.hist_B + ((int64_t)b * a.Hkv + h) * kHCopies * kHBins, cb);
   const float *re = a.ring + base * a.ring_mp + a.ring_slot;
+  {
+    // clear this segment's slice of the S histogram that the score kernel
+    // accumulates next (its readers of the previous layer are done)
+    const int nseg = st.seg_base[b + 1] - st.seg_base[b];
+    const int sl = 4 * ((kHBins / 4 + nseg - 1) / nseg);
+    unsigned *hs = a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins;
+    for (int q = sg * sl + 4 * t; q < min(kHBins, (sg + 1) * sl); q += 4 * NT)
+      *reinterpret_cast<u32x4 *>(hs + q) = u32x4{0u, 0u, 0u, 0u};
+  }
 
   // one round of loads: B and E + T over the window, E over the window
   // widened by the coherence radius
@@ -1909,6 +1912,16 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
   for (int j = kept + a.W + t; j < K + a.W; j += NT) tbl[j] = -1;
   __syncthreads();
 
+  {
+    // clear this part's slice of the B histogram for the next layer (its
+    // readers, the calibration and score kernels, are done)
+    constexpr int HB = kHCopies * kHBins;
+    const int sl = 4 * ((HB / 4 + a.parts - 1) / a.parts);
+    unsigned *hb = a.hist_B + ((int64_t)b * a.Hkv + h) * HB;
+    for (int q = part * sl + 4 * t; q < min(HB, (part + 1) * sl); q += 4 * NT)
+      *reinterpret_cast<u32x4 *>(hb + q) = u32x4{0u, 0u, 0u, 0u};
+  }
+
   // this part's rows of the compacted cache
   const int rows = K + a.W;
   const int per = (rows + a.parts - 1) / a.parts;
@@ -2016,6 +2029,21 @@ __global__ __launch_bounds__(256) void k_elem(ElemArgs a, SeqTable st) {
 hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s) {
   dim3 grid((unsigned)((a.T + 255) / 256), a.Hkv), block(256);
   hipLaunchKernelGGL(k_elem, grid, block, 0, s, a, st);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- fill
+// Zeroes n 32-bit words (16-byte aligned, n a multiple of 4).
+__global__ __launch_bounds__(256) void k_zero(unsigned *p, int64_t n) {
+  for (int64_t q = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x); q < n; q += 4 * (int64_t)gridDim.x * 256)
+    *reinterpret_cast<u32x4 *>(p + q) = u32x4{0u, 0u, 0u, 0u};
+}
+
+hipError_t launch_zero(unsigned *p, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (n % 4 || reinterpret_cast<uintptr_t>(p) % 16) return hipErrorInvalidValue;
+  const int64_t blocks = std::min<int64_t>(1024, (n / 4 + 255) / 256);
+  hipLaunchKernelGGL(k_zero, dim3((unsigned)blocks), dim3(256), 0, s, p, n);
   return hipGetLastError();
 }
 

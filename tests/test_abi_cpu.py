@@ -114,6 +114,14 @@ def test_calls_reject_bad_batches_and_order_before_enqueueing():
     # no prompt begun -> ORDER
     assert L.bacon_compress_layer(h, 0, C.byref(good.c), fake, fake, fake, fake, fake, fake,
                                   None) == bacon.ERR_ORDER
+    assert L.bacon_compress_layer_lse(h, 0, C.byref(good.c), fake, fake, fake, fake, fake, fake,
+                                      fake, None) == bacon.ERR_ORDER
+    # NULL or misaligned normalisers
+    assert L.bacon_compress_layer_lse(h, 0, C.byref(good.c), fake, fake, fake, None, fake, fake,
+                                      fake, None) == bacon.ERR_INVALID
+    assert L.bacon_compress_layer_lse(h, 0, C.byref(good.c), fake, fake, fake,
+                                      C.c_void_p(0x200002), fake, fake, fake,
+                                      None) == bacon.ERR_INVALID
     # sequence shorter than the window
     assert L.bacon_score(h, 0, C.byref(_batch([0, 10], [4]).c), fake, fake, None, fake, fake,
                          None) == bacon.ERR_INVALID

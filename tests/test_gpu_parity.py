@@ -47,7 +47,8 @@ CASES = {
 }
 
 
-def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=None):
+def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=None,
+             supplied_lse=False):
     import torch
     from paper_2606_14782_amd import bacon
     rtol = P.RTOL[wl.dtype]
@@ -57,10 +58,13 @@ def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=No
     orc = ref.Prompt.for_workload(wl, P.oracle_params(**(orc_kw or {})))
     ctx_s = P.make_ctx(wl, P.params_for(wl, **(gpu_kw or {}))) if split else None
     ctx_f = P.make_ctx(wl, P.params_for(wl, **(gpu_kw or {}))) if fused else None
+    ctx_l = P.make_ctx(wl, P.params_for(wl, **(gpu_kw or {}))) if supplied_lse else None
     if split:
         ctx_s.bacon_begin_prompt(batch)
     if fused:
         ctx_f.bacon_begin_prompt(batch)
+    if supplied_lse:
+        ctx_l.bacon_begin_prompt(batch)
     worst = {}
     stats = {"pairs": 0, "strict": 0, "swaps": 0}
     for layer in range(wl.num_layers):
@@ -84,6 +88,15 @@ def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=No
             P.check_idx(f"{name} L{layer} split", idx_split, r, wl, rtol)
             assert np.array_equal(P.tensor_bytes(ko), P.gather_rows(kb, idx_split, wl))
             assert np.array_equal(P.tensor_bytes(vo), P.gather_rows(vb, idx_split, wl))
+        if supplied_lse:
+            # the window-row normalisers given (here the oracle's, in float32)
+            lse = torch.from_numpy(np.ascontiguousarray(r["lse"], dtype=np.float32)).to(q.device)
+            idx, ko, vo = ctx_l.bacon_compress_layer_lse(layer, batch, q, k, v, lse)
+            torch.cuda.synchronize()
+            gl = idx.cpu().numpy()
+            P.check_idx(f"{name} L{layer} supplied-lse", gl, r, wl, rtol)
+            assert np.array_equal(P.tensor_bytes(ko), P.gather_rows(kb, gl, wl)), "K gather"
+            assert np.array_equal(P.tensor_bytes(vo), P.gather_rows(vb, gl, wl)), "V gather"
         if fused:
             idx, ko, vo = ctx_f.bacon_compress_layer(layer, batch, q, k, v)
             torch.cuda.synchronize()
@@ -109,6 +122,13 @@ def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=No
 @pytest.mark.parametrize("name", list(CASES))
 def test_workload_parity(name):
     run_case(name, CASES[name]())
+
+
+@pytest.mark.parametrize("name", ["tiny-fp32", "video-n32768", "ragged-small", "llava-small"])
+def test_supplied_normalisers(name):
+    """bacon_compress_layer_lse with the window-row normalisers given matches
+    the oracle like the fused call."""
+    run_case(name + "/lse", CASES[name](), split=False, supplied_lse=True)
 
 
 def _batch64():
