@@ -60,9 +60,9 @@ def kernel_bytes(name, wl, persist_m=4):
     vec = T * Hkv * 4                                   # one fp32 value per (position, KV head)
     ring = float(np.mean([(min(persist_m, l) + 1) * vec for l in range(wl.num_layers)]))
     kept_rows = sum(b + wl.window for b in wl.budgets)
-    if name == "window_lse":                            # K, Q_win
+    if name in ("window_lse", "window_lse_kr"):          # K, Q_win
         return ab["k"] + ab["q"]
-    if name == "window_score_calib":                    # K, Q_win, E history, B and E+T+L out
+    if name in ("window_score_calib", "window_score_calib_kr"):   # K, Q_win, E history, B and E+T out
         return ab["k"] + ab["q"] + ring + 2 * vec
     if name == "lse_merge":                             # per-chunk (max, sum) partials
         chunks = T / 512 + wl.batch

@@ -123,9 +123,10 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
 const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", "window_score_calib",
                               "segment_calib", "segment_score", "segment_cand",
                               "final_topk",    "select_calib",  "select_topk",
-                              "calib_elem",    "compact"};
+                              "calib_elem",    "compact",       "window_lse_kr",
+                              "window_score_calib_kr"};
 enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
-                KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_COUNT };
+                KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_COUNT };
 
 }  // namespace
 
@@ -139,6 +140,7 @@ struct bacon_ctx {
   int next_layer = 0;
   std::vector<int32_t> cu, budgets;
   int chunk_stages_override = 0;
+  bool kr_off = false;   // key-register passes switched off (streaming passes only)
   // profiling
   bool prof = false;
   std::vector<hipEvent_t> ev_pool;
@@ -216,7 +218,7 @@ bacon_status check_ptr(const void *p, const char *name, size_t align) {
 // edge_tables: the split calibrate path completes L next to chunk boundaries
 // from an LDS table of kEdgeEntries positions, which bounds the chunk count.
 SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out,
-                    bool edge_tables = true) {
+                    bool edge_tables = true, int force_chunk = 0) {
   SeqTable st{};
   st.batch = bt->batch;
   const bool bf16 = c->shape.dtype == BACON_BF16;
@@ -242,7 +244,7 @@ SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out,
     per_wg = std::max(per_wg, (min_chunk + tk - 1) / tk);
   }
   per_wg = std::min(per_wg, kMaxChunk / tk);
-  const int chunk = tk * per_wg;
+  const int chunk = force_chunk > 0 ? force_chunk : tk * per_wg;
   int cb = 0, ib = 0, kb = 0, sb = 0;
   for (int b = 0; b < bt->batch; ++b) {
     const int n = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
@@ -391,6 +393,7 @@ bacon_status bacon_init(bacon_ctx **ctx, const bacon_shape *shape, const bacon_p
   c->ws_bytes = ws_bytes;
   c->L = L;
   if (const char *e = std::getenv("BACON_CHUNK_STAGES")) c->chunk_stages_override = std::atoi(e);
+  if (const char *e = std::getenv("BACON_KEY_REGISTERS")) c->kr_off = std::atoi(e) == 0;
   *ctx = c;
   return BACON_OK;
 }
@@ -559,9 +562,18 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   TRY(check_ptr(d_k_out, "k_out", 16));
   TRY(check_ptr(d_v_out, "v_out", 16));
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf16 = c->shape.dtype == BACON_BF16;
+  const bool w32 = c->shape.window == 32;
   int chunk = 0;
-  const SeqTable st = make_table(c, bt, &chunk, false);
-  TRY(check_lds(c, bt, chunk, true, -1));
+  SeqTable st{};
+  // key-register passes where they cover the shape, else the streaming passes
+  const bool kr = !c->kr_off && kr_supported(bf16, c->shape.head_dim, c->L.rpad);
+  if (kr) {
+    st = make_table(c, bt, &chunk, false, kr_keys(bf16, c->shape.head_dim));
+  } else {
+    st = make_table(c, bt, &chunk, false);
+    TRY(check_lds(c, bt, chunk, true, -1));
+  }
   int kmax = 0;
   for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, bt->budgets[b]);
   if (final_lds_bytes(kmax, c->shape.window) > (size_t)kLdsBytes)
@@ -572,8 +584,6 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   a.lse_in = d_lse;
   ring_slots(c, layer, &a.ring_write, &a.ring_cnt);
   a.ring_mp = c->L.ring_mp;
-  const bool bf16 = c->shape.dtype == BACON_BF16;
-  const bool w32 = c->shape.window == 32;
   SegArgs g{};
   g.Hkv = c->shape.num_kv_heads;
   g.W = c->shape.window;
@@ -615,11 +625,19 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   g.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
   // final workgroups per (sequence, KV head): about one round over the CUs
   g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
-  if (!d_lse) {
-    TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
-    TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+  if (kr) {
+    if (!d_lse) {
+      TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+      TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+    }
+    TRY(timed(c, KI_FUSED_KR, s, [&] { return launch_krpass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
+  } else {
+    if (!d_lse) {
+      TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+      TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+    }
+    TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
   }
-  TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
   TRY(timed(c, KI_SEGCAL, s, [&] { return launch_segcal(g, st, s); }));
   TRY(timed(c, KI_SEGSCORE, s, [&] { return launch_segscore(g, st, s); }));
   TRY(timed(c, KI_SEGCAND, s, [&] { return launch_segcand(g, st, s); }));

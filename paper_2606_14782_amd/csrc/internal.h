@@ -21,6 +21,7 @@ constexpr int kHBins = 8192;        // bins of the select histograms (32 per oct
 constexpr int kHCopies = 2;         // copies of the B histogram the fused pass spreads its atomics over
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU (and per workgroup) on gfx950
 constexpr int kEdgeEntries = 1024;      // positions next to chunk boundaries the select stages
+constexpr int kKrWaves = 4;             // waves of a key-register pass workgroup
 
 // Per-sequence layout, passed by value to every kernel.
 struct SeqTable {
@@ -146,6 +147,14 @@ int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk);
 
 hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
                        const SeqTable &st, hipStream_t s);
+// Key-register passes (bf16, up to 128 window rows): keys per workgroup, LDS,
+// whether a shape is covered, and the launch of pass 1 (PASS_LSE) or the
+// fused pass 2 (PASS_FUSED).
+int kr_keys(bool bf16, int head_dim);
+int kr_lds_bytes(bool bf16, int head_dim, int rpad);
+bool kr_supported(bool bf16, int head_dim, int rpad);
+hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
+                         const SeqTable &st, hipStream_t s);
 // LDS a select workgroup needs (static + dynamic) for sequences up to max_len.
 size_t select_lds_bytes(int mode, int max_len);
 hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,

@@ -26,6 +26,8 @@
 // One workgroup per (sequence, KV head) runs the same steps over the whole
 // sequence for the split calls.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 #include <math.h>
 #include <stdint.h>
 
@@ -42,6 +44,8 @@ typedef __attribute__((address_space(1))) void g_void;
 // s_waitcnt immediate (gfx9 encoding) waiting for vmcnt = 0 only:
 // vmcnt bits [3:0] and [15:14] zero, expcnt [6:4] and lgkmcnt [11:8] at max.
 constexpr int kWaitVm0 = 0x0F70;
+// ... and for lgkmcnt = 0 only (vmcnt at its maximum 63, expcnt at max).
+constexpr int kWaitLgkm0 = 0xC07F;
 
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kLog2e = 1.44269504088896341f;
@@ -102,6 +106,26 @@ __device__ __forceinline__ float key_float(unsigned k) {
 // produce, share bin 0, so the bins stay monotone in the key.
 __device__ __forceinline__ int hbin(unsigned key) {
   return key >= 0x80000000u ? (int)((key >> 18) & (unsigned)(kHBins - 1)) : 0;
+}
+
+// A copy of v the compiler cannot see through: stops it from hoisting address
+// arithmetic of one phase and keeping it live through the next.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// The value as produced at this point of the program: uses of it wait for
+// its loads here, and no later arithmetic moves above.
+__device__ __forceinline__ void pin(u32x4 &v) {
+  unsigned x = v.x, y = v.y, z = v.z, w = v.w;
+  asm volatile("" : "+v"(x), "+v"(y), "+v"(z), "+v"(w));
+  v = u32x4{x, y, z, w};
+}
+__device__ __forceinline__ void pin(float4 &v) {
+  float x = v.x, y = v.y, z = v.z, w = v.w;
+  asm volatile("" : "+v"(x), "+v"(y), "+v"(z), "+v"(w));
+  v = make_float4(x, y, z, w);
 }
 
 // Row (or column) of accumulator register `reg` in the 32x32 output layout.
@@ -565,6 +589,404 @@ hipError_t launch_pass(int mode, bool bf16, int head_dim, bool w32, const PassAr
   return launch_pass_m<PASS_FUSED>(bf16, head_dim, w32, a, st, s);
 }
 
+// ---------------------------------------------------------------- key-register passes
+// The two K passes for bf16 keys with up to 128 window rows, in a second
+// design: waves own keys instead of query rows.  A workgroup of kKrWaves
+// waves takes the chunk of kr_keys() keys of one KV head; each wave loads its
+// KT key tiles straight into registers, in the MFMA operand layout (lane l:
+// key l % 32, the 16-byte units of the k-slice l / 32), which is the A operand
+// of pass 1 (D = K Q^T) and the B operand of pass 2 (D = Q K^T).  The window
+// queries sit in LDS, swizzled like the key stages.  A wave's key loads are
+// all in flight at once and each tile is worked on as soon as it has landed;
+// pass 2 sums B and Q over the rows inside the wave, so the tiles need no
+// workgroup barrier.  Pass 1 writes per-chunk (max, sum) partials that the
+// merge kernel turns into the row normalisers, as in the streaming design.
+template <bool BF16, int D>
+struct KrCfg {
+  static constexpr int NU = PassCfg<BF16, D>::NU;
+  static constexpr int KT = 32 / NU < 4 ? 32 / NU : 4;   // key tiles per wave: up to 128 registers of keys
+  static constexpr int KPW = kKrWaves * KT * 32;         // keys per workgroup
+};
+
+int kr_keys(bool bf16, int head_dim) {
+  if (bf16) return head_dim == 128 ? KrCfg<true, 128>::KPW : KrCfg<true, 64>::KPW;
+  return head_dim == 128 ? KrCfg<false, 128>::KPW : KrCfg<false, 64>::KPW;
+}
+
+// Row tiles a workgroup holds for Rpad window rows (0: not covered).
+static int kr_row_tiles(int rpad) { return rpad <= 64 ? 2 : (rpad <= 128 ? 4 : 0); }
+
+// LDS map of a key-register workgroup (bytes), NR = 32 * row tiles:
+//   qbuf  max(NR * ROWB, 4 * kHBins)        window queries; the B histogram after pass 2
+//   part  kKrWaves * NR float2              per-wave row partials (pass 1)
+//   nlc   NR floats                         -lse / c2 of each row (pass 2)
+//   tsum  KPW floats                        T of the chunk's keys (fused)
+//   cb    KPW floats                        B of the chunk's keys (fused)
+int kr_lds_bytes(bool bf16, int head_dim, int rpad) {
+  const int nr = 32 * kr_row_tiles(rpad), rowb = head_dim * (bf16 ? 2 : 4), kpw = kr_keys(bf16, head_dim);
+  return std::max(nr * rowb, 4 * kHBins) + 8 * kKrWaves * nr + 4 * nr + 8 * kpw;
+}
+
+template <int MODE, int D, bool W32, int NRT>
+// two workgroups per CU: at most 256 registers per wave
+__global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTable st) {
+  using C = PassCfg<true, D>;
+  constexpr int NU = C::NU, KT = KrCfg<true, D>::KT, KPW = KrCfg<true, D>::KPW;
+  constexpr int NT = 64 * kKrWaves, NR = 32 * NRT;
+  constexpr bool FUSED = MODE == PASS_FUSED;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63, half = lane >> 5, l32 = lane & 31;
+  const int h = blockIdx.y, gchunk = blockIdx.x;
+  const int b = find_seq(st, gchunk);
+  const int c = gchunk - st.chunk_base[b];
+  const int n = st.cu[b + 1] - st.cu[b];
+  const int k0 = c * KPW, k1 = min(n, k0 + KPW);
+  const int W = a.W, wfirst = n - W;
+  const int64_t vrow = (int64_t)h * a.T + st.cu[b];      // [Hkv, T] index of the sequence's position 0
+
+  unsigned char *qbuf = smem;
+  float2 *part = reinterpret_cast<float2 *>(smem + max(NR * C::ROWB, 4 * kHBins));
+  float *nlc = reinterpret_cast<float *>(part + kKrWaves * NR);
+  float *tsum = nlc + NR;
+  float *cb = tsum + KPW;
+
+  // ---- loads, in this order: the window queries, the row normalisers and
+  // the E history of the thread's keys (pass 2), the first key tile; once the
+  // first group is in LDS, the other key tiles.  Everything goes through
+  // registers, so each use waits only for its own loads.  Query slot s of a
+  // row holds piece s ^ (row & SWM); rows past the last real one repeat it
+  // (their results are discarded).
+  constexpr int QP = NR * C::PIECES / NT;                  // query pieces per thread
+  u32x4 qv[QP];
+#pragma unroll
+  for (int j = 0; j < QP; ++j) {
+    const int i = t + j * NT, row = i / C::PIECES, pc = i % C::PIECES;
+    const int rr = min(row, a.R - 1), g = rr / W, w = rr - g * W;
+    qv[j] = *reinterpret_cast<const u32x4 *>(static_cast<const unsigned char *>(a.q) +
+        ((int64_t)(b * W + w) * a.Hq + (int64_t)h * a.G + g) * C::ROWB + 16 * pc);
+  }
+  constexpr int KPT = FUSED ? KPW / NT : 1;                // keys per thread for T
+  float4 rv[KPT][kMaxRing / 4];
+  float lsev = 0.f;
+  if constexpr (FUSED) {
+    // row normalisers: merged from pass 1 (log2 units), or the caller's
+    // natural-log normalisers of the window rows [B, Hq, W]
+    {
+      const int r = min(t, a.R - 1), g = r / W, w = r - g * W;
+      const float *src = a.lse_in ? a.lse_in + ((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w
+                                  : a.lse2 + ((int64_t)b * a.Hkv + h) * a.Rpad + r;
+      lsev = *src;
+    }
+    const int nq = a.ring_mp >> 2;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const int key = min(k0 + t + j * NT, k1 - 1);
+      const float4 *rp = reinterpret_cast<const float4 *>(a.ring + (vrow + key) * a.ring_mp);
+#pragma unroll
+      for (int q = 0; q < kMaxRing / 4; ++q) rv[j][q] = rp[opaque(min(q, nq - 1))];
+    }
+  }
+  const int64_t kstride = (int64_t)a.Hkv * C::ROWB;
+  const unsigned char *kb = static_cast<const unsigned char *>(a.k) +
+                            ((int64_t)st.cu[b] * a.Hkv + h) * C::ROWB + 16 * half;
+  u32x4 kr[KT][NU];
+  auto load_tile = [&](int kt) {
+    const int key = min(k0 + (wave * KT + kt) * 32 + l32, k1 - 1);
+    const unsigned char *kp = kb + (int64_t)key * kstride;
+#pragma unroll
+    for (int u = 0; u < NU; ++u) kr[kt][u] = *reinterpret_cast<const u32x4 *>(kp + 32 * u);
+  };
+  asm volatile("" ::: "memory");
+  load_tile(0);
+  asm volatile("" ::: "memory");
+  // the first group is taken here, after the first key tile was issued
+#pragma unroll
+  for (int j = 0; j < QP; ++j) pin(qv[j]);
+  if constexpr (FUSED) {
+    asm volatile("" : "+v"(lsev));
+#pragma unroll
+    for (int j = 0; j < KPT; ++j)
+#pragma unroll
+      for (int q = 0; q < kMaxRing / 4; ++q) pin(rv[j][q]);
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      float ts = 0.f;
+#pragma unroll
+      for (int q = 0; q < kMaxRing / 4; ++q) {
+        ts += (4 * q + 0 < a.ring_cnt) ? rv[j][q].x : 0.f;
+        ts += (4 * q + 1 < a.ring_cnt) ? rv[j][q].y : 0.f;
+        ts += (4 * q + 2 < a.ring_cnt) ? rv[j][q].z : 0.f;
+        ts += (4 * q + 3 < a.ring_cnt) ? rv[j][q].w : 0.f;
+      }
+      tsum[t + j * NT] = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
+    }
+    // pad rows (and rows past Rpad) get lse = +inf: probability 0
+    if (a.lse_in) lsev *= kLog2e;
+    if (t < NR) nlc[t] = t < a.R ? -lsev / a.c2 : -INFINITY;
+  }
+#pragma unroll
+  for (int j = 0; j < QP; ++j) {
+    const int i = t + j * NT, row = i / C::PIECES, pc = i % C::PIECES;
+    *reinterpret_cast<u32x4 *>(qbuf + row * C::ROWB + 16 * (pc ^ (row & C::SWM))) = qv[j];
+  }
+  // the LDS writes are visible to the workgroup after the barrier (a bare one:
+  // the fence of __syncthreads would also wait for the key tile in flight)
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int kt = 1; kt < KT; ++kt) load_tile(kt);
+  asm volatile("" ::: "memory");
+
+  // byte offsets of this lane's operand pieces 2u + half of query row l32 of a
+  // row tile, from the tile's first row
+  int koff[NU];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) koff[u] = l32 * C::ROWB + 16 * ((2 * u + half) ^ (l32 & C::SWM));
+  // key tile kt against the NRT row tiles: each key unit feeds one MFMA chain
+  // per row tile.  The query fragments of unit u + 1 are read while the MFMAs
+  // of unit u run; scheduling barriers keep the compiler from reading further
+  // ahead (the keys take half of the register file).
+  auto tiles = [&](int kt, int j0, auto &acc, bool keys_first) {
+    constexpr int NJ = sizeof(acc) / sizeof(acc[0]);
+    u32x4 qf[2][NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      qf[0][j] = *reinterpret_cast<const u32x4 *>(qbuf + (j0 + j) * 32 * C::ROWB + koff[0]);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      if (u + 1 < NU) {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          qf[(u + 1) & 1][j] = *reinterpret_cast<const u32x4 *>(qbuf + (j0 + j) * 32 * C::ROWB + koff[u + 1]);
+      }
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        acc[j] = keys_first ? mfma_unit<true>(kr[kt][u], qf[u & 1][j], acc[j])
+                            : mfma_unit<true>(qf[u & 1][j], kr[kt][u], acc[j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  if constexpr (MODE == PASS_LSE) {
+    // ---- pass 1: per-row running max (raw logits) and sum of exp2 over the
+    // wave's keys; tiles away from the sequence end and the window take the
+    // unmasked, branch-free update
+    float m_run[NRT], l_run[NRT];
+#pragma unroll
+    for (int j = 0; j < NRT; ++j) { m_run[j] = -INFINITY; l_run[j] = 0.f; }
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      f32x16 acc[NRT];
+#pragma unroll
+      for (int j = 0; j < NRT; ++j) acc[j] = f32x16{};
+      tiles(kt, 0, acc, true);
+      // acc[j][reg]: key kbase + acc_row(reg, half), row j*32 + l32
+      const int kbase = k0 + (wave * KT + kt) * 32;
+      if (!((kbase + 31 >= k1) || (kbase + 31 > wfirst))) {
+#pragma unroll
+        for (int j = 0; j < NRT; ++j) {
+          float av[16];
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) av[reg] = acc[j][reg];
+          const float mn = fmaxf(m_run[j], tree_max16(av));
+          const float off = -mn * a.c2;
+          float ev[16];
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) ev[reg] = __builtin_amdgcn_exp2f(fmaf(av[reg], a.c2, off));
+          l_run[j] = fmaf(l_run[j], __builtin_amdgcn_exp2f(fmaf(m_run[j], a.c2, off)), tree_sum16(ev));
+          m_run[j] = mn;
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < NRT; ++j) {
+          const int r = j * 32 + l32;
+          const int tpos = wfirst + (r < a.R ? r % W : W - 1);
+          float av[16];
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) {
+            const int key = kbase + acc_row(reg, half);
+            av[reg] = (key < k1 && key <= tpos) ? acc[j][reg] : -INFINITY;
+          }
+          const float mn = fmaxf(m_run[j], tree_max16(av));
+          const float off = mn == -INFINITY ? 0.f : -mn * a.c2;
+          float ev[16];
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) ev[reg] = __builtin_amdgcn_exp2f(fmaf(av[reg], a.c2, off));
+          l_run[j] = fmaf(l_run[j], __builtin_amdgcn_exp2f(fmaf(m_run[j], a.c2, off)), tree_sum16(ev));
+          m_run[j] = mn;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < NRT; ++j) {
+      const float mo = xor32(m_run[j], half), lo = xor32(l_run[j], half);
+      const float m = fmaxf(m_run[j], mo);
+      float l = 0.f;
+      if (m != -INFINITY)
+        l = l_run[j] * __builtin_amdgcn_exp2f((m_run[j] - m) * a.c2) + lo * __builtin_amdgcn_exp2f((mo - m) * a.c2);
+      if (half == 0) part[wave * NR + j * 32 + l32] = make_float2(m == -INFINITY ? -INFINITY : m * a.c2, l);
+    }
+    __syncthreads();
+    // the workgroup's partial of each row (waves in order)
+    for (int r = t; r < a.Rpad; r += NT) {
+      float mx = -INFINITY, sx = 0.f;
+      for (int w = 0; w < kKrWaves; ++w) mx = fmaxf(mx, part[w * NR + r].x);
+      if (mx != -INFINITY)
+        for (int w = 0; w < kKrWaves; ++w) {
+          const float2 pw = part[w * NR + r];
+          if (pw.x != -INFINITY) sx += pw.y * __builtin_amdgcn_exp2f(pw.x - mx);
+        }
+      a.partials[((int64_t)h * st.total_chunks + gchunk) * a.Rpad + r] = make_float2(mx, sx);
+    }
+  } else {
+    // ---- pass 2: B and Q of the wave's keys, summed over the rows in-lane.
+    // The accumulators start at -lse / c2 of their rows, so exp2(c2 * acc) is
+    // the softmax probability.
+    constexpr int RG = NRT < 2 ? NRT : 2;                  // row tiles per MFMA group
+    // accumulator registers of the last query of each group, per row tile
+    uint32_t lastm[NRT];
+#pragma unroll
+    for (int j = 0; j < NRT; ++j) {
+      lastm[j] = 0;
+      if constexpr (!W32) {
+#pragma unroll
+        for (int reg = 0; reg < 16; ++reg) {
+          const int r = j * 32 + acc_row(reg, half);
+          if (r < a.R && (r % W) == W - 1) lastm[j] |= 1u << reg;
+        }
+      }
+    }
+    const float inv_gw = 1.f / (float)(a.G * W), inv_g = 1.f / (float)a.G;
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      const int kbase = k0 + (wave * KT + kt) * 32, key = kbase + l32;
+      const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
+      float bsum = 0.f, qsum = 0.f;
+#pragma unroll
+      for (int j0 = 0; j0 < NRT; j0 += RG) {
+        // the starting values are read again for every group (opaque offset):
+        // held across the tiles they would take 16 * NRT registers
+        f32x16 acc[RG];
+        const float *nb = nlc + opaque(4 * half);
+#pragma unroll
+        for (int j = 0; j < RG; ++j) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float4 v = *reinterpret_cast<const float4 *>(nb + (j0 + j) * 32 + 8 * i);
+            acc[j][4 * i + 0] = v.x;
+            acc[j][4 * i + 1] = v.y;
+            acc[j][4 * i + 2] = v.z;
+            acc[j][4 * i + 3] = v.w;
+          }
+        }
+        tiles(kt, j0, acc, false);
+        // acc[j][reg]: row (j0+j)*32 + acc_row(reg, half), key kbase + l32
+#pragma unroll
+        for (int j = 0; j < RG; ++j) {
+          float p[16];
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) p[reg] = __builtin_amdgcn_exp2f(acc[j][reg] * a.c2);
+          if (edge) {
+#pragma unroll
+            for (int reg = 0; reg < 16; ++reg) {
+              const int r = (j0 + j) * 32 + acc_row(reg, half);
+              const int wr = r < a.R ? r % W : W;
+              if (!(key < k1 && key - wfirst <= wr)) p[reg] = 0.f;
+            }
+          }
+          bsum += tree_sum16(p);
+          if constexpr (W32) {
+            qsum += half ? p[15] : 0.f;
+          } else {
+#pragma unroll
+            for (int reg = 0; reg < 16; ++reg) qsum += ((lastm[j0 + j] >> reg) & 1u) ? p[reg] : 0.f;
+          }
+        }
+      }
+      // E, T, the history append, B and E + T out; half h of a wave writes
+      // the key tiles of parity h
+      bsum += xor32(bsum, half);
+      qsum += xor32(qsum, half);
+      const int kl = (wave * KT + kt) * 32 + l32;
+      if ((kt & 1) == half && key < k1) {
+        const float Bv = bsum * inv_gw, Qv = qsum * inv_g;
+        const float E = (Qv > Bv) ? (Qv - Bv) : 0.f;
+        const float Tv = tsum[kl];
+        const int64_t pos = vrow + key;
+        a.ring[pos * a.ring_mp + a.ring_write] = E;
+        a.vec_B[pos] = Bv;
+        // E + T; the select kernel adds L = P_r E from the history
+        a.vec_VP[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
+        cb[kl] = Bv;
+      }
+    }
+    __syncthreads();
+
+    // B histogram of the chunk's candidates, as in the streaming pass
+    unsigned *hist = reinterpret_cast<unsigned *>(qbuf);
+    const int ncnd = max(0, min(k1, wfirst) - k0);
+    int blo = kHBins, bhi = -1;
+    for (int p = t; p < ncnd; p += NT) {
+      const int q = hbin(float_key(cb[p]));
+      blo = min(blo, q);
+      bhi = max(bhi, q);
+    }
+    blo = __reduce_min_sync(~0ull, blo);
+    bhi = __reduce_max_sync(~0ull, bhi);
+    int *mm = reinterpret_cast<int *>(part);
+    if (lane == 0) { mm[wave] = blo; mm[kKrWaves + wave] = bhi; }
+    __syncthreads();
+    blo = kHBins;
+    bhi = -1;
+    for (int w = 0; w < kKrWaves; ++w) {
+      blo = min(blo, mm[w]);
+      bhi = max(bhi, mm[kKrWaves + w]);
+    }
+    for (int q = blo + t; q <= bhi; q += NT) hist[q] = 0u;
+    __syncthreads();
+    for (int p = t; p < ncnd; p += NT) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
+    __syncthreads();
+    const int copy = (blockIdx.y * gridDim.x + blockIdx.x) % kHCopies;
+    unsigned *gh = a.hist_B + (((int64_t)b * a.Hkv + h) * kHCopies + copy) * kHBins;
+    for (int q = blo + t; q <= bhi; q += NT) {
+      const unsigned cnt = hist[q];
+      if (cnt) atomicAdd(&gh[q], cnt);
+    }
+  }
+}
+
+template <int MODE, int D, bool W32, int NRT>
+static hipError_t launch_kr_t(const PassArgs &a, const SeqTable &st, hipStream_t s) {
+  const int lds = kr_lds_bytes(true, D, a.Rpad);
+  if (lds > kLdsBytes) return hipErrorInvalidValue;
+  auto kern = k_krpass<MODE, D, W32, NRT>;
+  allow_lds(kern, lds);
+  hipLaunchKernelGGL(kern, dim3(st.total_chunks, a.Hkv), dim3(64 * kKrWaves), lds, s, a, st);
+  return hipGetLastError();
+}
+
+template <int MODE, int D>
+static hipError_t launch_kr_d(bool w32, const PassArgs &a, const SeqTable &st, hipStream_t s) {
+  if (kr_row_tiles(a.Rpad) == 2)
+    return w32 ? launch_kr_t<MODE, D, true, 2>(a, st, s) : launch_kr_t<MODE, D, false, 2>(a, st, s);
+  return w32 ? launch_kr_t<MODE, D, true, 4>(a, st, s) : launch_kr_t<MODE, D, false, 4>(a, st, s);
+}
+
+bool kr_supported(bool bf16, int head_dim, int rpad) {
+  return bf16 && kr_row_tiles(rpad) > 0 && kr_lds_bytes(bf16, head_dim, rpad) <= kLdsBytes;
+}
+
+hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
+                         const SeqTable &st, hipStream_t s) {
+  if (!kr_supported(bf16, head_dim, a.Rpad) || (mode != PASS_LSE && mode != PASS_FUSED))
+    return hipErrorInvalidValue;
+  if (mode == PASS_LSE)
+    return head_dim == 128 ? launch_kr_d<PASS_LSE, 128>(false, a, st, s) : launch_kr_d<PASS_LSE, 64>(false, a, st, s);
+  return head_dim == 128 ? launch_kr_d<PASS_FUSED, 128>(w32, a, st, s) : launch_kr_d<PASS_FUSED, 64>(w32, a, st, s);
+}
+
 // ---------------------------------------------------------------- block helpers
 // Shared scratch of the block-wide primitives for NT threads.
 template <int NT>
@@ -982,13 +1404,6 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
 using SelShared = SelSharedT<kSelThreads>;
 
 // ---------------------------------------------------------------- select kernel
-// A copy of v the compiler cannot see through: stops it from hoisting address
-// arithmetic of one phase and keeping it live through the next.
-__device__ __forceinline__ int opaque(int v) {
-  asm volatile("" : "+v"(v));
-  return v;
-}
-
 // LDS: S padded by one word per kSelPer (thread-contiguous reads hit distinct
 // banks), reused as the slot table.
 __device__ __forceinline__ int pad32(int i) { return i + i / kSelPer; }

@@ -131,6 +131,15 @@ def test_supplied_normalisers(name):
     run_case(name + "/lse", CASES[name](), split=False, supplied_lse=True)
 
 
+@pytest.mark.parametrize("name", ["video-n32768", "llava-small", "ragged-small"])
+def test_streaming_passes(name, monkeypatch):
+    """The two streaming K passes (the path of fp32 keys and of more than 128
+    window rows), forced on shapes that take the key-register passes."""
+    monkeypatch.setenv("BACON_KEY_REGISTERS", "0")
+    run_case(name + "/streaming", CASES[name](), split=False)
+    run_case(name + "/streaming-lse", CASES[name](), split=False, fused=False, supplied_lse=True)
+
+
 def _batch64():
     rng = np.random.default_rng(64)
     lens = tuple(int(x) for x in rng.integers(40, 401, size=64))
