@@ -118,8 +118,34 @@ def trace_summary(d: str, md: str, command: str, title: str) -> None:
     print("\n".join(lines))
 
 
+def sq_summary(dirs, md: str, command: str, title: str) -> None:
+    """Markdown table of the mean per-dispatch value of every counter of one
+    or more --pmc runs (e.g. SQ_ counters), per library kernel."""
+    agg = {}
+    for d in dirs:
+        for r in _rows(d):
+            name = library_name(r["Kernel_Name"])
+            if name is not None:
+                agg.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    counters = sorted({c for cs in agg.values() for c in cs})
+    lines = [f"# {title}", "", f"commands (from /tmp with TMPDIR=/tmp): `{command}`", "",
+             f"kernel sources: {source_sha()}", "",
+             "Mean value per dispatch, summed over the device (cycle counters in the units "
+             "rocprofv3 reports).", "",
+             "| kernel | " + " | ".join(counters) + " |",
+             "|---|" + "---|" * len(counters)]
+    for name in sorted(agg):
+        cs = agg[name]
+        cells = [f"{sum(cs[c]) / len(cs[c]):.0f}" if c in cs else "" for c in counters]
+        lines.append(f"| {name} | " + " | ".join(cells) + " |")
+    with open(md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
+    ap.add_argument("--sq", nargs="*")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
     ap.add_argument("--out")
@@ -128,6 +154,9 @@ def main():
     ap.add_argument("--md", required=True)
     ap.add_argument("--command", default="")
     args = ap.parse_args()
+    if args.sq:
+        sq_summary(args.sq, args.md, args.command, args.title)
+        return
     if args.trace:
         trace_summary(args.trace, args.md, args.command, args.title)
         return
