@@ -165,6 +165,19 @@ void bacon_ref_pool(int n, int kernel, const double *x, double *out) {
   }
 }
 
+/* Max pool of S over the candidates (the max-pooling variant, reading). */
+void bacon_ref_pool_max(int n, int kernel, const double *x, double *out) {
+  const int half = kernel / 2;
+  for (int i = 0; i < n; ++i) {
+    const int lo = (i - half < 0) ? 0 : i - half;
+    const int hi = (i + half > n - 1) ? n - 1 : i + half;
+    double mx = x[lo];
+    for (int u = lo + 1; u <= hi; ++u)
+      if (x[u] > mx) mx = x[u];
+    out[i] = mx;
+  }
+}
+
 static int g_threads = 0;
 void bacon_ref_set_threads(int n) { g_threads = n; }
 int bacon_ref_get_threads(void) {
@@ -222,9 +235,19 @@ static void one_head(const bacon_ref_cfg *c, int layer, int b, int h, int batch,
   lam = bacon_ref_lambda(nc, B, V, K, c->rho, c->gamma, c->eps, &sb, &sv, &mcount);
   if (!c->use_last_query) lam = 0.0;
 
-  /* a5: final score, pooling over I, top-K */
+  /* a5: final score (Eq. bacon_score), pooling over I, top-K */
   for (int i = 0; i < n; ++i) S[i] = B[i] + lam * V[i];
-  if (nc > 0) bacon_ref_pool(nc, c->pool_kernel, S, P);
+  if (nc > 0) {
+    if (c->pool_mode == BACON_REF_POOL_MAX_S) {
+      bacon_ref_pool_max(nc, c->pool_kernel, S, P);
+    } else if (c->pool_mode == BACON_REF_POOL_MEAN_B) {
+      /* pooling before calibration: the window score is pooled, V is not */
+      bacon_ref_pool(nc, c->pool_kernel, B, P);
+      for (int i = 0; i < nc; ++i) P[i] += lam * V[i];
+    } else {
+      bacon_ref_pool(nc, c->pool_kernel, S, P);
+    }
+  }
   int32_t *idx_out = o->idx ? o->idx + (long)cu_idx[b] * Hkv + (long)h * K : NULL;
   int32_t *tmp = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K > 0 ? K : 1));
   const int kept = bacon_ref_topk(nc, P, K, tmp);
@@ -265,7 +288,8 @@ int bacon_ref_layer(const bacon_ref_cfg *c, int layer, int batch,
   if (batch < 1 || layer < 0 || c->num_kv_heads < 1 || c->num_q_heads % c->num_kv_heads)
     return -1;
   if (c->window < 1 || c->head_dim < 1 || c->radius < 0 || c->persist_m < 0 ||
-      c->persist_m > 64 || c->pool_kernel < 1 || (c->pool_kernel & 1) == 0)
+      c->persist_m > 64 || c->pool_kernel < 1 || (c->pool_kernel & 1) == 0 ||
+      c->pool_mode < BACON_REF_POOL_MEAN_S || c->pool_mode > BACON_REF_POOL_MEAN_B)
     return -1;
   for (int b = 0; b < batch; ++b)
     if (cu[b + 1] - cu[b] < c->window || budgets[b] < 1) return -1;

@@ -18,7 +18,8 @@
  *                                                   (Sec. 4.4, Eqs. scale_matching_*, lambda_solution)
  *   score         S = B + lambda V                  (Eq. bacon_score)
  *   selection     top-K over the candidate set      (Eq. topk_selection), after an
- *                 average pool of S (the SnapKV pooling convention)
+ *                 average pool of S (the SnapKV pooling convention), or one of
+ *                 the pooling variants of pool_mode
  *   cache         keep {K_i, V_i : i selected} plus the window rows.
  *
  * Readings where the paper is silent (each also listed in the design notes):
@@ -49,6 +50,13 @@ extern "C" {
 
 enum { BACON_REF_TERM_E = 1, BACON_REF_TERM_L = 2, BACON_REF_TERM_T = 4 };
 
+/* How the score is pooled over I before the top-K (the method does not pool;
+ * the pooling and its variants are readings):
+ *   MEAN_S  average pool of S = B + lambda V (default)
+ *   MAX_S   max pool of S
+ *   MEAN_B  average pool of B only, before calibration: pool(B) + lambda V */
+enum { BACON_REF_POOL_MEAN_S = 0, BACON_REF_POOL_MAX_S = 1, BACON_REF_POOL_MEAN_B = 2 };
+
 typedef struct {
   int num_q_heads, num_kv_heads, head_dim, window;
   int radius;         /* r of the coherence neighbourhood (paper default 5)   */
@@ -59,6 +67,7 @@ typedef struct {
   int pool_kernel;    /* odd width of the average pool of S; 1 = off          */
   int use_last_query; /* 0 = window score only (S = B)                        */
   int terms;          /* bit mask of E, L, T included in V (7 = all)          */
+  int pool_mode;      /* BACON_REF_POOL_*                                     */
 } bacon_ref_cfg;
 
 /* Outputs of one layer; any pointer may be NULL to skip it. */
@@ -101,6 +110,9 @@ double bacon_ref_lambda(int n_cand, const double *B, const double *V, int budget
 
 /* Centred average pool of odd width `kernel` over x[0..n-1]. */
 void bacon_ref_pool(int n, int kernel, const double *x, double *out);
+
+/* Centred max pool of odd width `kernel` over x[0..n-1] (truncated at the ends). */
+void bacon_ref_pool_max(int n, int kernel, const double *x, double *out);
 
 /* One layer of a packed batch.  e_hist is the caller's E history
  * [num_layers, Hkv, T]; layers < layer are read, layer `layer` is written.

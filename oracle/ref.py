@@ -35,7 +35,8 @@ class _Cfg(C.Structure):
     _fields_ = [("num_q_heads", C.c_int), ("num_kv_heads", C.c_int), ("head_dim", C.c_int),
                 ("window", C.c_int), ("radius", C.c_int), ("persist_m", C.c_int),
                 ("rho", C.c_double), ("gamma", C.c_double), ("eps", C.c_double),
-                ("pool_kernel", C.c_int), ("use_last_query", C.c_int), ("terms", C.c_int)]
+                ("pool_kernel", C.c_int), ("use_last_query", C.c_int), ("terms", C.c_int),
+                ("pool_mode", C.c_int)]
 
 
 class _Out(C.Structure):
@@ -64,6 +65,7 @@ def lib() -> C.CDLL:
                                        C.c_double, _dp, _dp, _ip]
         L.bacon_ref_lambda.restype = C.c_double
         L.bacon_ref_pool.argtypes = [C.c_int, C.c_int, _dp, _dp]
+        L.bacon_ref_pool_max.argtypes = [C.c_int, C.c_int, _dp, _dp]
         L.bacon_ref_layer.argtypes = [C.POINTER(_Cfg), C.c_int, C.c_int, _ip, _ip, _fp, _fp,
                                       _dp, C.POINTER(_Out)]
         L.bacon_ref_layer.restype = C.c_int
@@ -161,6 +163,13 @@ def pool(x: np.ndarray, kernel: int) -> np.ndarray:
     return out
 
 
+def pool_max(x: np.ndarray, kernel: int) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.zeros_like(x)
+    lib().bacon_ref_pool_max(len(x), kernel, _d(x), _d(out))
+    return out
+
+
 # ---------------------------------------------------------------- whole layers
 
 @dataclass
@@ -172,6 +181,7 @@ class Params:
     eps: float = 1e-12
     use_last_query: int = 1
     terms: int = 7
+    pool_mode: int = 0          # 0 mean of S, 1 max of S, 2 mean of B before calibration
 
 
 class Prompt:
@@ -181,7 +191,8 @@ class Prompt:
                  cu_seqlens, budgets, params: Params | None = None):
         p = params or Params()
         self.cfg = _Cfg(num_q_heads, num_kv_heads, head_dim, window, p.radius, p.persist_m,
-                        p.rho, p.gamma, p.eps, pool_kernel, p.use_last_query, p.terms)
+                        p.rho, p.gamma, p.eps, pool_kernel, p.use_last_query, p.terms,
+                        p.pool_mode)
         self.cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
         self.budgets = np.ascontiguousarray(budgets, dtype=np.int32)
         self.batch = len(self.budgets)

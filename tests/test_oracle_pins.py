@@ -381,3 +381,81 @@ def test_terms_mask_zero_gives_window_score(oracle):
     for o in outs:
         assert np.all(o["V"] == 0.0)
         assert np.array_equal(o["S"], o["B"])
+
+
+# --------------------------------------------------------------- pooling variants
+
+@pytest.mark.parametrize("n,k", [(1, 7), (9, 1), (50, 5), (50, 7), (6, 13), (200, 33)])
+def test_max_pool_matches_library_filter(oracle, n, k):
+    """The max pool over the truncated window equals scipy's maximum filter with
+    edge replication (replicated edge values never exceed the in-range max)."""
+    from scipy.ndimage import maximum_filter1d
+    x = np.random.default_rng(7 * n + k).standard_normal(n)
+    got = oracle.pool_max(x, k)
+    assert np.array_equal(got, maximum_filter1d(x, size=k, mode="nearest"))
+    assert np.all(got >= x)
+    if k == 1:
+        assert np.array_equal(got, x)
+
+
+@pytest.mark.parametrize("k", [3, 5, 9])
+def test_max_pool_dilation(oracle, k):
+    """Two max pools of half-width h make one of half-width 2h (the box is a
+    structuring element: dilations compose by Minkowski sum)."""
+    x = np.random.default_rng(k).standard_normal(120)
+    twice = oracle.pool_max(oracle.pool_max(x, k), k)
+    assert np.array_equal(twice, oracle.pool_max(x, 2 * k - 1))
+
+
+def _pool_modes(oracle, wl, **kw):
+    return [_run(oracle, wl, oracle.Params(pool_mode=m, **kw)) for m in (0, 1, 2)]
+
+
+def test_pool_modes_reduce_without_pooling(oracle):
+    """Pool width 1: every pooling variant is the unpooled S."""
+    wl = _wl_small(num_layers=3).with_(pool_kernel=1)
+    runs = _pool_modes(oracle, wl)
+    for l in range(wl.num_layers):
+        for _, outs, _ in runs[1:]:
+            assert np.array_equal(outs[l]["S_pool"], runs[0][1][l]["S_pool"])
+            assert np.array_equal(outs[l]["idx"], runs[0][1][l]["idx"])
+
+
+def test_pool_before_calibration_reductions(oracle):
+    """Mean pool of B before calibration: with no evidence (V = 0) it is the mean
+    pool of S; otherwise it differs from it by exactly lambda (V - pool(V))."""
+    wl = _wl_small(num_layers=3)
+    (p0, o0, _), _, (p2, o2, _) = _pool_modes(oracle, wl, terms=0)
+    for a, c in zip(o0, o2):
+        assert np.array_equal(a["S_pool"], c["S_pool"])
+        assert np.array_equal(a["idx"], c["idx"])
+    (p0, o0, _), _, (p2, o2, _) = _pool_modes(oracle, wl)
+    for l in range(wl.num_layers):
+        for b in range(wl.batch):
+            nc = wl.seq_lens[b] - wl.window
+            for h in range(wl.num_kv_heads):
+                V = _seq_view(p0, o0[l], "V", b, h)[:nc]
+                lam = o0[l]["lambda"][b, h]
+                assert o2[l]["lambda"][b, h] == lam
+                diff = _seq_view(p2, o2[l], "S_pool", b, h)[:nc] - _seq_view(p0, o0[l], "S_pool", b, h)[:nc]
+                assert np.allclose(diff, lam * (V - _box(V, wl.pool_kernel)), atol=1e-15, rtol=1e-9)
+
+
+def test_max_pool_selection(oracle):
+    """Max pool of S: the pooled score dominates S, is S's windowed max, and the
+    kept set is the brute-force top-K of it (lambda and the scale-matching set
+    do not depend on the pooling)."""
+    from scipy.ndimage import maximum_filter1d
+    wl = _wl_small(num_layers=3)
+    (p0, o0, _), (p1, o1, _), _ = _pool_modes(oracle, wl)
+    for l in range(wl.num_layers):
+        for b in range(wl.batch):
+            nc = wl.seq_lens[b] - wl.window
+            K = wl.budgets[b]
+            for h in range(wl.num_kv_heads):
+                assert o1[l]["lambda"][b, h] == o0[l]["lambda"][b, h]
+                S = _seq_view(p1, o1[l], "S", b, h)[:nc]
+                Sp = _seq_view(p1, o1[l], "S_pool", b, h)[:nc]
+                assert np.array_equal(Sp, maximum_filter1d(S, size=wl.pool_kernel, mode="nearest"))
+                ref = sorted(sorted(range(nc), key=lambda i: (-Sp[i], i))[:K])
+                assert p1.idx_of(o1[l], b, h).tolist() == ref
