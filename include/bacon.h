@@ -17,7 +17,8 @@
  *   lambda = gamma Std_M(B) / (Std_M(V) + eps), M = top-min(rho K, |I|) of B over I
  *                                      (Sec. 4.4, Eqs. scale_matching_size/set, lambda_solution)
  *   S   = B + lambda V                  (Eq. bacon_score)
- *   kept = TopK over I of avgpool_k(S)  (Eq. topk_selection, with the SnapKV pooling)
+ *   kept = TopK over I of pool_k(S)    (Eq. topk_selection, with the SnapKV pooling;
+ *                                      pool_mode picks a variant, see bacon_params)
  *   compacted cache = {K_i, V_i : i kept} followed by the W window rows.
  *
  * Conventions (readings of points the paper leaves open):
@@ -82,7 +83,22 @@ enum { BACON_TERM_E = 1, BACON_TERM_L = 2, BACON_TERM_T = 4 };
 
 /* Method parameters.  Defaults (bacon_default_params): radius 5 and
  * persist_m 4 (Sec. 4.3), rho 2 (Sec. 4.4), gamma 1 and eps 1e-12 (the paper
- * gives no value), pool_kernel 7, use_last_query 1, terms E|L|T. */
+ * gives no value), pool_kernel 7, use_last_query 1, terms E|L|T,
+ * pool_mode BACON_POOL_MEAN_S. */
+/* Pooling of the score over the candidate set before the top-K.  The method
+ * itself does not pool; the average pool of S is the SnapKV convention it is
+ * used with, and the variants serve ablations.  All use a centred window of
+ * pool_kernel positions truncated to the candidate set, and every variant
+ * keeps the scale-matching set and lambda on the unpooled B.
+ *   BACON_POOL_MEAN_S  mean of S = B + lambda V over the window
+ *   BACON_POOL_MAX_S   max of S over the window
+ *   BACON_POOL_MEAN_B  mean of B over the window, before calibration, plus
+ *                      lambda V: pool(B) + lambda V.  In this mode
+ *                      bacon_calibrate returns that pooled score on the
+ *                      candidates (B + lambda V on the window rows) and
+ *                      bacon_select_topk ranks its S without pooling. */
+typedef enum { BACON_POOL_MEAN_S = 0, BACON_POOL_MAX_S = 1, BACON_POOL_MEAN_B = 2 } bacon_pool_mode;
+
 typedef struct {
   int32_t radius;          /* r of the coherence neighbourhood, 0..16        */
   int32_t persist_m;       /* m, persistence depth, 0..16                    */
@@ -92,6 +108,7 @@ typedef struct {
   int32_t pool_kernel;     /* odd width of the average pool of S, 1..33      */
   int32_t use_last_query;  /* 1 = BACON; 0 = window score only (S = B)       */
   uint32_t terms;          /* subset of BACON_TERM_E|L|T included in V       */
+  int32_t pool_mode;       /* BACON_POOL_MEAN_S (default), _MAX_S, _MEAN_B   */
 } bacon_params;
 
 /* Static shape of the model and the largest batch a context will see. */

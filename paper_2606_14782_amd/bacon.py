@@ -30,7 +30,11 @@ ENTRY_POINTS = [
 class Params(C.Structure):
     _fields_ = [("radius", C.c_int32), ("persist_m", C.c_int32), ("rho", C.c_float),
                 ("gamma", C.c_float), ("eps", C.c_float), ("pool_kernel", C.c_int32),
-                ("use_last_query", C.c_int32), ("terms", C.c_uint32)]
+                ("use_last_query", C.c_int32), ("terms", C.c_uint32), ("pool_mode", C.c_int32)]
+
+
+# pooling of the score before the top-K (bacon_pool_mode)
+POOL_MEAN_S, POOL_MAX_S, POOL_MEAN_B = 0, 1, 2
 
 
 class Shape(C.Structure):

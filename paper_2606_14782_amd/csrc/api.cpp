@@ -80,6 +80,8 @@ bacon_status check_params(const bacon_params *p) {
   if (p->use_last_query != 0 && p->use_last_query != 1)
     return fail(BACON_ERR_INVALID, "use_last_query must be 0 or 1");
   if (p->terms & ~7u) return fail(BACON_ERR_INVALID, "terms has unknown bits");
+  if (p->pool_mode < BACON_POOL_MEAN_S || p->pool_mode > BACON_POOL_MEAN_B)
+    return fail(BACON_ERR_INVALID, "pool_mode must be 0, 1 or 2");
   return BACON_OK;
 }
 
@@ -311,6 +313,7 @@ SelArgs sel_args(const bacon_ctx *c) {
   a.T = s.max_total_tokens;
   a.radius = p.radius;
   a.pool_half = p.pool_kernel / 2;
+  a.pool_mode = p.pool_mode;
   a.rho = p.rho;
   a.gamma = p.gamma;
   a.eps = p.eps;
@@ -320,7 +323,6 @@ SelArgs sel_args(const bacon_ctx *c) {
   a.vec_VP = reinterpret_cast<const float *>(c->ws + c->L.vec_vp);
   a.vp_chunk = 1 << 30;
   a.lambda_ws = reinterpret_cast<float *>(c->ws + c->L.lambda);
-  a.row_bytes = s.head_dim * (s.dtype == BACON_BF16 ? 2 : 4);
   return a;
 }
 
@@ -361,6 +363,7 @@ void bacon_default_params(bacon_params *p) {
   p->gamma = 1.0f;
   p->eps = 1e-12f;
   p->pool_kernel = 7;
+  p->pool_mode = BACON_POOL_MEAN_S;
   p->use_last_query = 1;
   p->terms = BACON_TERM_E | BACON_TERM_L | BACON_TERM_T;
 }
@@ -590,6 +593,7 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   g.T = T;
   g.radius = c->params.radius;
   g.pool_half = c->params.pool_kernel / 2;
+  g.pool_mode = c->params.pool_mode;
   g.vp_chunk = chunk;
   g.rho = c->params.rho;
   g.gamma = c->params.gamma;

@@ -64,12 +64,13 @@ struct PassArgs {
   uint32_t terms;
 };
 
-enum SelMode { SEL_FUSED = 0, SEL_CALIB = 1, SEL_TOPK = 2 };
+enum SelMode { SEL_CALIB = 1, SEL_TOPK = 2 };
+enum PoolMode { POOL_MEAN_S = 0, POOL_MAX_S = 1, POOL_MEAN_B = 2 };
 
 struct SelArgs {
   int Hkv, W;
   int64_t T;
-  int radius, pool_half;
+  int radius, pool_half, pool_mode;
   int vp_chunk;            // chunk size of the in-chunk L partial in vec_VP
   float rho, gamma, eps;
   int use_last_query;
@@ -82,19 +83,14 @@ struct SelArgs {
   float *out_S, *out_V, *out_E;  // SEL_CALIB optional outputs [Hkv, T]
   float *out_lambda;       // optional [B, Hkv]
   float *lambda_ws;        // [B, Hkv]
-  int32_t *idx;            // SEL_FUSED / SEL_TOPK output
-  // fused gather
-  const void *k, *v;
-  void *k_out, *v_out;
-  int row_bytes;
-  int do_gather;
+  int32_t *idx;            // SEL_TOPK output
 };
 
 // Histogram select of the fused pass (calibration, score and final kernels).
 struct SegArgs {
   int Hkv, W;
   int64_t T;
-  int radius, pool_half, vp_chunk;
+  int radius, pool_half, pool_mode, vp_chunk;
   float rho, gamma, eps;
   int use_last_query;
   uint32_t terms;

@@ -1543,21 +1543,27 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     }
     // S = B + lambda V (Eq. bacon_score), in place of B; each thread touches
     // only its own positions.
+    // With pooling before calibration the candidates get pool(B) + lambda V
+    // instead, the score the top-K then ranks unpooled.
+    const bool mean_b = a.pool_mode == POOL_MEAN_B;
+    const int hp = a.pool_half;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
       const int i = tt + j * kSelThreads;
       if (i < n) {
-        const float S = fmaf(lam, vp[j], arr[pad32(i)]);
-        if constexpr (MODE == SEL_CALIB) {
-          a.out_S[base + i] = S;
-          if (a.out_V) a.out_V[base + i] = vp[j];
-          if (a.out_E) a.out_E[base + i] = re[(int64_t)i * a.ring_mp];
-        } else {
-          arr[pad32(i)] = S;
+        float bi = arr[pad32(i)];
+        if (mean_b && i < nc) {
+          const int lo = max(0, i - hp), hi = min(nc - 1, i + hp);
+          double acc = 0.0;
+          for (int u = lo; u <= hi; ++u) acc += (double)arr[pad32(u)];
+          bi = (float)(acc / (double)(hi - lo + 1));
         }
+        a.out_S[base + i] = fmaf(lam, vp[j], bi);
+        if (a.out_V) a.out_V[base + i] = vp[j];
+        if (a.out_E) a.out_E[base + i] = re[(int64_t)i * a.ring_mp];
       }
     }
-    if constexpr (MODE == SEL_CALIB) return;
+    return;
   } else {
     float sv[PER];
 #pragma unroll
@@ -1569,14 +1575,31 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
   __syncthreads();
 
   // Pooled score over I and its keys, contiguous ownership: positions
-  // [t*PER, t*PER + PER).  Sliding window sums in double.
+  // [t*PER, t*PER + PER).  The mean pool slides window sums in double; the
+  // max pool scans each window; with pooling before calibration S is taken
+  // as it is.
   const int i0 = t * PER;
   unsigned key[PER];
   {
     const int hp = a.pool_half;
 #pragma unroll
     for (int j = 0; j < PER; ++j) key[j] = 0u;
-    if (i0 < nc) {
+    if (i0 < nc && a.pool_mode == POOL_MEAN_B) {
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        if (i0 + j < nc) key[j] = float_key(arr[pad32(i0 + j)]);
+    } else if (i0 < nc && a.pool_mode == POOL_MAX_S) {
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const int i = i0 + j;
+        if (i < nc) {
+          const int lo = max(0, i - hp), hi = min(nc - 1, i + hp);
+          float mx = arr[pad32(lo)];
+          for (int u = lo + 1; u <= hi; ++u) mx = fmaxf(mx, arr[pad32(u)]);
+          key[j] = float_key(mx);
+        }
+      }
+    } else if (i0 < nc) {
       int lo = max(0, i0 - hp), hi = min(nc - 1, i0 + hp);
       double acc = 0.0;
       for (int u = lo; u <= hi; ++u) acc += (double)arr[pad32(u)];
@@ -1633,40 +1656,6 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
   }
   for (int j = kept + t; j < K; j += kSelThreads) idx[j] = -1;
 
-  if constexpr (MODE == SEL_FUSED) {
-    if (!a.do_gather) return;
-    for (int w = t; w < a.W; w += kSelThreads) tbl[kept + w] = nc + w;
-    __syncthreads();
-    const int pieces = a.row_bytes / 16;
-    const int total = (K + a.W) * pieces;
-    const unsigned char *ks = static_cast<const unsigned char *>(a.k);
-    const unsigned char *vs = static_cast<const unsigned char *>(a.v);
-    unsigned char *ko = static_cast<unsigned char *>(a.k_out);
-    unsigned char *vo = static_cast<unsigned char *>(a.v_out);
-    constexpr int BATCH = 5;
-    for (int q0 = t; q0 < total; q0 += BATCH * kSelThreads) {
-      u32x4 kv[BATCH], vv[BATCH];
-      int64_t dst[BATCH];
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        const int q = min(q0 + u * kSelThreads, total - 1);
-        const int r = q / pieces, p = q - r * pieces;
-        const int src = (r < kept + a.W) ? tbl[r] : -1;
-        dst[u] = ((int64_t)(st.kept_base[b] + r) * a.Hkv + h) * a.row_bytes + 16 * p;
-        const int64_t so = ((int64_t)(st.cu[b] + max(src, 0)) * a.Hkv + h) * a.row_bytes + 16 * p;
-        kv[u] = *reinterpret_cast<const u32x4 *>(ks + so);
-        vv[u] = *reinterpret_cast<const u32x4 *>(vs + so);
-        if (src < 0) { kv[u] = u32x4{0u, 0u, 0u, 0u}; vv[u] = u32x4{0u, 0u, 0u, 0u}; }
-      }
-#pragma unroll
-      for (int u = 0; u < BATCH; ++u) {
-        if (q0 + u * kSelThreads < total) {
-          *reinterpret_cast<u32x4 *>(ko + dst[u]) = kv[u];
-          *reinterpret_cast<u32x4 *>(vo + dst[u]) = vv[u];
-        }
-      }
-    }
-  }
 }
 
 size_t select_lds_bytes(int mode, int max_len) {
@@ -1682,10 +1671,7 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
   dim3 grid(st.batch, a.Hkv), block(kSelThreads);
   const size_t lds = select_lds_bytes(mode, max_len) - sizeof(SelShared);
   if (lds + sizeof(SelShared) > kLdsBytes) return hipErrorInvalidValue;
-  if (mode == SEL_FUSED) {
-    allow_lds(k_select<SEL_FUSED>, lds);
-    hipLaunchKernelGGL((k_select<SEL_FUSED>), grid, block, lds, s, a, st);
-  } else if (mode == SEL_CALIB) {
+  if (mode == SEL_CALIB) {
     allow_lds(k_select<SEL_CALIB>, lds);
     hipLaunchKernelGGL((k_select<SEL_CALIB>), grid, block, lds, s, a, st);
   } else {
@@ -2095,13 +2081,20 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
   const int64_t hrow = ((int64_t)b * a.Hkv + h) * kHBins;
   for (int q = t; q < kHBins; q += NT) hist[q] = 0u;
 
-  // the segment's pooled B and V do not depend on lambda: in flight first
+  // what the pooled score is made of does not depend on lambda: in flight
+  // first.  Mean of S: the pooled B and V (pool(B + lambda V) = pool(B) +
+  // lambda pool(V)); mean of B before calibration: pooled B and V itself.
+  // (The max of S reads B and V over the widened segment after lambda.)
+  const bool max_s = a.pool_mode == POOL_MAX_S;
   float pb[PER], pv[PER];
+  {
+    const float *vsrc = a.pool_mode == POOL_MEAN_B ? a.vec_V : a.vec_pV;
 #pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int q = min(t + j * NT, max(ncand - 1, 0));
-    pb[j] = a.vec_pB[base + i0 + q];
-    pv[j] = a.vec_pV[base + i0 + q];
+    for (int j = 0; j < PER; ++j) {
+      const int q = min(t + j * NT, max(ncand - 1, 0));
+      pb[j] = max_s ? 0.f : a.vec_pB[base + i0 + q];
+      pv[j] = max_s ? 0.f : vsrc[base + i0 + q];
+    }
   }
 
   int M = (int)floorf(a.rho * (float)st.budget[b]);
@@ -2154,13 +2147,47 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
 
   // pooled score keys of the segment, and their histogram
   __syncthreads();
+  if (max_s) {
+    // S over the segment widened by the pool halo in LDS (the moment scratch
+    // is free now), -inf outside the candidate set, then the max over each
+    // pool window
+    float *sw = reinterpret_cast<float *>(mom);
+    const int w0 = i0 - kPoolHalo;                   // position of window slot 0
+    float wb[kSegWinJ], wv[kSegWinJ];
 #pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int q = t + j * NT;
-    if (q < ncand) {
-      const unsigned key = float_key(fmaf(lam, pv[j], pb[j]));
-      a.vec_S[base + i0 + q] = key;
-      atomicAdd(&hist[hbin(key)], 1u);
+    for (int j = 0; j < kSegWinJ; ++j) {
+      const int u = min(max(w0 + t + j * NT, 0), n - 1);
+      wb[j] = a.vec_B[base + u];
+      wv[j] = a.vec_V[base + u];
+    }
+#pragma unroll
+    for (int j = 0; j < kSegWinJ; ++j) {
+      const int q = t + j * NT, u = w0 + q;
+      if (q < kSegWin) sw[q] = (u >= 0 && u < nc) ? fmaf(lam, wv[j], wb[j]) : -INFINITY;
+    }
+    __syncthreads();
+    const int hp = a.pool_half;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int q = t + j * NT;
+      if (q < ncand) {
+        const int i = i0 + q, lo = max(0, i - hp), hi = min(nc - 1, i + hp);
+        float mx = sw[lo - w0];
+        for (int u = lo + 1; u <= hi; ++u) mx = fmaxf(mx, sw[u - w0]);
+        const unsigned key = float_key(mx);
+        a.vec_S[base + i] = key;
+        atomicAdd(&hist[hbin(key)], 1u);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int q = t + j * NT;
+      if (q < ncand) {
+        const unsigned key = float_key(fmaf(lam, pv[j], pb[j]));
+        a.vec_S[base + i0 + q] = key;
+        atomicAdd(&hist[hbin(key)], 1u);
+      }
     }
   }
   __syncthreads();

@@ -55,6 +55,15 @@ def close(name, got, want, rtol):
     return worst
 
 
+def candidate_mask(wl):
+    """[Hkv, T] mask of the candidate positions (all but each sequence's window)."""
+    m = np.zeros((wl.num_kv_heads, wl.total_tokens), bool)
+    for b in range(wl.batch):
+        c0, c1 = int(wl.cu_seqlens[b]), int(wl.cu_seqlens[b + 1])
+        m[:, c0:c1 - wl.window] = True
+    return m
+
+
 def seq_slices(wl):
     cu = wl.cu_seqlens
     return [(int(cu[b]), int(cu[b + 1])) for b in range(wl.batch)]

@@ -49,6 +49,7 @@ def test_defaults_follow_the_paper():
     assert (p.radius, p.persist_m, p.rho) == (5, 4, 2.0)
     assert p.gamma == 1.0 and p.use_last_query == 1 and p.terms == 7
     assert p.pool_kernel % 2 == 1
+    assert p.pool_mode == bacon.POOL_MEAN_S
 
 
 @pytest.mark.parametrize("kw,expect_zero", [
@@ -69,7 +70,8 @@ def test_workspace_size_validates_shape(kw, expect_zero):
 
 @pytest.mark.parametrize("kw", [{"radius": -1}, {"radius": 17}, {"persist_m": 17}, {"rho": 0.0},
                                 {"gamma": -1.0}, {"pool_kernel": 4}, {"pool_kernel": 35},
-                                {"use_last_query": 2}, {"terms": 8}])
+                                {"use_last_query": 2}, {"terms": 8}, {"pool_mode": -1},
+                                {"pool_mode": 3}])
 def test_bad_params_rejected(kw):
     assert _ws(_shape(), bacon.default_params(**kw)) == 0
 

@@ -80,9 +80,13 @@ def run_case(name, wl, gpu_kw=None, orc_kw=None, split=True, fused=True, make=No
             idx = ctx_s.bacon_select_topk(batch, cal["S"])
             ko, vo = ctx_s.bacon_compact(batch, k, v, idx)
             torch.cuda.synchronize()
+            want = dict(r)
+            if (gpu_kw or {}).get("pool_mode") == 2:
+                # pooling before calibration: the candidates' score is pool(B) + lambda V
+                want["S"] = np.where(P.candidate_mask(wl), r["S_pool"], r["S"])
             for key, got in (("lse", lse), ("B", B), ("Q", Q), ("E", cal["E"]), ("V", cal["V"]),
                              ("S", cal["S"]), ("lambda", cal["lambda"])):
-                w = P.close(f"{name} L{layer} {key}", got.cpu().numpy(), r[key], rtol)
+                w = P.close(f"{name} L{layer} {key}", got.cpu().numpy(), want[key], rtol)
                 worst[key] = max(worst.get(key, 0.0), w)
             idx_split = idx.cpu().numpy()
             P.check_idx(f"{name} L{layer} split", idx_split, r, wl, rtol)
@@ -190,6 +194,17 @@ EDGE = {
     # candidate) and a budget above half the candidate set
     "M-over-segment": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 7, "bf16", (8000,),
                                               (1500,), ((30, 7000),), 4, 18)),
+    # pooling variants: max of S, and mean of B before calibration, over
+    # several segments with a pool halo that crosses them
+    "pool-max-s": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 9, "bf16", (5000, 2070),
+                                          (100, 40), ((30, 4000), (0, 2000)), 4, 23),
+                       gpu=dict(pool_mode=1), orc=dict(pool_mode=1)),
+    "pool-mean-b": dict(wl=inputs.Workload("edge", 3, 8, 2, 128, 32, 9, "bf16", (5000, 2070),
+                                           (100, 40), ((30, 4000), (0, 2000)), 4, 24),
+                        gpu=dict(pool_mode=2), orc=dict(pool_mode=2)),
+    "pool-max-s-fp32": dict(wl=inputs.Workload("edge", 2, 4, 2, 64, 20, 33, "fp32", (3000, 333),
+                                               (64, 40), ((10, 2500), (5, 300)), 2, 25),
+                            gpu=dict(pool_mode=1), orc=dict(pool_mode=1)),
     # the largest window-row block: G*W = 256 rows (eight row tiles)
     "rows256-g8-w32": dict(wl=inputs.Workload("edge", 3, 16, 2, 128, 32, 7, "bf16", (3000, 1500),
                                               (100, 40), ((30, 2500), (0, 1200)), 4, 20)),
