@@ -148,9 +148,13 @@ bacon_status bacon_init(bacon_ctx **ctx, const bacon_shape *shape, const bacon_p
 /* Destroys the host context (the workspace stays the caller's). */
 bacon_status bacon_free(bacon_ctx *ctx);
 
-/* Starts a prompt: fixes the batch layout used by every layer until the next
- * call and resets the layer counter; the E history starts empty.  Enqueues a
- * small clearing kernel on `stream` (a hipStream_t). */
+/* Starts a prompt: fixes the sequences (cu_seqlens) used by every layer until
+ * the next call and resets the layer counter; the E history starts empty.
+ * The budgets of later calls may differ from layer to layer (a per-layer budget
+ * schedule: the budget K_{l,h} of the backbone method, Sec. 4 Preliminaries):
+ * each call keeps its own
+ * batch's budgets and sizes its outputs by them.  Enqueues a small clearing
+ * kernel on `stream` (a hipStream_t). */
 bacon_status bacon_begin_prompt(bacon_ctx *ctx, const bacon_batch *batch, void *stream);
 
 /* Window score and last-query score of one layer (Eqs. window_score,

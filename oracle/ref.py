@@ -206,8 +206,12 @@ class Prompt:
         return cls(wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window,
                    wl.pool_kernel, wl.cu_seqlens, wl.budgets_arr, params)
 
-    def layer(self, layer: int, q_win: np.ndarray, k: np.ndarray) -> dict:
+    def layer(self, layer: int, q_win: np.ndarray, k: np.ndarray, budgets=None) -> dict:
+        """One layer; ``budgets`` overrides the prompt's per-sequence budgets for
+        this layer only (a per-layer budget schedule)."""
         B_, Hq, Hkv, W, T = self.batch, self.Hq, self.Hkv, self.W, self.T
+        bud = self.budgets if budgets is None else np.ascontiguousarray(budgets, dtype=np.int32)
+        assert bud.shape == self.budgets.shape
         q_win = np.ascontiguousarray(q_win, dtype=np.float32)
         k = np.ascontiguousarray(k, dtype=np.float32)
         assert q_win.shape == (B_ * W, Hq, self.d) and k.shape == (T, Hkv, self.d)
@@ -216,12 +220,12 @@ class Prompt:
         r = {"lse": np.zeros((B_, Hq, W)), "B": vec(), "Q": vec(), "E": vec(), "L": vec(),
              "T": vec(), "V": vec(), "S": vec(), "S_pool": vec(), "lambda": sc(),
              "sigma_B": sc(), "sigma_V": sc(), "m_count": np.zeros((B_, Hkv), np.int32),
-             "idx": np.zeros(int(self.budgets.sum()) * Hkv, np.int32),
-             "n_kept": np.zeros((B_, Hkv), np.int32)}
+             "idx": np.zeros(int(bud.sum()) * Hkv, np.int32),
+             "n_kept": np.zeros((B_, Hkv), np.int32), "budgets": bud}
         out = _Out(_d(r["lse"]), _d(r["B"]), _d(r["Q"]), _d(r["E"]), _d(r["L"]), _d(r["T"]),
                    _d(r["V"]), _d(r["S"]), _d(r["S_pool"]), _d(r["lambda"]), _d(r["sigma_B"]),
                    _d(r["sigma_V"]), _i(r["m_count"]), _i(r["idx"]), _i(r["n_kept"]))
-        rc = lib().bacon_ref_layer(C.byref(self.cfg), layer, B_, _i(self.cu), _i(self.budgets),
+        rc = lib().bacon_ref_layer(C.byref(self.cfg), layer, B_, _i(self.cu), _i(bud),
                                    _f(q_win), _f(k), _d(self.e_hist), C.byref(out))
         if rc != 0:
             raise ValueError("oracle rejected the layer arguments")
@@ -229,18 +233,20 @@ class Prompt:
 
     def idx_of(self, r: dict, b: int, h: int) -> np.ndarray:
         """Kept positions of (sequence b, KV head h), without -1 padding."""
-        off = int(self.budgets[:b].sum()) * self.Hkv + h * int(self.budgets[b])
-        ids = r["idx"][off:off + int(self.budgets[b])]
+        bud = r.get("budgets", self.budgets)
+        off = int(bud[:b].sum()) * self.Hkv + h * int(bud[b])
+        ids = r["idx"][off:off + int(bud[b])]
         return ids[ids >= 0]
 
     def compact(self, r: dict, k_bytes: np.ndarray, v_bytes: np.ndarray, elem_size: int):
-        rows = int((self.budgets + self.W).sum())
+        bud = r.get("budgets", self.budgets)
+        rows = int((bud + self.W).sum())
         shape = (rows, self.Hkv, self.d * elem_size)
         k_out = np.zeros(shape, np.uint8)
         v_out = np.zeros(shape, np.uint8)
         kb = np.ascontiguousarray(k_bytes).view(np.uint8)
         vb = np.ascontiguousarray(v_bytes).view(np.uint8)
-        lib().bacon_ref_compact(self.batch, _i(self.cu), _i(self.budgets), self.Hkv, self.d,
+        lib().bacon_ref_compact(self.batch, _i(self.cu), _i(bud), self.Hkv, self.d,
                                 self.W, elem_size, _i(r["idx"]), _i(r["n_kept"]),
                                 kb.ctypes.data, vb.ctypes.data, k_out.ctypes.data,
                                 v_out.ctypes.data)

@@ -197,10 +197,11 @@ bacon_status check_batch(const bacon_ctx *c, const bacon_batch *bt) {
 
 bacon_status check_prompt_batch(const bacon_ctx *c, const bacon_batch *bt) {
   if (!c->prompt) return fail(BACON_ERR_ORDER, "no prompt begun (call bacon_begin_prompt)");
+  // the sequences are fixed for the prompt; the budgets may change from layer
+  // to layer (a per-layer budget schedule)
   if (bt->batch + 1 != (int)c->cu.size() ||
-      memcmp(bt->cu_seqlens, c->cu.data(), c->cu.size() * sizeof(int32_t)) != 0 ||
-      memcmp(bt->budgets, c->budgets.data(), c->budgets.size() * sizeof(int32_t)) != 0)
-    return fail(BACON_ERR_INVALID, "batch differs from the one given to bacon_begin_prompt");
+      memcmp(bt->cu_seqlens, c->cu.data(), c->cu.size() * sizeof(int32_t)) != 0)
+    return fail(BACON_ERR_INVALID, "batch sequences differ from the ones given to bacon_begin_prompt");
   return BACON_OK;
 }
 

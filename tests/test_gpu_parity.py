@@ -144,6 +144,35 @@ def test_streaming_passes(name, monkeypatch):
     run_case(name + "/streaming-lse", CASES[name](), split=False, fused=False, supplied_lse=True)
 
 
+@pytest.mark.parametrize("name", ["ragged-small", "video-small"])
+def test_per_layer_budget_schedule(name):
+    """Budgets that change from layer to layer within a prompt (a shrinking
+    per-layer schedule per sequence): the fused call matches the oracle run
+    with the same schedule, and the compacted cache follows each layer's
+    budgets."""
+    import torch
+    from paper_2606_14782_amd import bacon, budgets as sched
+    wl = CASES[name]()
+    per = [sched.pyramid(int(k), wl.num_layers, 0.25) for k in wl.budgets]
+    orc = ref.Prompt.for_workload(wl, P.oracle_params())
+    ctx = P.make_ctx(wl)
+    ctx.bacon_begin_prompt(bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr))
+    rtol = P.RTOL[wl.dtype]
+    for layer in range(wl.num_layers):
+        bl = tuple(per[b][layer] for b in range(wl.batch))
+        wll = wl.with_(budgets=bl)
+        x = inputs.layer_inputs(wl, layer)
+        r = orc.layer(layer, x["q_win"], x["k"], budgets=np.array(bl, np.int32))
+        batch = bacon.BatchLayout(wl.cu_seqlens, wll.budgets_arr)
+        idx, ko, vo = ctx.bacon_compress_layer(layer, batch, P.to_dev(x["q_win"], wl),
+                                               P.to_dev(x["k"], wl), P.to_dev(x["v"], wl))
+        torch.cuda.synchronize()
+        gi = idx.cpu().numpy()
+        P.check_idx(f"{name}/schedule L{layer}", gi, r, wll, rtol)
+        assert np.array_equal(P.tensor_bytes(ko), P.gather_rows(P.as_bytes(x["k"], wl), gi, wll))
+        assert np.array_equal(P.tensor_bytes(vo), P.gather_rows(P.as_bytes(x["v"], wl), gi, wll))
+
+
 def _batch64():
     rng = np.random.default_rng(64)
     lens = tuple(int(x) for x in rng.integers(40, 401, size=64))

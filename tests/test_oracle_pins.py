@@ -459,3 +459,30 @@ def test_max_pool_selection(oracle):
                 assert np.array_equal(Sp, maximum_filter1d(S, size=wl.pool_kernel, mode="nearest"))
                 ref = sorted(sorted(range(nc), key=lambda i: (-Sp[i], i))[:K])
                 assert p1.idx_of(o1[l], b, h).tolist() == ref
+
+
+# --------------------------------------------------------------- per-layer budgets
+
+def test_per_layer_budgets_leave_history_unchanged(oracle):
+    """A per-layer budget schedule changes only each layer's selection: E, L, T
+    and V, and so every later layer's evidence, are the same as with a fixed
+    budget, and layer l equals a prompt run with budget K_l throughout."""
+    from paper_2606_14782_amd import budgets as sched
+    wl = _wl_small(num_layers=5)
+    per = [sched.pyramid(int(k), wl.num_layers, 0.25) for k in wl.budgets]
+    p = oracle.Prompt.for_workload(wl)
+    fixed = oracle.Prompt.for_workload(wl)
+    for l in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, l)
+        bl = np.array([per[b][l] for b in range(wl.batch)], np.int32)
+        r = p.layer(l, x["q_win"], x["k"], budgets=bl)
+        f = fixed.layer(l, x["q_win"], x["k"])
+        for key in ("B", "Q", "E", "L", "T", "V"):
+            assert np.array_equal(r[key], f[key])
+        # the same layer from a prompt that used budget K_l at every layer
+        q = oracle.Prompt.for_workload(wl.with_(budgets=tuple(int(v) for v in bl)))
+        for j in range(l + 1):
+            xj = inputs.layer_inputs(wl, j)
+            g = q.layer(j, xj["q_win"], xj["k"])
+        assert np.array_equal(g["idx"], r["idx"])
+        assert np.array_equal(g["S_pool"], r["S_pool"])
