@@ -62,13 +62,13 @@ def kernel_bytes(name, wl, persist_m=4):
     kept_rows = sum(b + wl.window for b in wl.budgets)
     if name in ("window_lse", "window_lse_kr"):          # K, Q_win
         return ab["k"] + ab["q"]
-    if name in ("window_score_calib", "window_score_calib_kr"):   # K, Q_win, E history, B and E+T out
-        return ab["k"] + ab["q"] + ring + 2 * vec
+    if name in ("window_score_calib", "window_score_calib_kr"):   # K, Q_win; E and B out
+        return ab["k"] + ab["q"] + 2 * vec
     if name == "lse_merge":                             # per-chunk (max, sum) partials
         chunks = T / 512 + wl.batch
         return Hkv * chunks * wl.group * wl.window * 8
-    if name == "segment_calib":                         # B, E+T+L in; V, pooled B and V out
-        return 5 * vec
+    if name == "segment_calib":                         # B, E history in; V, pooled B and V out
+        return 4 * vec + ring
     if name == "segment_score":                         # pooled B and V in; score keys out
         return 3 * vec
     if name == "segment_cand":                          # score keys in

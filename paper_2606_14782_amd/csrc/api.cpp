@@ -38,7 +38,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct Layout {
   size_t ring, vec_b, vec_vp, vec_v, vec_pb, vec_pv, vec_s, hist_b, hist_s, list_bk, list_bp, list_bv,
       list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, total;
-  int rpad, slots, ring_mp;
+  int rpad, slots;
   int64_t chunks_cap;
 };
 
@@ -89,13 +89,14 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   Layout L{};
   const int G = s->num_q_heads / s->num_kv_heads;
   L.rpad = ((G * s->window + 31) / 32) * 32;
-  L.slots = p->persist_m > 0 ? p->persist_m : 1;
-  L.ring_mp = 4 * ((L.slots + 3) / 4);
+  // E history: m + 1 slot vectors, so the slot a layer writes is never one of
+  // the m its persistence term reads
+  L.slots = p->persist_m + 1;
   const int tk = 32 * std::min(L.rpad / 32, 4);
   L.chunks_cap = (s->max_total_tokens + tk - 1) / tk + s->max_batch;
   const size_t vec = (size_t)s->num_kv_heads * (size_t)s->max_total_tokens * sizeof(float);
   size_t off = 0;
-  L.ring = off;     off += align256((size_t)L.ring_mp * vec);
+  L.ring = off;     off += align256((size_t)L.slots * vec);
   L.vec_b = off;    off += align256(vec);
   L.vec_vp = off;   off += align256(vec);
   L.vec_v = off;    off += align256(vec);
@@ -298,8 +299,9 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   return a;
 }
 
-// History slots for layer `layer`: E of layer j lives in slot j % max(m, 1),
-// so the previous min(m, layer) layers occupy slots 0 .. cnt-1.
+// History slots for layer `layer`: E of layer j lives in slot j % (m + 1), so
+// the previous cnt = min(m, layer) layers are the slots wr - cnt .. wr - 1
+// (mod m + 1), none of them wr.
 void ring_slots(const bacon_ctx *c, int layer, int *wr, int *cnt) {
   *cnt = std::min(c->params.persist_m, layer);
   *wr = layer % c->L.slots;
@@ -478,7 +480,8 @@ bacon_status bacon_calibrate(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
   e.in_Q = d_Q;
   e.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
   ring_slots(c, layer, &e.ring_write, &e.ring_cnt);
-  e.ring_mp = c->L.ring_mp;
+  e.ring_slots = c->L.slots;
+  e.ring_stride = (int64_t)c->shape.num_kv_heads * T;
   e.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
   e.Hkv = c->shape.num_kv_heads;
   e.radius = c->params.radius;
@@ -492,7 +495,7 @@ bacon_status bacon_calibrate(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
   a.vec_B = d_B;
   a.vp_chunk = chunk;   // same chunking as the fused pass
   a.ring = e.ring;
-  a.ring_mp = c->L.ring_mp;
+  a.ring_stride = e.ring_stride;
   a.ring_slot = e.ring_write;
   a.out_S = d_S;
   a.out_V = d_V;
@@ -586,8 +589,9 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
   a.T = T;
   a.lse_in = d_lse;
-  ring_slots(c, layer, &a.ring_write, &a.ring_cnt);
-  a.ring_mp = c->L.ring_mp;
+  int ring_cnt = 0;
+  ring_slots(c, layer, &a.ring_write, &ring_cnt);
+  a.ring_stride = (int64_t)c->shape.num_kv_heads * T;
   SegArgs g{};
   g.Hkv = c->shape.num_kv_heads;
   g.W = c->shape.window;
@@ -604,8 +608,10 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   g.vec_B = a.vec_B;
   g.vec_VP = a.vec_VP;
   g.ring = a.ring;
-  g.ring_mp = c->L.ring_mp;
+  g.ring_stride = a.ring_stride;
+  g.ring_slots = c->L.slots;
   g.ring_slot = a.ring_write;
+  g.ring_cnt = ring_cnt;
   g.vec_V = reinterpret_cast<float *>(c->ws + c->L.vec_v);
   g.vec_pB = reinterpret_cast<float *>(c->ws + c->L.vec_pb);
   g.vec_pV = reinterpret_cast<float *>(c->ws + c->L.vec_pv);

@@ -54,12 +54,11 @@ struct PassArgs {
   // PASS_SCORE
   float *out_B, *out_Q; // [Hkv, T]
   // PASS_FUSED
-  float *ring;          // [Hkv, T, ring_mp] E history, slot l % max(m,1) holds layer l
-  int ring_mp;          // slots per position, padded to a multiple of 4
+  float *ring;          // [slots, Hkv, T] E history; slot l % slots holds layer l
+  int64_t ring_stride;  // Hkv * T, floats between slots
   int ring_write;       // slot receiving this layer's E
-  int ring_cnt;         // earlier layers averaged into T (they occupy slots 0..cnt-1)
   float *vec_B;         // [Hkv, T] window score
-  float *vec_VP;        // [Hkv, T] E + T + in-chunk part of L (per the terms mask)
+  float *vec_VP;        // [Hkv, T] unused by the fused pass (the calibration kernel forms V)
   int radius;
   uint32_t terms;
 };
@@ -77,8 +76,9 @@ struct SelArgs {
   uint32_t terms;
   const float *vec_B;      // [Hkv, T]
   const float *vec_VP;     // [Hkv, T]
-  const float *ring;       // [Hkv, T, ring_mp] E history
-  int ring_mp, ring_slot;  // slot of this layer's E
+  const float *ring;       // [slots, Hkv, T] E history
+  int64_t ring_stride;     // Hkv * T
+  int ring_slot;           // slot of this layer's E
   const float *in_S;       // SEL_TOPK: user S [Hkv, T]
   float *out_S, *out_V, *out_E;  // SEL_CALIB optional outputs [Hkv, T]
   float *out_lambda;       // optional [B, Hkv]
@@ -95,8 +95,10 @@ struct SegArgs {
   int use_last_query;
   uint32_t terms;
   const float *vec_B, *vec_VP;   // [Hkv, T]
-  const float *ring;             // [Hkv, T, ring_mp]
-  int ring_mp, ring_slot;
+  const float *ring;             // [slots, Hkv, T] E history
+  int64_t ring_stride;           // Hkv * T
+  int ring_slots, ring_slot;     // slot count; slot of this layer's E
+  int ring_cnt;                  // earlier layers averaged into T: slots ring_slot - cnt .. ring_slot - 1
   float *vec_V;                  // [Hkv, T] V = E + L + T over I
   float *vec_pB, *vec_pV;        // [Hkv, T] pooled B and V over I
   unsigned *vec_S;               // [Hkv, T] keys of the pooled score over I
@@ -122,7 +124,8 @@ struct SegArgs {
 struct ElemArgs {           // split calibrate: E, T, L, ring update
   const float *in_B, *in_Q;
   float *ring;
-  int ring_mp, ring_write, ring_cnt;
+  int64_t ring_stride;
+  int ring_slots, ring_write, ring_cnt;
   float *vec_VP;
   int Hkv, radius, chunk;
   int64_t T;

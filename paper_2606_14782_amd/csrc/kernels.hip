@@ -314,16 +314,6 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
   for (int s = 0; s < nstages; ++s) {
     const int buf = s & 1;
     const int ntile = min(tk, k1 - (k0 + s * tk));
-    // E history of this stage's keys (slots 0..ring_mp-1 of the position),
-    // consumed by the stage epilogue; clamped so the loads are unconditional.
-    float4 rv[kMaxRing / 4];
-    if constexpr (MODE == PASS_FUSED) {
-      const int64_t pos = (int64_t)h * a.T + st.cu[b] + k0 + s * tk + min(t, ntile - 1);
-      const float4 *rp = reinterpret_cast<const float4 *>(a.ring + pos * a.ring_mp);
-      const int nq = a.ring_mp >> 2;
-#pragma unroll
-      for (int q = 0; q < kMaxRing / 4; ++q) rv[q] = rp[min(q, nq - 1)];
-    }
     if (s + 1 < nstages) fetch(s + 1);
     const unsigned char *kl = kbuf + buf * tk * C::ROWB;
     // The tiles of a stage are unrolled (a tile's row offset is a constant in
@@ -424,20 +414,10 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           a.out_B[pos] = Bv;
           a.out_Q[pos] = Qv;
         } else {
-          const float E = (Qv > Bv) ? (Qv - Bv) : 0.f;
-          float ts = 0.f;
-#pragma unroll
-          for (int q = 0; q < kMaxRing / 4; ++q) {
-            ts += (4 * q + 0 < a.ring_cnt) ? rv[q].x : 0.f;
-            ts += (4 * q + 1 < a.ring_cnt) ? rv[q].y : 0.f;
-            ts += (4 * q + 2 < a.ring_cnt) ? rv[q].z : 0.f;
-            ts += (4 * q + 3 < a.ring_cnt) ? rv[q].w : 0.f;
-          }
-          const float Tv = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
-          a.ring[pos * a.ring_mp + a.ring_write] = E;
+          // E (Eq. boundary_residual) to this layer's history slot; the
+          // calibration kernel forms L, T and V from the history
+          a.ring[a.ring_write * a.ring_stride + pos] = (Qv > Bv) ? (Qv - Bv) : 0.f;
           a.vec_B[pos] = Bv;
-          // E + T; the select kernel adds L = P_r E from the history
-          a.vec_VP[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
           cb[s * tk + t] = Bv;
         }
       }
@@ -620,11 +600,10 @@ static int kr_row_tiles(int rpad) { return rpad <= 64 ? 2 : (rpad <= 128 ? 4 : 0
 //   qbuf  max(NR * ROWB, 4 * kHBins)        window queries; the B histogram after pass 2
 //   part  kKrWaves * NR float2              per-wave row partials (pass 1)
 //   nlc   NR floats                         -lse / c2 of each row (pass 2)
-//   tsum  KPW floats                        T of the chunk's keys (fused)
 //   cb    KPW floats                        B of the chunk's keys (fused)
 int kr_lds_bytes(bool bf16, int head_dim, int rpad) {
   const int nr = 32 * kr_row_tiles(rpad), rowb = head_dim * (bf16 ? 2 : 4), kpw = kr_keys(bf16, head_dim);
-  return std::max(nr * rowb, 4 * kHBins) + 8 * kKrWaves * nr + 4 * nr + 8 * kpw;
+  return std::max(nr * rowb, 4 * kHBins) + 8 * kKrWaves * nr + 4 * nr + 4 * kpw;
 }
 
 template <int MODE, int D, bool W32, int NRT>
@@ -647,12 +626,11 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTabl
   unsigned char *qbuf = smem;
   float2 *part = reinterpret_cast<float2 *>(smem + max(NR * C::ROWB, 4 * kHBins));
   float *nlc = reinterpret_cast<float *>(part + kKrWaves * NR);
-  float *tsum = nlc + NR;
-  float *cb = tsum + KPW;
+  float *cb = nlc + NR;
 
-  // ---- loads, in this order: the window queries, the row normalisers and
-  // the E history of the thread's keys (pass 2), the first key tile; once the
-  // first group is in LDS, the other key tiles.  Everything goes through
+  // ---- loads, in this order: the window queries, the row normalisers
+  // (pass 2), the first key tile; once the first group is in LDS, the other
+  // key tiles.  Everything goes through
   // registers, so each use waits only for its own loads.  Query slot s of a
   // row holds piece s ^ (row & SWM); rows past the last real one repeat it
   // (their results are discarded).
@@ -665,26 +643,14 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTabl
     qv[j] = *reinterpret_cast<const u32x4 *>(static_cast<const unsigned char *>(a.q) +
         ((int64_t)(b * W + w) * a.Hq + (int64_t)h * a.G + g) * C::ROWB + 16 * pc);
   }
-  constexpr int KPT = FUSED ? KPW / NT : 1;                // keys per thread for T
-  float4 rv[KPT][kMaxRing / 4];
   float lsev = 0.f;
   if constexpr (FUSED) {
     // row normalisers: merged from pass 1 (log2 units), or the caller's
     // natural-log normalisers of the window rows [B, Hq, W]
-    {
-      const int r = min(t, a.R - 1), g = r / W, w = r - g * W;
-      const float *src = a.lse_in ? a.lse_in + ((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w
-                                  : a.lse2 + ((int64_t)b * a.Hkv + h) * a.Rpad + r;
-      lsev = *src;
-    }
-    const int nq = a.ring_mp >> 2;
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-      const int key = min(k0 + t + j * NT, k1 - 1);
-      const float4 *rp = reinterpret_cast<const float4 *>(a.ring + (vrow + key) * a.ring_mp);
-#pragma unroll
-      for (int q = 0; q < kMaxRing / 4; ++q) rv[j][q] = rp[opaque(min(q, nq - 1))];
-    }
+    const int r = min(t, a.R - 1), g = r / W, w = r - g * W;
+    const float *src = a.lse_in ? a.lse_in + ((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w
+                                : a.lse2 + ((int64_t)b * a.Hkv + h) * a.Rpad + r;
+    lsev = *src;
   }
   const int64_t kstride = (int64_t)a.Hkv * C::ROWB;
   const unsigned char *kb = static_cast<const unsigned char *>(a.k) +
@@ -704,22 +670,6 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTabl
   for (int j = 0; j < QP; ++j) pin(qv[j]);
   if constexpr (FUSED) {
     asm volatile("" : "+v"(lsev));
-#pragma unroll
-    for (int j = 0; j < KPT; ++j)
-#pragma unroll
-      for (int q = 0; q < kMaxRing / 4; ++q) pin(rv[j][q]);
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-      float ts = 0.f;
-#pragma unroll
-      for (int q = 0; q < kMaxRing / 4; ++q) {
-        ts += (4 * q + 0 < a.ring_cnt) ? rv[j][q].x : 0.f;
-        ts += (4 * q + 1 < a.ring_cnt) ? rv[j][q].y : 0.f;
-        ts += (4 * q + 2 < a.ring_cnt) ? rv[j][q].z : 0.f;
-        ts += (4 * q + 3 < a.ring_cnt) ? rv[j][q].w : 0.f;
-      }
-      tsum[t + j * NT] = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
-    }
     // pad rows (and rows past Rpad) get lse = +inf: probability 0
     if (a.lse_in) lsev *= kLog2e;
     if (t < NR) nlc[t] = t < a.R ? -lsev / a.c2 : -INFINITY;
@@ -905,20 +855,18 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTabl
           }
         }
       }
-      // E, T, the history append, B and E + T out; half h of a wave writes
-      // the key tiles of parity h
+      // E to the history and B out; half h of a wave writes the key tiles of
+      // parity h
       bsum += xor32(bsum, half);
       qsum += xor32(qsum, half);
       const int kl = (wave * KT + kt) * 32 + l32;
       if ((kt & 1) == half && key < k1) {
         const float Bv = bsum * inv_gw, Qv = qsum * inv_g;
-        const float E = (Qv > Bv) ? (Qv - Bv) : 0.f;
-        const float Tv = tsum[kl];
         const int64_t pos = vrow + key;
-        a.ring[pos * a.ring_mp + a.ring_write] = E;
+        // E (Eq. boundary_residual) to this layer's history slot; the
+        // calibration kernel forms L, T and V from the history
+        a.ring[a.ring_write * a.ring_stride + pos] = (Qv > Bv) ? (Qv - Bv) : 0.f;
         a.vec_B[pos] = Bv;
-        // E + T; the select kernel adds L = P_r E from the history
-        a.vec_VP[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f);
         cb[kl] = Bv;
       }
     }
@@ -1433,11 +1381,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     const int nedge = nbnd * 2 * r;
     float *edge = reinterpret_cast<float *>(cpos + kCandCap);     // E at those positions
     float *fixt = edge + kEdgeCap;                                // their L correction
-    const float *re = a.ring + base * a.ring_mp + a.ring_slot;
+    const float *re = a.ring + a.ring_slot * a.ring_stride + base;   // E of this layer
     for (int q = t; q < nedge; q += kSelThreads) {
       const int c = q / (2 * r) + 1, o = q - (c - 1) * 2 * r;
       const int u = c * CH - r + o;
-      const float e = re[(int64_t)min(max(u, 0), n - 1) * a.ring_mp];
+      const float e = re[min(max(u, 0), n - 1)];
       edge[q] = (u >= 0 && u < n) ? e : 0.f;
     }
     __syncthreads();
@@ -1560,7 +1508,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
         }
         a.out_S[base + i] = fmaf(lam, vp[j], bi);
         if (a.out_V) a.out_V[base + i] = vp[j];
-        if (a.out_E) a.out_E[base + i] = re[(int64_t)i * a.ring_mp];
+        if (a.out_E) a.out_E[base + i] = re[i];
       }
     }
     return;
@@ -1841,11 +1789,18 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   int M = (int)floorf(a.rho * (float)st.budget[b]);
   M = max(0, min(M, nc));
   const bool calib = M > 0 && a.use_last_query;
-  // the bins of the B histogram (accumulated by the fused pass), in flight
-  // with the loads below
-  unsigned cb[kHPer];
-  if (calib) load_bins<kHCopies>(a.hist_B + ((int64_t)b * a.Hkv + h) * kHCopies * kHBins, cb);
-  const float *re = a.ring + base * a.ring_mp + a.ring_slot;
+  // the bins of the B histogram (accumulated by the fused pass, in kHCopies
+  // copies): loaded raw and summed once the window loads below are in flight
+  u32x4 hv[kHCopies][kHPer / 4];
+  {
+    const unsigned *gh = a.hist_B + ((int64_t)b * a.Hkv + h) * kHCopies * kHBins;
+#pragma unroll
+    for (int c = 0; c < kHCopies; ++c)
+#pragma unroll
+      for (int q = 0; q < kHPer / 4; ++q)
+        hv[c][q] = reinterpret_cast<const u32x4 *>(gh + (int64_t)c * kHBins + kHPer * t)[q];
+  }
+  const float *re = a.ring + a.ring_slot * a.ring_stride + base;   // E of this layer
   {
     // clear this segment's slice of the S histogram that the score kernel
     // accumulates next (its readers of the previous layer are done)
@@ -1856,33 +1811,56 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
       *reinterpret_cast<u32x4 *>(hs + q) = u32x4{0u, 0u, 0u, 0u};
   }
 
-  // one round of loads: B and E + T over the window, E over the window
-  // widened by the coherence radius
+  // one round of loads: B and T (the earlier layers' E, oldest first) over
+  // the window, E over the window widened by the coherence radius
   {
     const int tt = opaque(t);
-    float bv[kSegWinJ], vv[kSegWinJ], ev[kSegEJ];
+    float bv[kSegWinJ], tv[kSegWinJ], ev[kSegEJ];
 #pragma unroll
     for (int j = 0; j < kSegWinJ; ++j) {
       const int u = min(max(w0 + tt + j * NT, 0), n - 1);
       bv[j] = a.vec_B[base + u];
-      vv[j] = a.vec_VP[base + u];
+      tv[j] = 0.f;
     }
 #pragma unroll
     for (int j = 0; j < kSegEJ; ++j) {
       const int u = min(max(w0 - kMaxRadius + tt + j * NT, 0), n - 1);
-      ev[j] = re[(int64_t)u * a.ring_mp];
+      ev[j] = re[u];
+    }
+    const bool use_t = (a.terms & 4u) && a.ring_cnt > 0;
+    if (use_t) {
+      // four earlier layers per round, all loads of a round in flight; past
+      // the oldest layer the slot index repeats (an L2 hit) and is not added
+      for (int l0 = 0; l0 < a.ring_cnt; l0 += 4) {
+        float x[4][kSegWinJ];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int l = max(a.ring_cnt - l0 - i, 1);       // oldest first
+          const float *rt = a.ring + ((a.ring_slot - l + a.ring_slots) % a.ring_slots) * a.ring_stride + base;
+#pragma unroll
+          for (int j = 0; j < kSegWinJ; ++j) x[i][j] = rt[min(max(w0 + tt + j * NT, 0), n - 1)];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < kSegWinJ; ++j) tv[j] += (l0 + i < a.ring_cnt) ? x[i][j] : 0.f;
+      }
     }
 #pragma unroll
     for (int j = 0; j < kSegEJ; ++j)
       if (tt + j * NT < kSegE) Es[tt + j * NT] = ev[j];
     __syncthreads();
-    // V = E + T + L, L = P_r E over the sequence-truncated neighbourhood
+    // V = E + L + T (Eq. structurally_calibrated_evidence, per the terms
+    // mask), L = P_r E over the sequence-truncated neighbourhood
+    // (Eq. intra_layer_coherence), T the mean of the earlier layers' E
+    // (Eq. inter_layer_persistence)
+    const float inv_cnt = a.ring_cnt ? 1.f / (float)a.ring_cnt : 0.f;
 #pragma unroll
     for (int j = 0; j < kSegWinJ; ++j) {
       const int q = tt + j * NT;
       if (q < kSegWin) {
         const int u = w0 + q;
-        float v = vv[j];
+        float v = ((a.terms & 1u) ? Es[q + kMaxRadius] : 0.f) + (use_t ? tv[j] * inv_cnt : 0.f);
         if (use_l && u >= 0 && u < n) {
           const int lo = max(0, u - r), hi = min(n - 1, u + r);
           float sum = 0.f;
@@ -1919,6 +1897,14 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
 
   // boundary bin of the top-M of B, and the segment's list of candidates at
   // or above it (key, position, V) in position order
+  unsigned cb[kHPer];
+#pragma unroll
+  for (int q = 0; q < kHPer / 4; ++q) {
+    u32x4 x = hv[0][q];
+#pragma unroll
+    for (int c = 1; c < kHCopies; ++c) x += hv[c][q];
+    cb[4 * q + 0] = x.x; cb[4 * q + 1] = x.y; cb[4 * q + 2] = x.z; cb[4 * q + 3] = x.w;
+  }
   bins_boundary<kHPer, NT>(cb, M, ss);
   const int beta = ss.bc_i[0], above = ss.bc_i[1];
   const unsigned cntb = ss.bc_u[2];
@@ -2451,8 +2437,10 @@ __global__ __launch_bounds__(256) void k_elem(ElemArgs a, SeqTable st) {
     return (Qv > Bv) ? (Qv - Bv) : 0.f;
   };
   const float E = resid(pos);
+  // T: the previous ring_cnt layers, oldest first
   float ts = 0.f;
-  for (int j = 0; j < a.ring_cnt; ++j) ts += a.ring[pos * a.ring_mp + j];
+  for (int j = a.ring_cnt; j >= 1; --j)
+    ts += a.ring[((a.ring_write - j + a.ring_slots) % a.ring_slots) * a.ring_stride + pos];
   const float Tv = a.ring_cnt ? ts / (float)a.ring_cnt : 0.f;
   // part of L with neighbours inside the position's chunk, as the fused pass
   // forms it (the select kernel adds the neighbours across chunk boundaries)
@@ -2464,7 +2452,7 @@ __global__ __launch_bounds__(256) void k_elem(ElemArgs a, SeqTable st) {
     for (int u = max(lo, k0); u <= min(hi, k1 - 1); ++u) s += resid(row + s0 + u);
     L = s / (float)(hi - lo + 1);
   }
-  a.ring[pos * a.ring_mp + a.ring_write] = E;
+  a.ring[a.ring_write * a.ring_stride + pos] = E;
   a.vec_VP[pos] = ((a.terms & 1u) ? E : 0.f) + ((a.terms & 4u) ? Tv : 0.f) + L;
 }
 
