@@ -1948,8 +1948,8 @@ __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t ba
   L.cap = cs;
   const int tt = opaque(t);
   rec = *recp;                                   // first: it heads the longest chain
-  int c = 0;
-  if (tt < L.nseg) c = cnts[(int64_t)h * st.total_segs + st.seg_base[b] + tt];
+  // unconditional (clamped) so that no branch waits for the loads in flight
+  int c = cnts[(int64_t)h * st.total_segs + st.seg_base[b] + min(tt, L.nseg - 1)];
 #pragma unroll
   for (int j = 0; j < kListSpec; ++j) {
     const int e = tt + j * NT, s = min(e / cs, L.nseg - 1);
@@ -1958,6 +1958,9 @@ __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t ba
     p[j] = lpos[o];
     if constexpr (WITH_V) v[j] = lv[o];
   }
+  // the record is uniform: taken here, so that moving it to scalar registers
+  // waits for it only after the list loads are issued
+  asm volatile("" : "+v"(rec.x), "+v"(rec.y), "+v"(rec.z), "+v"(rec.w));
 #pragma unroll
   for (int j = kListSpec; j < kListPer; ++j) k[j] = 0u;
   if (t < kMaxSegs) scnt[t] = t < L.nseg ? c : 0;
