@@ -190,7 +190,7 @@ int bacon_ref_get_threads(void) {
 
 /* One (sequence, KV head) of one layer: every step in the paper's order. */
 static void one_head(const bacon_ref_cfg *c, int layer, int b, int h, int batch,
-                     const int32_t *cu, const int32_t *budgets, const int32_t *cu_idx,
+                     const int32_t *cu, const int32_t *budgets, const long *idx_off,
                      const float *q_win, const float *k, double *e_hist, long T,
                      bacon_ref_out *o) {
   const int Hq = c->num_q_heads, Hkv = c->num_kv_heads, d = c->head_dim, W = c->window;
@@ -198,7 +198,7 @@ static void one_head(const bacon_ref_cfg *c, int layer, int b, int h, int batch,
   const int n = cu[b + 1] - cu[b];
   const long off = (long)h * T + cu[b];
   const int n_cand = n - W;              /* candidate set I = [0, n - W) */
-  const int K = budgets[b];
+  const int K = budgets[(long)b * Hkv + h];     /* budget of this (sequence, KV head) */
   (void)batch;
 
   double *B = (double *)malloc(sizeof(double) * (size_t)n);
@@ -248,7 +248,7 @@ static void one_head(const bacon_ref_cfg *c, int layer, int b, int h, int batch,
       bacon_ref_pool(nc, c->pool_kernel, S, P);
     }
   }
-  int32_t *idx_out = o->idx ? o->idx + (long)cu_idx[b] * Hkv + (long)h * K : NULL;
+  int32_t *idx_out = o->idx ? o->idx + idx_off[(long)b * Hkv + h] : NULL;
   int32_t *tmp = (int32_t *)malloc(sizeof(int32_t) * (size_t)(K > 0 ? K : 1));
   const int kept = bacon_ref_topk(nc, P, K, tmp);
   if (idx_out) {
@@ -291,22 +291,25 @@ int bacon_ref_layer(const bacon_ref_cfg *c, int layer, int batch,
       c->persist_m > 64 || c->pool_kernel < 1 || (c->pool_kernel & 1) == 0 ||
       c->pool_mode < BACON_REF_POOL_MEAN_S || c->pool_mode > BACON_REF_POOL_MEAN_B)
     return -1;
-  for (int b = 0; b < batch; ++b)
-    if (cu[b + 1] - cu[b] < c->window || budgets[b] < 1) return -1;
-  const long T = cu[batch];
-  int32_t *cu_idx = (int32_t *)malloc(sizeof(int32_t) * (size_t)(batch + 1));
-  cu_idx[0] = 0;
-  for (int b = 0; b < batch; ++b) cu_idx[b + 1] = cu_idx[b] + budgets[b];
   const int pairs = batch * c->num_kv_heads;
+  for (int b = 0; b < batch; ++b)
+    if (cu[b + 1] - cu[b] < c->window) return -1;
+  for (int p = 0; p < pairs; ++p)
+    if (budgets[p] < 1) return -1;
+  const long T = cu[batch];
+  /* kept indices of (b, h) start after those of every earlier pair */
+  long *idx_off = (long *)malloc(sizeof(long) * (size_t)(pairs + 1));
+  idx_off[0] = 0;
+  for (int p = 0; p < pairs; ++p) idx_off[p + 1] = idx_off[p] + budgets[p];
 #ifdef _OPENMP
   const int nt = bacon_ref_get_threads();
 #pragma omp parallel for schedule(dynamic, 1) num_threads(nt)
 #endif
   for (int p = 0; p < pairs; ++p) {
     one_head(c, layer, p / c->num_kv_heads, p % c->num_kv_heads, batch, cu, budgets,
-             cu_idx, q_win, k, e_hist, T, o);
+             idx_off, q_win, k, e_hist, T, o);
   }
-  free(cu_idx);
+  free(idx_off);
   return 0;
 }
 
@@ -320,11 +323,16 @@ void bacon_ref_compact(int batch, const int32_t *cu, const int32_t *budgets,
   long out_row0 = 0, idx0 = 0;
   for (int b = 0; b < batch; ++b) {
     const int n = cu[b + 1] - cu[b];
-    const int K = budgets[b];
+    /* rows per head of this sequence: the largest budget of its heads, plus W */
+    int C = 0;
+    for (int h = 0; h < Hkv; ++h)
+      if (budgets[(long)b * Hkv + h] > C) C = budgets[(long)b * Hkv + h];
     for (int h = 0; h < Hkv; ++h) {
+      const int K = budgets[(long)b * Hkv + h];
       const int kept = n_kept[(long)b * Hkv + h];
-      const int32_t *ib = idx + idx0 * Hkv + (long)h * K;
-      for (int j = 0; j < K + W; ++j) {
+      const int32_t *ib = idx + idx0;
+      idx0 += K;
+      for (int j = 0; j < C + W; ++j) {
         long src = -1;
         if (j < kept) src = ib[j];
         else if (j < kept + W) src = n - W + (j - kept);
@@ -339,7 +347,6 @@ void bacon_ref_compact(int batch, const int32_t *cu, const int32_t *budgets,
         }
       }
     }
-    out_row0 += K + W;
-    idx0 += K;
+    out_row0 += C + W;
   }
 }

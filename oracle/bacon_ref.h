@@ -35,8 +35,10 @@
  * values (bf16 inputs are widened exactly).  Layouts:
  *   q_win [B*W, Hq, d], k and v [T, Hkv, d] packed by cu_seqlens,
  *   per-position vectors [Hkv, T], per-(b,h) scalars [B, Hkv],
- *   kept indices per sequence b at offset Hkv*sum_{b'<b} budget_b', head-major,
- *   positions relative to the sequence start, ascending, -1 padded.
+ *   budgets [B, Hkv]: keys kept by each (sequence, KV head);
+ *   kept indices of (b, h) after those of every earlier pair in (b, h) order,
+ *   positions relative to the sequence start, ascending, -1 padded;
+ *   compacted rows per sequence: C_b + W per head, C_b = max_h budget(b, h).
  */
 #ifndef BACON_REF_H
 #define BACON_REF_H
@@ -114,17 +116,19 @@ void bacon_ref_pool(int n, int kernel, const double *x, double *out);
 /* Centred max pool of odd width `kernel` over x[0..n-1] (truncated at the ends). */
 void bacon_ref_pool_max(int n, int kernel, const double *x, double *out);
 
-/* One layer of a packed batch.  e_hist is the caller's E history
- * [num_layers, Hkv, T]; layers < layer are read, layer `layer` is written.
- * Returns 0, or -1 on invalid arguments. */
+/* One layer of a packed batch.  budgets [batch, Hkv] are the keys kept by each
+ * (sequence, KV head).  e_hist is the caller's E history [num_layers, Hkv, T];
+ * layers < layer are read, layer `layer` is written.  Returns 0, or -1 on
+ * invalid arguments. */
 int bacon_ref_layer(const bacon_ref_cfg *cfg, int layer, int batch,
                     const int32_t *cu_seqlens, const int32_t *budgets,
                     const float *q_win, const float *k,
                     double *e_hist, bacon_ref_out *out);
 
 /* Compacted cache of one layer: per sequence b and KV head h, rows
- * [kept positions ascending][window positions][zero rows up to budget+W],
- * written to [sum_b (budget_b + W), Hkv, d] with elements of elem_size bytes. */
+ * [kept positions ascending][window positions][zero rows up to C_b + W],
+ * C_b = max_h budget(b, h), written to [sum_b (C_b + W), Hkv, d] with elements
+ * of elem_size bytes.  budgets [batch, Hkv]. */
 void bacon_ref_compact(int batch, const int32_t *cu_seqlens, const int32_t *budgets,
                        int num_kv_heads, int head_dim, int window, size_t elem_size,
                        const int32_t *idx, const int32_t *n_kept,

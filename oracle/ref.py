@@ -206,12 +206,18 @@ class Prompt:
         return cls(wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window,
                    wl.pool_kernel, wl.cu_seqlens, wl.budgets_arr, params)
 
-    def layer(self, layer: int, q_win: np.ndarray, k: np.ndarray, budgets=None) -> dict:
-        """One layer; ``budgets`` overrides the prompt's per-sequence budgets for
-        this layer only (a per-layer budget schedule)."""
+    def layer(self, layer: int, q_win: np.ndarray, k: np.ndarray, budgets=None,
+              head_budgets=None) -> dict:
+        """One layer.  ``budgets`` overrides the prompt's per-sequence budgets
+        for this layer only (a per-layer budget schedule); ``head_budgets``
+        [batch, Hkv] gives every (sequence, KV head) its own budget."""
         B_, Hq, Hkv, W, T = self.batch, self.Hq, self.Hkv, self.W, self.T
         bud = self.budgets if budgets is None else np.ascontiguousarray(budgets, dtype=np.int32)
         assert bud.shape == self.budgets.shape
+        if head_budgets is None:
+            bh = np.ascontiguousarray(np.repeat(bud[:, None], Hkv, axis=1), dtype=np.int32)
+        else:
+            bh = np.ascontiguousarray(head_budgets, dtype=np.int32).reshape(B_, Hkv)
         q_win = np.ascontiguousarray(q_win, dtype=np.float32)
         k = np.ascontiguousarray(k, dtype=np.float32)
         assert q_win.shape == (B_ * W, Hq, self.d) and k.shape == (T, Hkv, self.d)
@@ -220,33 +226,36 @@ class Prompt:
         r = {"lse": np.zeros((B_, Hq, W)), "B": vec(), "Q": vec(), "E": vec(), "L": vec(),
              "T": vec(), "V": vec(), "S": vec(), "S_pool": vec(), "lambda": sc(),
              "sigma_B": sc(), "sigma_V": sc(), "m_count": np.zeros((B_, Hkv), np.int32),
-             "idx": np.zeros(int(bud.sum()) * Hkv, np.int32),
-             "n_kept": np.zeros((B_, Hkv), np.int32), "budgets": bud}
+             "idx": np.zeros(int(bh.sum()), np.int32),
+             "n_kept": np.zeros((B_, Hkv), np.int32), "budgets": bh}
         out = _Out(_d(r["lse"]), _d(r["B"]), _d(r["Q"]), _d(r["E"]), _d(r["L"]), _d(r["T"]),
                    _d(r["V"]), _d(r["S"]), _d(r["S_pool"]), _d(r["lambda"]), _d(r["sigma_B"]),
                    _d(r["sigma_V"]), _i(r["m_count"]), _i(r["idx"]), _i(r["n_kept"]))
-        rc = lib().bacon_ref_layer(C.byref(self.cfg), layer, B_, _i(self.cu), _i(bud),
+        rc = lib().bacon_ref_layer(C.byref(self.cfg), layer, B_, _i(self.cu), _i(bh),
                                    _f(q_win), _f(k), _d(self.e_hist), C.byref(out))
         if rc != 0:
             raise ValueError("oracle rejected the layer arguments")
         return r
 
+    def _bh(self, r: dict) -> np.ndarray:
+        return r.get("budgets", np.repeat(self.budgets[:, None], self.Hkv, axis=1))
+
     def idx_of(self, r: dict, b: int, h: int) -> np.ndarray:
         """Kept positions of (sequence b, KV head h), without -1 padding."""
-        bud = r.get("budgets", self.budgets)
-        off = int(bud[:b].sum()) * self.Hkv + h * int(bud[b])
-        ids = r["idx"][off:off + int(bud[b])]
+        bh = self._bh(r)
+        off = int(bh.reshape(-1)[:b * self.Hkv + h].sum())
+        ids = r["idx"][off:off + int(bh[b, h])]
         return ids[ids >= 0]
 
     def compact(self, r: dict, k_bytes: np.ndarray, v_bytes: np.ndarray, elem_size: int):
-        bud = r.get("budgets", self.budgets)
-        rows = int((bud + self.W).sum())
+        bh = np.ascontiguousarray(self._bh(r), dtype=np.int32)
+        rows = int((bh.max(axis=1) + self.W).sum())
         shape = (rows, self.Hkv, self.d * elem_size)
         k_out = np.zeros(shape, np.uint8)
         v_out = np.zeros(shape, np.uint8)
         kb = np.ascontiguousarray(k_bytes).view(np.uint8)
         vb = np.ascontiguousarray(v_bytes).view(np.uint8)
-        lib().bacon_ref_compact(self.batch, _i(self.cu), _i(bud), self.Hkv, self.d,
+        lib().bacon_ref_compact(self.batch, _i(self.cu), _i(bh), self.Hkv, self.d,
                                 self.W, elem_size, _i(r["idx"]), _i(r["n_kept"]),
                                 kb.ctypes.data, vb.ctypes.data, k_out.ctypes.data,
                                 v_out.ctypes.data)

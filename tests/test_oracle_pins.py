@@ -486,3 +486,40 @@ def test_per_layer_budgets_leave_history_unchanged(oracle):
             g = q.layer(j, xj["q_win"], xj["k"])
         assert np.array_equal(g["idx"], r["idx"])
         assert np.array_equal(g["S_pool"], r["S_pool"])
+
+
+# --------------------------------------------------------------- per-head budgets
+
+def test_head_budgets_match_uniform_runs(oracle):
+    """A (sequence, KV head) with its own budget K_bh selects exactly what a run
+    with budget K_bh everywhere selects for it (lambda's set size rho*K_bh
+    included), and the compacted rows of a sequence pad every head to its
+    largest budget."""
+    wl = _wl_small(num_layers=3)
+    rng = np.random.default_rng(5)
+    hb = rng.integers(1, 60, size=(wl.batch, wl.num_kv_heads)).astype(np.int32)
+    p = oracle.Prompt.for_workload(wl)
+    outs, ins = [], []
+    for l in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, l)
+        ins.append(x)
+        outs.append(p.layer(l, x["q_win"], x["k"], head_budgets=hb))
+    for K in sorted(set(hb.reshape(-1).tolist())):
+        u = oracle.Prompt.for_workload(wl.with_(budgets=(int(K),) * wl.batch))
+        for l in range(wl.num_layers):
+            r = u.layer(l, ins[l]["q_win"], ins[l]["k"])
+            for b in range(wl.batch):
+                for h in range(wl.num_kv_heads):
+                    if hb[b, h] != K:
+                        continue
+                    assert outs[l]["lambda"][b, h] == r["lambda"][b, h]
+                    assert np.array_equal(p.idx_of(outs[l], b, h), u.idx_of(r, b, h))
+    ko, vo = p.compact(outs[-1], ins[-1]["k"], ins[-1]["v"], 4)
+    C = hb.max(axis=1)
+    assert ko.shape[0] == int((C + wl.window).sum())
+    r0 = 0
+    for b in range(wl.batch):
+        for h in range(wl.num_kv_heads):
+            kept = int(outs[-1]["n_kept"][b, h])
+            assert not ko[r0 + kept + wl.window:r0 + C[b] + wl.window, h].any()
+        r0 += C[b] + wl.window
