@@ -36,13 +36,14 @@
  *   score vectors  [Hkv, T] float32 (B, Q, E, V, S)
  *   lse     [B, Hq, W] float32, natural-log normaliser of each window row
  *   lambda  [B, Hkv] float32
- *   idx     int32; sequence b owns Hkv*budget_b entries starting at
- *           Hkv * sum_{b'<b} budget_b', head-major ([h][j]); entries are
+ *   idx     int32; (b, h) owns K_{b,h} entries after those of every earlier
+ *           pair in (b, h) order (with one budget per sequence: Hkv*budget_b
+ *           entries from Hkv * sum_{b'<b} budget_b', head-major); entries are
  *           positions relative to the sequence start, ascending, and -1 where
- *           the candidate set holds fewer than budget_b positions.
- *   k_out, v_out [sum_b (budget_b + W), Hkv, d]; for each (b, h) the rows are
- *           the kept rows in ascending position, then the W window rows, then
- *           zero rows up to budget_b + W.
+ *           the candidate set holds fewer than K_{b,h} positions.
+ *   k_out, v_out [sum_b (C_b + W), Hkv, d], C_b = max_h K_{b,h}; for each
+ *           (b, h) the rows are the kept rows in ascending position, then the
+ *           W window rows, then zero rows up to C_b + W.
  *
  * Element type: BACON_FP32 (float) or BACON_BF16 (bfloat16) for q, k, v and
  * the compacted cache; all scores are float32.  head_dim is 64 or 128.
@@ -123,12 +124,18 @@ typedef struct {
   bacon_dtype dtype;
 } bacon_shape;
 
-/* A packed batch.  Both arrays live in HOST memory and are copied by the call.
- * cu_seqlens[0] = 0 and W <= N_b = cu_seqlens[b+1]-cu_seqlens[b] <= 32768. */
+/* A packed batch.  The arrays live in HOST memory and are copied by the call.
+ * cu_seqlens[0] = 0 and W <= N_b = cu_seqlens[b+1]-cu_seqlens[b] <= 32768.
+ * Budgets: `head_budgets` [batch][num_kv_heads], when not NULL, gives every
+ * (sequence, KV head) its own budget K_{b,h} >= 1 (a head-wise allocation of
+ * the backbone method, Sec. 4 Preliminaries, kept as it is); otherwise every
+ * KV head of sequence b keeps budgets[b] >= 1 (budgets may be NULL when
+ * head_budgets is given). */
 typedef struct {
   int32_t batch;
-  const int32_t *cu_seqlens;  /* [batch + 1] */
-  const int32_t *budgets;     /* [batch], keys kept per KV head, >= 1 */
+  const int32_t *cu_seqlens;    /* [batch + 1] */
+  const int32_t *budgets;       /* [batch], keys kept per KV head, >= 1 */
+  const int32_t *head_budgets;  /* optional [batch * num_kv_heads], >= 1 */
 } bacon_batch;
 
 typedef struct bacon_ctx bacon_ctx;
@@ -205,7 +212,7 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *ctx, int32_t layer, const bacon
 
 /* Sizes of the outputs for a batch: idx entries and compacted rows. */
 int64_t bacon_idx_count(const bacon_batch *batch, int32_t num_kv_heads);
-int64_t bacon_kept_rows(const bacon_batch *batch, int32_t window);
+int64_t bacon_kept_rows(const bacon_batch *batch, int32_t num_kv_heads, int32_t window);
 
 /* Per-kernel timing with hipEvents around every launch of the context.
  * bacon_profile_read waits for the recorded events, fills up to `max`

@@ -45,7 +45,7 @@ class Shape(C.Structure):
 
 class Batch(C.Structure):
     _fields_ = [("batch", C.c_int32), ("cu_seqlens", C.POINTER(C.c_int32)),
-                ("budgets", C.POINTER(C.c_int32))]
+                ("budgets", C.POINTER(C.c_int32)), ("head_budgets", C.POINTER(C.c_int32))]
 
 
 class KernelTime(C.Structure):
@@ -86,7 +86,7 @@ def lib() -> C.CDLL:
                                                vp, vp, vp, vp]
         L.bacon_idx_count.argtypes = [C.POINTER(Batch), C.c_int32]
         L.bacon_idx_count.restype = C.c_int64
-        L.bacon_kept_rows.argtypes = [C.POINTER(Batch), C.c_int32]
+        L.bacon_kept_rows.argtypes = [C.POINTER(Batch), C.c_int32, C.c_int32]
         L.bacon_kept_rows.restype = C.c_int64
         L.bacon_profile_enable.argtypes = [vp, C.c_int32]
         L.bacon_profile_read.argtypes = [vp, C.POINTER(KernelTime), C.c_int32]
@@ -116,13 +116,18 @@ def default_params(**overrides) -> Params:
 
 
 class BatchLayout:
-    """Host copy of a packed batch (cu_seqlens, per-sequence budgets)."""
+    """Host copy of a packed batch: cu_seqlens, per-sequence budgets, and
+    optionally a budget per (sequence, KV head) [batch, Hkv]."""
 
-    def __init__(self, cu_seqlens, budgets):
+    def __init__(self, cu_seqlens, budgets, head_budgets=None):
         self.cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
         self.budgets = np.ascontiguousarray(budgets, dtype=np.int32)
+        self.head_budgets = (None if head_budgets is None else
+                             np.ascontiguousarray(head_budgets, dtype=np.int32).reshape(len(self.budgets), -1))
+        hb = (None if self.head_budgets is None else
+              self.head_budgets.ctypes.data_as(C.POINTER(C.c_int32)))
         self.c = Batch(len(self.budgets), self.cu.ctypes.data_as(C.POINTER(C.c_int32)),
-                       self.budgets.ctypes.data_as(C.POINTER(C.c_int32)))
+                       self.budgets.ctypes.data_as(C.POINTER(C.c_int32)), hb)
 
     @property
     def total(self) -> int:
@@ -131,8 +136,8 @@ class BatchLayout:
     def idx_count(self, num_kv_heads: int) -> int:
         return int(lib().bacon_idx_count(C.byref(self.c), num_kv_heads))
 
-    def kept_rows(self, window: int) -> int:
-        return int(lib().bacon_kept_rows(C.byref(self.c), window))
+    def kept_rows(self, window: int, num_kv_heads: int = 1) -> int:
+        return int(lib().bacon_kept_rows(C.byref(self.c), num_kv_heads, window))
 
 
 def _ptr(t):
@@ -206,7 +211,7 @@ class Context:
 
     def _kv_out(self, batch: BatchLayout, like):
         import torch
-        rows = batch.kept_rows(self.shape.window)
+        rows = batch.kept_rows(self.shape.window, self.shape.num_kv_heads)
         shp = (rows, self.shape.num_kv_heads, self.shape.head_dim)
         return (torch.empty(shp, dtype=like.dtype, device=like.device),
                 torch.empty(shp, dtype=like.dtype, device=like.device))

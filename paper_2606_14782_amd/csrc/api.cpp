@@ -37,7 +37,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t ring, vec_b, vec_vp, vec_v, vec_pb, vec_pv, vec_s, hist_b, hist_s, list_bk, list_bp, list_bv,
-      list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, total;
+      list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, hb, total;
   int rpad, slots;
   int64_t chunks_cap;
 };
@@ -119,6 +119,7 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.partials = off; off += align256((size_t)s->num_kv_heads * L.chunks_cap * L.rpad * sizeof(float2));
   L.lse2 = off;     off += align256((size_t)s->max_batch * s->num_kv_heads * L.rpad * sizeof(float));
   L.lambda = off;   off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(float));
+  L.hb = off;       off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(int2));
   L.total = off;
   return L;
 }
@@ -141,7 +142,7 @@ struct bacon_ctx {
   Layout L;
   bool prompt = false;
   int next_layer = 0;
-  std::vector<int32_t> cu, budgets;
+  std::vector<int32_t> cu;
   int chunk_stages_override = 0;
   bool kr_off = false;   // key-register passes switched off (streaming passes only)
   // profiling
@@ -178,7 +179,8 @@ bacon_status check_batch(const bacon_ctx *c, const bacon_batch *bt) {
   if (!bt) return fail(BACON_ERR_INVALID, "batch is NULL");
   if (bt->batch < 1 || bt->batch > c->shape.max_batch)
     return fail(BACON_ERR_INVALID, "batch size %d outside [1, %d]", bt->batch, c->shape.max_batch);
-  if (!bt->cu_seqlens || !bt->budgets) return fail(BACON_ERR_INVALID, "batch arrays are NULL");
+  if (!bt->cu_seqlens || (!bt->budgets && !bt->head_budgets))
+    return fail(BACON_ERR_INVALID, "batch arrays are NULL");
   if (bt->cu_seqlens[0] != 0) return fail(BACON_ERR_INVALID, "cu_seqlens[0] must be 0");
   for (int b = 0; b < bt->batch; ++b) {
     const int64_t n = (int64_t)bt->cu_seqlens[b + 1] - bt->cu_seqlens[b];
@@ -188,7 +190,13 @@ bacon_status check_batch(const bacon_ctx *c, const bacon_batch *bt) {
     if (n > kMaxSeqLen)
       return fail(BACON_ERR_UNSUPPORTED, "sequence %d has %lld tokens (max %d)", b, (long long)n,
                   kMaxSeqLen);
-    if (bt->budgets[b] < 1) return fail(BACON_ERR_INVALID, "budget of sequence %d must be >= 1", b);
+    if (bt->head_budgets) {
+      for (int h = 0; h < c->shape.num_kv_heads; ++h)
+        if (bt->head_budgets[(int64_t)b * c->shape.num_kv_heads + h] < 1)
+          return fail(BACON_ERR_INVALID, "budget of sequence %d, KV head %d must be >= 1", b, h);
+    } else if (bt->budgets[b] < 1) {
+      return fail(BACON_ERR_INVALID, "budget of sequence %d must be >= 1", b);
+    }
   }
   if (bt->cu_seqlens[bt->batch] > c->shape.max_total_tokens)
     return fail(BACON_ERR_INVALID, "total tokens %d exceed max_total_tokens %lld",
@@ -218,6 +226,18 @@ bacon_status check_ptr(const void *p, const char *name, size_t align) {
     bacon_status _s = (x);         \
     if (_s != BACON_OK) return _s; \
   } while (0)
+
+// Budget of (sequence b, KV head h), and the largest budget of sequence b's
+// heads (its rows per head in the compacted cache, less W).
+int batch_head_budget(const bacon_batch *bt, int hkv, int b, int h) {
+  return bt->head_budgets ? bt->head_budgets[(int64_t)b * hkv + h] : bt->budgets[b];
+}
+int batch_seq_rows(const bacon_batch *bt, int hkv, int b) {
+  if (!bt->head_budgets) return bt->budgets[b];
+  int m = 0;
+  for (int h = 0; h < hkv; ++h) m = std::max(m, batch_head_budget(bt, hkv, b, h));
+  return m;
+}
 
 // edge_tables: the split calibrate path completes L next to chunk boundaries
 // from an LDS table of kEdgeEntries positions, which bounds the chunk count.
@@ -255,13 +275,13 @@ SeqTable make_table(const bacon_ctx *c, const bacon_batch *bt, int *chunk_out,
     const int nseg = (n + kSegLen - 1) / kSegLen;
     st.cu[b] = bt->cu_seqlens[b];
     st.chunk_base[b] = cb;
-    st.budget[b] = bt->budgets[b];
+    st.budget[b] = batch_seq_rows(bt, c->shape.num_kv_heads, b);
     st.idx_base[b] = ib;
     st.kept_base[b] = kb;
     st.seg_base[b] = sb;
     cb += (n + chunk - 1) / chunk;
-    ib += bt->budgets[b];
-    kb += bt->budgets[b] + c->shape.window;
+    for (int h = 0; h < c->shape.num_kv_heads; ++h) ib += batch_head_budget(bt, c->shape.num_kv_heads, b, h);
+    kb += st.budget[b] + c->shape.window;
     sb += nseg;
   }
   st.cu[bt->batch] = bt->cu_seqlens[bt->batch];
@@ -297,6 +317,33 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   a.terms = c->params.terms;
   (void)st;
   return a;
+}
+
+// Per-head budgets of the batch into the workspace table (budget, idx offset
+// within the sequence), or NULL with one budget per sequence.  The table rides
+// in the arguments of small kernels on the stream, ahead of the select.
+bacon_status head_table(bacon_ctx *c, const bacon_batch *bt, hipStream_t s, const int2 **out) {
+  *out = nullptr;
+  if (!bt->head_budgets) return BACON_OK;
+  const int hkv = c->shape.num_kv_heads;
+  int2 *dst = reinterpret_cast<int2 *>(c->ws + c->L.hb);
+  HbChunk ch{};
+  const int n = bt->batch * hkv;
+  int off = 0;
+  for (int p = 0; p < n; ++p) {
+    if (p % hkv == 0) off = 0;
+    const int k = bt->head_budgets[p];
+    ch.v[ch.n++] = make_int2(k, off);
+    off += k;
+    if (ch.n == kHbChunk || p == n - 1) {
+      const hipError_t e = launch_set_hb(ch, dst, s);
+      if (e != hipSuccess) return hip_fail(e, "budget table");
+      ch.base += ch.n;
+      ch.n = 0;
+    }
+  }
+  *out = dst;
+  return BACON_OK;
 }
 
 // History slots for layer `layer`: E of layer j lives in slot j % (m + 1), so
@@ -415,7 +462,7 @@ bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *strea
   if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
   TRY(check_batch(c, bt));
   c->cu.assign(bt->cu_seqlens, bt->cu_seqlens + bt->batch + 1);
-  c->budgets.assign(bt->budgets, bt->budgets + bt->batch);
+
   // layer 0 reads no history; the B histogram of the select starts at zero
   // (each layer's final kernel clears it for the next)
   const hipError_t e = launch_zero(reinterpret_cast<unsigned *>(c->ws + c->L.hist_b),
@@ -501,6 +548,7 @@ bacon_status bacon_calibrate(bacon_ctx *c, int32_t layer, const bacon_batch *bt,
   a.out_V = d_V;
   a.out_E = d_E;
   a.out_lambda = d_lambda;
+  TRY(head_table(c, bt, s, &a.hb));
   TRY(timed(c, KI_SEL_CALIB, s, [&] { return launch_select(SEL_CALIB, max_len(bt), a, st, s); }));
   c->next_layer = layer + 1;
   return BACON_OK;
@@ -520,6 +568,7 @@ bacon_status bacon_select_topk(bacon_ctx *c, const bacon_batch *bt, const float 
   a.T = bt->cu_seqlens[bt->batch];
   a.in_S = d_S;
   a.idx = d_idx;
+  TRY(head_table(c, bt, s, &a.hb));
   return timed(c, KI_SEL_TOPK, s, [&] { return launch_select(SEL_TOPK, max_len(bt), a, st, s); });
 }
 
@@ -544,6 +593,7 @@ bacon_status bacon_compact(bacon_ctx *c, const bacon_batch *bt, const void *d_k,
   a.Hkv = c->shape.num_kv_heads;
   a.W = c->shape.window;
   a.row_bytes = c->shape.head_dim * (c->shape.dtype == BACON_BF16 ? 2 : 4);
+  TRY(head_table(c, bt, s, &a.hb));
   return timed(c, KI_COMPACT, s, [&] { return launch_compact(a, st, s); });
 }
 
@@ -582,7 +632,7 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
     TRY(check_lds(c, bt, chunk, true, -1));
   }
   int kmax = 0;
-  for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, bt->budgets[b]);
+  for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, batch_seq_rows(bt, c->shape.num_kv_heads, b));
   if (final_lds_bytes(kmax, c->shape.window) > (size_t)kLdsBytes)
     return fail(BACON_ERR_UNSUPPORTED, "budget %d needs more LDS than a CU has", kmax);
   const int64_t T = bt->cu_seqlens[bt->batch];
@@ -636,6 +686,7 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   g.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
   // final workgroups per (sequence, KV head): about one round over the CUs
   g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
+  TRY(head_table(c, bt, s, &g.hb));
   if (kr) {
     if (!d_lse) {
       TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
@@ -677,16 +728,17 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *c, int32_t layer, const bacon_b
 }
 
 int64_t bacon_idx_count(const bacon_batch *bt, int32_t num_kv_heads) {
-  if (!bt || !bt->budgets || bt->batch < 1) return 0;
+  if (!bt || (!bt->budgets && !bt->head_budgets) || bt->batch < 1 || num_kv_heads < 1) return 0;
   int64_t n = 0;
-  for (int b = 0; b < bt->batch; ++b) n += bt->budgets[b];
-  return n * num_kv_heads;
+  for (int b = 0; b < bt->batch; ++b)
+    for (int h = 0; h < num_kv_heads; ++h) n += batch_head_budget(bt, num_kv_heads, b, h);
+  return n;
 }
 
-int64_t bacon_kept_rows(const bacon_batch *bt, int32_t window) {
-  if (!bt || !bt->budgets || bt->batch < 1) return 0;
+int64_t bacon_kept_rows(const bacon_batch *bt, int32_t num_kv_heads, int32_t window) {
+  if (!bt || (!bt->budgets && !bt->head_budgets) || bt->batch < 1 || num_kv_heads < 1) return 0;
   int64_t n = 0;
-  for (int b = 0; b < bt->batch; ++b) n += bt->budgets[b] + window;
+  for (int b = 0; b < bt->batch; ++b) n += batch_seq_rows(bt, num_kv_heads, b) + window;
   return n;
 }
 

@@ -31,8 +31,9 @@ struct SeqTable {
   int32_t seg_base[kMaxBatch + 1];      // first select segment of each sequence
   int32_t cu[kMaxBatch + 1];            // token offsets
   int32_t chunk_base[kMaxBatch + 1];    // first chunk of each sequence
-  int32_t budget[kMaxBatch];            // kept keys per KV head
-  int32_t idx_base[kMaxBatch];          // sum of budgets before b
+  int32_t budget[kMaxBatch];            // kept keys per KV head (the largest head budget
+                                        // when the heads have their own)
+  int32_t idx_base[kMaxBatch];          // idx entries before sequence b (all its heads)
   int32_t kept_base[kMaxBatch];         // sum of (budget + W) before b
 };
 
@@ -84,6 +85,7 @@ struct SelArgs {
   float *out_lambda;       // optional [B, Hkv]
   float *lambda_ws;        // [B, Hkv]
   int32_t *idx;            // SEL_TOPK output
+  const int2 *hb;          // optional [B, Hkv] (budget, idx offset in the sequence)
 };
 
 // Histogram select of the fused pass (calibration, score and final kernels).
@@ -119,6 +121,7 @@ struct SegArgs {
   void *k_out, *v_out;
   int row_bytes;
   int parts;                     // final-kernel workgroups per (sequence, KV head)
+  const int2 *hb;                // optional [B, Hkv] (budget, idx offset in the sequence)
 };
 
 struct ElemArgs {           // split calibrate: E, T, L, ring update
@@ -137,7 +140,25 @@ struct CompactArgs {
   const void *k, *v;
   void *k_out, *v_out;
   int Hkv, W, row_bytes;
+  const int2 *hb;          // optional [B, Hkv] (budget, idx offset in the sequence)
 };
+
+// Budget and idx offset (within its sequence) of (sequence b, KV head h);
+// with one budget per sequence, hb is NULL.
+__host__ __device__ inline int head_budget(const SeqTable &st, const int2 *hb, int Hkv, int b, int h) {
+  return hb ? hb[b * Hkv + h].x : st.budget[b];
+}
+__host__ __device__ inline int64_t head_idx_base(const SeqTable &st, const int2 *hb, int Hkv, int b, int h) {
+  return (int64_t)st.idx_base[b] + (hb ? hb[b * Hkv + h].y : h * st.budget[b]);
+}
+
+// Writes n entries of a (budget, offset) table to dst[base ..] (device).
+constexpr int kHbChunk = 256;
+struct HbChunk {
+  int n, base;
+  int2 v[kHbChunk];
+};
+hipError_t launch_set_hb(const HbChunk &c, int2 *dst, hipStream_t s);
 
 // Keys per pipeline stage of the passes for a given number of row tiles.
 __host__ __device__ inline int stage_keys(int nw) { return 32 * (nw < 4 ? nw : 4); }

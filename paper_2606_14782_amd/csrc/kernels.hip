@@ -1365,7 +1365,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;                           // candidate set [0, nc)
-  const int K = st.budget[b];
+  const int K = head_budget(st, a.hb, a.Hkv, b, h);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
   // LDS: arr [pad32 extent of kMaxSeqLen], candidate list, then per-mode tables
   unsigned *ckey = reinterpret_cast<unsigned *>(arr + kArrWords);
@@ -1589,7 +1589,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     for (int j = 0; j < PER; ++j)
       msk |= (uint64_t)(key[j] > xk || (key[j] == xk && i0 + j <= pk) ? 1u : 0u) << j;
   }
-  int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
+  int32_t *idx = a.idx + head_idx_base(st, a.hb, a.Hkv, b, h);
   int *tbl = reinterpret_cast<int *>(arr);
   unsigned slot = block_excl_scan_u((unsigned)__popcll(msk), ss);
   {
@@ -1786,7 +1786,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   const int64_t base = (int64_t)h * a.T + st.cu[b];
   const int r = a.radius;
   const bool use_l = (a.terms & 2u) != 0;
-  int M = (int)floorf(a.rho * (float)st.budget[b]);
+  int M = (int)floorf(a.rho * (float)head_budget(st, a.hb, a.Hkv, b, h));
   M = max(0, min(M, nc));
   const bool calib = M > 0 && a.use_last_query;
   // the bins of the B histogram (accumulated by the fused pass, in kHCopies
@@ -2086,7 +2086,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
     }
   }
 
-  int M = (int)floorf(a.rho * (float)st.budget[b]);
+  int M = (int)floorf(a.rho * (float)head_budget(st, a.hb, a.Hkv, b, h));
   M = max(0, min(M, nc));
   float lam = 0.f;
   if (M > 0 && a.use_last_query) {
@@ -2202,7 +2202,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segcand(SegArgs a, SeqTable st)
   const int i0 = sg * kSegLen;
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  const int kept = min(st.budget[b], nc);
+  const int kept = min(head_budget(st, a.hb, a.Hkv, b, h), nc);
   if (kept <= 0 || kept == nc) return;               // none or all kept: no list needed
   unsigned cb[kHPer];
   load_bins<1>(a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, cb);
@@ -2290,10 +2290,11 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
   const int wave = t >> 6;
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
-  const int K = st.budget[b];
+  const int K = head_budget(st, a.hb, a.Hkv, b, h);  // this head's budget
+  const int C = st.budget[b];                         // rows per head of the sequence, less W
   const int kept = min(K, nc);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
+  int32_t *idx = a.idx + head_idx_base(st, a.hb, a.Hkv, b, h);
   if (kept > 0 && kept == nc) {
     // every candidate is kept
     for (int j = t; j < nc; j += NT) {
@@ -2340,7 +2341,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
   if (part == 0)
     for (int j = max(kept, 0) + t; j < K; j += NT) idx[j] = -1;
   for (int w = t; w < a.W; w += NT) tbl[kept + w] = nc + w;
-  for (int j = kept + a.W + t; j < K + a.W; j += NT) tbl[j] = -1;
+  for (int j = kept + a.W + t; j < C + a.W; j += NT) tbl[j] = -1;
   __syncthreads();
 
   {
@@ -2354,7 +2355,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
   }
 
   // this part's rows of the compacted cache
-  const int rows = K + a.W;
+  const int rows = C + a.W;
   const int per = (rows + a.parts - 1) / a.parts;
   const int r0 = part * per, r1 = min(rows, r0 + per);
   const int pieces = a.row_bytes / 16;
@@ -2490,11 +2491,11 @@ __global__ __launch_bounds__(256) void k_compact(CompactArgs a, SeqTable st) {
   const int b = blockIdx.x, h = blockIdx.y;
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
-  const int K = st.budget[b];
+  const int K = head_budget(st, a.hb, a.Hkv, b, h);
   const int kept = min(K, nc);
-  const int32_t *idx = a.idx + (int64_t)st.idx_base[b] * a.Hkv + (int64_t)h * K;
+  const int32_t *idx = a.idx + head_idx_base(st, a.hb, a.Hkv, b, h);
   const int pieces = a.row_bytes / 16;
-  const int total = (K + a.W) * pieces;
+  const int total = (st.budget[b] + a.W) * pieces;   // rows per head of the sequence
   const int q0 = blockIdx.z * (256 * kCompactPer) + threadIdx.x;
   if (q0 >= total) return;
   const unsigned char *ks = static_cast<const unsigned char *>(a.k);
@@ -2529,6 +2530,15 @@ __global__ __launch_bounds__(256) void k_compact(CompactArgs a, SeqTable st) {
       *reinterpret_cast<u32x4 *>(vo + dst) = src[u] >= 0 ? vv[u] : z;
     }
   }
+}
+
+__global__ __launch_bounds__(kHbChunk) void k_set_hb(HbChunk c, int2 *dst) {
+  if ((int)threadIdx.x < c.n) dst[c.base + threadIdx.x] = c.v[threadIdx.x];
+}
+
+hipError_t launch_set_hb(const HbChunk &c, int2 *dst, hipStream_t s) {
+  hipLaunchKernelGGL(k_set_hb, dim3(1), dim3(kHbChunk), 0, s, c, dst);
+  return hipGetLastError();
 }
 
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s) {

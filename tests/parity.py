@@ -69,19 +69,28 @@ def seq_slices(wl):
     return [(int(cu[b]), int(cu[b + 1])) for b in range(wl.batch)]
 
 
-def check_idx(name, got, r, wl, rtol):
+def _head_budgets(wl, hb):
+    """[batch, Hkv] budgets: hb, or every head at its sequence's budget."""
+    if hb is not None:
+        return np.asarray(hb, np.int64).reshape(wl.batch, wl.num_kv_heads)
+    return np.repeat(np.asarray(wl.budgets, np.int64)[:, None], wl.num_kv_heads, axis=1)
+
+
+def check_idx(name, got, r, wl, rtol, hb=None):
     """Kept sets equal the oracle's except for positions whose pooled oracle
-    score is within rtol of the K-th kept score; also counts strict matches."""
+    score is within rtol of the K-th kept score; also counts strict matches.
+    hb: optional per-(sequence, KV head) budgets [batch, Hkv]."""
     W, Hkv = wl.window, wl.num_kv_heads
+    bh = _head_budgets(wl, hb)
     stats = {"pairs": 0, "strict": 0, "swaps": 0}
-    base = 0
+    off = 0
     for b, (s0, s1) in enumerate(seq_slices(wl)):
-        K = wl.budgets[b]
         nc = (s1 - s0) - W
         for h in range(Hkv):
-            off = base * Hkv + h * K
+            K = int(bh[b, h])
             g = np.asarray(got[off:off + K])
             o = np.asarray(r["idx"][off:off + K])
+            off += K
             kept = min(K, max(nc, 0))
             assert np.all(g[kept:] == -1), f"{name} b{b} h{h}: padding"
             gk = g[:kept]
@@ -99,27 +108,29 @@ def check_idx(name, got, r, wl, rtol):
                     f"{name} b{b} h{h}: position {i} differs, oracle score {P[i]:.9g} vs "
                     f"K-th {pK:.9g}")
             stats["swaps"] += len(gs - os_)
-        base += K
     return stats
 
 
-def gather_rows(x_bytes, idx, wl):
-    """Expected compacted rows for GPU indices (bit copy of the input rows)."""
+def gather_rows(x_bytes, idx, wl, hb=None):
+    """Expected compacted rows for GPU indices (bit copy of the input rows);
+    each sequence has max_h K + W rows per head, zero-padded."""
     W, Hkv = wl.window, wl.num_kv_heads
-    rows = int(np.sum(np.asarray(wl.budgets) + W))
+    bh = _head_budgets(wl, hb)
+    C = bh.max(axis=1)
+    rows = int(np.sum(C + W))
     row_b = x_bytes.shape[-1]
     out = np.zeros((rows, Hkv, row_b), np.uint8)
-    base, r0 = 0, 0
+    off, r0 = 0, 0
     for b, (s0, s1) in enumerate(seq_slices(wl)):
-        K = wl.budgets[b]
         n = s1 - s0
         for h in range(Hkv):
-            g = idx[(base * Hkv + h * K):(base * Hkv + h * K + K)]
+            K = int(bh[b, h])
+            g = idx[off:off + K]
+            off += K
             kept = g[g >= 0]
             src = np.concatenate([kept, np.arange(n - W, n)]).astype(np.int64)
             out[r0:r0 + len(src), h] = x_bytes[s0 + src, h]
-        base += K
-        r0 += K + W
+        r0 += int(C[b]) + W
     return out
 
 

@@ -4,6 +4,7 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
 
 from paper_2606_14782_amd import bacon
@@ -163,3 +164,13 @@ def test_status_strings():
     L = bacon.lib()
     for s in range(6):
         assert L.bacon_status_string(s)
+
+
+def test_counts_with_head_budgets():
+    """idx entries and compacted rows with a budget per (sequence, KV head)."""
+    hb = np.array([[3, 7], [5, 1]], np.int32)
+    b = bacon.BatchLayout([0, 100, 300], [4, 4], head_budgets=hb)
+    assert b.idx_count(2) == 3 + 7 + 5 + 1
+    assert b.kept_rows(8, 2) == (7 + 8) + (5 + 8)
+    u = bacon.BatchLayout([0, 100, 300], [4, 6])
+    assert u.idx_count(2) == 2 * (4 + 6) and u.kept_rows(8, 2) == (4 + 8) + (6 + 8)

@@ -173,6 +173,41 @@ def test_per_layer_budget_schedule(name):
         assert np.array_equal(P.tensor_bytes(vo), P.gather_rows(P.as_bytes(x["v"], wl), gi, wll))
 
 
+@pytest.mark.parametrize("name", ["ragged-small", "video-small", "llava-small"])
+def test_head_budgets(name):
+    """A budget per (sequence, KV head), as a head-wise allocation gives it:
+    the fused call and the split calls match the oracle, and the compacted
+    cache pads every head to its sequence's largest budget."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = CASES[name]()
+    rng = np.random.default_rng(11)
+    hb = rng.integers(1, 2 * max(wl.budgets) + 1, size=(wl.batch, wl.num_kv_heads)).astype(np.int32)
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr, head_budgets=hb)
+    orc = ref.Prompt.for_workload(wl, P.oracle_params())
+    ctx_f, ctx_s = P.make_ctx(wl), P.make_ctx(wl)
+    ctx_f.bacon_begin_prompt(batch)
+    ctx_s.bacon_begin_prompt(batch)
+    rtol = P.RTOL[wl.dtype]
+    for layer in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, layer)
+        r = orc.layer(layer, x["q_win"], x["k"], head_budgets=hb)
+        q, k, v = P.to_dev(x["q_win"], wl), P.to_dev(x["k"], wl), P.to_dev(x["v"], wl)
+        kb, vb = P.as_bytes(x["k"], wl), P.as_bytes(x["v"], wl)
+        idx, ko, vo = ctx_f.bacon_compress_layer(layer, batch, q, k, v)
+        B, Q, _ = ctx_s.bacon_score(layer, batch, q, k)
+        cal = ctx_s.bacon_calibrate(layer, batch, B, Q)
+        idx_s = ctx_s.bacon_select_topk(batch, cal["S"])
+        ko_s, vo_s = ctx_s.bacon_compact(batch, k, v, idx_s)
+        torch.cuda.synchronize()
+        P.close(f"{name}/heads L{layer} lambda", cal["lambda"].cpu().numpy(), r["lambda"], rtol)
+        for tag, gi, kk, vv in (("fused", idx, ko, vo), ("split", idx_s, ko_s, vo_s)):
+            g = gi.cpu().numpy()
+            P.check_idx(f"{name}/heads L{layer} {tag}", g, r, wl, rtol, hb=hb)
+            assert np.array_equal(P.tensor_bytes(kk), P.gather_rows(kb, g, wl, hb=hb)), tag
+            assert np.array_equal(P.tensor_bytes(vv), P.gather_rows(vb, g, wl, hb=hb)), tag
+
+
 def _batch64():
     rng = np.random.default_rng(64)
     lens = tuple(int(x) for x in rng.integers(40, 401, size=64))
