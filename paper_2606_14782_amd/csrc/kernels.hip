@@ -936,6 +936,17 @@ hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const Pass
 }
 
 // ---------------------------------------------------------------- block helpers
+// Workgroup barrier for LDS traffic: waits for this wave's LDS operations
+// only.  The fence of __syncthreads also waits for every global load and
+// store the wave has in flight, which the select kernels never need: none
+// of them reads global memory another of its threads wrote in the same
+// launch; their threads exchange data through LDS only.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 // Shared scratch of the block-wide primitives for NT threads.
 template <int NT>
 struct SelSharedT {
@@ -1017,16 +1028,16 @@ __device__ __forceinline__ unsigned block_reduce_u(unsigned v, SelSharedT<NT> &s
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   v = OP == 0 ? wave_min_u(v) : OP == 1 ? wave_max_u(v) : wave_sum_u(v);
   if (lane == 0) ss.red_u[wave] = v;
-  __syncthreads();
+  lds_barrier();
   if (wave == 0) {
     const unsigned id = OP == 0 ? 0xffffffffu : 0u;
     unsigned x = (lane < NT / 64) ? ss.red_u[lane] : id;
     x = OP == 0 ? wave_min_u(x) : OP == 1 ? wave_max_u(x) : wave_sum_u(x);
     if (lane == 0) ss.bc_u[0] = x;
   }
-  __syncthreads();
+  lds_barrier();
   const unsigned r = ss.bc_u[0];
-  __syncthreads();
+  lds_barrier();
   return r;
 }
 
@@ -1036,15 +1047,15 @@ __device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, do
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   v0 = wave_sum_d(v0); v1 = wave_sum_d(v1); v2 = wave_sum_d(v2); v3 = wave_sum_d(v3);
   if (lane == 0) { ss.red_d[0][wave] = v0; ss.red_d[1][wave] = v1; ss.red_d[2][wave] = v2; ss.red_d[3][wave] = v3; }
-  __syncthreads();
+  lds_barrier();
   if (t < 4) {
     double s = 0.0;
     for (int w = 0; w < NT / 64; ++w) s += ss.red_d[t][w];
     ss.bc_d[t] = s;
   }
-  __syncthreads();
+  lds_barrier();
   out[0] = ss.bc_d[0]; out[1] = ss.bc_d[1]; out[2] = ss.bc_d[2]; out[3] = ss.bc_d[3];
-  __syncthreads();
+  lds_barrier();
 }
 
 // Exclusive prefix sum over threads in index order.
@@ -1053,10 +1064,10 @@ __device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelSharedT<NT>
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const unsigned x = wave_incl_sum_u(v);
   if (lane == 63) ss.red_u[wave] = x;
-  __syncthreads();
+  lds_barrier();
   unsigned before = 0;
   for (int w = 0; w < wave; ++w) before += ss.red_u[w];
-  __syncthreads();
+  lds_barrier();
   return before + x - v;
 }
 
@@ -1077,7 +1088,7 @@ __device__ __forceinline__ void bins_boundary(const unsigned *cb, int need, SelS
   const unsigned tot = lane63_u(pre);
   unsigned suf = tot - pre + c;        // inclusive suffix sum within the wave
   if (lane == 0) ss.red_u[wave] = tot;
-  __syncthreads();
+  lds_barrier();
   unsigned higher = 0;                 // counted elements in later waves
 #pragma unroll
   for (int w = 0; w < NT / 64; ++w) higher += (w > wave) ? ss.red_u[w] : 0u;
@@ -1096,7 +1107,7 @@ __device__ __forceinline__ void bins_boundary(const unsigned *cb, int need, SelS
     ss.bc_u[2] = bc;
   }
   if (t == 0) ss.bc_u[3] = suf;
-  __syncthreads();
+  lds_barrier();
 }
 
 // The same over ss.hist (kHistBins bins).
@@ -1123,7 +1134,7 @@ __device__ __forceinline__ void compact_ballot(InF in, KeyF key, PosF pos, unsig
 #pragma unroll
   for (int j = 0; j < PER; ++j) wc += (unsigned)__popcll(__ballot(in(j)));
   if (lane == 0) ss.red_u[wave] = wc;
-  __syncthreads();
+  lds_barrier();
   unsigned off = 0;
 #pragma unroll
   for (int w = 0; w < NW; ++w) off += (w < wave) ? ss.red_u[w] : 0u;
@@ -1141,7 +1152,7 @@ __device__ __forceinline__ void compact_ballot(InF in, KeyF key, PosF pos, unsig
     }
     off += (unsigned)__popcll(m);
   }
-  __syncthreads();
+  lds_barrier();
 }
 
 // The need-th entry (1-based) of C <= NT listed entries under the tie rule
@@ -1159,10 +1170,19 @@ __device__ __forceinline__ void rank_pick(int C, int need, const unsigned *ckey,
   if (q < C) {
     kq = ckey[q];
     pq = cpos[q];
-    for (int p = sub; p < C; p += tpe) {
-      const unsigned kp = ckey[p];
-      const int pp = cpos[p];
-      rk += (kp > kq || (kp == kq && pp < pq)) ? 1u : 0u;
+    // four entries per round, all read before the first compare
+    for (int p = sub; p < C; p += 4 * tpe) {
+      unsigned kp[4];
+      int pp[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int r = min(p + u * tpe, C - 1);
+        kp[u] = ckey[r];
+        pp[u] = cpos[r];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        rk += (p + u * tpe < C && (kp[u] > kq || (kp[u] == kq && pp[u] < pq))) ? 1u : 0u;
     }
   }
   if (tpe > 1) rk += swz<1>(rk);
@@ -1174,10 +1194,10 @@ __device__ __forceinline__ void rank_pick(int C, int need, const unsigned *ckey,
     ss.bc_u[1] = kq;
     ss.bc_i[2] = pq;
   }
-  __syncthreads();
+  lds_barrier();
   xk = ss.bc_u[1];
   pthr = ss.bc_i[2];
-  __syncthreads();
+  lds_barrier();
 }
 
 // k-th largest key among the block's non-zero keys (1 <= k <= count), by
@@ -1199,13 +1219,13 @@ __device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int 
     const unsigned range = hi - lo;
     const int sh = max(0, 32 - __clz((int)range) - 11);
     for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
       const unsigned x = key(j);
       if (x >= lo && x <= hi) atomicAdd(&ss.hist[(x - lo) >> sh], 1u);
     }
-    __syncthreads();
+    lds_barrier();
     hist_boundary(need, ss);
     const int bs = ss.bc_i[0];
     need -= ss.bc_i[1];
@@ -1214,7 +1234,7 @@ __device__ __forceinline__ void block_select(KeyF key, int k, unsigned &xk, int 
     const unsigned nhi = (hi - nlo <= span) ? hi : nlo + span;
     lo = nlo;
     hi = nhi;
-    __syncthreads();
+    lds_barrier();
   }
   xk = lo;
 }
@@ -1247,7 +1267,7 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
   lo = wave_min_u(lo);
   hi = wave_max_u(hi);
   if (lane == 0) { ss.red_u[wave] = lo; ss.red_u2[wave] = hi; }
-  __syncthreads();
+  lds_barrier();
   lo = 0xffffffffu;
   hi = 0u;
 #pragma unroll
@@ -1259,7 +1279,7 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     const unsigned x = key(j);
     if (x >= lo && hi >= lo) atomicAdd(&ss.hist[(x - lo) >> sh0], 1u);
   }
-  __syncthreads();
+  lds_barrier();
   hist_boundary(k, ss);
   const unsigned counted = ss.bc_u[3];
   bool fallback = counted < (unsigned)k;                // boundary below the binned range
@@ -1271,7 +1291,7 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     C = ss.hist[b0];
     fallback = C > (unsigned)kCandCap;
   }
-  __syncthreads();
+  lds_barrier();
   if (fallback) {
     int nd;
     block_select<PER>(key, k, xk, nd, ss);
@@ -1306,19 +1326,19 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     sh -= nb;
     const unsigned bm = (1u << nb) - 1u;
     for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
-    __syncthreads();
+    lds_barrier();
     for (int q = t; q < (int)C; q += NT) {
       const unsigned d = ckey[q] - blo;
       if ((d & pmask) == pre) atomicAdd(&ss.hist[(d >> sh) & bm], 1u);
     }
-    __syncthreads();
+    lds_barrier();
     hist_boundary(need, ss);
     const unsigned bl = (unsigned)ss.bc_i[0];
     need -= ss.bc_i[1];
     E = ss.hist[bl];
     pre |= bl << sh;
     pmask |= bm << sh;
-    __syncthreads();
+    lds_barrier();
   }
   xk = blo + pre;
   if (E == (unsigned)need) {
@@ -1332,19 +1352,19 @@ __device__ __forceinline__ void block_threshold(KeyF key, PosF pos, int k, unsig
     ps -= nb;
     const unsigned bm = (1u << nb) - 1u;
     for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
-    __syncthreads();
+    lds_barrier();
     for (int q = t; q < (int)C; q += NT) {
       if (ckey[q] != xk) continue;
       const unsigned d = 0x7fffu - (unsigned)cpos[q];   // larger d = lower position
       if ((d & ppm) == ppre) atomicAdd(&ss.hist[(d >> ps) & bm], 1u);
     }
-    __syncthreads();
+    lds_barrier();
     hist_boundary(need, ss);
     const unsigned bl = (unsigned)ss.bc_i[0];
     need -= ss.bc_i[1];
     ppre |= bl << ps;
     ppm |= bm << ps;
-    __syncthreads();
+    lds_barrier();
   }
   pthr = (int)(0x7fffu - ppre);
 }
@@ -1388,7 +1408,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
       const float e = re[min(max(u, 0), n - 1)];
       edge[q] = (u >= 0 && u < n) ? e : 0.f;
     }
-    __syncthreads();
+    lds_barrier();
     for (int q = t; q < nedge; q += kSelThreads) {
       const int c = q / (2 * r) + 1, o = q - (c - 1) * 2 * r;
       const int i = c * CH - r + o;                 // position next to boundary c*CH
@@ -1420,7 +1440,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
       for (int j = 0; j < PER; ++j)
         if (tt + j * kSelThreads < n) arr[pad32(tt + j * kSelThreads)] = bv[j];
     }
-    __syncthreads();
+    lds_barrier();
     // Scale-matching set: top M = min(rho K, |I|) of B over I (Eq. scale_matching_set).
     int M = (int)floorf(a.rho * (float)K);
     if (M > nc) M = nc;
@@ -1520,7 +1540,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     for (int j = 0; j < PER; ++j)
       if (t + j * kSelThreads < nc) arr[pad32(t + j * kSelThreads)] = sv[j];
   }
-  __syncthreads();
+  lds_barrier();
 
   // Pooled score over I and its keys, contiguous ownership: positions
   // [t*PER, t*PER + PER).  The mean pool slides window sums in double; the
@@ -1571,7 +1591,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
       }
     }
   }
-  __syncthreads();   // pooled values read; arr is reused as the slot table
+  lds_barrier();   // pooled values read; arr is reused as the slot table
 
   // Top-K over I (Eq. topk_selection), emitted in ascending position.
   const int kept = min(K, nc);
@@ -1691,7 +1711,7 @@ __device__ __forceinline__ void ordered_bases(uint32_t msk, unsigned *pre) {
     const uint64_t m = __ballot((msk >> j) & 1u);
     if (lane == 0) pre[j * NW + wave] = (unsigned)__popcll(m);
   }
-  __syncthreads();
+  lds_barrier();
   if (wave == 0) {
     unsigned x[E], s = 0;
 #pragma unroll
@@ -1708,7 +1728,7 @@ __device__ __forceinline__ void ordered_bases(uint32_t msk, unsigned *pre) {
     }
     if (lane == 63) pre[NE] = incl;
   }
-  __syncthreads();
+  lds_barrier();
 }
 __device__ __forceinline__ unsigned lane_rank(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
@@ -1750,7 +1770,7 @@ __device__ __forceinline__ void hist_threshold(const unsigned *gh, KeyF key, Pos
   const int beta = ss.bc_i[0];
   const int need = k - ss.bc_i[1];
   const unsigned C = ss.bc_u[2];
-  __syncthreads();
+  lds_barrier();
   if (C <= (unsigned)kCandCap) {
     compact_ballot<PER, NT>([&](int j) { const unsigned x = key(j); return x != 0u && hbin(x) == beta; },
                             key, pos, ckey, cpos, ss);
@@ -1849,7 +1869,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
 #pragma unroll
     for (int j = 0; j < kSegEJ; ++j)
       if (tt + j * NT < kSegE) Es[tt + j * NT] = ev[j];
-    __syncthreads();
+    lds_barrier();
     // V = E + L + T (Eq. structurally_calibrated_evidence, per the terms
     // mask), L = P_r E over the sequence-truncated neighbourhood
     // (Eq. intra_layer_coherence), T the mean of the earlier layers' E
@@ -1872,7 +1892,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // V, and the pooled B and V over I (truncated windows), of the segment's candidates
   const int hp = a.pool_half;
@@ -1964,9 +1984,12 @@ __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t ba
 #pragma unroll
   for (int j = kListSpec; j < kListPer; ++j) k[j] = 0u;
   if (t < kMaxSegs) scnt[t] = t < L.nseg ? c : 0;
-  __syncthreads();
-  const int over = (t < kMaxSegs && scnt[t] > cs) ? 1 : 0;
-  if (__syncthreads_or(over) == 0) {
+  lds_barrier();
+  // every thread reads all counts: no second barrier, no wait for the lists
+  bool over = false;
+#pragma unroll
+  for (int s = 0; s < kMaxSegs; ++s) over |= scnt[s] > cs;
+  if (!over) {
     L.fits = true;
 #pragma unroll
     for (int j = 0; j < kListSpec; ++j) {
@@ -2037,13 +2060,13 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
         if (o >= 0 && o < kMomChunk) mom[o] = make_float2(xb[j], a.vec_V[base + t + j * NT]);
       }
     }
-    __syncthreads();
+    lds_barrier();
     const int cnt = min(kMomChunk, M - r0);
     for (int e = t; e < cnt; e += NT) {
       const double db = (double)mom[e].x - bref, dv = (double)mom[e].y;
       s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
     }
-    __syncthreads();
+    lds_barrier();
   }
   part[0] = s0; part[1] = s1; part[2] = s2; part[3] = s3;
 }
@@ -2057,7 +2080,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[kAllPer * NW + 1];
   __shared__ float2 mom[kMomChunk];
-  __shared__ int scnt[kMaxSegs];
+  __shared__ __align__(16) int scnt[kMaxSegs];
   const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
@@ -2135,7 +2158,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
   }
 
   // pooled score keys of the segment, and their histogram
-  __syncthreads();
+  lds_barrier();
   if (max_s) {
     // S over the segment widened by the pool halo in LDS (the moment scratch
     // is free now), -inf outside the candidate set, then the max over each
@@ -2154,7 +2177,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
       const int q = t + j * NT, u = w0 + q;
       if (q < kSegWin) sw[q] = (u >= 0 && u < nc) ? fmaf(lam, wv[j], wb[j]) : -INFINITY;
     }
-    __syncthreads();
+    lds_barrier();
     const int hp = a.pool_half;
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -2179,7 +2202,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   unsigned *gh = a.hist_S + hrow;
   for (int q = t; q < kHBins; q += NT) {
     const unsigned c = hist[q];
@@ -2285,7 +2308,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
   __shared__ int cpos[kCandCap];
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[kAllPer * NW + 1];
-  __shared__ int scnt[kMaxSegs];
+  __shared__ __align__(16) int scnt[kMaxSegs];
   const int part = blockIdx.x, b = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
   const int wave = t >> 6;
   const int n = st.cu[b + 1] - st.cu[b];
@@ -2342,7 +2365,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
     for (int j = max(kept, 0) + t; j < K; j += NT) idx[j] = -1;
   for (int w = t; w < a.W; w += NT) tbl[kept + w] = nc + w;
   for (int j = kept + a.W + t; j < C + a.W; j += NT) tbl[j] = -1;
-  __syncthreads();
+  lds_barrier();
 
   {
     // clear this part's slice of the B histogram for the next layer (its
