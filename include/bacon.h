@@ -210,6 +210,19 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *ctx, int32_t layer, const bacon
                                       const float *d_lse, int32_t *d_idx, void *d_k_out,
                                       void *d_v_out, void *stream);
 
+/* The window-row normalisers alone (Sec. 4.1): writes d_lse [B, Hq, W]
+ * float32 as bacon_compress_layer_lse reads them (natural log of the sum of
+ * exp(q_w . k_i / sqrt(d)) over the row's causal keys), from one pass over
+ * K.  Reads and writes no history, so it needs no begin_prompt and may run
+ * for any layer at any time; it uses the context's normaliser scratch, so
+ * calls of one context must not overlap each other (bacon_compress_layer
+ * uses the same scratch; bacon_compress_layer_lse does not).  This lets a
+ * caller form the normalisers of layer l+1 on a second stream while layer l
+ * is selected and compacted.  d_lse must be a 4-byte-aligned device pointer
+ * (INVALID otherwise); the caller keeps ownership. */
+bacon_status bacon_window_lse(bacon_ctx *ctx, const bacon_batch *batch, const void *d_q_win,
+                              const void *d_k, float *d_lse, void *stream);
+
 /* Sizes of the outputs for a batch: idx entries and compacted rows. */
 int64_t bacon_idx_count(const bacon_batch *batch, int32_t num_kv_heads);
 int64_t bacon_kept_rows(const bacon_batch *batch, int32_t num_kv_heads, int32_t window);

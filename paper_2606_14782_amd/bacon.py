@@ -21,7 +21,8 @@ TERM_E, TERM_L, TERM_T = 1, 2, 4
 ENTRY_POINTS = [
     "bacon_default_params", "bacon_workspace_bytes", "bacon_init", "bacon_free",
     "bacon_begin_prompt", "bacon_score", "bacon_calibrate", "bacon_select_topk",
-    "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_idx_count",
+    "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_window_lse",
+    "bacon_idx_count",
     "bacon_kept_rows",
     "bacon_profile_enable", "bacon_profile_read", "bacon_status_string", "bacon_last_error",
 ]
@@ -84,6 +85,7 @@ def lib() -> C.CDLL:
                                            vp, vp]
         L.bacon_compress_layer_lse.argtypes = [vp, C.c_int32, C.POINTER(Batch), vp, vp, vp, vp,
                                                vp, vp, vp, vp]
+        L.bacon_window_lse.argtypes = [vp, C.POINTER(Batch), vp, vp, vp, vp]
         L.bacon_idx_count.argtypes = [C.POINTER(Batch), C.c_int32]
         L.bacon_idx_count.restype = C.c_int64
         L.bacon_kept_rows.argtypes = [C.POINTER(Batch), C.c_int32, C.c_int32]
@@ -96,7 +98,8 @@ def lib() -> C.CDLL:
         L.bacon_last_error.restype = C.c_char_p
         for name in ("bacon_init", "bacon_free", "bacon_begin_prompt", "bacon_score",
                      "bacon_calibrate", "bacon_select_topk", "bacon_compact",
-                     "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_profile_enable"):
+                     "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_window_lse",
+                     "bacon_profile_enable"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -250,6 +253,17 @@ class Context:
                                               _ptr(k_out), _ptr(v_out), _stream()))
         return idx, k_out, v_out
 
+    def bacon_window_lse(self, batch: BatchLayout, q_win, k, out=None):
+        """The window-row normalisers lse [B, Hq, W] (natural log) alone, as
+        bacon_compress_layer_lse takes them."""
+        import torch
+        s = self.shape
+        lse = out if out is not None else torch.empty(
+            (batch.c.batch, s.num_q_heads, s.window), dtype=torch.float32, device=k.device)
+        _check(lib().bacon_window_lse(self._h, C.byref(batch.c), _ptr(q_win), _ptr(k), _ptr(lse),
+                                      _stream()))
+        return lse
+
     def bacon_profile_enable(self, enable=True):
         _check(lib().bacon_profile_enable(self._h, 1 if enable else 0))
 
@@ -287,3 +301,7 @@ def bacon_compress_layer(ctx: Context, layer, batch, q_win, k, v, out=None):
 
 def bacon_compress_layer_lse(ctx: Context, layer, batch, q_win, k, v, lse, out=None):
     return ctx.bacon_compress_layer_lse(layer, batch, q_win, k, v, lse, out)
+
+
+def bacon_window_lse(ctx: Context, batch, q_win, k, out=None):
+    return ctx.bacon_window_lse(batch, q_win, k, out)

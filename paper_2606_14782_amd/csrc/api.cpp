@@ -727,6 +727,36 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *c, int32_t layer, const bacon_b
   return compress(c, layer, bt, d_q_win, d_k, d_v, d_lse, d_idx, d_k_out, d_v_out, stream);
 }
 
+bacon_status bacon_window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d_q_win,
+                              const void *d_k, float *d_lse, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  TRY(check_ptr(d_q_win, "q_win", 16));
+  TRY(check_ptr(d_k, "k", 16));
+  TRY(check_ptr(d_lse, "lse", 4));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool bf16 = c->shape.dtype == BACON_BF16;
+  int chunk = 0;
+  SeqTable st{};
+  const bool kr = !c->kr_off && kr_supported(bf16, c->shape.head_dim, c->L.rpad);
+  if (kr) {
+    st = make_table(c, bt, &chunk, false, kr_keys(bf16, c->shape.head_dim));
+  } else {
+    st = make_table(c, bt, &chunk, false);
+    TRY(check_lds(c, bt, chunk, true, -1));
+  }
+  PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
+  a.T = bt->cu_seqlens[bt->batch];
+  a.lse_user = d_lse;
+  if (kr) {
+    TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+  } else {
+    TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
+  }
+  TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+  return BACON_OK;
+}
+
 int64_t bacon_idx_count(const bacon_batch *bt, int32_t num_kv_heads) {
   if (!bt || (!bt->budgets && !bt->head_budgets) || bt->batch < 1 || num_kv_heads < 1) return 0;
   int64_t n = 0;

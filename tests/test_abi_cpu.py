@@ -128,6 +128,14 @@ def test_calls_reject_bad_batches_and_order_before_enqueueing():
     # sequence shorter than the window
     assert L.bacon_score(h, 0, C.byref(_batch([0, 10], [4]).c), fake, fake, None, fake, fake,
                          None) == bacon.ERR_INVALID
+    # window normalisers alone: NULL or misaligned pointers, short sequences
+    assert L.bacon_window_lse(h, C.byref(good.c), fake, fake, None, None) == bacon.ERR_INVALID
+    assert L.bacon_window_lse(h, C.byref(good.c), fake, fake, C.c_void_p(0x200002),
+                              None) == bacon.ERR_INVALID
+    assert L.bacon_window_lse(h, C.byref(good.c), None, fake, fake, None) == bacon.ERR_INVALID
+    assert L.bacon_window_lse(h, C.byref(_batch([0, 10], [4]).c), fake, fake, fake,
+                              None) == bacon.ERR_INVALID
+    assert L.bacon_window_lse(None, C.byref(good.c), fake, fake, fake, None) == bacon.ERR_INVALID
     # too many tokens for the context
     assert L.bacon_score(h, 0, C.byref(_batch([0, 5000], [4]).c), fake, fake, None, fake, fake,
                          None) == bacon.ERR_INVALID

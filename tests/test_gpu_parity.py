@@ -135,6 +135,37 @@ def test_supplied_normalisers(name):
     run_case(name + "/lse", CASES[name](), split=False, supplied_lse=True)
 
 
+@pytest.mark.parametrize("name,streaming", [("tiny-fp32", False), ("ragged-small", False),
+                                            ("video-n32768", False), ("ragged-small", True)])
+def test_window_lse(name, streaming, monkeypatch):
+    """bacon_window_lse: the window-row normalisers alone match the oracle's,
+    and fed to bacon_compress_layer_lse they give the oracle's kept sets."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    if streaming:
+        monkeypatch.setenv("BACON_KEY_REGISTERS", "0")
+    wl = CASES[name]().with_(num_layers=2)
+    rtol = P.RTOL[wl.dtype]
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    orc = ref.Prompt.for_workload(wl, P.oracle_params())
+    ctx = P.make_ctx(wl, P.params_for(wl))
+    ctx.bacon_begin_prompt(batch)
+    for layer in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, layer)
+        r = orc.layer(layer, x["q_win"], x["k"])
+        q, k, v = P.to_dev(x["q_win"], wl), P.to_dev(x["k"], wl), P.to_dev(x["v"], wl)
+        P.log(f"[window_lse {name}{' streaming' if streaming else ''}] layer {layer}")
+        lse = ctx.bacon_window_lse(batch, q, k)
+        torch.cuda.synchronize()
+        P.close(f"{name} L{layer} window_lse", lse.cpu().numpy(), r["lse"], rtol)
+        idx, ko, vo = ctx.bacon_compress_layer_lse(layer, batch, q, k, v, lse)
+        torch.cuda.synchronize()
+        gi = idx.cpu().numpy()
+        P.check_idx(f"{name} L{layer} window_lse + compress_layer_lse", gi, r, wl, rtol)
+        assert np.array_equal(P.tensor_bytes(ko), P.gather_rows(P.as_bytes(x["k"], wl), gi, wl))
+        del q, k, v
+
+
 @pytest.mark.parametrize("name", ["video-n32768", "llava-small", "ragged-small"])
 def test_streaming_passes(name, monkeypatch):
     """The two streaming K passes (the path of fp32 keys and of more than 128
