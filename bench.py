@@ -1,7 +1,10 @@
 """Benchmark of the BACON prefill KV-compression pass on one MI355X.
 
 One step = the whole pass of a prompt: bacon_begin_prompt and
-bacon_compress_layer for every layer (score -> calibrate -> select -> compact),
+bacon_compress_prompt over every layer (score -> calibrate -> select ->
+compact per layer, the next layer's normaliser pass in the launch of this
+layer's scoring pass); the per-layer calls (bacon_compress_layer) are timed
+beside it,
 on the 32K-token long-video GQA workload (32 layers, 32 query / 8 KV heads,
 d = 128, window 32, budget 256, bf16).  Inputs are synthetic, seeded, and
 resident in HBM before timing starts.
@@ -64,6 +67,8 @@ def kernel_bytes(name, wl, persist_m=4):
         return ab["k"] + ab["q"]
     if name in ("window_score_calib", "window_score_calib_kr"):   # K, Q_win; E and B out
         return ab["k"] + ab["q"] + 2 * vec
+    if name == "window_score_calib_lse_kr":             # both passes: two layers' K and Q_win
+        return 2 * (ab["k"] + ab["q"]) + 2 * vec
     if name == "lse_merge":                             # per-chunk (max, sum) partials
         chunks = T / 512 + wl.batch
         return Hkv * chunks * wl.group * wl.window * 8
@@ -169,6 +174,10 @@ def main():
 
     def step():
         ctx.bacon_begin_prompt(batch)
+        ctx.bacon_compress_prompt(0, batch, qs, ks, vs, outs=outs)
+
+    def step_layers():
+        ctx.bacon_begin_prompt(batch)
         for l in range(wl.num_layers):
             ctx.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l], out=outs[l])
 
@@ -212,6 +221,17 @@ def main():
     achieved = kbytes / (per_kernel[dom]["avg_us"] * 1e-6) / 1e9
     traffic = measured_traffic(dom)
 
+    # The per-layer calls over the same prompt (no next-layer pass in the
+    # scoring launch), for comparison.
+    for _ in range(args.warmup):
+        step_layers()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step_layers()
+    torch.cuda.synchronize()
+    ms_step_layers = 1e3 * (time.perf_counter() - t0) / args.steps
+
     # The same pass with the window-row normalisers supplied, as a prefill
     # attention that returns its softmax normalisers would (the first K pass and
     # the merge are skipped); reported beside the headline, never as it.
@@ -223,8 +243,7 @@ def main():
 
     def step_lse():
         ctx.bacon_begin_prompt(batch)
-        for l in range(wl.num_layers):
-            ctx.bacon_compress_layer_lse(l, batch, qs[l], ks[l], vs[l], lses[l], out=outs[l])
+        ctx.bacon_compress_prompt(0, batch, qs, ks, vs, lses=lses, outs=outs)
 
     for _ in range(args.warmup):
         step_lse()
@@ -267,9 +286,15 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": dom,
                      "bytes_per_launch": kbytes, "avg_us": per_kernel[dom]["avg_us"]},
         "kernels": per_kernel,
+        "per_layer_calls": {
+            "note": "bacon_compress_layer called for each layer (pass 1 of a layer in its own "
+                    "launch)",
+            "ms_per_layer": ms_step_layers / wl.num_layers,
+            "value": keys_step / (ms_step_layers * 1e-3), "unit": "keys/s"},
         "supplied_lse": {
             "note": "window-row softmax normalisers given by the prefill attention "
-                    "(bacon_compress_layer_lse); the first K pass and the merge are skipped",
+                    "(bacon_compress_prompt with lse); the first K pass and the merge are "
+                    "skipped",
             "ms_per_layer": ms_step_lse / wl.num_layers,
             "value": keys_step / (ms_step_lse * 1e-3), "unit": "keys/s"},
     }

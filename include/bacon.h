@@ -210,6 +210,25 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *ctx, int32_t layer, const bacon
                                       const float *d_lse, int32_t *d_idx, void *d_k_out,
                                       void *d_v_out, void *stream);
 
+/* The whole pass for layers first_layer .. first_layer + num_layers - 1 of a
+ * prompt (compression at the end of prefill, when every layer's cache is
+ * there): the same results as bacon_compress_layer (or, when d_lse is not
+ * NULL, bacon_compress_layer_lse) called for each layer in order, bit for
+ * bit.  With every layer's inputs at hand, the K pass that forms the next
+ * layer's normalisers runs in the same launch as this layer's scoring pass
+ * (one launch fewer per layer, and the two passes fill each other's idle
+ * CUs).  The per-layer arguments are host arrays of num_layers device
+ * pointers each, in the layouts of bacon_compress_layer; d_lse is NULL or
+ * such an array.  first_layer must be the prompt's next layer (ORDER
+ * otherwise) and the range must end within num_layers (ORDER).  Every
+ * pointer is checked before the first launch (INVALID if NULL or
+ * misaligned); the caller keeps ownership of all buffers. */
+bacon_status bacon_compress_prompt(bacon_ctx *ctx, const bacon_batch *batch, int32_t first_layer,
+                                   int32_t num_layers, const void *const *d_q_win,
+                                   const void *const *d_k, const void *const *d_v,
+                                   const float *const *d_lse, int32_t *const *d_idx,
+                                   void *const *d_k_out, void *const *d_v_out, void *stream);
+
 /* The window-row normalisers alone (Sec. 4.1): writes d_lse [B, Hq, W]
  * float32 as bacon_compress_layer_lse reads them (natural log of the sum of
  * exp(q_w . k_i / sqrt(d)) over the row's causal keys), from one pass over

@@ -21,7 +21,8 @@ TERM_E, TERM_L, TERM_T = 1, 2, 4
 ENTRY_POINTS = [
     "bacon_default_params", "bacon_workspace_bytes", "bacon_init", "bacon_free",
     "bacon_begin_prompt", "bacon_score", "bacon_calibrate", "bacon_select_topk",
-    "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_window_lse",
+    "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_compress_prompt",
+    "bacon_window_lse",
     "bacon_idx_count",
     "bacon_kept_rows",
     "bacon_profile_enable", "bacon_profile_read", "bacon_status_string", "bacon_last_error",
@@ -86,6 +87,8 @@ def lib() -> C.CDLL:
         L.bacon_compress_layer_lse.argtypes = [vp, C.c_int32, C.POINTER(Batch), vp, vp, vp, vp,
                                                vp, vp, vp, vp]
         L.bacon_window_lse.argtypes = [vp, C.POINTER(Batch), vp, vp, vp, vp]
+        L.bacon_compress_prompt.argtypes = [vp, C.POINTER(Batch), C.c_int32, C.c_int32, vp, vp, vp,
+                                            vp, vp, vp, vp, vp]
         L.bacon_idx_count.argtypes = [C.POINTER(Batch), C.c_int32]
         L.bacon_idx_count.restype = C.c_int64
         L.bacon_kept_rows.argtypes = [C.POINTER(Batch), C.c_int32, C.c_int32]
@@ -99,6 +102,7 @@ def lib() -> C.CDLL:
         for name in ("bacon_init", "bacon_free", "bacon_begin_prompt", "bacon_score",
                      "bacon_calibrate", "bacon_select_topk", "bacon_compact",
                      "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_window_lse",
+                     "bacon_compress_prompt",
                      "bacon_profile_enable"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -253,6 +257,26 @@ class Context:
                                               _ptr(k_out), _ptr(v_out), _stream()))
         return idx, k_out, v_out
 
+    def bacon_compress_prompt(self, first_layer, batch: BatchLayout, q_wins, ks, vs, lses=None,
+                              outs=None):
+        """The pass over layers first_layer .. first_layer + len(ks) - 1 in one
+        call; returns [(idx, k_out, v_out)] per layer."""
+        import torch
+        n = len(ks)
+        if outs is None:
+            outs = []
+            for k in ks:
+                idx = torch.empty(batch.idx_count(self.shape.num_kv_heads), dtype=torch.int32,
+                                  device=k.device)
+                outs.append((idx, *self._kv_out(batch, k)))
+        arr = lambda xs: (C.c_void_p * n)(*[x.data_ptr() for x in xs])
+        lse_arr = arr(lses) if lses is not None else None
+        _check(lib().bacon_compress_prompt(
+            self._h, C.byref(batch.c), first_layer, n, arr(q_wins), arr(ks), arr(vs), lse_arr,
+            arr([o[0] for o in outs]), arr([o[1] for o in outs]), arr([o[2] for o in outs]),
+            _stream()))
+        return outs
+
     def bacon_window_lse(self, batch: BatchLayout, q_win, k, out=None):
         """The window-row normalisers lse [B, Hq, W] (natural log) alone, as
         bacon_compress_layer_lse takes them."""
@@ -301,6 +325,10 @@ def bacon_compress_layer(ctx: Context, layer, batch, q_win, k, v, out=None):
 
 def bacon_compress_layer_lse(ctx: Context, layer, batch, q_win, k, v, lse, out=None):
     return ctx.bacon_compress_layer_lse(layer, batch, q_win, k, v, lse, out)
+
+
+def bacon_compress_prompt(ctx: Context, first_layer, batch, q_wins, ks, vs, lses=None, outs=None):
+    return ctx.bacon_compress_prompt(first_layer, batch, q_wins, ks, vs, lses, outs)
 
 
 def bacon_window_lse(ctx: Context, batch, q_win, k, out=None):

@@ -128,9 +128,10 @@ const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", 
                               "segment_calib", "segment_score", "segment_cand",
                               "final_topk",    "select_calib",  "select_topk",
                               "calib_elem",    "compact",       "window_lse_kr",
-                              "window_score_calib_kr"};
+                              "window_score_calib_kr", "window_score_calib_lse_kr"};
 enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
-                KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_COUNT };
+                KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_DUAL_KR,
+                KI_COUNT };
 
 }  // namespace
 
@@ -602,9 +603,16 @@ bacon_status bacon_compact(bacon_ctx *c, const bacon_batch *bt, const void *d_k,
 namespace {
 
 // The fused pass of one layer; d_lse (caller normalisers) skips pass 1.
+// Within a prompt call: lse_merged says that pass 1 of this layer already ran
+// (with the previous layer's pass 2) and its normalisers are merged; next_q
+// and next_k, when not NULL, are the next layer's inputs, whose pass 1 then
+// runs in the launch of this layer's pass 2.  *dual_out reports whether it did.
 bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
                       const void *d_k, const void *d_v, const float *d_lse, int32_t *d_idx,
-                      void *d_k_out, void *d_v_out, void *stream) {
+                      void *d_k_out, void *d_v_out, void *stream, bool lse_merged = false,
+                      const void *next_q = nullptr, const void *next_k = nullptr,
+                      bool *dual_out = nullptr) {
+  if (dual_out) *dual_out = false;
   if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
   TRY(check_batch(c, bt));
   TRY(check_prompt_batch(c, bt));
@@ -688,11 +696,21 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
   TRY(head_table(c, bt, s, &g.hb));
   if (kr) {
-    if (!d_lse) {
+    if (!d_lse && !lse_merged) {
       TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
       TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
     }
-    TRY(timed(c, KI_FUSED_KR, s, [&] { return launch_krpass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
+    if (!d_lse && next_q) {
+      // this layer's pass 2 with the next layer's pass 1, then the next
+      // layer's merge (this pass 2 has read the merged normalisers by then)
+      PassArgs an = pass_args(c, st, chunk, next_q, next_k);
+      an.T = T;
+      TRY(timed(c, KI_DUAL_KR, s, [&] { return launch_krdual(bf16, c->shape.head_dim, w32, a, an, st, s); }));
+      TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(an, st, s); }));
+      if (dual_out) *dual_out = true;
+    } else {
+      TRY(timed(c, KI_FUSED_KR, s, [&] { return launch_krpass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
+    }
   } else {
     if (!d_lse) {
       TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
@@ -725,6 +743,42 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *c, int32_t layer, const bacon_b
   if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
   TRY(check_ptr(d_lse, "lse", 4));
   return compress(c, layer, bt, d_q_win, d_k, d_v, d_lse, d_idx, d_k_out, d_v_out, stream);
+}
+
+bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t first_layer,
+                                   int32_t num_layers, const void *const *d_q_win,
+                                   const void *const *d_k, const void *const *d_v,
+                                   const float *const *d_lse, int32_t *const *d_idx,
+                                   void *const *d_k_out, void *const *d_v_out, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  if (num_layers < 1) return fail(BACON_ERR_INVALID, "num_layers %d must be >= 1", num_layers);
+  if (!d_q_win || !d_k || !d_v || !d_idx || !d_k_out || !d_v_out)
+    return fail(BACON_ERR_INVALID, "a per-layer pointer array is NULL");
+  if (first_layer != c->next_layer)
+    return fail(BACON_ERR_ORDER, "layer %d given, layer %d expected next", first_layer, c->next_layer);
+  if ((int64_t)first_layer + num_layers > c->shape.num_layers)
+    return fail(BACON_ERR_ORDER, "layers %d..%d beyond num_layers %d", first_layer,
+                first_layer + num_layers - 1, c->shape.num_layers);
+  // every layer's arguments are checked before the first launch
+  for (int i = 0; i < num_layers; ++i) {
+    TRY(check_ptr(d_q_win[i], "q_win", 16));
+    TRY(check_ptr(d_k[i], "k", 16));
+    TRY(check_ptr(d_v[i], "v", 16));
+    TRY(check_ptr(d_idx[i], "idx", 4));
+    TRY(check_ptr(d_k_out[i], "k_out", 16));
+    TRY(check_ptr(d_v_out[i], "v_out", 16));
+    if (d_lse) TRY(check_ptr(d_lse[i], "lse", 4));
+  }
+  bool merged = false;
+  for (int i = 0; i < num_layers; ++i) {
+    const bool more = i + 1 < num_layers && !d_lse;
+    bool dual = false;
+    TRY(compress(c, first_layer + i, bt, d_q_win[i], d_k[i], d_v[i], d_lse ? d_lse[i] : nullptr,
+                 d_idx[i], d_k_out[i], d_v_out[i], stream, merged,
+                 more ? d_q_win[i + 1] : nullptr, more ? d_k[i + 1] : nullptr, &dual));
+    merged = dual;
+  }
+  return BACON_OK;
 }
 
 bacon_status bacon_window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d_q_win,

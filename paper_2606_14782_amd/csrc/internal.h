@@ -175,6 +175,9 @@ int kr_lds_bytes(bool bf16, int head_dim, int rpad);
 bool kr_supported(bool bf16, int head_dim, int rpad);
 hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
                          const SeqTable &st, hipStream_t s);
+// Pass 2 of one layer (a2) with pass 1 of the next layer (a1) in one launch.
+hipError_t launch_krdual(bool bf16, int head_dim, bool w32, const PassArgs &a2, const PassArgs &a1,
+                         const SeqTable &st, hipStream_t s);
 // LDS a select workgroup needs (static + dynamic) for sequences up to max_len.
 size_t select_lds_bytes(int mode, int max_len);
 hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,

@@ -606,16 +606,16 @@ int kr_lds_bytes(bool bf16, int head_dim, int rpad) {
   return std::max(nr * rowb, 4 * kHBins) + 8 * kKrWaves * nr + 4 * nr + 4 * kpw;
 }
 
+// One workgroup of a key-register pass: chunk gchunk of the sequences' keys
+// of KV head h.
 template <int MODE, int D, bool W32, int NRT>
-// two workgroups per CU: at most 256 registers per wave
-__global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTable st) {
+__device__ __forceinline__ void krpass_body(const PassArgs &a, const SeqTable &st, int gchunk, int h) {
   using C = PassCfg<true, D>;
   constexpr int NU = C::NU, KT = KrCfg<true, D>::KT, KPW = KrCfg<true, D>::KPW;
   constexpr int NT = 64 * kKrWaves, NR = 32 * NRT;
   constexpr bool FUSED = MODE == PASS_FUSED;
   extern __shared__ __align__(16) unsigned char smem[];
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63, half = lane >> 5, l32 = lane & 31;
-  const int h = blockIdx.y, gchunk = blockIdx.x;
   const int b = find_seq(st, gchunk);
   const int c = gchunk - st.chunk_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
@@ -896,13 +896,53 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTabl
     __syncthreads();
     for (int p = t; p < ncnd; p += NT) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
     __syncthreads();
-    const int copy = (blockIdx.y * gridDim.x + blockIdx.x) % kHCopies;
+    const int copy = (h * st.total_chunks + gchunk) % kHCopies;
     unsigned *gh = a.hist_B + (((int64_t)b * a.Hkv + h) * kHCopies + copy) * kHBins;
     for (int q = blo + t; q <= bhi; q += NT) {
       const unsigned cnt = hist[q];
       if (cnt) atomicAdd(&gh[q], cnt);
     }
   }
+}
+
+// two workgroups per CU: at most 256 registers per wave
+template <int MODE, int D, bool W32, int NRT>
+__global__ __launch_bounds__(64 * kKrWaves, 2) void k_krpass(PassArgs a, SeqTable st) {
+  krpass_body<MODE, D, W32, NRT>(a, st, blockIdx.x, blockIdx.y);
+}
+
+// Pass 2 of one layer (a2) and pass 1 of the next (a1) in one grid: the first
+// total_chunks columns of workgroups take a2, the others a1.  Both layers
+// share the batch (one SeqTable); the two halves touch disjoint buffers
+// (pass 2 reads the merged normalisers and writes E, B and the B histogram;
+// pass 1 writes the per-chunk partials).  One launch instead of two, and the
+// workgroups of pass 1 fill the CUs that pass 2 leaves idle at its end.
+template <int D, bool W32, int NRT>
+__global__ __launch_bounds__(64 * kKrWaves, 2) void k_krdual(PassArgs a2, PassArgs a1, SeqTable st) {
+  if ((int)blockIdx.x < st.total_chunks)
+    krpass_body<PASS_FUSED, D, W32, NRT>(a2, st, blockIdx.x, blockIdx.y);
+  else
+    krpass_body<PASS_LSE, D, false, NRT>(a1, st, blockIdx.x - st.total_chunks, blockIdx.y);
+}
+
+template <int D, bool W32, int NRT>
+static hipError_t launch_dual_t(const PassArgs &a2, const PassArgs &a1, const SeqTable &st,
+                                hipStream_t s) {
+  const int lds = kr_lds_bytes(true, D, a2.Rpad);
+  if (lds > kLdsBytes) return hipErrorInvalidValue;
+  auto kern = k_krdual<D, W32, NRT>;
+  allow_lds(kern, lds);
+  hipLaunchKernelGGL(kern, dim3(2 * st.total_chunks, a2.Hkv), dim3(64 * kKrWaves), lds, s, a2, a1,
+                     st);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_dual_d(bool w32, const PassArgs &a2, const PassArgs &a1, const SeqTable &st,
+                                hipStream_t s) {
+  if (kr_row_tiles(a2.Rpad) == 2)
+    return w32 ? launch_dual_t<D, true, 2>(a2, a1, st, s) : launch_dual_t<D, false, 2>(a2, a1, st, s);
+  return w32 ? launch_dual_t<D, true, 4>(a2, a1, st, s) : launch_dual_t<D, false, 4>(a2, a1, st, s);
 }
 
 template <int MODE, int D, bool W32, int NRT>
@@ -924,6 +964,12 @@ static hipError_t launch_kr_d(bool w32, const PassArgs &a, const SeqTable &st, h
 
 bool kr_supported(bool bf16, int head_dim, int rpad) {
   return bf16 && kr_row_tiles(rpad) > 0 && kr_lds_bytes(bf16, head_dim, rpad) <= kLdsBytes;
+}
+
+hipError_t launch_krdual(bool bf16, int head_dim, bool w32, const PassArgs &a2, const PassArgs &a1,
+                         const SeqTable &st, hipStream_t s) {
+  if (!kr_supported(bf16, head_dim, a2.Rpad) || a1.Rpad != a2.Rpad) return hipErrorInvalidValue;
+  return head_dim == 128 ? launch_dual_d<128>(w32, a2, a1, st, s) : launch_dual_d<64>(w32, a2, a1, st, s);
 }
 
 hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,

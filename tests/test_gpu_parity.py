@@ -135,6 +135,58 @@ def test_supplied_normalisers(name):
     run_case(name + "/lse", CASES[name](), split=False, supplied_lse=True)
 
 
+@pytest.mark.parametrize("name", ["video-small", "ragged-small", "llava-small", "qwen2vl-small",
+                                  "tiny-fp32", "video-n32768"])
+def test_prompt_call_equals_layer_calls(name):
+    """bacon_compress_prompt (the next layer's normaliser pass in the launch of
+    this layer's scoring pass) gives the per-layer calls' outputs bit for bit,
+    whole or split into two calls, and with the normalisers supplied."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = CASES[name]()
+    wl = wl.with_(num_layers=min(wl.num_layers, 5))
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+    qs = [P.to_dev(x["q_win"], wl) for x in xs]
+    ks = [P.to_dev(x["k"], wl) for x in xs]
+    vs = [P.to_dev(x["v"], wl) for x in xs]
+    P.log(f"[prompt {name}] {wl.num_layers} layers")
+    ref_ctx = P.make_ctx(wl, P.params_for(wl))
+    ref_ctx.bacon_begin_prompt(batch)
+    want = [ref_ctx.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l]) for l in range(wl.num_layers)]
+    ctx = P.make_ctx(wl, P.params_for(wl))
+    ctx.bacon_begin_prompt(batch)
+    got = ctx.bacon_compress_prompt(0, batch, qs, ks, vs)
+    ctx.bacon_begin_prompt(batch)
+    cut = wl.num_layers // 2
+    got2 = (ctx.bacon_compress_prompt(0, batch, qs[:cut], ks[:cut], vs[:cut]) +
+            ctx.bacon_compress_prompt(cut, batch, qs[cut:], ks[cut:], vs[cut:]))
+    torch.cuda.synchronize()
+    for l in range(wl.num_layers):
+        for i, what in enumerate(("idx", "k_out", "v_out")):
+            assert torch.equal(got[l][i], want[l][i]), f"layer {l} {what}"
+            assert torch.equal(got2[l][i], want[l][i]), f"layer {l} {what} (two calls)"
+    # normalisers supplied: the prompt call equals bacon_compress_layer_lse
+    lses = [ctx.bacon_window_lse(batch, qs[l], ks[l]) for l in range(wl.num_layers)]
+    ref_ctx.bacon_begin_prompt(batch)
+    want = [ref_ctx.bacon_compress_layer_lse(l, batch, qs[l], ks[l], vs[l], lses[l])
+            for l in range(wl.num_layers)]
+    ctx.bacon_begin_prompt(batch)
+    got = ctx.bacon_compress_prompt(0, batch, qs, ks, vs, lses=lses)
+    torch.cuda.synchronize()
+    for l in range(wl.num_layers):
+        for i, what in enumerate(("idx", "k_out", "v_out")):
+            assert torch.equal(got[l][i], want[l][i]), f"layer {l} {what} (normalisers given)"
+    # and against the oracle on the first layers
+    orc = ref.Prompt.for_workload(wl, P.oracle_params())
+    ctx.bacon_begin_prompt(batch)
+    got = ctx.bacon_compress_prompt(0, batch, qs, ks, vs)
+    torch.cuda.synchronize()
+    for l in range(min(2, wl.num_layers)):
+        r = orc.layer(l, xs[l]["q_win"], xs[l]["k"])
+        P.check_idx(f"{name} L{l} prompt call", got[l][0].cpu().numpy(), r, wl, P.RTOL[wl.dtype])
+
+
 @pytest.mark.parametrize("name,streaming", [("tiny-fp32", False), ("ragged-small", False),
                                             ("video-n32768", False), ("ragged-small", True)])
 def test_window_lse(name, streaming, monkeypatch):
