@@ -128,10 +128,11 @@ const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", 
                               "segment_calib", "segment_score", "segment_cand",
                               "final_topk",    "select_calib",  "select_topk",
                               "calib_elem",    "compact",       "window_lse_kr",
-                              "window_score_calib_kr", "window_score_calib_lse_kr"};
+                              "window_score_calib_kr", "window_score_calib_lse_kr",
+                              "segment_calib_lse_merge"};
 enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
                 KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_DUAL_KR,
-                KI_COUNT };
+                KI_SEGCAL_MERGE, KI_COUNT };
 
 }  // namespace
 
@@ -695,18 +696,21 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   // final workgroups per (sequence, KV head): about one round over the CUs
   g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
   TRY(head_table(c, bt, s, &g.hb));
+  PassArgs an{};                 // the next layer's pass 1, when it runs in this layer's launches
+  bool merge_next = false;
   if (kr) {
     if (!d_lse && !lse_merged) {
       TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
       TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
     }
     if (!d_lse && next_q) {
-      // this layer's pass 2 with the next layer's pass 1, then the next
-      // layer's merge (this pass 2 has read the merged normalisers by then)
-      PassArgs an = pass_args(c, st, chunk, next_q, next_k);
+      // this layer's pass 2 with the next layer's pass 1; the next layer's
+      // merge runs in the calibration launch (this pass 2 has read the
+      // merged normalisers by then)
+      an = pass_args(c, st, chunk, next_q, next_k);
       an.T = T;
       TRY(timed(c, KI_DUAL_KR, s, [&] { return launch_krdual(bf16, c->shape.head_dim, w32, a, an, st, s); }));
-      TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(an, st, s); }));
+      merge_next = true;
       if (dual_out) *dual_out = true;
     } else {
       TRY(timed(c, KI_FUSED_KR, s, [&] { return launch_krpass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
@@ -718,7 +722,9 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
     }
     TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
   }
-  TRY(timed(c, KI_SEGCAL, s, [&] { return launch_segcal(g, st, s); }));
+  TRY(timed(c, merge_next ? KI_SEGCAL_MERGE : KI_SEGCAL, s, [&] {
+    return merge_next ? launch_segcal_merge(g, an, st, s) : launch_segcal(g, st, s);
+  }));
   TRY(timed(c, KI_SEGSCORE, s, [&] { return launch_segscore(g, st, s); }));
   TRY(timed(c, KI_SEGCAND, s, [&] { return launch_segcand(g, st, s); }));
   TRY(timed(c, KI_FINAL, s, [&] { return launch_segfinal(g, st, kmax, s); }));

@@ -185,6 +185,9 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
 hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_lse_merge(const PassArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_segcal(const SegArgs &a, const SeqTable &st, hipStream_t s);
+// The same with the next layer's row normalisers merged from m's partials.
+hipError_t launch_segcal_merge(const SegArgs &a, const PassArgs &m, const SeqTable &st,
+                               hipStream_t s);
 hipError_t launch_segscore(const SegArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_segcand(const SegArgs &a, const SeqTable &st, hipStream_t s);
 // LDS of the final workgroup for budgets up to max_budget.

@@ -509,11 +509,13 @@ static hipError_t launch_pass_m(bool bf16, int d, bool w32, const PassArgs &a, c
 // over the chunks congruent to t / 16 (mod 16), kMergeBatch loads in flight
 // per batch; the 16 parts of a row are combined through LDS in a fixed order.
 constexpr int kMergeRows = 16, kMergeParts = 16, kMergeBatch = 8;
-__global__ __launch_bounds__(kMergeRows * kMergeParts) void k_lse_merge(PassArgs a, SeqTable st) {
-  __shared__ float2 mrg[kMergeParts][kMergeRows];
-  const int rg = blockIdx.x, b = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
+constexpr int kMergeThreads = kMergeRows * kMergeParts;
+// Row group rg of (sequence b, KV head h) by the kMergeThreads threads t of
+// one group; `valid` false: the group only takes part in the barrier.
+__device__ __forceinline__ void merge_rows(const PassArgs &a, const SeqTable &st, int rg, int b,
+                                           int h, int t, float2 (*mrg)[kMergeRows], bool valid) {
   const int row = rg * kMergeRows + (t % kMergeRows), part = t / kMergeRows;
-  const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
+  const int nch = valid ? st.chunk_base[b + 1] - st.chunk_base[b] : 0;
   const float2 *pp = a.partials + ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad + row;
   float mm = -INFINITY, ll = 0.f;
   for (int c0 = part; c0 < nch; c0 += kMergeParts * kMergeBatch) {
@@ -537,7 +539,7 @@ __global__ __launch_bounds__(kMergeRows * kMergeParts) void k_lse_merge(PassArgs
   }
   mrg[part][t % kMergeRows] = make_float2(mm, ll);
   __syncthreads();
-  if (t < kMergeRows) {
+  if (valid && t < kMergeRows) {
     float mx = -INFINITY;
     for (int q = 0; q < kMergeParts; ++q) mx = fmaxf(mx, mrg[q][t].x);
     float sx = 0.f;
@@ -555,10 +557,15 @@ __global__ __launch_bounds__(kMergeRows * kMergeParts) void k_lse_merge(PassArgs
   }
 }
 
+__global__ __launch_bounds__(kMergeThreads) void k_lse_merge(PassArgs a, SeqTable st) {
+  __shared__ float2 mrg[kMergeParts][kMergeRows];
+  merge_rows(a, st, blockIdx.x, blockIdx.y, blockIdx.z, threadIdx.x, mrg, true);
+}
+
 hipError_t launch_lse_merge(const PassArgs &a, const SeqTable &st, hipStream_t s) {
   if (a.Rpad % kMergeRows) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_lse_merge, dim3(a.Rpad / kMergeRows, st.batch, a.Hkv),
-                     dim3(kMergeRows * kMergeParts), 0, s, a, st);
+                     dim3(kMergeThreads), 0, s, a, st);
   return hipGetLastError();
 }
 
@@ -1835,13 +1842,13 @@ struct ListView {
 };
 
 // Calibration kernel (segment_calib).
-__global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) {
+__device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st, int gs, int h) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ float Bs[kSegWin], Vs[kSegWin];
   __shared__ float Es[kSegE];
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[PER * NW + 1];
-  const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
+  const int t = threadIdx.x;
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
@@ -1992,6 +1999,29 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   }
   if (t == 0) a.cntB[(int64_t)h * st.total_segs + gs] = (int)pre[PER * NW];
   if (sg == 0 && t == 0) a.recB[b * a.Hkv + h] = make_int4(beta, above, M - above, (int)cntb);
+}
+
+__global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) {
+  segcal_body(a, st, blockIdx.x, blockIdx.y);
+}
+
+// The calibration kernel with the next layer's row normalisers merged by
+// extra workgroups (columns past total_segs; each takes kSegThreads /
+// kMergeThreads row groups of one sequence).  The two jobs share no data;
+// one launch saves a kernel boundary per layer.
+__global__ __launch_bounds__(kSegThreads) void k_segcal_merge(SegArgs a, PassArgs m, SeqTable st) {
+  if ((int)blockIdx.x < st.total_segs) {
+    segcal_body(a, st, blockIdx.x, blockIdx.y);
+    return;
+  }
+  constexpr int groups = kSegThreads / kMergeThreads;
+  __shared__ float2 mrg[groups][kMergeParts][kMergeRows];
+  const int per_seq = (m.Rpad / kMergeRows + groups - 1) / groups;
+  const int q = blockIdx.x - st.total_segs, b = q / per_seq;
+  const int grp = threadIdx.x / kMergeThreads;
+  const int rg = (q - b * per_seq) * groups + grp;
+  merge_rows(m, st, rg, b, blockIdx.y, threadIdx.x % kMergeThreads, mrg[grp],
+             rg * kMergeRows < m.Rpad);
 }
 
 // Loads the selection record and the segments' lists of a (sequence, KV
@@ -2469,6 +2499,16 @@ size_t final_lds_bytes(int max_budget, int window) {
 hipError_t launch_segcal(const SegArgs &a, const SeqTable &st, hipStream_t s) {
   dim3 grid(st.total_segs, a.Hkv), block(kSegThreads);
   hipLaunchKernelGGL(k_segcal, grid, block, 0, s, a, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_segcal_merge(const SegArgs &a, const PassArgs &m, const SeqTable &st,
+                               hipStream_t s) {
+  if (m.Rpad % kMergeRows || m.Hkv != a.Hkv) return hipErrorInvalidValue;
+  constexpr int groups = kSegThreads / kMergeThreads;
+  const int per_seq = (m.Rpad / kMergeRows + groups - 1) / groups;
+  dim3 grid(st.total_segs + st.batch * per_seq, a.Hkv), block(kSegThreads);
+  hipLaunchKernelGGL(k_segcal_merge, grid, block, 0, s, a, m, st);
   return hipGetLastError();
 }
 
