@@ -74,8 +74,11 @@ def kernel_bytes(name, wl, persist_m=4):
         return Hkv * chunks * wl.group * wl.window * 8
     if name == "segment_calib":                         # B, E history in; V, pooled B and V out
         return 4 * vec + ring
-    if name == "segment_calib_lse_merge":               # the same, plus the next layer's partials
-        return 4 * vec + ring + kernel_bytes("lse_merge", wl, persist_m)
+    if name == "segment_calib_cand":                    # calibration, the previous layer's lists,
+        return sum(kernel_bytes(k, wl, persist_m)      # the next layer's normaliser merge
+                   for k in ("segment_calib", "segment_cand", "lse_merge"))
+    if name == "segment_score_final":                   # scores, the previous layer's top-K
+        return sum(kernel_bytes(k, wl, persist_m) for k in ("segment_score", "final_topk"))
     if name == "segment_score":                         # pooled B and V in; score keys out
         return 3 * vec
     if name == "segment_cand":                          # score keys in

@@ -36,7 +36,8 @@ _NAMES = [
     (r"bacon::k_krpass<0,", "window_lse_kr"),
     (r"bacon::k_krpass<2,", "window_score_calib_kr"),
     (r"bacon::k_krdual<", "window_score_calib_lse_kr"),
-    (r"bacon::k_segcal_merge\b", "segment_calib_lse_merge"),
+    (r"bacon::k_sel_a\b", "segment_calib_cand"),
+    (r"bacon::k_sel_b\b", "segment_score_final"),
     (r"bacon::k_segcal\b", "segment_calib"),
     (r"bacon::k_segscore\b", "segment_score"),
     (r"bacon::k_segcand\b", "segment_cand"),

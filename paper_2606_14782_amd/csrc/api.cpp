@@ -38,6 +38,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct Layout {
   size_t ring, vec_b, vec_vp, vec_v, vec_pb, vec_pv, vec_s, hist_b, hist_s, list_bk, list_bp, list_bv,
       list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, hb, total;
+  size_t vec_s_stride, hist_b_stride, hist_s_stride;   // the two copies by layer parity
   int rpad, slots;
   int64_t chunks_cap;
 };
@@ -102,10 +103,13 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.vec_v = off;    off += align256(vec);
   L.vec_pb = off;   off += align256(vec);
   L.vec_pv = off;   off += align256(vec);
-  L.vec_s = off;    off += align256(vec);
+  L.vec_s_stride = align256(vec);
+  L.vec_s = off;    off += 2 * L.vec_s_stride;                 // by layer parity
   const size_t hist = (size_t)s->max_batch * s->num_kv_heads * kHBins * sizeof(unsigned);
-  L.hist_b = off;   off += align256(hist * kHCopies);
-  L.hist_s = off;   off += align256(hist);
+  L.hist_b_stride = align256(hist * kHCopies);
+  L.hist_s_stride = align256(hist);
+  L.hist_b = off;   off += 2 * L.hist_b_stride;                // by layer parity
+  L.hist_s = off;   off += 2 * L.hist_s_stride;
   L.list_bk = off;  off += align256(vec);
   L.list_bp = off;  off += align256(vec);
   L.list_bv = off;  off += align256(vec);
@@ -129,10 +133,10 @@ const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", 
                               "final_topk",    "select_calib",  "select_topk",
                               "calib_elem",    "compact",       "window_lse_kr",
                               "window_score_calib_kr", "window_score_calib_lse_kr",
-                              "segment_calib_lse_merge"};
+                              "segment_calib_cand", "segment_score_final"};
 enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
                 KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_DUAL_KR,
-                KI_SEGCAL_MERGE, KI_COUNT };
+                KI_SEL_A, KI_SEL_B, KI_COUNT };
 
 }  // namespace
 
@@ -468,7 +472,7 @@ bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *strea
   // layer 0 reads no history; the B histogram of the select starts at zero
   // (each layer's final kernel clears it for the next)
   const hipError_t e = launch_zero(reinterpret_cast<unsigned *>(c->ws + c->L.hist_b),
-                                   (int64_t)bt->batch * c->shape.num_kv_heads * kHCopies * kHBins,
+                                   (int64_t)(2 * c->L.hist_b_stride / sizeof(unsigned)),
                                    static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "clear");
   c->prompt = true;
@@ -603,22 +607,27 @@ bacon_status bacon_compact(bacon_ctx *c, const bacon_batch *bt, const void *d_k,
 
 namespace {
 
-// The fused pass of one layer; d_lse (caller normalisers) skips pass 1.
-// Within a prompt call: lse_merged says that pass 1 of this layer already ran
-// (with the previous layer's pass 2) and its normalisers are merged; next_q
-// and next_k, when not NULL, are the next layer's inputs, whose pass 1 then
-// runs in the launch of this layer's pass 2.  *dual_out reports whether it did.
-bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
-                      const void *d_k, const void *d_v, const float *d_lse, int32_t *d_idx,
-                      void *d_k_out, void *d_v_out, void *stream, bool lse_merged = false,
-                      const void *next_q = nullptr, const void *next_k = nullptr,
-                      bool *dual_out = nullptr) {
-  if (dual_out) *dual_out = false;
-  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+// Everything the launches of one layer of the fused pass need.
+struct LayerRun {
+  int layer = 0;
+  bool bf16 = false, w32 = false, kr = false;
+  int chunk = 0, kmax = 0;
+  SeqTable st{};
+  PassArgs a{};
+  SegArgs g{};
+  const float *lse = nullptr;   // caller normalisers (pass 1 skipped)
+};
+
+// Checks one layer's arguments and builds its launch arguments; enqueues
+// nothing.  The layer order is the caller's to check.  Buffers that a layer
+// of the next pair may write while this layer's select is still in flight
+// (the B and S histograms and the score keys) alternate with the layer's
+// parity.
+bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
+                        const void *d_k, const void *d_v, const float *d_lse, int32_t *d_idx,
+                        void *d_k_out, void *d_v_out, LayerRun &r) {
   TRY(check_batch(c, bt));
   TRY(check_prompt_batch(c, bt));
-  if (layer != c->next_layer)
-    return fail(BACON_ERR_ORDER, "layer %d given, layer %d expected next", layer, c->next_layer);
   if (layer >= c->shape.num_layers)
     return fail(BACON_ERR_ORDER, "layer %d beyond num_layers %d", layer, c->shape.num_layers);
   TRY(check_ptr(d_q_win, "q_win", 16));
@@ -627,38 +636,41 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   TRY(check_ptr(d_idx, "idx", 4));
   TRY(check_ptr(d_k_out, "k_out", 16));
   TRY(check_ptr(d_v_out, "v_out", 16));
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const bool bf16 = c->shape.dtype == BACON_BF16;
-  const bool w32 = c->shape.window == 32;
-  int chunk = 0;
-  SeqTable st{};
+  r.layer = layer;
+  r.lse = d_lse;
+  r.bf16 = c->shape.dtype == BACON_BF16;
+  r.w32 = c->shape.window == 32;
   // key-register passes where they cover the shape, else the streaming passes
-  const bool kr = !c->kr_off && kr_supported(bf16, c->shape.head_dim, c->L.rpad);
-  if (kr) {
-    st = make_table(c, bt, &chunk, false, kr_keys(bf16, c->shape.head_dim));
+  r.kr = !c->kr_off && kr_supported(r.bf16, c->shape.head_dim, c->L.rpad);
+  if (r.kr) {
+    r.st = make_table(c, bt, &r.chunk, false, kr_keys(r.bf16, c->shape.head_dim));
   } else {
-    st = make_table(c, bt, &chunk, false);
-    TRY(check_lds(c, bt, chunk, true, -1));
+    r.st = make_table(c, bt, &r.chunk, false);
+    TRY(check_lds(c, bt, r.chunk, true, -1));
   }
-  int kmax = 0;
-  for (int b = 0; b < bt->batch; ++b) kmax = std::max(kmax, batch_seq_rows(bt, c->shape.num_kv_heads, b));
-  if (final_lds_bytes(kmax, c->shape.window) > (size_t)kLdsBytes)
-    return fail(BACON_ERR_UNSUPPORTED, "budget %d needs more LDS than a CU has", kmax);
+  r.kmax = 0;
+  for (int b = 0; b < bt->batch; ++b) r.kmax = std::max(r.kmax, batch_seq_rows(bt, c->shape.num_kv_heads, b));
+  if (final_lds_bytes(r.kmax, c->shape.window) > (size_t)kLdsBytes)
+    return fail(BACON_ERR_UNSUPPORTED, "budget %d needs more LDS than a CU has", r.kmax);
+  const int par = layer & 1;
   const int64_t T = bt->cu_seqlens[bt->batch];
-  PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
+  PassArgs &a = r.a;
+  a = pass_args(c, r.st, r.chunk, d_q_win, d_k);
   a.T = T;
   a.lse_in = d_lse;
+  a.hist_B += (size_t)par * c->L.hist_b_stride / sizeof(unsigned);
   int ring_cnt = 0;
   ring_slots(c, layer, &a.ring_write, &ring_cnt);
   a.ring_stride = (int64_t)c->shape.num_kv_heads * T;
-  SegArgs g{};
+  SegArgs &g = r.g;
+  g = SegArgs{};
   g.Hkv = c->shape.num_kv_heads;
   g.W = c->shape.window;
   g.T = T;
   g.radius = c->params.radius;
   g.pool_half = c->params.pool_kernel / 2;
   g.pool_mode = c->params.pool_mode;
-  g.vp_chunk = chunk;
+  g.vp_chunk = r.chunk;
   g.rho = c->params.rho;
   g.gamma = c->params.gamma;
   g.eps = c->params.eps;
@@ -674,9 +686,9 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   g.vec_V = reinterpret_cast<float *>(c->ws + c->L.vec_v);
   g.vec_pB = reinterpret_cast<float *>(c->ws + c->L.vec_pb);
   g.vec_pV = reinterpret_cast<float *>(c->ws + c->L.vec_pv);
-  g.vec_S = reinterpret_cast<unsigned *>(c->ws + c->L.vec_s);
+  g.vec_S = reinterpret_cast<unsigned *>(c->ws + c->L.vec_s + (size_t)par * c->L.vec_s_stride);
   g.hist_B = a.hist_B;
-  g.hist_S = reinterpret_cast<unsigned *>(c->ws + c->L.hist_s);
+  g.hist_S = reinterpret_cast<unsigned *>(c->ws + c->L.hist_s + (size_t)par * c->L.hist_s_stride);
   g.listB_key = reinterpret_cast<unsigned *>(c->ws + c->L.list_bk);
   g.listB_pos = reinterpret_cast<int *>(c->ws + c->L.list_bp);
   g.listB_v = reinterpret_cast<float *>(c->ws + c->L.list_bv);
@@ -692,42 +704,71 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   g.v = d_v;
   g.k_out = d_k_out;
   g.v_out = d_v_out;
-  g.row_bytes = c->shape.head_dim * (bf16 ? 2 : 4);
+  g.row_bytes = c->shape.head_dim * (r.bf16 ? 2 : 4);
   // final workgroups per (sequence, KV head): about one round over the CUs
   g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
-  TRY(head_table(c, bt, s, &g.hb));
-  PassArgs an{};                 // the next layer's pass 1, when it runs in this layer's launches
-  bool merge_next = false;
-  if (kr) {
-    if (!d_lse && !lse_merged) {
-      TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
-      TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+  return BACON_OK;
+}
+
+// The K passes of a layer.  lse_merged: its pass 1 ran with the previous
+// layer's pass 2 and its normalisers are merged.  next (NULL or the next
+// layer's pass 1 arguments): that pass 1 runs in this layer's pass-2 launch.
+bacon_status stage_pass(bacon_ctx *c, const LayerRun &r, bool lse_merged, const PassArgs *next,
+                        hipStream_t s) {
+  const int d = c->shape.head_dim;
+  if (r.kr) {
+    if (!r.lse && !lse_merged) {
+      TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, r.bf16, d, false, r.a, r.st, s); }));
+      TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(r.a, r.st, s); }));
     }
-    if (!d_lse && next_q) {
-      // this layer's pass 2 with the next layer's pass 1; the next layer's
-      // merge runs in the calibration launch (this pass 2 has read the
-      // merged normalisers by then)
-      an = pass_args(c, st, chunk, next_q, next_k);
-      an.T = T;
-      TRY(timed(c, KI_DUAL_KR, s, [&] { return launch_krdual(bf16, c->shape.head_dim, w32, a, an, st, s); }));
-      merge_next = true;
-      if (dual_out) *dual_out = true;
-    } else {
-      TRY(timed(c, KI_FUSED_KR, s, [&] { return launch_krpass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
-    }
-  } else {
-    if (!d_lse) {
-      TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
-      TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
-    }
-    TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, bf16, c->shape.head_dim, w32, a, st, s); }));
+    if (next)
+      return timed(c, KI_DUAL_KR, s, [&] { return launch_krdual(r.bf16, d, r.w32, r.a, *next, r.st, s); });
+    return timed(c, KI_FUSED_KR, s, [&] { return launch_krpass(PASS_FUSED, r.bf16, d, r.w32, r.a, r.st, s); });
   }
-  TRY(timed(c, merge_next ? KI_SEGCAL_MERGE : KI_SEGCAL, s, [&] {
-    return merge_next ? launch_segcal_merge(g, an, st, s) : launch_segcal(g, st, s);
-  }));
-  TRY(timed(c, KI_SEGSCORE, s, [&] { return launch_segscore(g, st, s); }));
-  TRY(timed(c, KI_SEGCAND, s, [&] { return launch_segcand(g, st, s); }));
-  TRY(timed(c, KI_FINAL, s, [&] { return launch_segfinal(g, st, kmax, s); }));
+  if (!r.lse) {
+    TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, r.bf16, d, false, r.a, r.st, s); }));
+    TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(r.a, r.st, s); }));
+  }
+  return timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, r.bf16, d, r.w32, r.a, r.st, s); });
+}
+
+// Calibration of r's layer, with the previous layer's candidate lists and the
+// next layer's row normalisers in the same launch when given.
+bacon_status stage_a(bacon_ctx *c, const LayerRun &r, const LayerRun *prev, const PassArgs *next,
+                     hipStream_t s) {
+  if (!prev && !next) return timed(c, KI_SEGCAL, s, [&] { return launch_segcal(r.g, r.st, s); });
+  return timed(c, KI_SEL_A, s, [&] {
+    return launch_sel_a(r.g, prev ? &prev->g : nullptr, next, r.st, s);
+  });
+}
+
+// Scores of r's layer, with the previous layer's final top-K and compaction.
+bacon_status stage_b(bacon_ctx *c, const LayerRun &r, const LayerRun *prev, hipStream_t s) {
+  if (!prev) return timed(c, KI_SEGSCORE, s, [&] { return launch_segscore(r.g, r.st, s); });
+  return timed(c, KI_SEL_B, s, [&] { return launch_sel_b(r.g, &prev->g, r.st, prev->kmax, s); });
+}
+
+// Candidate lists, final top-K and compaction of r's layer.
+bacon_status stage_tail(bacon_ctx *c, const LayerRun &r, hipStream_t s) {
+  TRY(timed(c, KI_SEGCAND, s, [&] { return launch_segcand(r.g, r.st, s); }));
+  return timed(c, KI_FINAL, s, [&] { return launch_segfinal(r.g, r.st, r.kmax, s); });
+}
+
+// The fused pass of one layer; d_lse (caller normalisers) skips pass 1.
+bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
+                      const void *d_k, const void *d_v, const float *d_lse, int32_t *d_idx,
+                      void *d_k_out, void *d_v_out, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  if (layer != c->next_layer)
+    return fail(BACON_ERR_ORDER, "layer %d given, layer %d expected next", layer, c->next_layer);
+  LayerRun r;
+  TRY(plan_layer(c, layer, bt, d_q_win, d_k, d_v, d_lse, d_idx, d_k_out, d_v_out, r));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  TRY(head_table(c, bt, s, &r.g.hb));
+  TRY(stage_pass(c, r, false, nullptr, s));
+  TRY(stage_a(c, r, nullptr, nullptr, s));
+  TRY(stage_b(c, r, nullptr, s));
+  TRY(stage_tail(c, r, s));
   c->next_layer = layer + 1;
   return BACON_OK;
 }
@@ -775,15 +816,33 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
     TRY(check_ptr(d_v_out[i], "v_out", 16));
     if (d_lse) TRY(check_ptr(d_lse[i], "lse", 4));
   }
+  // every layer is planned (and checked) before the first launch
+  std::vector<LayerRun> runs(num_layers);
+  for (int i = 0; i < num_layers; ++i)
+    TRY(plan_layer(c, first_layer + i, bt, d_q_win[i], d_k[i], d_v[i], d_lse ? d_lse[i] : nullptr,
+                   d_idx[i], d_k_out[i], d_v_out[i], runs[i]));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int2 *hb = nullptr;
+  TRY(head_table(c, bt, s, &hb));
+  for (LayerRun &r : runs) r.g.hb = hb;
+  // Layers in flight at once: layer l's candidate lists run in the launch of
+  // layer l+1's calibration, its final top-K and compaction in the launch of
+  // layer l+1's scores (when that launch's LDS fits), and layer l+1's pass 1
+  // in the launch of layer l's pass 2.
+  const bool overlap = sel_b_lds_bytes(runs[0].kmax, c->shape.window) <= (size_t)kLdsBytes;
   bool merged = false;
   for (int i = 0; i < num_layers; ++i) {
-    const bool more = i + 1 < num_layers && !d_lse;
-    bool dual = false;
-    TRY(compress(c, first_layer + i, bt, d_q_win[i], d_k[i], d_v[i], d_lse ? d_lse[i] : nullptr,
-                 d_idx[i], d_k_out[i], d_v_out[i], stream, merged,
-                 more ? d_q_win[i + 1] : nullptr, more ? d_k[i + 1] : nullptr, &dual));
-    merged = dual;
+    const LayerRun &r = runs[i];
+    const LayerRun *prev = (overlap && i > 0) ? &runs[i - 1] : nullptr;
+    const PassArgs *next = (r.kr && !r.lse && i + 1 < num_layers) ? &runs[i + 1].a : nullptr;
+    TRY(stage_pass(c, r, merged, next, s));
+    TRY(stage_a(c, r, prev, next, s));
+    TRY(stage_b(c, r, prev, s));
+    if (!overlap) TRY(stage_tail(c, r, s));
+    merged = next != nullptr;
+    c->next_layer = r.layer + 1;
   }
+  if (overlap) TRY(stage_tail(c, runs[num_layers - 1], s));
   return BACON_OK;
 }
 

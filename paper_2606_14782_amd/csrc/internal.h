@@ -185,9 +185,16 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
 hipError_t launch_elem(const ElemArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_lse_merge(const PassArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_segcal(const SegArgs &a, const SeqTable &st, hipStream_t s);
-// The same with the next layer's row normalisers merged from m's partials.
-hipError_t launch_segcal_merge(const SegArgs &a, const PassArgs &m, const SeqTable &st,
-                               hipStream_t s);
+// Launches with work of two or three layers of a prompt: the calibration of
+// g's layer with the previous layer's candidate lists (gp, may be NULL) and
+// the next layer's row normalisers (m, may be NULL); the scores of g's layer
+// with the previous layer's final top-K and compaction (gp, may be NULL).
+hipError_t launch_sel_a(const SegArgs &g, const SegArgs *gp, const PassArgs *m, const SeqTable &st,
+                       hipStream_t s);
+hipError_t launch_sel_b(const SegArgs &g, const SegArgs *gp, const SeqTable &st, int max_budget,
+                        hipStream_t s);
+// LDS of a k_sel_b workgroup (static of both jobs plus the row table).
+size_t sel_b_lds_bytes(int max_budget, int window);
 hipError_t launch_segscore(const SegArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_segcand(const SegArgs &a, const SeqTable &st, hipStream_t s);
 // LDS of the final workgroup for budgets up to max_budget.

@@ -2005,25 +2005,6 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
   segcal_body(a, st, blockIdx.x, blockIdx.y);
 }
 
-// The calibration kernel with the next layer's row normalisers merged by
-// extra workgroups (columns past total_segs; each takes kSegThreads /
-// kMergeThreads row groups of one sequence).  The two jobs share no data;
-// one launch saves a kernel boundary per layer.
-__global__ __launch_bounds__(kSegThreads) void k_segcal_merge(SegArgs a, PassArgs m, SeqTable st) {
-  if ((int)blockIdx.x < st.total_segs) {
-    segcal_body(a, st, blockIdx.x, blockIdx.y);
-    return;
-  }
-  constexpr int groups = kSegThreads / kMergeThreads;
-  __shared__ float2 mrg[groups][kMergeParts][kMergeRows];
-  const int per_seq = (m.Rpad / kMergeRows + groups - 1) / groups;
-  const int q = blockIdx.x - st.total_segs, b = q / per_seq;
-  const int grp = threadIdx.x / kMergeThreads;
-  const int rg = (q - b * per_seq) * groups + grp;
-  merge_rows(m, st, rg, b, blockIdx.y, threadIdx.x % kMergeThreads, mrg[grp],
-             rg * kMergeRows < m.Rpad);
-}
-
 // Loads the selection record and the segments' lists of a (sequence, KV
 // head) into registers as one sequence of entries e = t + j*NT in (segment,
 // slot) order, which is position order.  First round: kListSpec slots per
@@ -2148,7 +2129,9 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
 }
 
 // Score kernel (segment_score).
-__global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st) {
+// (The select bodies take their arguments by value: a reference to a kernel
+// argument that reaches an out-of-line call costs a stack copy and spills.)
+__device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int gs, int h) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ unsigned hist[kHBins];
   __shared__ unsigned ckey[kCandCap];
@@ -2157,7 +2140,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
   __shared__ unsigned pre[kAllPer * NW + 1];
   __shared__ float2 mom[kMomChunk];
   __shared__ __align__(16) int scnt[kMaxSegs];
-  const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
+  const int t = threadIdx.x;
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
@@ -2288,11 +2271,11 @@ __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st
 
 // Candidate kernel (segment_cand): the boundary bin of the top-K of the
 // pooled score and the segment's list of entries at or above it.
-__global__ __launch_bounds__(kSegThreads) void k_segcand(SegArgs a, SeqTable st) {
+__device__ __forceinline__ void segcand_body(SegArgs a, const SeqTable &st, int gs, int h) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[PER * NW + 1];
-  const int t = threadIdx.x, h = blockIdx.y, gs = blockIdx.x;
+  const int t = threadIdx.x;
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
@@ -2377,7 +2360,8 @@ __device__ __attribute__((noinline)) void whole_topk(const SegArgs &a, int64_t b
 // select the same top-K; part 0 writes the indices, each part gathers its
 // share of the compacted rows (kept positions, the W window rows, zero rows
 // up to K + W).
-__global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st) {
+__device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int part, int b,
+                                           int h) {
   constexpr int NT = kSegThreads, NW = NT / 64;
   extern __shared__ __align__(16) int tbl[];         // [K + W] source position of each row
   __shared__ unsigned ckey[kCandCap];
@@ -2385,7 +2369,7 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[kAllPer * NW + 1];
   __shared__ __align__(16) int scnt[kMaxSegs];
-  const int part = blockIdx.x, b = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
+  const int t = threadIdx.x;
   const int wave = t >> 6;
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
@@ -2490,6 +2474,54 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
   }
 }
 
+__global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st) {
+  segscore_body(a, st, blockIdx.x, blockIdx.y);
+}
+
+__global__ __launch_bounds__(kSegThreads) void k_segcand(SegArgs a, SeqTable st) {
+  segcand_body(a, st, blockIdx.x, blockIdx.y);
+}
+
+__global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st) {
+  final_body(a, st, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// Launches that carry work of two or three layers (a prompt's layers in
+// flight at once; the jobs of one launch share no buffer, see the host's
+// schedule).  Columns of workgroups, per KV head (blockIdx.y):
+//  * k_sel_a: [0, ncand) the candidate lists of the previous layer (gp),
+//    [ncand, ncand + nmerge) the next layer's row normalisers (m; each
+//    workgroup takes kSegThreads / kMergeThreads row groups of a sequence),
+//    then the calibration of this layer (g).  The short jobs come first, so
+//    that they hold CUs only briefly.
+//  * k_sel_b: [0, nfinal) the final top-K and compaction of the previous
+//    layer (parts per sequence), then the scores of this layer.
+__global__ __launch_bounds__(kSegThreads) void k_sel_a(SegArgs g, SegArgs gp, PassArgs m, SeqTable st,
+                                                      int ncand, int nmerge) {
+  const int x = blockIdx.x, h = blockIdx.y;
+  if (x < ncand) {
+    segcand_body(gp, st, x, h);
+  } else if (x < ncand + nmerge) {
+    constexpr int groups = kSegThreads / kMergeThreads;
+    __shared__ float2 mrg[groups][kMergeParts][kMergeRows];
+    const int per_seq = (m.Rpad / kMergeRows + groups - 1) / groups;
+    const int q = x - ncand, b = q / per_seq;
+    const int grp = threadIdx.x / kMergeThreads;
+    const int rg = (q - b * per_seq) * groups + grp;
+    merge_rows(m, st, rg, b, h, threadIdx.x % kMergeThreads, mrg[grp], rg * kMergeRows < m.Rpad);
+  } else {
+    segcal_body(g, st, x - ncand - nmerge, h);
+  }
+}
+
+__global__ __launch_bounds__(kSegThreads) void k_sel_b(SegArgs g, SegArgs gp, SeqTable st, int nfinal) {
+  const int x = blockIdx.x, h = blockIdx.y;
+  if (x < nfinal)
+    final_body(gp, st, x % gp.parts, x / gp.parts, h);
+  else
+    segscore_body(g, st, x - nfinal, h);
+}
+
 size_t final_lds_bytes(int max_budget, int window) {
   return (size_t)(max_budget + window) * sizeof(int) + 2 * kCandCap * sizeof(unsigned) +
          sizeof(SelSharedT<kSegThreads>) + (kAllPer * (kSegThreads / 64) + 1) * sizeof(unsigned) +
@@ -2502,13 +2534,36 @@ hipError_t launch_segcal(const SegArgs &a, const SeqTable &st, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_segcal_merge(const SegArgs &a, const PassArgs &m, const SeqTable &st,
-                               hipStream_t s) {
-  if (m.Rpad % kMergeRows || m.Hkv != a.Hkv) return hipErrorInvalidValue;
+hipError_t launch_sel_a(const SegArgs &g, const SegArgs *gp, const PassArgs *m, const SeqTable &st,
+                       hipStream_t s) {
   constexpr int groups = kSegThreads / kMergeThreads;
-  const int per_seq = (m.Rpad / kMergeRows + groups - 1) / groups;
-  dim3 grid(st.total_segs + st.batch * per_seq, a.Hkv), block(kSegThreads);
-  hipLaunchKernelGGL(k_segcal_merge, grid, block, 0, s, a, m, st);
+  int nmerge = 0;
+  if (m) {
+    if (m->Rpad % kMergeRows || m->Hkv != g.Hkv) return hipErrorInvalidValue;
+    nmerge = st.batch * ((m->Rpad / kMergeRows + groups - 1) / groups);
+  }
+  const int ncand = gp ? st.total_segs : 0;
+  dim3 grid(ncand + nmerge + st.total_segs, g.Hkv), block(kSegThreads);
+  hipLaunchKernelGGL(k_sel_a, grid, block, 0, s, g, gp ? *gp : g, m ? *m : PassArgs{}, st, ncand,
+                     nmerge);
+  return hipGetLastError();
+}
+
+size_t sel_b_lds_bytes(int max_budget, int window) {
+  hipFuncAttributes fa{};
+  if (hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(k_sel_b)) != hipSuccess) return SIZE_MAX;
+  return fa.sharedSizeBytes + (size_t)(max_budget + window) * sizeof(int);
+}
+
+hipError_t launch_sel_b(const SegArgs &g, const SegArgs *gp, const SeqTable &st, int max_budget,
+                        hipStream_t s) {
+  const size_t lds = gp ? (size_t)(max_budget + g.W) * sizeof(int) : 0;
+  if (gp && (sel_b_lds_bytes(max_budget, g.W) > (size_t)kLdsBytes || gp->parts < 1))
+    return hipErrorInvalidValue;
+  const int nfinal = gp ? gp->parts * st.batch : 0;
+  allow_lds(k_sel_b, lds);
+  hipLaunchKernelGGL(k_sel_b, dim3(nfinal + st.total_segs, g.Hkv), dim3(kSegThreads), lds, s, g,
+                     gp ? *gp : g, st, nfinal);
   return hipGetLastError();
 }
 
