@@ -187,6 +187,43 @@ def test_prompt_call_equals_layer_calls(name):
         P.check_idx(f"{name} L{l} prompt call", got[l][0].cpu().numpy(), r, wl, P.RTOL[wl.dtype])
 
 
+PROMPT_VARIANTS = [
+    ("max of S", {"pool_mode": 1}),
+    ("mean of B", {"pool_mode": 2}),
+    ("S = B", {"use_last_query": 0}),
+    ("radius 0, m 0", {"radius": 0, "persist_m": 0}),
+    ("m 8, terms E+T", {"persist_m": 8, "terms": 5}),
+]
+
+
+@pytest.mark.parametrize("variant", range(len(PROMPT_VARIANTS)), ids=[v[0] for v in PROMPT_VARIANTS])
+def test_prompt_call_variants(variant):
+    """The prompt call equals the per-layer calls bit for bit under other
+    pooling, evidence and persistence settings, and with a budget per
+    (sequence, KV head); the variants read other buffers in the select."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    _, kw = PROMPT_VARIANTS[variant]
+    wl = CASES["ragged-small"]().with_(num_layers=4)
+    rng = np.random.default_rng(5 + variant)
+    hb = rng.integers(1, 2 * max(wl.budgets) + 1, size=(wl.batch, wl.num_kv_heads)).astype(np.int32)
+    for batch in (bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr),
+                  bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr, head_budgets=hb)):
+        xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+        qs = [P.to_dev(x["q_win"], wl) for x in xs]
+        ks = [P.to_dev(x["k"], wl) for x in xs]
+        vs = [P.to_dev(x["v"], wl) for x in xs]
+        a, b = P.make_ctx(wl, P.params_for(wl, **kw)), P.make_ctx(wl, P.params_for(wl, **kw))
+        a.bacon_begin_prompt(batch)
+        want = [a.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l]) for l in range(wl.num_layers)]
+        b.bacon_begin_prompt(batch)
+        got = b.bacon_compress_prompt(0, batch, qs, ks, vs)
+        torch.cuda.synchronize()
+        for l in range(wl.num_layers):
+            for i, what in enumerate(("idx", "k_out", "v_out")):
+                assert torch.equal(got[l][i], want[l][i]), f"{PROMPT_VARIANTS[variant][0]} L{l} {what}"
+
+
 @pytest.mark.parametrize("name,streaming", [("tiny-fp32", False), ("ragged-small", False),
                                             ("video-n32768", False), ("ragged-small", True)])
 def test_window_lse(name, streaming, monkeypatch):
