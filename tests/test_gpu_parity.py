@@ -187,6 +187,32 @@ def test_prompt_call_equals_layer_calls(name):
         P.check_idx(f"{name} L{l} prompt call", got[l][0].cpu().numpy(), r, wl, P.RTOL[wl.dtype])
 
 
+def test_prompt_calls_mix_with_layer_calls():
+    """Prompt calls and per-layer calls in one prompt (layers 0-1 in a prompt
+    call, 2 alone, 3 alone in a prompt call, 4 per layer) give the per-layer
+    outputs: the history and the parity buffers carry over between them."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = CASES["video-small"]().with_(num_layers=5)
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+    qs = [P.to_dev(x["q_win"], wl) for x in xs]
+    ks = [P.to_dev(x["k"], wl) for x in xs]
+    vs = [P.to_dev(x["v"], wl) for x in xs]
+    a, b = P.make_ctx(wl), P.make_ctx(wl)
+    a.bacon_begin_prompt(batch)
+    want = [a.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l]) for l in range(wl.num_layers)]
+    b.bacon_begin_prompt(batch)
+    got = b.bacon_compress_prompt(0, batch, qs[:2], ks[:2], vs[:2])
+    got.append(b.bacon_compress_layer(2, batch, qs[2], ks[2], vs[2]))
+    got += b.bacon_compress_prompt(3, batch, qs[3:4], ks[3:4], vs[3:4])
+    got.append(b.bacon_compress_layer(4, batch, qs[4], ks[4], vs[4]))
+    torch.cuda.synchronize()
+    for l in range(wl.num_layers):
+        for i, what in enumerate(("idx", "k_out", "v_out")):
+            assert torch.equal(got[l][i], want[l][i]), f"layer {l} {what}"
+
+
 PROMPT_VARIANTS = [
     ("max of S", {"pool_mode": 1}),
     ("mean of B", {"pool_mode": 2}),
