@@ -821,11 +821,9 @@ __device__ __forceinline__ void krpass_body(const PassArgs &a, const SeqTable &s
       const int kbase = k0 + (wave * KT + kt) * 32, key = kbase + l32;
       const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
       float bsum = 0.f, qsum = 0.f;
-#pragma unroll
-      for (int j0 = 0; j0 < NRT; j0 += RG) {
-        // the starting values are read again for every group (opaque offset):
-        // held across the tiles they would take 16 * NRT registers
-        f32x16 acc[RG];
+      // the starting values are read again for every group (opaque offset):
+      // held across the tiles they would take 16 * NRT registers
+      auto seed = [&](int j0, f32x16 *acc) {
         const float *nb = nlc + opaque(4 * half);
 #pragma unroll
         for (int j = 0; j < RG; ++j) {
@@ -838,8 +836,9 @@ __device__ __forceinline__ void krpass_body(const PassArgs &a, const SeqTable &s
             acc[j][4 * i + 3] = v.w;
           }
         }
-        tiles(kt, j0, acc, false);
-        // acc[j][reg]: row (j0+j)*32 + acc_row(reg, half), key kbase + l32
+      };
+      // acc[j][reg]: row (j0+j)*32 + acc_row(reg, half), key kbase + l32
+      auto post = [&](int j0, const f32x16 *acc) {
 #pragma unroll
         for (int j = 0; j < RG; ++j) {
           float p[16];
@@ -860,6 +859,25 @@ __device__ __forceinline__ void krpass_body(const PassArgs &a, const SeqTable &s
 #pragma unroll
             for (int reg = 0; reg < 16; ++reg) qsum += ((lastm[j0 + j] >> reg) & 1u) ? p[reg] : 0.f;
           }
+        }
+      };
+      if constexpr (NRT == 2 * RG && W32) {
+        // both groups' MFMAs issued before the first group's exps and sums,
+        // which then run while the matrix unit works on the second group
+        f32x16 acc0[RG], acc1[RG];
+        seed(0, acc0);
+        tiles(kt, 0, acc0, false);
+        seed(RG, acc1);
+        tiles(kt, RG, acc1, false);
+        post(0, acc0);
+        post(RG, acc1);
+      } else {
+#pragma unroll
+        for (int j0 = 0; j0 < NRT; j0 += RG) {
+          f32x16 acc[RG];
+          seed(j0, acc);
+          tiles(kt, j0, acc, false);
+          post(j0, acc);
         }
       }
       // E to the history and B out; half h of a wave writes the key tiles of
