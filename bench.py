@@ -105,6 +105,21 @@ def measured_traffic(kernel):
     return None if k is None else float(k["bytes_per_launch"])
 
 
+def median_step_ms(fn, steps):
+    """Median duration of `steps` calls of fn, each bracketed by HIP events on
+    the current stream (no host synchronisation between calls)."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return float(np.median([e0.elapsed_time(e1) for e0, e1 in evs]))
+
+
 def cpu_baseline(wl, budget_s, gpu_idx=None):
     """The fp64 oracle on this host, on layers 0.. of the same workload until
     about budget_s seconds have been spent (layers run in order)."""
@@ -125,17 +140,38 @@ def cpu_baseline(wl, budget_s, gpu_idx=None):
             agree = agree and bool(np.array_equal(r["idx"], gpu_idx[layers]))
         layers += 1
     keys = wl.total_tokens * wl.num_kv_heads * layers
+    # the same oracle on one thread, on the first layer of a fresh prompt
+    ref.set_threads(1)
+    p1 = ref.Prompt.for_workload(wl)
+    x = inputs.layer_inputs(wl, 0)
+    t0 = time.perf_counter()
+    p1.layer(0, x["q_win"], x["k"])
+    one = time.perf_counter() - t0
+    ref.set_threads(threads)
     return {"value": keys / spent, "unit": "keys/s", "cores": used, "kind": "oracle",
             "sample": f"layers 0-{layers - 1} of the {wl.num_layers}-layer workload "
                       f"({spent:.1f} s, OpenMP over (sequence, KV head))",
             "ms_per_layer": 1e3 * spent / layers,
+            "one_thread": {"value": wl.total_tokens * wl.num_kv_heads / one, "unit": "keys/s",
+                           "ms_per_layer": 1e3 * one, "sample": "layer 0"},
+            "cpu_model": _cpu_model(),
             "kept_sets_identical_to_gpu": agree if gpu_idx is not None else None}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3, help="workload index (default: 32K video)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -203,13 +239,32 @@ def main():
     gpu_idx = [o[0].cpu().numpy() for o in outs[:8]]
 
     log(f"timing {args.steps} steps")
+    # each step bracketed by events on the stream (no host sync between
+    # steps); the headline is the median step, the wall clock is kept beside it
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for e0, e1 in evs:
+        e0.record()
         step()
+        e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_step = 1e3 * wall / args.steps
+    step_ms = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    ms_step = float(np.median(step_ms))
+    ms_step_wall = 1e3 * wall / args.steps
+
+    # one layer alone (a fresh prompt's layer 0), host-synchronised: latency
+    single = []
+    for _ in range(20):
+        ctx.bacon_begin_prompt(batch)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        ctx.bacon_compress_layer(0, batch, qs[0], ks[0], vs[0], out=outs[0])
+        torch.cuda.synchronize()
+        single.append(time.perf_counter() - t1)
+    single_us = 1e6 * float(np.median(single))
 
     # Same region again with HIP events around every launch (on the pass's stream).
     ctx.bacon_profile_enable(True)
@@ -230,12 +285,7 @@ def main():
     # scoring launch), for comparison.
     for _ in range(args.warmup):
         step_layers()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step_layers()
-    torch.cuda.synchronize()
-    ms_step_layers = 1e3 * (time.perf_counter() - t0) / args.steps
+    ms_step_layers = median_step_ms(step_layers, args.steps)
 
     # The same pass with the window-row normalisers supplied, as a prefill
     # attention that returns its softmax normalisers would (the first K pass and
@@ -252,12 +302,7 @@ def main():
 
     for _ in range(args.warmup):
         step_lse()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step_lse()
-    torch.cuda.synchronize()
-    ms_step_lse = 1e3 * (time.perf_counter() - t0) / args.steps
+    ms_step_lse = median_step_ms(step_lse, args.steps)
 
     ab = algorithmic_bytes(wl)
     ms_layer = ms_step / wl.num_layers
@@ -273,6 +318,12 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_step,
         "ms_per_layer": ms_layer,
+        "ms_per_step_wall_mean": ms_step_wall,
+        "timing": f"median of {args.steps} prompt steps, each bracketed by HIP events on the "
+                  f"pass's stream (one stream)",
+        "qk_scores_per_s": wl.num_q_heads * wl.window * wl.total_tokens * wl.num_layers
+                           / (ms_step * 1e-3),
+        "single_layer_us": single_us,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
