@@ -1271,6 +1271,41 @@ __device__ __forceinline__ void rank_pick(int C, int need, const unsigned *ckey,
   lds_barrier();
 }
 
+// The need-th entry (1-based) of C <= NT listed entries that share key bits
+// 31..18 (one bin of the select histograms), under the tie rule.  Up to
+// kRankDirect entries are ranked directly (each against all others, a cost
+// that grows with C^2); more are first narrowed to their sub-bin of key bits
+// 17..7 by one LDS histogram round, and only that sub-bin is ranked.  The
+// list (ckey, cpos) is overwritten.
+constexpr int kRankDirect = 192;
+template <int NT>
+__device__ __forceinline__ void rank_pick_bin(int C, int need, unsigned *ckey, int *cpos,
+                                              SelSharedT<NT> &ss, unsigned &xk, int &pthr) {
+  if (C <= kRankDirect) {
+    rank_pick<NT>(C, need, ckey, cpos, ss, xk, pthr);
+    return;
+  }
+  const int t = threadIdx.x;
+  for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
+  unsigned k = 0;
+  int p = 0;
+  if (t < C) {
+    k = ckey[t];
+    p = cpos[t];
+  }
+  const unsigned sub = (k >> 7) & (unsigned)(kHistBins - 1);
+  lds_barrier();
+  if (t < C) atomicAdd(&ss.hist[sub], 1u);
+  lds_barrier();
+  hist_boundary<NT>(need, ss);
+  const unsigned s2 = (unsigned)ss.bc_i[0];
+  const int need2 = need - ss.bc_i[1];
+  const int C2 = (int)ss.bc_u[2];
+  compact_ballot<1, NT>([&](int) { return t < C && sub == s2; }, [&](int) { return k; },
+                        [&](int) { return p; }, ckey, cpos, ss);
+  rank_pick<NT>(C2, need2, ckey, cpos, ss, xk, pthr);
+}
+
 // k-th largest key among the block's non-zero keys (1 <= k <= count), by
 // MSB-first 11-bit histogram narrowing of the candidate range over all
 // elements.  Returns the key value xk and need = k - #{keys > xk}.
@@ -1845,7 +1880,7 @@ __device__ __forceinline__ void hist_threshold(const unsigned *gh, KeyF key, Pos
   if (C <= (unsigned)kCandCap) {
     compact_ballot<PER, NT>([&](int j) { const unsigned x = key(j); return x != 0u && hbin(x) == beta; },
                             key, pos, ckey, cpos, ss);
-    rank_pick<NT>((int)C, need, ckey, cpos, ss, xk, pthr);
+    rank_pick_bin<NT>((int)C, need, ckey, cpos, ss, xk, pthr);
   } else {
     block_threshold<PER>(key, pos, k, xk, pthr, ss, ckey, cpos);
   }
@@ -2205,7 +2240,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
                                    ckey, cpos, ss);
       unsigned xm;
       int pm;
-      rank_pick<NT>(rec.w, rec.z, ckey, cpos, ss, xm, pm);
+      rank_pick_bin<NT>(rec.w, rec.z, ckey, cpos, ss, xm, pm);
       // population moments over the set, B shifted by its smallest member
       // (the boundary key), in double
       const double bref = (double)key_float(xm);
@@ -2415,7 +2450,7 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
                                    ckey, cpos, ss);
       unsigned xk;
       int pk;
-      rank_pick<NT>(rec.w, rec.z, ckey, cpos, ss, xk, pk);
+      rank_pick_bin<NT>(rec.w, rec.z, ckey, cpos, ss, xk, pk);
       uint32_t msk = 0;
 #pragma unroll
       for (int j = 0; j < kListPer; ++j)
