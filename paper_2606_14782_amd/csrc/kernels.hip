@@ -1143,6 +1143,7 @@ __device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelSharedT<NT>
 }
 
 constexpr int kCandCap = 1024;   // LDS list of boundary-bin candidates
+constexpr int kSegCandCap = 2 * kSegThreads;   // the same in the select kernels of the fused pass
 
 // Boundary search over bin counts held in registers (larger bin = larger
 // keys): thread t holds the BPT consecutive bins starting at BPT*t.  For the
@@ -1195,10 +1196,10 @@ __device__ __forceinline__ void hist_boundary(int need, SelSharedT<NT> &ss) {
 // (wave, element slot, lane) order, through ballots (no atomics); returns
 // nothing, the list length is the caller's count (entries beyond the
 // kCandCap slots of the list are dropped).  Ends with a barrier.
-template <int PER, int NT, typename InF, typename KeyF, typename PosF>
+template <int PER, int NT, int CAPI = kCandCap, typename InF, typename KeyF, typename PosF>
 __device__ __forceinline__ void compact_ballot(InF in, KeyF key, PosF pos, unsigned *ckey, int *cpos,
                                                SelSharedT<NT> &ss) {
-  constexpr unsigned CAP = kCandCap;
+  constexpr unsigned CAP = CAPI;
   constexpr int NW = NT / 64;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   unsigned wc = 0;
@@ -1228,11 +1229,32 @@ __device__ __forceinline__ void compact_ballot(InF in, KeyF key, PosF pos, unsig
 
 // The need-th entry (1-based) of C <= NT listed entries under the tie rule
 // (key descending, position ascending): xk = its key, pthr = its position.
-// Every entry is ranked against all others by tpe consecutive lanes.
+// Every entry is ranked against all others by tpe consecutive lanes.  Lists
+// of NT < C <= 2*NT entries (a boundary bin of exact ties) are ranked two
+// entries per thread, each against all others: correct, and slow.
 template <int NT>
 __device__ __forceinline__ void rank_pick(int C, int need, const unsigned *ckey, const int *cpos,
                                           SelSharedT<NT> &ss, unsigned &xk, int &pthr) {
   const int t = threadIdx.x;
+  if (C > NT) {
+    const bool two = t + NT < C;
+    const unsigned k0 = ckey[t], k1 = two ? ckey[t + NT] : 0u;
+    const int p0 = cpos[t], p1 = two ? cpos[t + NT] : 0;
+    unsigned r0 = 0, r1 = 0;
+    for (int q = 0; q < C; ++q) {
+      const unsigned kq = ckey[q];
+      const int pq = cpos[q];
+      r0 += (kq > k0 || (kq == k0 && pq < p0)) ? 1u : 0u;
+      r1 += (kq > k1 || (kq == k1 && pq < p1)) ? 1u : 0u;
+    }
+    if (r0 == (unsigned)(need - 1)) { ss.bc_u[1] = k0; ss.bc_i[2] = p0; }
+    if (two && r1 == (unsigned)(need - 1)) { ss.bc_u[1] = k1; ss.bc_i[2] = p1; }
+    lds_barrier();
+    xk = ss.bc_u[1];
+    pthr = ss.bc_i[2];
+    lds_barrier();
+    return;
+  }
   int tpe = 1;
   while (tpe < 32 && 2 * tpe * C <= NT) tpe *= 2;
   const int q = t / tpe, sub = t & (tpe - 1);
@@ -1271,7 +1293,7 @@ __device__ __forceinline__ void rank_pick(int C, int need, const unsigned *ckey,
   lds_barrier();
 }
 
-// The need-th entry (1-based) of C <= NT listed entries that share key bits
+// The need-th entry (1-based) of C <= 2*NT listed entries that share key bits
 // 31..18 (one bin of the select histograms), under the tie rule.  Up to
 // kRankDirect entries are ranked directly (each against all others, a cost
 // that grows with C^2); more are first narrowed to their sub-bin of key bits
@@ -1287,22 +1309,28 @@ __device__ __forceinline__ void rank_pick_bin(int C, int need, unsigned *ckey, i
   }
   const int t = threadIdx.x;
   for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
-  unsigned k = 0;
-  int p = 0;
-  if (t < C) {
-    k = ckey[t];
-    p = cpos[t];
+  unsigned k[2] = {0u, 0u}, sub[2];
+  int p[2] = {0, 0};
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (t + j * NT < C) {
+      k[j] = ckey[t + j * NT];
+      p[j] = cpos[t + j * NT];
+    }
+    sub[j] = (k[j] >> 7) & (unsigned)(kHistBins - 1);
   }
-  const unsigned sub = (k >> 7) & (unsigned)(kHistBins - 1);
   lds_barrier();
-  if (t < C) atomicAdd(&ss.hist[sub], 1u);
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    if (t + j * NT < C) atomicAdd(&ss.hist[sub[j]], 1u);
   lds_barrier();
   hist_boundary<NT>(need, ss);
   const unsigned s2 = (unsigned)ss.bc_i[0];
   const int need2 = need - ss.bc_i[1];
   const int C2 = (int)ss.bc_u[2];
-  compact_ballot<1, NT>([&](int) { return t < C && sub == s2; }, [&](int) { return k; },
-                        [&](int) { return p; }, ckey, cpos, ss);
+  compact_ballot<2, NT, kSegCandCap>([&](int j) { return t + j * NT < C && sub[j] == s2; },
+                                     [&](int j) { return k[j]; }, [&](int j) { return p[j]; },
+                                     ckey, cpos, ss);
   rank_pick<NT>(C2, need2, ckey, cpos, ss, xk, pthr);
 }
 
@@ -2187,8 +2215,8 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
 __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int gs, int h) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ unsigned hist[kHBins];
-  __shared__ unsigned ckey[kCandCap];
-  __shared__ int cpos[kCandCap];
+  __shared__ unsigned ckey[kSegCandCap];
+  __shared__ int cpos[kSegCandCap];
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[kAllPer * NW + 1];
   __shared__ float2 mom[kMomChunk];
@@ -2233,9 +2261,9 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
     load_lists<true>(st, b, base, n, h, a.recB + b * a.Hkv + h, a.listB_key, a.listB_pos, a.listB_v,
                      a.cntB, scnt, L, rec, lk, lp, lv);
     double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    if (L.fits && rec.w <= kCandCap) {
+    if (L.fits && rec.w <= kSegCandCap) {
       // the boundary bin's entries, ranked under the tie rule
-      compact_ballot<kListPer, NT>([&](int j) { return lk[j] != 0u && hbin(lk[j]) == rec.x; },
+      compact_ballot<kListPer, NT, kSegCandCap>([&](int j) { return lk[j] != 0u && hbin(lk[j]) == rec.x; },
                                    [&](int j) { return lk[j]; }, [&](int j) { return lp[j]; },
                                    ckey, cpos, ss);
       unsigned xm;
@@ -2417,8 +2445,8 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
                                            int h) {
   constexpr int NT = kSegThreads, NW = NT / 64;
   extern __shared__ __align__(16) int tbl[];         // [K + W] source position of each row
-  __shared__ unsigned ckey[kCandCap];
-  __shared__ int cpos[kCandCap];
+  __shared__ unsigned ckey[kSegCandCap];
+  __shared__ int cpos[kSegCandCap];
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[kAllPer * NW + 1];
   __shared__ __align__(16) int scnt[kMaxSegs];
@@ -2444,8 +2472,8 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
     ListView L;
     load_lists<false>(st, b, base, n, h, a.recS + b * a.Hkv + h, a.listS_key, a.listS_pos, nullptr,
                       a.cntS, scnt, L, rec, lk, lp, nullptr);
-    if (L.fits && rec.w <= kCandCap) {
-      compact_ballot<kListPer, NT>([&](int j) { return lk[j] != 0u && hbin(lk[j]) == rec.x; },
+    if (L.fits && rec.w <= kSegCandCap) {
+      compact_ballot<kListPer, NT, kSegCandCap>([&](int j) { return lk[j] != 0u && hbin(lk[j]) == rec.x; },
                                    [&](int j) { return lk[j]; }, [&](int j) { return lp[j]; },
                                    ckey, cpos, ss);
       unsigned xk;
@@ -2576,7 +2604,7 @@ __global__ __launch_bounds__(kSegThreads) void k_sel_b(SegArgs g, SegArgs gp, Se
 }
 
 size_t final_lds_bytes(int max_budget, int window) {
-  return (size_t)(max_budget + window) * sizeof(int) + 2 * kCandCap * sizeof(unsigned) +
+  return (size_t)(max_budget + window) * sizeof(int) + 2 * kSegCandCap * sizeof(unsigned) +
          sizeof(SelSharedT<kSegThreads>) + (kAllPer * (kSegThreads / 64) + 1) * sizeof(unsigned) +
          kMaxSegs * sizeof(int);
 }
