@@ -67,7 +67,7 @@ def kernel_bytes(name, wl, persist_m=4):
         return ab["k"] + ab["q"]
     if name in ("window_score_calib", "window_score_calib_kr"):   # K, Q_win; E and B out
         return ab["k"] + ab["q"] + 2 * vec
-    if name == "window_score_calib_lse_kr":             # both passes: two layers' K and Q_win
+    if name in ("window_score_calib_lse", "window_score_calib_lse_kr"):  # both passes: two layers' K and Q_win
         return 2 * (ab["k"] + ab["q"]) + 2 * vec
     if name == "lse_merge":                             # per-chunk (max, sum) partials
         chunks = T / 512 + wl.batch

@@ -133,10 +133,11 @@ const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", 
                               "final_topk",    "select_calib",  "select_topk",
                               "calib_elem",    "compact",       "window_lse_kr",
                               "window_score_calib_kr", "window_score_calib_lse_kr",
-                              "segment_calib_cand", "segment_score_final"};
+                              "segment_calib_cand", "segment_score_final",
+                              "window_score_calib_lse"};
 enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
                 KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_DUAL_KR,
-                KI_SEL_A, KI_SEL_B, KI_COUNT };
+                KI_SEL_A, KI_SEL_B, KI_DUAL, KI_COUNT };
 
 }  // namespace
 
@@ -712,7 +713,8 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
 
 // The K passes of a layer.  lse_merged: its pass 1 ran with the previous
 // layer's pass 2 and its normalisers are merged.  next (NULL or the next
-// layer's pass 1 arguments): that pass 1 runs in this layer's pass-2 launch.
+// layer's pass 1 arguments): that pass 1 runs in this layer's pass-2 launch
+// (bf16 keys; fp32 keys: in a launch right after it).
 bacon_status stage_pass(bacon_ctx *c, const LayerRun &r, bool lse_merged, const PassArgs *next,
                         hipStream_t s) {
   const int d = c->shape.head_dim;
@@ -725,11 +727,16 @@ bacon_status stage_pass(bacon_ctx *c, const LayerRun &r, bool lse_merged, const 
       return timed(c, KI_DUAL_KR, s, [&] { return launch_krdual(r.bf16, d, r.w32, r.a, *next, r.st, s); });
     return timed(c, KI_FUSED_KR, s, [&] { return launch_krpass(PASS_FUSED, r.bf16, d, r.w32, r.a, r.st, s); });
   }
-  if (!r.lse) {
+  if (!r.lse && !lse_merged) {
     TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, r.bf16, d, false, r.a, r.st, s); }));
     TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(r.a, r.st, s); }));
   }
-  return timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, r.bf16, d, r.w32, r.a, r.st, s); });
+  if (next && r.bf16)
+    return timed(c, KI_DUAL, s, [&] { return launch_pass_dual(r.bf16, d, r.w32, r.a, *next, r.st, s); });
+  TRY(timed(c, KI_FUSED, s, [&] { return launch_pass(PASS_FUSED, r.bf16, d, r.w32, r.a, r.st, s); }));
+  if (next)   // fp32 keys: the next layer's pass 1 in a launch of its own
+    return timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, r.bf16, d, false, *next, r.st, s); });
+  return BACON_OK;
 }
 
 // Calibration of r's layer, with the previous layer's candidate lists and the
@@ -834,7 +841,7 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
   for (int i = 0; i < num_layers; ++i) {
     const LayerRun &r = runs[i];
     const LayerRun *prev = (overlap && i > 0) ? &runs[i - 1] : nullptr;
-    const PassArgs *next = (r.kr && !r.lse && i + 1 < num_layers) ? &runs[i + 1].a : nullptr;
+    const PassArgs *next = (!r.lse && i + 1 < num_layers) ? &runs[i + 1].a : nullptr;
     TRY(stage_pass(c, r, merged, next, s));
     TRY(stage_a(c, r, prev, next, s));
     TRY(stage_b(c, r, prev, s));

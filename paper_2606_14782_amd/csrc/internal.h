@@ -175,6 +175,9 @@ int kr_lds_bytes(bool bf16, int head_dim, int rpad);
 bool kr_supported(bool bf16, int head_dim, int rpad);
 hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const PassArgs &a,
                          const SeqTable &st, hipStream_t s);
+// Streaming pass 2 of one layer (a2) with streaming pass 1 of the next (a1).
+hipError_t launch_pass_dual(bool bf16, int head_dim, bool w32, const PassArgs &a2, const PassArgs &a1,
+                            const SeqTable &st, hipStream_t s);
 // Pass 2 of one layer (a2) with pass 1 of the next layer (a1) in one launch.
 hipError_t launch_krdual(bool bf16, int head_dim, bool w32, const PassArgs &a2, const PassArgs &a1,
                          const SeqTable &st, hipStream_t s);

@@ -179,16 +179,16 @@ int pass_lds_bytes(int mode, bool bf16, int head_dim, int rpad, int chunk) {
   return bytes;
 }
 
+// One workgroup of a streaming pass: chunk gchunk of the sequences' keys of
+// KV head h.
 template <int MODE, bool BF16, int D, bool W32>
-__global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
+__device__ __forceinline__ void pass_body(const PassArgs &a, const SeqTable &st, int gchunk, int h) {
   using C = PassCfg<BF16, D>;
   extern __shared__ __align__(16) unsigned char smem[];
   const int nw = blockDim.x >> 6;
   const int nt = blockDim.x;
   const int tk = stage_keys(nw);
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63, half = lane >> 5, l32 = lane & 31;
-  const int h = blockIdx.y;
-  const int gchunk = blockIdx.x;
   const int b = find_seq(st, gchunk);
   const int c = gchunk - st.chunk_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
@@ -455,7 +455,7 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
     __syncthreads();
     for (int p = t; p < ncnd; p += nt) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
     __syncthreads();
-    const int copy = (blockIdx.y * gridDim.x + blockIdx.x) % kHCopies;
+    const int copy = (h * st.total_chunks + gchunk) % kHCopies;
     unsigned *gh = a.hist_B + (((int64_t)b * a.Hkv + h) * kHCopies + copy) * kHBins;
     for (int q = blo + t; q <= bhi; q += nt) {
       const unsigned cnt = hist[q];
@@ -476,6 +476,48 @@ __global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
           make_float2(m == -INFINITY ? -INFINITY : m * a.c2, l);
     }
   }
+}
+
+template <int MODE, bool BF16, int D, bool W32>
+__global__ __launch_bounds__(512) void k_pass(PassArgs a, SeqTable st) {
+  pass_body<MODE, BF16, D, W32>(a, st, blockIdx.x, blockIdx.y);
+}
+
+// Pass 2 of one layer (a2) and pass 1 of the next (a1) in one grid, as the
+// key-register k_krdual: the first total_chunks columns take a2.
+template <bool BF16, int D, bool W32>
+__global__ __launch_bounds__(512) void k_pass_dual(PassArgs a2, PassArgs a1, SeqTable st) {
+  if ((int)blockIdx.x < st.total_chunks)
+    pass_body<PASS_FUSED, BF16, D, W32>(a2, st, blockIdx.x, blockIdx.y);
+  else
+    pass_body<PASS_LSE, BF16, D, false>(a1, st, blockIdx.x - st.total_chunks, blockIdx.y);
+}
+
+template <bool BF16, int D, bool W32>
+static hipError_t launch_pass_dual_t(const PassArgs &a2, const PassArgs &a1, const SeqTable &st,
+                                     hipStream_t s) {
+  const int nw = a2.Rpad / 32;
+  const int lds = std::max(pass_lds_bytes(PASS_FUSED, BF16, D, a2.Rpad, a2.chunk),
+                           pass_lds_bytes(PASS_LSE, BF16, D, a1.Rpad, a1.chunk));
+  if (lds > kLdsBytes || a1.Rpad != a2.Rpad || a1.chunk != a2.chunk) return hipErrorInvalidValue;
+  dim3 grid(2 * st.total_chunks, a2.Hkv), block(64 * nw);
+  allow_lds(k_pass_dual<BF16, D, W32>, lds);
+  hipLaunchKernelGGL((k_pass_dual<BF16, D, W32>), grid, block, lds, s, a2, a1, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_pass_dual(bool bf16, int d, bool w32, const PassArgs &a2, const PassArgs &a1,
+                            const SeqTable &st, hipStream_t s) {
+  if (bf16) {
+    if (d == 128) return w32 ? launch_pass_dual_t<true, 128, true>(a2, a1, st, s)
+                             : launch_pass_dual_t<true, 128, false>(a2, a1, st, s);
+    return w32 ? launch_pass_dual_t<true, 64, true>(a2, a1, st, s)
+               : launch_pass_dual_t<true, 64, false>(a2, a1, st, s);
+  }
+  if (d == 128) return w32 ? launch_pass_dual_t<false, 128, true>(a2, a1, st, s)
+                           : launch_pass_dual_t<false, 128, false>(a2, a1, st, s);
+  return w32 ? launch_pass_dual_t<false, 64, true>(a2, a1, st, s)
+             : launch_pass_dual_t<false, 64, false>(a2, a1, st, s);
 }
 
 template <int MODE, bool BF16, int D, bool W32>
