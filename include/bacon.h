@@ -214,10 +214,13 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *ctx, int32_t layer, const bacon
  * prompt (compression at the end of prefill, when every layer's cache is
  * there): the same results as bacon_compress_layer (or, when d_lse is not
  * NULL, bacon_compress_layer_lse) called for each layer in order, bit for
- * bit.  With every layer's inputs at hand, the K pass that forms the next
- * layer's normalisers runs in the same launch as this layer's scoring pass
- * (one launch fewer per layer, and the two passes fill each other's idle
- * CUs).  The per-layer arguments are host arrays of num_layers device
+ * bit.  With every layer's inputs at hand, two layers are in flight: the K
+ * pass that forms the next layer's normalisers runs in the launch of this
+ * layer's scoring pass, their merge in this layer's calibration launch, and
+ * this layer's candidate lists and final top-K and compaction in the next
+ * layer's calibration and score launches: three launches per layer, all on
+ * `stream`.  A layer's outputs are complete when the call's work on the
+ * stream is.  The per-layer arguments are host arrays of num_layers device
  * pointers each, in the layouts of bacon_compress_layer; d_lse is NULL or
  * such an array.  first_layer must be the prompt's next layer (ORDER
  * otherwise) and the range must end within num_layers (ORDER).  Every
