@@ -1853,6 +1853,10 @@ hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable
 //  * final_topk (`parts` workgroups per (sequence, KV head)): the top-K from
 //    the lists, the kept positions in ascending order, and each workgroup's
 //    share of the compacted cache rows.
+// Boundary bins of up to kSegCandCap entries are resolved on the lists
+// (large ones narrowed to a sub-bin first).  In a prompt call the four run
+// as two launches per layer that also carry the previous and next layers'
+// work (k_sel_a, k_sel_b).
 constexpr int kSegPer = kSegLen / kSegThreads;             // positions per thread (strided)
 constexpr int kSegWin = kSegLen + 2 * kPoolHalo;           // segment plus pool halo
 constexpr int kSegWinJ = (kSegWin + kSegThreads - 1) / kSegThreads;
