@@ -213,6 +213,33 @@ def test_prompt_calls_mix_with_layer_calls():
             assert torch.equal(got[l][i], want[l][i]), f"layer {l} {what}"
 
 
+def test_prompt_call_with_a_budget_too_large_to_overlap():
+    """A budget whose row table does not fit beside the score kernel's LDS:
+    the prompt call keeps each layer's select to its own launches, and still
+    equals the per-layer calls and the oracle."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = inputs.Workload("big-budget", 3, 8, 2, 128, 32, 7, "bf16", (16384, 5000), (11000, 4000),
+                         ((32, 16000), (32, 4700)), 0, 31)
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+    qs = [P.to_dev(x["q_win"], wl) for x in xs]
+    ks = [P.to_dev(x["k"], wl) for x in xs]
+    vs = [P.to_dev(x["v"], wl) for x in xs]
+    a, b = P.make_ctx(wl), P.make_ctx(wl)
+    a.bacon_begin_prompt(batch)
+    want = [a.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l]) for l in range(wl.num_layers)]
+    b.bacon_begin_prompt(batch)
+    got = b.bacon_compress_prompt(0, batch, qs, ks, vs)
+    torch.cuda.synchronize()
+    orc = ref.Prompt.for_workload(wl, P.oracle_params())
+    for l in range(wl.num_layers):
+        for i, what in enumerate(("idx", "k_out", "v_out")):
+            assert torch.equal(got[l][i], want[l][i]), f"layer {l} {what}"
+        r = orc.layer(l, xs[l]["q_win"], xs[l]["k"])
+        P.check_idx(f"big-budget L{l}", got[l][0].cpu().numpy(), r, wl, P.RTOL[wl.dtype])
+
+
 PROMPT_VARIANTS = [
     ("max of S", {"pool_mode": 1}),
     ("mean of B", {"pool_mode": 2}),
