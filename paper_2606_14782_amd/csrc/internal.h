@@ -18,7 +18,7 @@ constexpr int kSegLen = 2048;       // positions per segment of the histogram se
 constexpr int kSegThreads = 1024;
 constexpr int kPoolHalo = 16;       // largest pool half-width
 constexpr int kHBins = 8192;        // bins of the select histograms (32 per octave of a float)
-constexpr int kHCopies = 2;         // copies of the B histogram the fused pass spreads its atomics over
+constexpr int kHCopies = 1;         // copies of the B histogram the fused pass spreads its atomics over
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU (and per workgroup) on gfx950
 constexpr int kEdgeEntries = 1024;      // positions next to chunk boundaries the select stages
 constexpr int kKrWaves = 4;             // waves of a key-register pass workgroup
