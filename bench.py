@@ -11,9 +11,11 @@ resident in HBM before timing starts.
 
 Prints one JSON line: keys scored per second (positions x KV heads x layers
 per second), ms per step and per layer, a roofline entry for the dominant
-kernel (algorithmic bytes / mean launch time from HIP events recorded around
-each launch on the pass's stream) and the fp64 CPU oracle timed on a bounded
-sample of the same workload.
+kernel (its algorithmic bytes -- the per-layer bytes of the pass that the
+launch completes: K read once, Q_win, E written -- over its mean launch time
+from HIP events recorded around each launch on the pass's stream), the same
+prompt call on every workload shape, and the fp64 CPU oracle timed on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -55,37 +57,59 @@ def algorithmic_bytes(wl, persist_m=4):
             "layers": per_layer}
 
 
+# Kernels (library timing names) by what they complete of a layer's pass.
+# K passes that finish a layer's window score: its K read once, Q_win, E out.
+SCORE_PASSES = ("window_score_calib_lse_kr", "window_score_calib_lse", "window_score_calib_kr",
+                "window_score_calib", "window_score_single")
+# Kernels whose work is only an intermediate of this design (a second read of
+# K for the normalisers, the normaliser merge, pooled vectors, score keys and
+# candidate lists): no algorithmic bytes of their own.
+DESIGN_ONLY = ("window_lse_kr", "window_lse", "lse_merge", "segment_score", "segment_cand")
+
+
 def kernel_bytes(name, wl, persist_m=4):
-    """Algorithmic bytes of one launch of a kernel of the fused pass (mean over
-    layers): what the kernel must read and write at minimum in this design."""
+    """Algorithmic bytes (the per-layer units above) of the work one launch of
+    a kernel of the measured path completes, mean over layers.  The launches
+    of one layer add up to algorithmic_bytes()'s layer mean:
+      K pass that finishes the window score   K + Q_win + E written
+      calibration (segment_calib)             the earlier layers' E read for T
+      final top-K and compaction              kept and window rows of K and V
+                                              read and written, the indices
+    A launch that holds the jobs of two layers (window_score_calib_lse*: pass 2
+    of layer l with pass 1 of layer l+1) completes one layer's K pass."""
     ab = algorithmic_bytes(wl, persist_m)
     T, Hkv = wl.total_tokens, wl.num_kv_heads
     vec = T * Hkv * 4                                   # one fp32 value per (position, KV head)
-    ring = float(np.mean([(min(persist_m, l) + 1) * vec for l in range(wl.num_layers)]))
+    hist_reads = float(np.mean([min(persist_m, l) * vec for l in range(wl.num_layers)]))
     kept_rows = sum(b + wl.window for b in wl.budgets)
-    if name in ("window_lse", "window_lse_kr"):          # K, Q_win
-        return ab["k"] + ab["q"]
-    if name in ("window_score_calib", "window_score_calib_kr"):   # K, Q_win; E and B out
-        return ab["k"] + ab["q"] + 2 * vec
-    if name in ("window_score_calib_lse", "window_score_calib_lse_kr"):  # both passes: two layers' K and Q_win
-        return 2 * (ab["k"] + ab["q"]) + 2 * vec
-    if name == "lse_merge":                             # per-chunk (max, sum) partials
-        chunks = T / 512 + wl.batch
-        return Hkv * chunks * wl.group * wl.window * 8
-    if name == "segment_calib":                         # B, E history in; V, pooled B and V out
-        return 4 * vec + ring
+    if name in SCORE_PASSES:
+        return ab["k"] + ab["q"] + vec
+    if name in DESIGN_ONLY:
+        return 0.0
+    if name == "segment_calib":
+        return hist_reads
+    if name == "final_topk":
+        return 2 * 2 * kept_rows * Hkv * wl.head_dim * wl.elem_size + 4 * sum(wl.budgets) * Hkv
     if name == "segment_calib_cand":                    # calibration, the previous layer's lists,
         return sum(kernel_bytes(k, wl, persist_m)      # the next layer's normaliser merge
                    for k in ("segment_calib", "segment_cand", "lse_merge"))
     if name == "segment_score_final":                   # scores, the previous layer's top-K
         return sum(kernel_bytes(k, wl, persist_m) for k in ("segment_score", "final_topk"))
-    if name == "segment_score":                         # pooled B and V in; score keys out
-        return 3 * vec
-    if name == "segment_cand":                          # score keys in
-        return vec
-    if name == "final_topk":                            # kept + window rows of K and V in and out
-        return 2 * 2 * kept_rows * Hkv * wl.head_dim * wl.elem_size + 4 * sum(wl.budgets) * Hkv
     return 0.0
+
+
+def design_bytes(name, wl, persist_m=4):
+    """Bytes a launch moves in this design at minimum (beside the algorithmic
+    ones): the dual launch reads two layers' K, pass 1 reads K again."""
+    ab = algorithmic_bytes(wl, persist_m)
+    vec = wl.total_tokens * wl.num_kv_heads * 4
+    if name in ("window_score_calib_lse_kr", "window_score_calib_lse"):
+        return 2 * (ab["k"] + ab["q"]) + 2 * vec
+    if name in ("window_lse_kr", "window_lse"):
+        return ab["k"] + ab["q"]
+    if name in ("window_score_calib_kr", "window_score_calib", "window_score_single"):
+        return ab["k"] + ab["q"] + 2 * vec
+    return kernel_bytes(name, wl, persist_m)
 
 
 def measured_traffic(kernel):
@@ -158,6 +182,45 @@ def cpu_baseline(wl, budget_s, gpu_idx=None):
             "kept_sets_identical_to_gpu": agree if gpu_idx is not None else None}
 
 
+def prompt_rate(idx, steps, warmup):
+    """The prompt call (bacon_begin_prompt + bacon_compress_prompt over every
+    layer) on workload idx at its full shape: median step over `steps`."""
+    import torch
+    from paper_2606_14782_amd import bacon, inputs
+    wl = inputs.workload(idx)
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    qs, ks, vs = [], [], []
+    for l in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, l)
+        qs.append(torch.from_numpy(x["q_win"]).to(dev).to(tdt))
+        ks.append(torch.from_numpy(x["k"]).to(dev).to(tdt))
+        vs.append(torch.from_numpy(x["v"]).to(dev).to(tdt))
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    ctx = bacon.Context(wl.num_layers, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window,
+                        wl.batch, wl.total_tokens, wl.dtype,
+                        bacon.default_params(pool_kernel=wl.pool_kernel))
+    outs = None
+
+    def step():
+        nonlocal outs
+        ctx.bacon_begin_prompt(batch)
+        outs = ctx.bacon_compress_prompt(0, batch, qs, ks, vs, outs=outs)
+
+    for _ in range(warmup):
+        step()
+    ms = median_step_ms(step, steps)
+    ab = algorithmic_bytes(wl)
+    us_layer = 1e3 * ms / wl.num_layers
+    keys = wl.total_tokens * wl.num_kv_heads / (us_layer * 1e-6)
+    del qs, ks, vs, outs, ctx
+    torch.cuda.empty_cache()
+    return {"workload": wl.name, "layers": wl.num_layers, "us_per_layer": us_layer,
+            "keys_per_s": keys, "bytes_per_layer": ab["layer_mean"],
+            "hbm_frac": ab["layer_mean"] / (us_layer * 1e-6) / 1e9 / HBM_PEAK_GBS,
+            "steps": steps}
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -176,6 +239,8 @@ def main():
     ap.add_argument("--workload", type=int, default=3, help="workload index (default: 32K video)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the prompt call on the other workload shapes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain fp32 copy of COPY_BYTES (read and written once) whose "
                          "HBM counters scale the kernels' counters")
@@ -274,12 +339,15 @@ def main():
     torch.cuda.synchronize()
     kt = ctx.bacon_profile_read()
     ctx.bacon_profile_enable(False)
-    per_kernel = {k: {"launches": n, "avg_us": 1e3 * ms / n} for k, (n, ms) in kt.items()}
+    per_kernel = {k: {"launches": n, "avg_us": 1e3 * ms / n, "algorithmic_bytes": kernel_bytes(k, wl),
+                      "design_bytes": design_bytes(k, wl)} for k, (n, ms) in kt.items()}
     dom = max((k for k in per_kernel if kernel_bytes(k, wl) > 0),
               key=lambda k: per_kernel[k]["avg_us"])
     kbytes = kernel_bytes(dom, wl)
     achieved = kbytes / (per_kernel[dom]["avg_us"] * 1e-6) / 1e9
     traffic = measured_traffic(dom)
+    for k in per_kernel:
+        per_kernel[k]["measured_traffic"] = measured_traffic(k)
 
     # The per-layer calls over the same prompt (no next-layer pass in the
     # scoring launch), for comparison.
@@ -340,7 +408,12 @@ def main():
                      "frac_of_peak": pass_gbs / HBM_PEAK_GBS},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": dom,
-                     "bytes_per_launch": kbytes, "avg_us": per_kernel[dom]["avg_us"]},
+                     "bytes_per_launch": kbytes,
+                     "bytes_note": "algorithmic bytes of the work the launch completes: one "
+                                   "layer's K read once, Q_win and E written",
+                     "design_bytes_per_launch": design_bytes(dom, wl),
+                     "traffic_over_algorithmic": None if traffic is None else traffic / kbytes,
+                     "avg_us": per_kernel[dom]["avg_us"]},
         "kernels": per_kernel,
         "per_layer_calls": {
             "note": "bacon_compress_layer called for each layer (pass 1 of a layer in its own "
@@ -354,6 +427,21 @@ def main():
             "ms_per_layer": ms_step_lse / wl.num_layers,
             "value": keys_step / (ms_step_lse * 1e-3), "unit": "keys/s"},
     }
+    if not args.no_configs:
+        del qs, ks, vs, outs, lses
+        torch.cuda.empty_cache()
+        configs = []
+        for i in range(5):
+            if i == args.workload:
+                configs.append({"workload": wl.name, "layers": wl.num_layers,
+                                "us_per_layer": 1e3 * ms_layer,
+                                "keys_per_s": wl.total_tokens * wl.num_kv_heads / (ms_layer * 1e-3),
+                                "bytes_per_layer": ab["layer_mean"],
+                                "hbm_frac": pass_gbs / HBM_PEAK_GBS, "steps": args.steps})
+                continue
+            log(f"workload {i}: prompt call")
+            configs.append(prompt_rate(i, min(args.steps, 20), 2))
+        result["configs"] = configs
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, gpu_idx)

@@ -103,7 +103,8 @@ typedef enum { BACON_POOL_MEAN_S = 0, BACON_POOL_MAX_S = 1, BACON_POOL_MEAN_B = 
 typedef struct {
   int32_t radius;          /* r of the coherence neighbourhood, 0..16        */
   int32_t persist_m;       /* m, persistence depth, 0..16                    */
-  float rho;               /* scale-matching expansion, > 0                  */
+  double rho;              /* scale-matching expansion, > 0; M = floor(rho K)
+                              is formed in double (Eq. scale_matching_size) */
   float gamma;             /* calibration strength, >= 0                     */
   float eps;               /* stabiliser in lambda, >= 0                     */
   int32_t pool_kernel;     /* odd width of the average pool of S, 1..33      */
@@ -222,15 +223,21 @@ bacon_status bacon_compress_layer_lse(bacon_ctx *ctx, int32_t layer, const bacon
  * `stream`.  A layer's outputs are complete when the call's work on the
  * stream is.  The per-layer arguments are host arrays of num_layers device
  * pointers each, in the layouts of bacon_compress_layer; d_lse is NULL or
- * such an array.  first_layer must be the prompt's next layer (ORDER
- * otherwise) and the range must end within num_layers (ORDER).  Every
- * pointer is checked before the first launch (INVALID if NULL or
- * misaligned); the caller keeps ownership of all buffers. */
+ * such an array.  layer_batch is NULL (every layer keeps `batch`'s budgets)
+ * or a host array of num_layers batches, one per layer, each with the
+ * prompt's cu_seqlens and its own budgets or head_budgets: a per-layer
+ * budget schedule K_{l,h} of the backbone method (Sec. 4, Preliminaries);
+ * each layer's outputs are sized by its own batch.  first_layer must be the
+ * prompt's next layer (ORDER otherwise) and the range must end within
+ * num_layers (ORDER).  Every pointer and every layer's batch is checked
+ * before the first launch (INVALID if NULL, misaligned, or with other
+ * sequences); the caller keeps ownership of all buffers. */
 bacon_status bacon_compress_prompt(bacon_ctx *ctx, const bacon_batch *batch, int32_t first_layer,
                                    int32_t num_layers, const void *const *d_q_win,
                                    const void *const *d_k, const void *const *d_v,
                                    const float *const *d_lse, int32_t *const *d_idx,
-                                   void *const *d_k_out, void *const *d_v_out, void *stream);
+                                   void *const *d_k_out, void *const *d_v_out,
+                                   const bacon_batch *const *layer_batch, void *stream);
 
 /* The window-row normalisers alone (Sec. 4.1): writes d_lse [B, Hq, W]
  * float32 as bacon_compress_layer_lse reads them (natural log of the sum of
@@ -244,6 +251,21 @@ bacon_status bacon_compress_prompt(bacon_ctx *ctx, const bacon_batch *batch, int
  * (INVALID otherwise); the caller keeps ownership. */
 bacon_status bacon_window_lse(bacon_ctx *ctx, const bacon_batch *batch, const void *d_q_win,
                               const void *d_k, float *d_lse, void *stream);
+
+/* Test instrumentation of the fused calls (bacon_compress_layer, _lse and
+ * bacon_compress_prompt), whose intermediates otherwise stay in the
+ * workspace: with all three pointers set, every later layer l of those calls
+ * copies, once its lambda is formed,
+ *   its window score B           to d_B      + l * Hkv * T   ([Hkv, T] float32),
+ *   its evidence V = E + L + T   to d_V      + l * Hkv * T   ([Hkv, T]; valid on
+ *                                              the candidate positions only),
+ *   lambda                       to d_lambda + l * B * Hkv   ([B, Hkv]),
+ * with T the prompt's total tokens and B its batch size; the buffers must hold
+ * every layer the calls reach (the caller owns them, 4-byte aligned).  The
+ * copies are enqueued on the call's stream between the layer's launches, so
+ * the measured schedule itself is unchanged.  All NULL switches it off
+ * (the default); a mix of NULL and non-NULL is INVALID. */
+bacon_status bacon_debug_capture(bacon_ctx *ctx, float *d_B, float *d_V, float *d_lambda);
 
 /* Sizes of the outputs for a batch: idx entries and compacted rows. */
 int64_t bacon_idx_count(const bacon_batch *batch, int32_t num_kv_heads);

@@ -22,7 +22,7 @@ ENTRY_POINTS = [
     "bacon_default_params", "bacon_workspace_bytes", "bacon_init", "bacon_free",
     "bacon_begin_prompt", "bacon_score", "bacon_calibrate", "bacon_select_topk",
     "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_compress_prompt",
-    "bacon_window_lse",
+    "bacon_window_lse", "bacon_debug_capture",
     "bacon_idx_count",
     "bacon_kept_rows",
     "bacon_profile_enable", "bacon_profile_read", "bacon_status_string", "bacon_last_error",
@@ -30,7 +30,7 @@ ENTRY_POINTS = [
 
 
 class Params(C.Structure):
-    _fields_ = [("radius", C.c_int32), ("persist_m", C.c_int32), ("rho", C.c_float),
+    _fields_ = [("radius", C.c_int32), ("persist_m", C.c_int32), ("rho", C.c_double),
                 ("gamma", C.c_float), ("eps", C.c_float), ("pool_kernel", C.c_int32),
                 ("use_last_query", C.c_int32), ("terms", C.c_uint32), ("pool_mode", C.c_int32)]
 
@@ -88,7 +88,8 @@ def lib() -> C.CDLL:
                                                vp, vp, vp, vp]
         L.bacon_window_lse.argtypes = [vp, C.POINTER(Batch), vp, vp, vp, vp]
         L.bacon_compress_prompt.argtypes = [vp, C.POINTER(Batch), C.c_int32, C.c_int32, vp, vp, vp,
-                                            vp, vp, vp, vp, vp]
+                                            vp, vp, vp, vp, vp, vp]
+        L.bacon_debug_capture.argtypes = [vp, vp, vp, vp]
         L.bacon_idx_count.argtypes = [C.POINTER(Batch), C.c_int32]
         L.bacon_idx_count.restype = C.c_int64
         L.bacon_kept_rows.argtypes = [C.POINTER(Batch), C.c_int32, C.c_int32]
@@ -102,7 +103,7 @@ def lib() -> C.CDLL:
         for name in ("bacon_init", "bacon_free", "bacon_begin_prompt", "bacon_score",
                      "bacon_calibrate", "bacon_select_topk", "bacon_compact",
                      "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_window_lse",
-                     "bacon_compress_prompt",
+                     "bacon_compress_prompt", "bacon_debug_capture",
                      "bacon_profile_enable"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -258,24 +259,34 @@ class Context:
         return idx, k_out, v_out
 
     def bacon_compress_prompt(self, first_layer, batch: BatchLayout, q_wins, ks, vs, lses=None,
-                              outs=None):
+                              outs=None, layer_batches=None):
         """The pass over layers first_layer .. first_layer + len(ks) - 1 in one
-        call; returns [(idx, k_out, v_out)] per layer."""
+        call; returns [(idx, k_out, v_out)] per layer.  layer_batches: None, or
+        one BatchLayout per layer (same sequences, the layer's own budgets)."""
         import torch
         n = len(ks)
+        lb = layer_batches if layer_batches is not None else [batch] * n
         if outs is None:
             outs = []
-            for k in ks:
-                idx = torch.empty(batch.idx_count(self.shape.num_kv_heads), dtype=torch.int32,
+            for k, b in zip(ks, lb):
+                idx = torch.empty(b.idx_count(self.shape.num_kv_heads), dtype=torch.int32,
                                   device=k.device)
-                outs.append((idx, *self._kv_out(batch, k)))
+                outs.append((idx, *self._kv_out(b, k)))
         arr = lambda xs: (C.c_void_p * n)(*[x.data_ptr() for x in xs])
         lse_arr = arr(lses) if lses is not None else None
+        lb_arr = None
+        if layer_batches is not None:
+            lb_arr = (C.c_void_p * n)(*[C.cast(C.byref(b.c), C.c_void_p).value for b in layer_batches])
         _check(lib().bacon_compress_prompt(
             self._h, C.byref(batch.c), first_layer, n, arr(q_wins), arr(ks), arr(vs), lse_arr,
             arr([o[0] for o in outs]), arr([o[1] for o in outs]), arr([o[2] for o in outs]),
-            _stream()))
+            lb_arr, _stream()))
         return outs
+
+    def bacon_debug_capture(self, B=None, V=None, lam=None):
+        """Test instrumentation: per-layer copies of B, V [L, Hkv, T] and lambda
+        [L, B, Hkv] (float32 device tensors) from the fused calls; None turns it off."""
+        _check(lib().bacon_debug_capture(self._h, _ptr(B), _ptr(V), _ptr(lam)))
 
     def bacon_window_lse(self, batch: BatchLayout, q_win, k, out=None):
         """The window-row normalisers lse [B, Hq, W] (natural log) alone, as
@@ -327,8 +338,13 @@ def bacon_compress_layer_lse(ctx: Context, layer, batch, q_win, k, v, lse, out=N
     return ctx.bacon_compress_layer_lse(layer, batch, q_win, k, v, lse, out)
 
 
-def bacon_compress_prompt(ctx: Context, first_layer, batch, q_wins, ks, vs, lses=None, outs=None):
-    return ctx.bacon_compress_prompt(first_layer, batch, q_wins, ks, vs, lses, outs)
+def bacon_compress_prompt(ctx: Context, first_layer, batch, q_wins, ks, vs, lses=None, outs=None,
+                          layer_batches=None):
+    return ctx.bacon_compress_prompt(first_layer, batch, q_wins, ks, vs, lses, outs, layer_batches)
+
+
+def bacon_debug_capture(ctx: Context, B=None, V=None, lam=None):
+    return ctx.bacon_debug_capture(B, V, lam)
 
 
 def bacon_window_lse(ctx: Context, batch, q_win, k, out=None):

@@ -37,8 +37,8 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t ring, vec_b, vec_vp, vec_v, vec_pb, vec_pv, vec_s, hist_b, hist_s, list_bk, list_bp, list_bv,
-      list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, hb, total;
-  size_t vec_s_stride, hist_b_stride, hist_s_stride;   // the two copies by layer parity
+      list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, hb, sb, total;
+  size_t vec_s_stride, hist_b_stride, hist_s_stride, hb_stride, sb_stride;   // the two copies by layer parity
   int rpad, slots;
   int64_t chunks_cap;
 };
@@ -72,7 +72,7 @@ bacon_status check_params(const bacon_params *p) {
   if (p->radius < 0 || p->radius > 16) return fail(BACON_ERR_INVALID, "radius must be in [0, 16]");
   if (p->persist_m < 0 || p->persist_m > kMaxRing)
     return fail(BACON_ERR_INVALID, "persist_m must be in [0, %d]", kMaxRing);
-  if (!(p->rho > 0.f) || !std::isfinite(p->rho)) return fail(BACON_ERR_INVALID, "rho must be > 0");
+  if (!(p->rho > 0.0) || !std::isfinite(p->rho)) return fail(BACON_ERR_INVALID, "rho must be > 0");
   if (!(p->gamma >= 0.f) || !std::isfinite(p->gamma))
     return fail(BACON_ERR_INVALID, "gamma must be >= 0");
   if (!(p->eps >= 0.f) || !std::isfinite(p->eps)) return fail(BACON_ERR_INVALID, "eps must be >= 0");
@@ -123,7 +123,10 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.partials = off; off += align256((size_t)s->num_kv_heads * L.chunks_cap * L.rpad * sizeof(float2));
   L.lse2 = off;     off += align256((size_t)s->max_batch * s->num_kv_heads * L.rpad * sizeof(float));
   L.lambda = off;   off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(float));
-  L.hb = off;       off += align256((size_t)s->max_batch * s->num_kv_heads * sizeof(int2));
+  L.hb_stride = align256((size_t)s->max_batch * s->num_kv_heads * sizeof(int2));
+  L.hb = off;       off += 2 * L.hb_stride;                   // by layer parity
+  L.sb_stride = align256((size_t)s->max_batch * sizeof(int4));
+  L.sb = off;       off += 2 * L.sb_stride;                   // by layer parity
   L.total = off;
   return L;
 }
@@ -152,6 +155,8 @@ struct bacon_ctx {
   std::vector<int32_t> cu;
   int chunk_stages_override = 0;
   bool kr_off = false;   // key-register passes switched off (streaming passes only)
+  // test instrumentation (bacon_debug_capture): per-layer copies of B, V, lambda
+  float *cap_B = nullptr, *cap_V = nullptr, *cap_lambda = nullptr;
   // profiling
   bool prof = false;
   std::vector<hipEvent_t> ev_pool;
@@ -329,11 +334,12 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
 // Per-head budgets of the batch into the workspace table (budget, idx offset
 // within the sequence), or NULL with one budget per sequence.  The table rides
 // in the arguments of small kernels on the stream, ahead of the select.
-bacon_status head_table(bacon_ctx *c, const bacon_batch *bt, hipStream_t s, const int2 **out) {
+bacon_status head_table(bacon_ctx *c, const bacon_batch *bt, hipStream_t s, const int2 **out,
+                        int parity = 0) {
   *out = nullptr;
   if (!bt->head_budgets) return BACON_OK;
   const int hkv = c->shape.num_kv_heads;
-  int2 *dst = reinterpret_cast<int2 *>(c->ws + c->L.hb);
+  int2 *dst = reinterpret_cast<int2 *>(c->ws + c->L.hb + (size_t)parity * c->L.hb_stride);
   HbChunk ch{};
   const int n = bt->batch * hkv;
   int off = 0;
@@ -350,6 +356,22 @@ bacon_status head_table(bacon_ctx *c, const bacon_batch *bt, hipStream_t s, cons
     }
   }
   *out = dst;
+  return BACON_OK;
+}
+
+// The per-sequence budget fields (budget, idx base, kept-row base) of a
+// layer's batch into the workspace table of its parity, for the launches
+// that hold the jobs of two layers with different budgets.
+bacon_status seq_table(bacon_ctx *c, const SeqTable &st, hipStream_t s, const int4 **out, int parity) {
+  int2 *dst = reinterpret_cast<int2 *>(c->ws + c->L.sb + (size_t)parity * c->L.sb_stride);
+  HbChunk ch{};
+  for (int b = 0; b < st.batch; ++b) {
+    ch.v[ch.n++] = make_int2(st.budget[b], st.idx_base[b]);
+    ch.v[ch.n++] = make_int2(st.kept_base[b], 0);
+  }
+  const hipError_t e = launch_set_hb(ch, dst, s);
+  if (e != hipSuccess) return hip_fail(e, "budget table");
+  *out = reinterpret_cast<const int4 *>(dst);
   return BACON_OK;
 }
 
@@ -416,7 +438,7 @@ void bacon_default_params(bacon_params *p) {
   if (!p) return;
   p->radius = 5;
   p->persist_m = 4;
-  p->rho = 2.0f;
+  p->rho = 2.0;
   p->gamma = 1.0f;
   p->eps = 1e-12f;
   p->pool_kernel = 7;
@@ -761,6 +783,24 @@ bacon_status stage_tail(bacon_ctx *c, const LayerRun &r, hipStream_t s) {
   return timed(c, KI_FINAL, s, [&] { return launch_segfinal(r.g, r.st, r.kmax, s); });
 }
 
+// Test instrumentation: once r's layer has its lambda (after its score
+// stage), copies B, V and lambda into the capture buffers, before a later
+// launch overwrites them.
+bacon_status stage_capture(bacon_ctx *c, const LayerRun &r, const bacon_batch *bt, hipStream_t s) {
+  if (!c->cap_B) return BACON_OK;
+  const size_t vec = (size_t)c->shape.num_kv_heads * (size_t)bt->cu_seqlens[bt->batch];
+  const size_t sc = (size_t)bt->batch * c->shape.num_kv_heads;
+  hipError_t e = hipMemcpyAsync(c->cap_B + (size_t)r.layer * vec, r.g.vec_B, vec * sizeof(float),
+                                hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->cap_V + (size_t)r.layer * vec, r.g.vec_V, vec * sizeof(float),
+                       hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->cap_lambda + (size_t)r.layer * sc, r.g.lambda_ws, sc * sizeof(float),
+                       hipMemcpyDeviceToDevice, s);
+  return e == hipSuccess ? BACON_OK : hip_fail(e, "capture");
+}
+
 // The fused pass of one layer; d_lse (caller normalisers) skips pass 1.
 bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const void *d_q_win,
                       const void *d_k, const void *d_v, const float *d_lse, int32_t *d_idx,
@@ -771,10 +811,11 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   LayerRun r;
   TRY(plan_layer(c, layer, bt, d_q_win, d_k, d_v, d_lse, d_idx, d_k_out, d_v_out, r));
   hipStream_t s = static_cast<hipStream_t>(stream);
-  TRY(head_table(c, bt, s, &r.g.hb));
+  TRY(head_table(c, bt, s, &r.g.hb, layer & 1));
   TRY(stage_pass(c, r, false, nullptr, s));
   TRY(stage_a(c, r, nullptr, nullptr, s));
   TRY(stage_b(c, r, nullptr, s));
+  TRY(stage_capture(c, r, bt, s));
   TRY(stage_tail(c, r, s));
   c->next_layer = layer + 1;
   return BACON_OK;
@@ -803,7 +844,8 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
                                    int32_t num_layers, const void *const *d_q_win,
                                    const void *const *d_k, const void *const *d_v,
                                    const float *const *d_lse, int32_t *const *d_idx,
-                                   void *const *d_k_out, void *const *d_v_out, void *stream) {
+                                   void *const *d_k_out, void *const *d_v_out,
+                                   const bacon_batch *const *layer_batch, void *stream) {
   if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
   if (num_layers < 1) return fail(BACON_ERR_INVALID, "num_layers %d must be >= 1", num_layers);
   if (!d_q_win || !d_k || !d_v || !d_idx || !d_k_out || !d_v_out)
@@ -823,28 +865,38 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
     TRY(check_ptr(d_v_out[i], "v_out", 16));
     if (d_lse) TRY(check_ptr(d_lse[i], "lse", 4));
   }
-  // every layer is planned (and checked) before the first launch
+  // every layer is planned (and checked) before the first launch; a layer
+  // takes its own batch (budgets) when layer_batch is given
+  auto lbt = [&](int i) { return layer_batch ? layer_batch[i] : bt; };
+  if (layer_batch)
+    for (int i = 0; i < num_layers; ++i)
+      if (!layer_batch[i]) return fail(BACON_ERR_INVALID, "layer_batch[%d] is NULL", i);
   std::vector<LayerRun> runs(num_layers);
-  for (int i = 0; i < num_layers; ++i)
-    TRY(plan_layer(c, first_layer + i, bt, d_q_win[i], d_k[i], d_v[i], d_lse ? d_lse[i] : nullptr,
-                   d_idx[i], d_k_out[i], d_v_out[i], runs[i]));
+  int kmax = 0;
+  for (int i = 0; i < num_layers; ++i) {
+    TRY(plan_layer(c, first_layer + i, lbt(i), d_q_win[i], d_k[i], d_v[i],
+                   d_lse ? d_lse[i] : nullptr, d_idx[i], d_k_out[i], d_v_out[i], runs[i]));
+    kmax = std::max(kmax, runs[i].kmax);
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int2 *hb = nullptr;
-  TRY(head_table(c, bt, s, &hb));
-  for (LayerRun &r : runs) r.g.hb = hb;
   // Layers in flight at once: layer l's candidate lists run in the launch of
   // layer l+1's calibration, its final top-K and compaction in the launch of
   // layer l+1's scores (when that launch's LDS fits), and layer l+1's pass 1
-  // in the launch of layer l's pass 2.
-  const bool overlap = sel_b_lds_bytes(runs[0].kmax, c->shape.window) <= (size_t)kLdsBytes;
+  // in the launch of layer l's pass 2.  The per-head budget table of a
+  // layer (if any) alternates with its parity: it is written after the
+  // launch that held the final kernel of the layer two before.
+  const bool overlap = sel_b_lds_bytes(kmax, c->shape.window) <= (size_t)kLdsBytes;
   bool merged = false;
   for (int i = 0; i < num_layers; ++i) {
-    const LayerRun &r = runs[i];
+    LayerRun &r = runs[i];
+    TRY(head_table(c, lbt(i), s, &r.g.hb, r.layer & 1));
+    if (layer_batch) TRY(seq_table(c, r.st, s, &r.g.sb, r.layer & 1));
     const LayerRun *prev = (overlap && i > 0) ? &runs[i - 1] : nullptr;
     const PassArgs *next = (!r.lse && i + 1 < num_layers) ? &runs[i + 1].a : nullptr;
     TRY(stage_pass(c, r, merged, next, s));
     TRY(stage_a(c, r, prev, next, s));
     TRY(stage_b(c, r, prev, s));
+    TRY(stage_capture(c, r, lbt(i), s));
     if (!overlap) TRY(stage_tail(c, r, s));
     merged = next != nullptr;
     c->next_layer = r.layer + 1;
@@ -880,6 +932,21 @@ bacon_status bacon_window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d
     TRY(timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
   }
   TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
+  return BACON_OK;
+}
+
+bacon_status bacon_debug_capture(bacon_ctx *c, float *d_B, float *d_V, float *d_lambda) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  const int set = (d_B != nullptr) + (d_V != nullptr) + (d_lambda != nullptr);
+  if (set != 0 && set != 3) return fail(BACON_ERR_INVALID, "give all three capture buffers or none");
+  if (set) {
+    TRY(check_ptr(d_B, "B", 4));
+    TRY(check_ptr(d_V, "V", 4));
+    TRY(check_ptr(d_lambda, "lambda", 4));
+  }
+  c->cap_B = d_B;
+  c->cap_V = d_V;
+  c->cap_lambda = d_lambda;
   return BACON_OK;
 }
 

@@ -72,7 +72,8 @@ struct SelArgs {
   int64_t T;
   int radius, pool_half, pool_mode;
   int vp_chunk;            // chunk size of the in-chunk L partial in vec_VP
-  float rho, gamma, eps;
+  double rho;              // scale-matching expansion (double: M = floor(rho K) as the oracle forms it)
+  float gamma, eps;
   int use_last_query;
   uint32_t terms;
   const float *vec_B;      // [Hkv, T]
@@ -93,7 +94,8 @@ struct SegArgs {
   int Hkv, W;
   int64_t T;
   int radius, pool_half, pool_mode, vp_chunk;
-  float rho, gamma, eps;
+  double rho;                    // scale-matching expansion
+  float gamma, eps;
   int use_last_query;
   uint32_t terms;
   const float *vec_B, *vec_VP;   // [Hkv, T]
@@ -122,6 +124,9 @@ struct SegArgs {
   int row_bytes;
   int parts;                     // final-kernel workgroups per (sequence, KV head)
   const int2 *hb;                // optional [B, Hkv] (budget, idx offset in the sequence)
+  const int4 *sb;                // optional [B] (budget, idx base, kept-row base, 0) of this
+                                 // layer's batch, when it differs from the SeqTable's (a
+                                 // per-layer budget schedule: a launch holds two layers' jobs)
 };
 
 struct ElemArgs {           // split calibrate: E, T, L, ring update
@@ -143,13 +148,35 @@ struct CompactArgs {
   const int2 *hb;          // optional [B, Hkv] (budget, idx offset in the sequence)
 };
 
-// Budget and idx offset (within its sequence) of (sequence b, KV head h);
-// with one budget per sequence, hb is NULL.
-__host__ __device__ inline int head_budget(const SeqTable &st, const int2 *hb, int Hkv, int b, int h) {
-  return hb ? hb[b * Hkv + h].x : st.budget[b];
+// Size of the scale-matching set before the |I| cap (Sec. 4.4, Eq.
+// scale_matching_size): floor(rho K) with the product formed in double.
+__host__ __device__ inline int scale_set_size(double rho, int K) {
+  const double m = floor(rho * (double)K);
+  return m > 2147483647.0 ? 2147483647 : (int)m;
 }
-__host__ __device__ inline int64_t head_idx_base(const SeqTable &st, const int2 *hb, int Hkv, int b, int h) {
-  return (int64_t)st.idx_base[b] + (hb ? hb[b * Hkv + h].y : h * st.budget[b]);
+
+// Per-sequence budget fields of a layer's batch: from the table sb when
+// given, else from the SeqTable.  seq_budget is the largest budget of the
+// sequence's heads (its rows per head in the compacted cache, less W).
+__host__ __device__ inline int seq_budget(const SeqTable &st, const int4 *sb, int b) {
+  return sb ? sb[b].x : st.budget[b];
+}
+__host__ __device__ inline int seq_idx_base(const SeqTable &st, const int4 *sb, int b) {
+  return sb ? sb[b].y : st.idx_base[b];
+}
+__host__ __device__ inline int seq_kept_base(const SeqTable &st, const int4 *sb, int b) {
+  return sb ? sb[b].z : st.kept_base[b];
+}
+
+// Budget and idx offset of (sequence b, KV head h); with one budget per
+// sequence, hb is NULL.
+__host__ __device__ inline int head_budget(const SeqTable &st, const int2 *hb, int Hkv, int b, int h,
+                                           const int4 *sb = nullptr) {
+  return hb ? hb[b * Hkv + h].x : seq_budget(st, sb, b);
+}
+__host__ __device__ inline int64_t head_idx_base(const SeqTable &st, const int2 *hb, int Hkv, int b, int h,
+                                                 const int4 *sb = nullptr) {
+  return (int64_t)seq_idx_base(st, sb, b) + (hb ? hb[b * Hkv + h].y : h * seq_budget(st, sb, b));
 }
 
 // Writes n entries of a (budget, offset) table to dst[base ..] (device).

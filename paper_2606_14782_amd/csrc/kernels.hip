@@ -1618,7 +1618,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     }
     lds_barrier();
     // Scale-matching set: top M = min(rho K, |I|) of B over I (Eq. scale_matching_set).
-    int M = (int)floorf(a.rho * (float)K);
+    int M = scale_set_size(a.rho, K);
     if (M > nc) M = nc;
     if (M < 0) M = 0;
     const bool calib = M > 0 && a.use_last_query;
@@ -1666,11 +1666,19 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
         kmin = ((msk >> j) & 1ull) ? min(kmin, float_key(bv[j])) : kmin;
       kmin = block_reduce_u<0>(kmin, ss);
       const double bref = (double)key_float(kmin);
+      // V is shifted by the smallest V of the set as well: the variance is
+      // the same, and a set of equal V gives exactly 0
+      unsigned vmin = 0xffffffffu;
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        vmin = ((msk >> j) & 1ull) ? min(vmin, float_key(vp[j])) : vmin;
+      vmin = block_reduce_u<0>(vmin, ss);
+      const double vref = (double)key_float(vmin);
       double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         const bool in = (msk >> j) & 1ull;
-        const double db = in ? (double)bv[j] - bref : 0.0, dv = in ? (double)vp[j] : 0.0;
+        const double db = in ? (double)bv[j] - bref : 0.0, dv = in ? (double)vp[j] - vref : 0.0;
         s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
       }
       double sums[4];
@@ -1986,7 +1994,7 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
   const int64_t base = (int64_t)h * a.T + st.cu[b];
   const int r = a.radius;
   const bool use_l = (a.terms & 2u) != 0;
-  int M = (int)floorf(a.rho * (float)head_budget(st, a.hb, a.Hkv, b, h));
+  int M = scale_set_size(a.rho, head_budget(st, a.hb, a.Hkv, b, h, a.sb));
   M = max(0, min(M, nc));
   const bool calib = M > 0 && a.use_last_query;
   // the bins of the B histogram (accumulated by the fused pass, in kHCopies
@@ -2233,7 +2241,8 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
     msk |= (kj != 0u && (kj > xm || (kj == xm && posf(j) <= pm)) ? 1u : 0u) << j;
   }
   ordered_bases<kAllPer, NT>(msk, pre);
-  const double bref = (double)key_float(xm);
+  // both moments are taken from values shifted by the boundary member's
+  const double bref = (double)key_float(xm), vref = (double)a.vec_V[base + pm];
   for (int r0 = 0; r0 < M; r0 += kMomChunk) {
 #pragma unroll
     for (int j = 0; j < kAllPer; ++j) {
@@ -2247,7 +2256,7 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
     lds_barrier();
     const int cnt = min(kMomChunk, M - r0);
     for (int e = t; e < cnt; e += NT) {
-      const double db = (double)mom[e].x - bref, dv = (double)mom[e].y;
+      const double db = (double)mom[e].x - bref, dv = (double)mom[e].y - vref;
       s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
     }
     lds_barrier();
@@ -2267,6 +2276,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
   __shared__ unsigned pre[kAllPer * NW + 1];
   __shared__ float2 mom[kMomChunk];
   __shared__ __align__(16) int scnt[kMaxSegs];
+  __shared__ float vref_s;
   const int t = threadIdx.x;
   const int wave = t >> 6;
   const int b = find_seg(st, gs);
@@ -2295,7 +2305,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
     }
   }
 
-  int M = (int)floorf(a.rho * (float)head_budget(st, a.hb, a.Hkv, b, h));
+  int M = scale_set_size(a.rho, head_budget(st, a.hb, a.Hkv, b, h, a.sb));
   M = max(0, min(M, nc));
   float lam = 0.f;
   if (M > 0 && a.use_last_query) {
@@ -2315,13 +2325,18 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
       unsigned xm;
       int pm;
       rank_pick_bin<NT>(rec.w, rec.z, ckey, cpos, ss, xm, pm);
-      // population moments over the set, B shifted by its smallest member
-      // (the boundary key), in double
-      const double bref = (double)key_float(xm);
+      // population moments over the set in double, from values shifted by
+      // the boundary member's (its B is the set's smallest; the thread that
+      // holds the member posts its V): equal values give exactly 0
+#pragma unroll
+      for (int j = 0; j < kListPer; ++j)
+        if (lk[j] == xm && lp[j] == pm) vref_s = lv[j];
+      lds_barrier();
+      const double bref = (double)key_float(xm), vref = (double)vref_s;
 #pragma unroll
       for (int j = 0; j < kListPer; ++j) {
         if (lk[j] != 0u && (lk[j] > xm || (lk[j] == xm && lp[j] <= pm))) {
-          const double db = (double)key_float(lk[j]) - bref, dv = (double)lv[j];
+          const double db = (double)key_float(lk[j]) - bref, dv = (double)lv[j] - vref;
           s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
         }
       }
@@ -2411,7 +2426,7 @@ __device__ __forceinline__ void segcand_body(SegArgs a, const SeqTable &st, int 
   const int i0 = sg * kSegLen;
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  const int kept = min(head_budget(st, a.hb, a.Hkv, b, h), nc);
+  const int kept = min(head_budget(st, a.hb, a.Hkv, b, h, a.sb), nc);
   if (kept <= 0 || kept == nc) return;               // none or all kept: no list needed
   unsigned cb[kHPer];
   load_bins<1>(a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, cb);
@@ -2500,11 +2515,11 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
   const int wave = t >> 6;
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
-  const int K = head_budget(st, a.hb, a.Hkv, b, h);  // this head's budget
-  const int C = st.budget[b];                         // rows per head of the sequence, less W
+  const int K = head_budget(st, a.hb, a.Hkv, b, h, a.sb);   // this head's budget
+  const int C = seq_budget(st, a.sb, b);                   // rows per head of the sequence, less W
   const int kept = min(K, nc);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  int32_t *idx = a.idx + head_idx_base(st, a.hb, a.Hkv, b, h);
+  int32_t *idx = a.idx + head_idx_base(st, a.hb, a.Hkv, b, h, a.sb);
   if (kept > 0 && kept == nc) {
     // every candidate is kept
     for (int j = t; j < nc; j += NT) {
@@ -2592,7 +2607,7 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
       const int q = q0 + u * NT;
       if (q < total) {
         const int rr = r0 + q / pieces, p = q % pieces;
-        const int64_t dst = ((int64_t)(st.kept_base[b] + rr) * a.Hkv + h) * a.row_bytes + 16 * p;
+        const int64_t dst = ((int64_t)(seq_kept_base(st, a.sb, b) + rr) * a.Hkv + h) * a.row_bytes + 16 * p;
         const u32x4 z = u32x4{0u, 0u, 0u, 0u};
         *reinterpret_cast<u32x4 *>(ko + dst) = srcs[u] >= 0 ? kv[u] : z;
         *reinterpret_cast<u32x4 *>(vo + dst) = srcs[u] >= 0 ? vv[u] : z;

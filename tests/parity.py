@@ -9,8 +9,18 @@ import numpy as np
 from oracle import ref
 from paper_2606_14782_amd import inputs
 
-# Score tolerance: |x - x_ref| <= RTOL * (|x_ref| + mean |x_ref|)
+# Score tolerance: |x - x_ref| <= RTOL * (|x_ref| + mean |x_ref|) element by
+# element; near the selection boundaries the scores are also held to the
+# plain relative bound |x - x_ref| <= RTOL * |x_ref| (check_near_boundary).
 RTOL = {"fp32": 1e-5, "bf16": 1e-2}
+
+# A (sequence, KV head) whose oracle gaps at the M-th (scale-matching set)
+# and K-th (kept set) boundaries both exceed GAP_TOL relative must have
+# exactly the oracle's kept set.  The GPU's scores come from the same exact
+# inputs in fp32 with hardware exp2 and differ from the fp64 oracle by about
+# 1e-6 relative; GAP_TOL leaves a hundredfold margin.  Closer boundaries may
+# swap positions whose pooled scores agree within RTOL of the K-th score.
+GAP_TOL = 1e-4
 
 
 def log(*a):
@@ -76,13 +86,32 @@ def _head_budgets(wl, hb):
     return np.repeat(np.asarray(wl.budgets, np.int64)[:, None], wl.num_kv_heads, axis=1)
 
 
-def check_idx(name, got, r, wl, rtol, hb=None):
-    """Kept sets equal the oracle's except for positions whose pooled oracle
-    score is within rtol of the K-th kept score; also counts strict matches.
-    hb: optional per-(sequence, KV head) budgets [batch, Hkv]."""
+def rel_gap(vals, k):
+    """Relative gap between the k-th and (k+1)-th largest of vals; inf when
+    either does not exist (nothing to swap across)."""
+    n = len(vals)
+    if k <= 0 or k >= n:
+        return np.inf
+    part = np.partition(np.asarray(vals, np.float64), [n - k - 1, n - k])
+    a, c = part[n - k], part[n - k - 1]
+    return float((a - c) / max(abs(a), 1e-300))
+
+
+def check_idx(name, got, r, wl, rtol, hb=None, strict=False, stats=None):
+    """Kept sets against the oracle's.  With strict, or where the oracle's
+    relative gaps at the M-th boundary of B and at the K-th boundary of the
+    pooled score both exceed GAP_TOL, the set must be the oracle's exactly
+    (ties then follow score descending, position ascending); elsewhere it may
+    differ only in positions whose pooled oracle score is within rtol of the
+    K-th kept score.  hb: optional per-(sequence, KV head) budgets [batch,
+    Hkv].  Returns (and accumulates into stats) counts of pairs, exact sets,
+    pairs held to exactness, and swaps."""
     W, Hkv = wl.window, wl.num_kv_heads
     bh = _head_budgets(wl, hb)
-    stats = {"pairs": 0, "strict": 0, "swaps": 0}
+    if stats is None:
+        stats = {}
+    for key in ("pairs", "strict", "gated", "swaps"):
+        stats.setdefault(key, 0)
     off = 0
     for b, (s0, s1) in enumerate(seq_slices(wl)):
         nc = (s1 - s0) - W
@@ -98,10 +127,19 @@ def check_idx(name, got, r, wl, rtol, hb=None):
             assert kept == 0 or (gk.min() >= 0 and gk.max() < nc), f"{name} b{b} h{h}: range"
             gs, os_ = set(gk.tolist()), set(o[:kept].tolist())
             stats["pairs"] += 1
+            P = r["S_pool"][h, s0:s0 + nc]
+            M = int(r["m_count"][b, h])
+            exact = strict or (rel_gap(P, K) > GAP_TOL and
+                               (M == 0 or rel_gap(r["B"][h, s0:s0 + nc], M) > GAP_TOL))
+            stats["gated"] += int(exact)
             if gs == os_:
                 stats["strict"] += 1
                 continue
-            P = r["S_pool"][h, s0:s0 + nc]
+            assert not exact, (
+                f"{name} b{b} h{h}: kept set differs from the oracle's where it must be exact "
+                f"(strict={strict}, K-gap {rel_gap(P, K):.3g}, M-gap "
+                f"{rel_gap(r['B'][h, s0:s0 + nc], M):.3g}); GPU-only {sorted(gs - os_)[:8]}, "
+                f"oracle-only {sorted(os_ - gs)[:8]}")
             pK = float(P[list(os_)].min())
             for i in gs ^ os_:
                 assert abs(P[i] - pK) <= rtol * abs(pK), (
@@ -109,6 +147,37 @@ def check_idx(name, got, r, wl, rtol, hb=None):
                     f"K-th {pK:.9g}")
             stats["swaps"] += len(gs - os_)
     return stats
+
+
+def box_pool(x, k):
+    """Centred average of odd width k over x, truncated at the ends, in fp64
+    (the pooling convention; used on the GPU's unpooled scores)."""
+    x = np.asarray(x, np.float64)
+    n, half = len(x), k // 2
+    c = np.concatenate([[0.0], np.cumsum(x)])
+    i = np.arange(n)
+    lo, hi = np.maximum(i - half, 0), np.minimum(i + half, n - 1)
+    return (c[hi + 1] - c[lo]) / (hi - lo + 1)
+
+
+def check_near_boundary(name, got, want, order_by, k, rtol, width=32):
+    """The plain relative bound |x - x_ref| <= rtol |x_ref| on the positions the
+    oracle ranks k - width .. k + width by order_by (score descending, position
+    ascending): the scores the selection turns on."""
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    n = len(want)
+    if n == 0 or k <= 0:
+        return 0.0
+    k = min(k, n)
+    rank = np.lexsort((np.arange(n), -np.asarray(order_by, np.float64)))
+    sel = rank[max(0, k - width):min(n, k + width)]
+    err = np.abs(got[sel] - want[sel])
+    bad = err > rtol * np.abs(want[sel])
+    assert not bad.any(), (f"{name}: {int(bad.sum())} of {len(sel)} near-boundary values beyond "
+                           f"rtol {rtol}: first at position {int(sel[np.argmax(bad)])}, "
+                           f"{got[sel][bad][0]:.9g} vs {want[sel][bad][0]:.9g}")
+    return float(np.max(err / np.maximum(np.abs(want[sel]), 1e-300)))
 
 
 def gather_rows(x_bytes, idx, wl, hb=None):

@@ -131,19 +131,27 @@ def test_calls_reject_bad_batches_and_order_before_enqueueing():
     # prompt call: pointer arrays, layer range, order
     arr1 = (C.c_void_p * 1)(0x200000)
     assert L.bacon_compress_prompt(h, C.byref(good.c), 0, 1, None, arr1, arr1, None, arr1, arr1,
-                                   arr1, None) == bacon.ERR_INVALID
+                                   arr1, None, None) == bacon.ERR_INVALID
     assert L.bacon_compress_prompt(h, C.byref(good.c), 0, 0, arr1, arr1, arr1, None, arr1, arr1,
-                                   arr1, None) == bacon.ERR_INVALID
+                                   arr1, None, None) == bacon.ERR_INVALID
     assert L.bacon_compress_prompt(h, C.byref(good.c), 1, 1, arr1, arr1, arr1, None, arr1, arr1,
-                                   arr1, None) == bacon.ERR_ORDER
+                                   arr1, None, None) == bacon.ERR_ORDER
     assert L.bacon_compress_prompt(h, C.byref(good.c), 0, 9, arr1, arr1, arr1, None, arr1, arr1,
-                                   arr1, None) == bacon.ERR_ORDER
+                                   arr1, None, None) == bacon.ERR_ORDER
     bad = (C.c_void_p * 1)(0x200002)
     assert L.bacon_compress_prompt(h, C.byref(good.c), 0, 1, arr1, arr1, arr1, bad, arr1, arr1,
-                                   arr1, None) == bacon.ERR_INVALID
+                                   arr1, None, None) == bacon.ERR_INVALID
     # no prompt begun -> ORDER, before anything is enqueued
     assert L.bacon_compress_prompt(h, C.byref(good.c), 0, 1, arr1, arr1, arr1, None, arr1, arr1,
-                                   arr1, None) == bacon.ERR_ORDER
+                                   arr1, None, None) == bacon.ERR_ORDER
+    # a per-layer batch array with a NULL entry
+    nolb = (C.c_void_p * 1)(None)
+    assert L.bacon_compress_prompt(h, C.byref(good.c), 0, 1, arr1, arr1, arr1, None, arr1, arr1,
+                                   arr1, nolb, None) == bacon.ERR_INVALID
+    # capture buffers: all three or none
+    assert L.bacon_debug_capture(h, fake, None, fake) == bacon.ERR_INVALID
+    assert L.bacon_debug_capture(h, fake, fake, C.c_void_p(0x200002)) == bacon.ERR_INVALID
+    assert L.bacon_debug_capture(h, None, None, None) == bacon.OK
     # window normalisers alone: NULL or misaligned pointers, short sequences
     assert L.bacon_window_lse(h, C.byref(good.c), fake, fake, None, None) == bacon.ERR_INVALID
     assert L.bacon_window_lse(h, C.byref(good.c), fake, fake, C.c_void_p(0x200002),

@@ -87,6 +87,49 @@ def test_gqa_scores_are_group_means(oracle):
     assert np.allclose(dup["B"], s0["B"], atol=TOL, rtol=0)
 
 
+def test_packed_gqa_layer_slices_match_raw_tensors(oracle):
+    """Layer-level input slicing of the oracle: a packed batch of three
+    sequences of unequal lengths with a group of three query heads per KV
+    head.  For every (sequence, KV head), B, Q and the window-row normalisers
+    recomputed here from the raw packed tensors -- q_win [B*W, Hq, d] (row
+    b*W + w is position N_b - W + w; query head h*G + g belongs to KV head h)
+    and k [T, Hkv, d] at offsets cu_seqlens -- by a dense masked softmax
+    (scipy) equal the layer call's outputs (Sec. 4.1, Eqs. window_score,
+    last_query_score; App. A)."""
+    from scipy.special import logsumexp
+    Hq, Hkv, d, W = 6, 2, 16, 5
+    G = Hq // Hkv
+    lens = (23, 41, 9)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    q = _rand((len(lens) * W, Hq, d), 31)
+    k = _rand((int(cu[-1]), Hkv, d), 32)
+    p = oracle.Prompt(1, Hq, Hkv, d, W, 1, cu, np.array([3, 3, 3], np.int32))
+    r = p.layer(0, q, k)
+    for b, n in enumerate(lens):
+        c0 = int(cu[b])
+        for h in range(Hkv):
+            qs = q[b * W:(b + 1) * W, h * G:(h + 1) * G, :].astype(np.float64)   # [W, G, d]
+            ks = k[c0:c0 + n, h, :].astype(np.float64)                           # [n, d]
+            logits = np.einsum("wgc,ic->gwi", qs, ks) / math.sqrt(d)
+            pos = n - W + np.arange(W)
+            logits = np.where((np.arange(n)[None, :] > pos[:, None])[None], -np.inf, logits)
+            A = softmax(logits, axis=2)
+            assert np.allclose(r["B"][h, c0:c0 + n], A.mean(axis=(0, 1)), atol=TOL, rtol=0)
+            assert np.allclose(r["Q"][h, c0:c0 + n], A[:, W - 1, :].mean(axis=0), atol=TOL, rtol=0)
+            assert np.allclose(r["lse"][b, h * G:(h + 1) * G, :], logsumexp(logits, axis=2),
+                               atol=1e-12, rtol=0)
+    # nothing of another sequence leaks in: a change to sequence 1's keys
+    # leaves sequences 0 and 2 bit for bit
+    k2 = k.copy()
+    k2[cu[1]:cu[2]] *= np.float32(1.5)
+    r2 = oracle.Prompt(1, Hq, Hkv, d, W, 1, cu, np.array([3, 3, 3], np.int32)).layer(0, q, k2)
+    for b in (0, 2):
+        sl = slice(int(cu[b]), int(cu[b + 1]))
+        assert np.array_equal(r["B"][:, sl], r2["B"][:, sl])
+        assert np.array_equal(r["Q"][:, sl], r2["Q"][:, sl])
+    assert not np.allclose(r["B"][:, cu[1]:cu[2]], r2["B"][:, cu[1]:cu[2]])
+
+
 # --------------------------------------------------------------- residual E
 
 def test_residual_is_half_total_variation(oracle):
