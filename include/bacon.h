@@ -252,6 +252,24 @@ bacon_status bacon_compress_prompt(bacon_ctx *ctx, const bacon_batch *batch, int
 bacon_status bacon_window_lse(bacon_ctx *ctx, const bacon_batch *batch, const void *d_q_win,
                               const void *d_k, float *d_lse, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * bacon_window_lse without a context or workspace.  Writes d_lse [B, Hq, W]
+ * exactly as bacon_window_lse does (the same kernels).  The per-chunk
+ * partials and the merged normalisers live in a static device scratch of
+ * 4 MiB per GPU, which the library holds from the first call on that GPU
+ * until the process ends; a batch whose scratch (num_kv_heads * key chunks
+ * * padded window rows * 8 bytes, plus the merged normalisers) exceeds it
+ * returns BACON_ERR_WORKSPACE before anything is enqueued.  The call
+ * allocates nothing.  Every call on a GPU shares that GPU's scratch: calls
+ * that overlap on one GPU (other streams, other threads) race.  shape gives
+ * the model (max_batch and max_total_tokens bound the batch as for a
+ * context); the method parameters are irrelevant to the normalisers.
+ * Pointer and batch checks as for bacon_window_lse. */
+bacon_status bacon_window_lse_static(const bacon_shape *shape, const bacon_batch *batch,
+                                     const void *d_q_win, const void *d_k, float *d_lse,
+                                     void *stream);
+
 /* Test instrumentation of the fused calls (bacon_compress_layer, _lse and
  * bacon_compress_prompt), whose intermediates otherwise stay in the
  * workspace: with all three pointers set, every later layer l of those calls

@@ -22,7 +22,7 @@ ENTRY_POINTS = [
     "bacon_default_params", "bacon_workspace_bytes", "bacon_init", "bacon_free",
     "bacon_begin_prompt", "bacon_score", "bacon_calibrate", "bacon_select_topk",
     "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_compress_prompt",
-    "bacon_window_lse", "bacon_debug_capture",
+    "bacon_window_lse", "bacon_window_lse_static", "bacon_debug_capture",
     "bacon_idx_count",
     "bacon_kept_rows",
     "bacon_profile_enable", "bacon_profile_read", "bacon_status_string", "bacon_last_error",
@@ -90,6 +90,7 @@ def lib() -> C.CDLL:
         L.bacon_compress_prompt.argtypes = [vp, C.POINTER(Batch), C.c_int32, C.c_int32, vp, vp, vp,
                                             vp, vp, vp, vp, vp, vp]
         L.bacon_debug_capture.argtypes = [vp, vp, vp, vp]
+        L.bacon_window_lse_static.argtypes = [C.POINTER(Shape), C.POINTER(Batch), vp, vp, vp, vp]
         L.bacon_idx_count.argtypes = [C.POINTER(Batch), C.c_int32]
         L.bacon_idx_count.restype = C.c_int64
         L.bacon_kept_rows.argtypes = [C.POINTER(Batch), C.c_int32, C.c_int32]
@@ -103,7 +104,7 @@ def lib() -> C.CDLL:
         for name in ("bacon_init", "bacon_free", "bacon_begin_prompt", "bacon_score",
                      "bacon_calibrate", "bacon_select_topk", "bacon_compact",
                      "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_window_lse",
-                     "bacon_compress_prompt", "bacon_debug_capture",
+                     "bacon_compress_prompt", "bacon_debug_capture", "bacon_window_lse_static",
                      "bacon_profile_enable"):
             getattr(L, name).restype = C.c_int
         _lib = L
@@ -341,6 +342,17 @@ def bacon_compress_layer_lse(ctx: Context, layer, batch, q_win, k, v, lse, out=N
 def bacon_compress_prompt(ctx: Context, first_layer, batch, q_wins, ks, vs, lses=None, outs=None,
                           layer_batches=None):
     return ctx.bacon_compress_prompt(first_layer, batch, q_wins, ks, vs, lses, outs, layer_batches)
+
+
+def bacon_window_lse_static(shape: Shape, batch: BatchLayout, q_win, k, out=None):
+    """bacon_window_lse without a context or workspace (static device scratch);
+    returns lse [B, Hq, W] (out if given)."""
+    import torch
+    lse = out if out is not None else torch.empty(
+        (batch.c.batch, shape.num_q_heads, shape.window), dtype=torch.float32, device=k.device)
+    _check(lib().bacon_window_lse_static(C.byref(shape), C.byref(batch.c), _ptr(q_win), _ptr(k),
+                                         _ptr(lse), _stream()))
+    return lse
 
 
 def bacon_debug_capture(ctx: Context, B=None, V=None, lam=None):

@@ -319,12 +319,14 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   a.chunk = chunk;
   a.T = s.max_total_tokens;
   a.c2 = (float)(1.4426950408889634 / std::sqrt((double)s.head_dim));
-  a.partials = reinterpret_cast<float2 *>(c->ws + c->L.partials);
-  a.lse2 = reinterpret_cast<float *>(c->ws + c->L.lse2);
-  a.hist_B = reinterpret_cast<unsigned *>(c->ws + c->L.hist_b);
-  a.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
-  a.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
-  a.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
+  if (c->ws) {   // a context over no workspace (the static-scratch call) sets its own
+    a.partials = reinterpret_cast<float2 *>(c->ws + c->L.partials);
+    a.lse2 = reinterpret_cast<float *>(c->ws + c->L.lse2);
+    a.hist_B = reinterpret_cast<unsigned *>(c->ws + c->L.hist_b);
+    a.ring = reinterpret_cast<float *>(c->ws + c->L.ring);
+    a.vec_B = reinterpret_cast<float *>(c->ws + c->L.vec_b);
+    a.vec_VP = reinterpret_cast<float *>(c->ws + c->L.vec_vp);
+  }
   a.radius = c->params.radius;
   a.terms = c->params.terms;
   (void)st;
@@ -905,9 +907,17 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
   return BACON_OK;
 }
 
-bacon_status bacon_window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d_q_win,
-                              const void *d_k, float *d_lse, void *stream) {
-  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+}  // extern "C"
+
+namespace {
+
+// The window-row normalisers of one layer: pass 1 and the merge.  With
+// scratch NULL the per-chunk partials and merged normalisers go to the
+// context's workspace; otherwise to scratch (scratch_bytes long), which is
+// checked before anything is enqueued.
+bacon_status window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d_q_win, const void *d_k,
+                        float *d_lse, void *stream, char *scratch, size_t scratch_bytes,
+                        bool lookup_scratch) {
   TRY(check_batch(c, bt));
   TRY(check_ptr(d_q_win, "q_win", 16));
   TRY(check_ptr(d_k, "k", 16));
@@ -926,6 +936,20 @@ bacon_status bacon_window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d
   PassArgs a = pass_args(c, st, chunk, d_q_win, d_k);
   a.T = bt->cu_seqlens[bt->batch];
   a.lse_user = d_lse;
+  if (lookup_scratch) {
+    // partials [Hkv, chunks, Rpad] float2, then the merged normalisers [B, Hkv, Rpad]
+    const size_t part = align256((size_t)c->shape.num_kv_heads * st.total_chunks * c->L.rpad * sizeof(float2));
+    const size_t need = part + align256((size_t)bt->batch * c->shape.num_kv_heads * c->L.rpad * sizeof(float));
+    if (need > scratch_bytes)
+      return fail(BACON_ERR_WORKSPACE, "the batch needs %zu bytes of scratch; the static scratch holds %zu",
+                  need, scratch_bytes);
+    void *p = nullptr;
+    const hipError_t e = static_scratch(&p);
+    if (e != hipSuccess) return hip_fail(e, "static scratch");
+    scratch = static_cast<char *>(p);
+    a.partials = reinterpret_cast<float2 *>(scratch);
+    a.lse2 = reinterpret_cast<float *>(scratch + part);
+  }
   if (kr) {
     TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, bf16, c->shape.head_dim, false, a, st, s); }));
   } else {
@@ -933,6 +957,30 @@ bacon_status bacon_window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d
   }
   TRY(timed(c, KI_MERGE, s, [&] { return launch_lse_merge(a, st, s); }));
   return BACON_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+bacon_status bacon_window_lse(bacon_ctx *c, const bacon_batch *bt, const void *d_q_win,
+                              const void *d_k, float *d_lse, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  return window_lse(c, bt, d_q_win, d_k, d_lse, stream, nullptr, 0, false);
+}
+
+bacon_status bacon_window_lse_static(const bacon_shape *shape, const bacon_batch *bt,
+                                     const void *d_q_win, const void *d_k, float *d_lse,
+                                     void *stream) {
+  // a context on the stack, over no workspace: nothing is allocated
+  TRY(check_shape(shape));
+  bacon_ctx c;
+  c.shape = *shape;
+  bacon_default_params(&c.params);
+  c.L = layout_of(shape, &c.params);
+  c.ws = nullptr;
+  c.ws_bytes = 0;
+  return window_lse(&c, bt, d_q_win, d_k, d_lse, stream, nullptr, kStaticScratchBytes, true);
 }
 
 bacon_status bacon_debug_capture(bacon_ctx *c, float *d_B, float *d_V, float *d_lambda) {

@@ -22,6 +22,8 @@ constexpr int kHCopies = 1;         // copies of the B histogram the fused pass 
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU (and per workgroup) on gfx950
 constexpr int kEdgeEntries = 1024;      // positions next to chunk boundaries the select stages
 constexpr int kKrWaves = 4;             // waves of a key-register pass workgroup
+// Static device scratch of the allocation-free entry point (per GPU).
+constexpr size_t kStaticScratchBytes = 4u << 20;
 
 // Per-sequence layout, passed by value to every kernel.
 struct SeqTable {
@@ -232,5 +234,8 @@ size_t final_lds_bytes(int max_budget, int window);
 hipError_t launch_segfinal(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s);
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_zero(unsigned *p, int64_t n, hipStream_t s);
+// Device address of the static scratch on the current device (looked up
+// once per device); kStaticScratchBytes long.
+hipError_t static_scratch(void **ptr);
 
 }  // namespace bacon

@@ -152,6 +152,17 @@ def test_calls_reject_bad_batches_and_order_before_enqueueing():
     assert L.bacon_debug_capture(h, fake, None, fake) == bacon.ERR_INVALID
     assert L.bacon_debug_capture(h, fake, fake, C.c_void_p(0x200002)) == bacon.ERR_INVALID
     assert L.bacon_debug_capture(h, None, None, None) == bacon.OK
+    # the static-scratch normalisers: a batch whose scratch exceeds the static
+    # array is refused before the GPU is touched; a bad shape is refused
+    wide = _shape(num_q_heads=256, num_kv_heads=64, window=32, max_total_tokens=1 << 20,
+                  max_batch=1)
+    assert L.bacon_window_lse_static(C.byref(wide), C.byref(_batch([0, 32768], [4]).c), fake, fake,
+                                     fake, None) == bacon.ERR_WORKSPACE
+    assert b"static scratch" in L.bacon_last_error()
+    assert L.bacon_window_lse_static(C.byref(_shape(head_dim=96)), C.byref(good.c), fake, fake, fake,
+                                     None) == bacon.ERR_UNSUPPORTED
+    assert L.bacon_window_lse_static(None, C.byref(good.c), fake, fake, fake,
+                                     None) == bacon.ERR_INVALID
     # window normalisers alone: NULL or misaligned pointers, short sequences
     assert L.bacon_window_lse(h, C.byref(good.c), fake, fake, None, None) == bacon.ERR_INVALID
     assert L.bacon_window_lse(h, C.byref(good.c), fake, fake, C.c_void_p(0x200002),
