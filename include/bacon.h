@@ -285,6 +285,13 @@ bacon_status bacon_window_lse_static(const bacon_shape *shape, const bacon_batch
  * (the default); a mix of NULL and non-NULL is INVALID. */
 bacon_status bacon_debug_capture(bacon_ctx *ctx, float *d_B, float *d_V, float *d_lambda);
 
+/* Test instrumentation: waits for the device, then returns the context's
+ * device error word: 0, or 1 if a meeting of the single-read K pass ran out
+ * of its bounded wait (the results of that call are then unspecified; the
+ * next bacon_begin_prompt clears the word); -1 if it cannot be read.
+ * Synchronises the device, unlike every other call. */
+int32_t bacon_debug_device_errors(bacon_ctx *ctx);
+
 /* Sizes of the outputs for a batch: idx entries and compacted rows. */
 int64_t bacon_idx_count(const bacon_batch *batch, int32_t num_kv_heads);
 int64_t bacon_kept_rows(const bacon_batch *batch, int32_t num_kv_heads, int32_t window);

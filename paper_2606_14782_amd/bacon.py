@@ -22,7 +22,7 @@ ENTRY_POINTS = [
     "bacon_default_params", "bacon_workspace_bytes", "bacon_init", "bacon_free",
     "bacon_begin_prompt", "bacon_score", "bacon_calibrate", "bacon_select_topk",
     "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_compress_prompt",
-    "bacon_window_lse", "bacon_window_lse_static", "bacon_debug_capture",
+    "bacon_window_lse", "bacon_window_lse_static", "bacon_debug_capture", "bacon_debug_device_errors",
     "bacon_idx_count",
     "bacon_kept_rows",
     "bacon_profile_enable", "bacon_profile_read", "bacon_status_string", "bacon_last_error",
@@ -90,6 +90,8 @@ def lib() -> C.CDLL:
         L.bacon_compress_prompt.argtypes = [vp, C.POINTER(Batch), C.c_int32, C.c_int32, vp, vp, vp,
                                             vp, vp, vp, vp, vp, vp]
         L.bacon_debug_capture.argtypes = [vp, vp, vp, vp]
+        L.bacon_debug_device_errors.argtypes = [vp]
+        L.bacon_debug_device_errors.restype = C.c_int32
         L.bacon_window_lse_static.argtypes = [C.POINTER(Shape), C.POINTER(Batch), vp, vp, vp, vp]
         L.bacon_idx_count.argtypes = [C.POINTER(Batch), C.c_int32]
         L.bacon_idx_count.restype = C.c_int64
@@ -283,6 +285,10 @@ class Context:
             arr([o[0] for o in outs]), arr([o[1] for o in outs]), arr([o[2] for o in outs]),
             lb_arr, _stream()))
         return outs
+
+    def bacon_debug_device_errors(self) -> int:
+        """Test instrumentation: the device error word (synchronises)."""
+        return int(lib().bacon_debug_device_errors(self._h))
 
     def bacon_debug_capture(self, B=None, V=None, lam=None):
         """Test instrumentation: per-layer copies of B, V [L, Hkv, T] and lambda

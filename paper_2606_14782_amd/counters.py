@@ -37,6 +37,7 @@ _NAMES = [
     (r"bacon::k_krpass<2,", "window_score_calib_kr"),
     (r"bacon::k_krdual<", "window_score_calib_lse_kr"),
     (r"bacon::k_pass_dual<", "window_score_calib_lse"),
+    (r"bacon::k_single<", "window_score_single"),
     (r"bacon::k_sel_a\b", "segment_calib_cand"),
     (r"bacon::k_sel_b\b", "segment_score_final"),
     (r"bacon::k_segcal\b", "segment_calib"),

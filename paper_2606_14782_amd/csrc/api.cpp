@@ -37,7 +37,8 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
   size_t ring, vec_b, vec_vp, vec_v, vec_pb, vec_pv, vec_s, hist_b, hist_s, list_bk, list_bp, list_bv,
-      list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, hb, sb, total;
+      list_sk, list_sp, cnt_b, cnt_s, rec_b, rec_s, partials, lse2, lambda, hb, sb, sync, total;
+  size_t sync_bytes;
   size_t vec_s_stride, hist_b_stride, hist_s_stride, hb_stride, sb_stride;   // the two copies by layer parity
   int rpad, slots;
   int64_t chunks_cap;
@@ -109,6 +110,13 @@ Layout layout_of(const bacon_shape *s, const bacon_params *p) {
   L.hist_b_stride = align256(hist * kHCopies);
   L.hist_s_stride = align256(hist);
   L.hist_b = off;   off += 2 * L.hist_b_stride;                // by layer parity
+  // meeting words of the single-read pass (arrival and done counters per
+  // (sequence, KV head) on lines of their own, the error word, the published
+  // row normalisers), right after the B histograms so that one clearing
+  // launch covers both
+  L.sync_bytes = align256((size_t)(kSyncStride * s->max_batch * s->num_kv_heads + 1) * sizeof(unsigned)) +
+                 align256((size_t)s->max_batch * s->num_kv_heads * L.rpad * sizeof(unsigned));
+  L.sync = off;     off += L.sync_bytes;
   L.hist_s = off;   off += 2 * L.hist_s_stride;
   L.list_bk = off;  off += align256(vec);
   L.list_bp = off;  off += align256(vec);
@@ -137,10 +145,10 @@ const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", 
                               "calib_elem",    "compact",       "window_lse_kr",
                               "window_score_calib_kr", "window_score_calib_lse_kr",
                               "segment_calib_cand", "segment_score_final",
-                              "window_score_calib_lse"};
+                              "window_score_calib_lse", "window_score_single"};
 enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
                 KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_DUAL_KR,
-                KI_SEL_A, KI_SEL_B, KI_DUAL, KI_COUNT };
+                KI_SEL_A, KI_SEL_B, KI_DUAL, KI_SINGLE, KI_COUNT };
 
 }  // namespace
 
@@ -155,6 +163,8 @@ struct bacon_ctx {
   std::vector<int32_t> cu;
   int chunk_stages_override = 0;
   bool kr_off = false;   // key-register passes switched off (streaming passes only)
+  bool single_off = false;   // single-read pass switched off (two K passes)
+  int single_cap = -1;       // single-read workgroups the device holds at once (-1: not yet asked)
   // test instrumentation (bacon_debug_capture): per-layer copies of B, V, lambda
   float *cap_B = nullptr, *cap_V = nullptr, *cap_lambda = nullptr;
   // profiling
@@ -329,6 +339,12 @@ PassArgs pass_args(const bacon_ctx *c, const SeqTable &st, int chunk, const void
   }
   a.radius = c->params.radius;
   a.terms = c->params.terms;
+  if (c->ws) {
+    a.sync = reinterpret_cast<unsigned *>(c->ws + c->L.sync);
+    a.sync_groups = c->shape.max_batch * c->shape.num_kv_heads;
+    a.bcast = reinterpret_cast<unsigned *>(
+        c->ws + c->L.sync + align256((size_t)(kSyncStride * a.sync_groups + 1) * sizeof(unsigned)));
+  }
   (void)st;
   return a;
 }
@@ -478,6 +494,7 @@ bacon_status bacon_init(bacon_ctx **ctx, const bacon_shape *shape, const bacon_p
   c->L = L;
   if (const char *e = std::getenv("BACON_CHUNK_STAGES")) c->chunk_stages_override = std::atoi(e);
   if (const char *e = std::getenv("BACON_KEY_REGISTERS")) c->kr_off = std::atoi(e) == 0;
+  if (const char *e = std::getenv("BACON_SINGLE")) c->single_off = std::atoi(e) == 0;
   *ctx = c;
   return BACON_OK;
 }
@@ -496,8 +513,10 @@ bacon_status bacon_begin_prompt(bacon_ctx *c, const bacon_batch *bt, void *strea
 
   // layer 0 reads no history; the B histogram of the select starts at zero
   // (each layer's final kernel clears it for the next)
+  // (each layer's final kernel clears it for the next), and so do the
+  // meeting counters of the single-read pass
   const hipError_t e = launch_zero(reinterpret_cast<unsigned *>(c->ws + c->L.hist_b),
-                                   (int64_t)(2 * c->L.hist_b_stride / sizeof(unsigned)),
+                                   (int64_t)((2 * c->L.hist_b_stride + c->L.sync_bytes) / sizeof(unsigned)),
                                    static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "clear");
   c->prompt = true;
@@ -635,7 +654,7 @@ namespace {
 // Everything the launches of one layer of the fused pass need.
 struct LayerRun {
   int layer = 0;
-  bool bf16 = false, w32 = false, kr = false;
+  bool bf16 = false, w32 = false, kr = false, single = false;
   int chunk = 0, kmax = 0;
   SeqTable st{};
   PassArgs a{};
@@ -673,6 +692,17 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
     r.st = make_table(c, bt, &r.chunk, false);
     TRY(check_lds(c, bt, r.chunk, true, -1));
   }
+  // One read of K (the single-read pass) when its meeting can complete:
+  // workgroups run in grid order, chunk-major with the KV heads innermost,
+  // so at most the groups of one sequence are incomplete at a time, and
+  // all their chunks must fit on the GPU at once.  With normalisers given
+  // by the caller the key-register pass 2 alone already reads K once.
+  if (r.kr && !d_lse && !c->single_off) {
+    if (c->single_cap < 0) c->single_cap = single_resident_blocks(c->shape.head_dim, c->L.rpad);
+    int nmax = 0;
+    for (int b = 0; b < bt->batch; ++b) nmax = std::max(nmax, r.st.chunk_base[b + 1] - r.st.chunk_base[b]);
+    r.single = (int64_t)nmax * c->shape.num_kv_heads <= c->single_cap;
+  }
   r.kmax = 0;
   for (int b = 0; b < bt->batch; ++b) r.kmax = std::max(r.kmax, batch_seq_rows(bt, c->shape.num_kv_heads, b));
   if (final_lds_bytes(r.kmax, c->shape.window) > (size_t)kLdsBytes)
@@ -699,6 +729,9 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
   g.rho = c->params.rho;
   g.gamma = c->params.gamma;
   g.eps = c->params.eps;
+  // B of the single-read pass is formed from probabilities stored in fp16
+  // (unit roundoff 2^-11); the passes that keep them in fp32 leave B exact
+  g.b_floor = r.single ? 0x1p-11f : 0.f;
   g.use_last_query = c->params.use_last_query;
   g.terms = c->params.terms;
   g.vec_B = a.vec_B;
@@ -742,6 +775,8 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
 bacon_status stage_pass(bacon_ctx *c, const LayerRun &r, bool lse_merged, const PassArgs *next,
                         hipStream_t s) {
   const int d = c->shape.head_dim;
+  if (r.single)
+    return timed(c, KI_SINGLE, s, [&] { return launch_single(d, r.w32, r.a, r.st, s); });
   if (r.kr) {
     if (!r.lse && !lse_merged) {
       TRY(timed(c, KI_LSE_KR, s, [&] { return launch_krpass(PASS_LSE, r.bf16, d, false, r.a, r.st, s); }));
@@ -894,7 +929,10 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
     TRY(head_table(c, lbt(i), s, &r.g.hb, r.layer & 1));
     if (layer_batch) TRY(seq_table(c, r.st, s, &r.g.sb, r.layer & 1));
     const LayerRun *prev = (overlap && i > 0) ? &runs[i - 1] : nullptr;
-    const PassArgs *next = (!r.lse && i + 1 < num_layers) ? &runs[i + 1].a : nullptr;
+    // the next layer's pass 1 rides in this layer's pass-2 launch, unless the
+    // next layer reads K once (single-read pass) or has its normalisers given
+    const PassArgs *next = (!r.lse && !r.single && i + 1 < num_layers && !runs[i + 1].single)
+                               ? &runs[i + 1].a : nullptr;
     TRY(stage_pass(c, r, merged, next, s));
     TRY(stage_a(c, r, prev, next, s));
     TRY(stage_b(c, r, prev, s));
@@ -981,6 +1019,16 @@ bacon_status bacon_window_lse_static(const bacon_shape *shape, const bacon_batch
   c.ws = nullptr;
   c.ws_bytes = 0;
   return window_lse(&c, bt, d_q_win, d_k, d_lse, stream, nullptr, kStaticScratchBytes, true);
+}
+
+int32_t bacon_debug_device_errors(bacon_ctx *c) {
+  if (!c || !c->ws) return -1;
+  unsigned v = 0;
+  const size_t off = c->L.sync + (size_t)kSyncStride * c->shape.max_batch * c->shape.num_kv_heads * sizeof(unsigned);
+  if (hipDeviceSynchronize() != hipSuccess ||
+      hipMemcpy(&v, c->ws + off, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess)
+    return -1;
+  return (int32_t)v;
 }
 
 bacon_status bacon_debug_capture(bacon_ctx *c, float *d_B, float *d_V, float *d_lambda) {

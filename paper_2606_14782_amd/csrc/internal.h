@@ -22,6 +22,7 @@ constexpr int kHCopies = 1;         // copies of the B histogram the fused pass 
 constexpr int kLdsBytes = 160 * 1024;   // LDS per CU (and per workgroup) on gfx950
 constexpr int kEdgeEntries = 1024;      // positions next to chunk boundaries the select stages
 constexpr int kKrWaves = 4;             // waves of a key-register pass workgroup
+constexpr int kSyncStride = 64;          // words between groups' meeting counters (own 256-byte lines)
 // Static device scratch of the allocation-free entry point (per GPU).
 constexpr size_t kStaticScratchBytes = 4u << 20;
 
@@ -64,6 +65,13 @@ struct PassArgs {
   float *vec_VP;        // [Hkv, T] unused by the fused pass (the calibration kernel forms V)
   int radius;
   uint32_t terms;
+  // single-read pass: per group (sequence, KV head) an arrival and a done
+  // counter at sync[kSyncStride * group + {0, 1}], the error word at
+  // sync[kSyncStride * sync_groups], and the published row normalisers
+  // (bitwise complement of the float; 0 = not yet) at bcast[group * Rpad + row]
+  unsigned *sync;
+  unsigned *bcast;
+  int sync_groups;
 };
 
 enum SelMode { SEL_CALIB = 1, SEL_TOPK = 2 };
@@ -98,6 +106,10 @@ struct SegArgs {
   int radius, pool_half, pool_mode, vp_chunk;
   double rho;                    // scale-matching expansion
   float gamma, eps;
+  // relative rounding bound of B (0 when B is exact to fp32): a set whose
+  // Std(B) is at most b_floor times its mean B has no spread B resolves, and
+  // takes Std(B) = 0
+  float b_floor;
   int use_last_query;
   uint32_t terms;
   const float *vec_B, *vec_VP;   // [Hkv, T]
@@ -210,6 +222,13 @@ hipError_t launch_pass_dual(bool bf16, int head_dim, bool w32, const PassArgs &a
 // Pass 2 of one layer (a2) with pass 1 of the next layer (a1) in one launch.
 hipError_t launch_krdual(bool bf16, int head_dim, bool w32, const PassArgs &a2, const PassArgs &a1,
                          const SeqTable &st, hipStream_t s);
+// Single-read pass (bf16, up to 128 window rows): one launch per layer that
+// reads K once; needs a.sync (zeroed) and every chunk of the sequence's
+// groups resident at once (see single_resident_blocks).
+hipError_t launch_single(int head_dim, bool w32, const PassArgs &a, const SeqTable &st, hipStream_t s);
+// Workgroups of the single-read pass the device holds at once (0 if unknown).
+int single_resident_blocks(int head_dim, int rpad);
+int single_lds_bytes(int head_dim, int rpad);
 // LDS a select workgroup needs (static + dynamic) for sequences up to max_len.
 size_t select_lds_bytes(int mode, int max_len);
 hipError_t launch_select(int mode, int max_len, const SelArgs &a, const SeqTable &st,

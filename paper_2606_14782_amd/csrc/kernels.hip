@@ -82,6 +82,13 @@ __device__ __forceinline__ float tree_sum16(const float *x) {
   const float a2 = (x[8] + x[9]) + (x[10] + x[11]), a3 = (x[12] + x[13]) + (x[14] + x[15]);
   return (a0 + a1) + (a2 + a3);
 }
+__device__ __forceinline__ float tree_min16(const float *x) {
+  const float a0 = fminf(fminf(x[0], x[1]), fminf(x[2], x[3]));
+  const float a1 = fminf(fminf(x[4], x[5]), fminf(x[6], x[7]));
+  const float a2 = fminf(fminf(x[8], x[9]), fminf(x[10], x[11]));
+  const float a3 = fminf(fminf(x[12], x[13]), fminf(x[14], x[15]));
+  return fminf(fminf(a0, a1), fminf(a2, a3));
+}
 __device__ __forceinline__ float tree_max16(const float *x) {
   const float a0 = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
   const float a1 = fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7]));
@@ -1046,6 +1053,525 @@ hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const Pass
   if (mode == PASS_LSE)
     return head_dim == 128 ? launch_kr_d<PASS_LSE, 128>(false, a, st, s) : launch_kr_d<PASS_LSE, 64>(false, a, st, s);
   return head_dim == 128 ? launch_kr_d<PASS_FUSED, 128>(w32, a, st, s) : launch_kr_d<PASS_FUSED, 64>(w32, a, st, s);
+}
+
+// ---------------------------------------------------------------- single-read pass
+// One read of K per layer (bf16 keys, up to 128 window rows).  A workgroup of
+// kKrWaves waves holds kr_keys() keys of one KV head, loaded straight into
+// registers in the MFMA operand layout, as in the key-register passes.
+//
+//  * Pass 1 (D = K Q^T, a lane per query row) forms the probabilities of each
+//    key tile against the row's running max, which both halves of the wave
+//    share, and keeps them in registers as fp16 (the key registers of a tile
+//    are free once its MFMAs have run, so the register count of keys plus
+//    probabilities stays that of the keys).  What is stored is p - p_min
+//    times 2^15, p_min the smallest probability of the row in the tile: never
+//    less precise than p itself (0 <= p - p_min <= p), and far more precise
+//    where attention is near uniform and the residual Q - B cancels.  The max
+//    each tile used and p_min go to LDS.
+//  * The chunks of a (sequence, KV head) meet once: each publishes its
+//    per-row (max, sum) partial through to memory (agent-scope stores),
+//    counts itself on the group's arrival counter, and when all have arrived
+//    every workgroup merges all partials in chunk order into the same row
+//    normalisers.  The last workgroup to finish reading resets the counters.
+//    The waits are bounded: one that runs out sets the error word and goes
+//    on.  Workgroups are dispatched in grid order, chunk-major with the KV
+//    heads innermost, so the groups not yet complete are those of one
+//    sequence; the host launches this pass only when their chunks fit on the
+//    GPU at once.
+//  * Pass 2 turns each stored 32x32 block around with two MFMAs against the
+//    identity (a lane per key, the rows in registers), weights every row by
+//    exp2(tile max - lse) / 2^15 and sums the rows in-lane, and adds the
+//    tile's sum of the weighted p_min: B and Q without a second read of K or
+//    a second exp.  The tail (E to the history, B out,
+//    the B histogram) is that of the key-register pass 2.
+constexpr float kPScaleLog2 = 15.f;          // stored probabilities are p * 2^15 (<= 2^15)
+constexpr unsigned kMeetSpin = 1u << 20;     // polls of a published word before giving up
+
+__device__ __forceinline__ void store_agent(float2 *p, float2 v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long *>(p), __builtin_bit_cast(unsigned long long, v),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_agent(const float2 *p) {
+  return __builtin_bit_cast(float2, __hip_atomic_load(reinterpret_cast<const unsigned long long *>(p),
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ void store_agent(float *p, float v) {
+  __hip_atomic_store(reinterpret_cast<unsigned *>(p), __builtin_bit_cast(unsigned, v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_agent(const float *p) {
+  return __builtin_bit_cast(float, __hip_atomic_load(reinterpret_cast<const unsigned *>(p), __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT));
+}
+
+__device__ __forceinline__ void pin8(unsigned (&v)[8]) {
+  asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
+               "+v"(v[7]));
+}
+
+__device__ __forceinline__ unsigned pack_f16(float lo, float hi) {
+  typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+  const f16x2 v = {(_Float16)lo, (_Float16)hi};
+  return __builtin_bit_cast(unsigned, v);
+}
+
+// LDS map of a single-read workgroup (bytes), NR = 32 * row tiles:
+//   qbuf  max(NR * ROWB, 4 * kHBins)      window queries; the B histogram after pass 2
+//   part  max(kKrWaves * NR, NT) float2   per-wave row partials; merge scratch
+//   fac   kKrWaves * KT * NR floats       the max each tile used; then its row factors
+//   rmn   kKrWaves * KT * NR floats       p_min * 2^15 of each row in each tile
+//   lse   NR floats                       merged row normalisers (log2 units)
+//   cb    KPW floats                      B of the chunk's keys
+int single_lds_bytes(int head_dim, int rpad) {
+  const int nr = 32 * kr_row_tiles(rpad), rowb = head_dim * 2, kpw = kr_keys(true, head_dim);
+  const int kt = kpw / (32 * kKrWaves);
+  return std::max(nr * rowb, 4 * kHBins) + 8 * std::max(kKrWaves * nr, 64 * kKrWaves) +
+         8 * kKrWaves * kt * nr + 4 * nr + 4 * kpw;
+}
+
+template <int D, bool W32, int NRT>
+__global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTable st) {
+  using C = PassCfg<true, D>;
+  constexpr int NU = C::NU, KT = KrCfg<true, D>::KT, KPW = KrCfg<true, D>::KPW;
+  constexpr int NT = 64 * kKrWaves, NR = 32 * NRT;
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int s_go;
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63, half = lane >> 5, l32 = lane & 31;
+  const int h = (int)blockIdx.x % a.Hkv, gchunk = (int)blockIdx.x / a.Hkv;
+  const int b = find_seq(st, gchunk);
+  const int c = gchunk - st.chunk_base[b];
+  const int n = st.cu[b + 1] - st.cu[b];
+  const int nch = st.chunk_base[b + 1] - st.chunk_base[b];
+  const int k0 = c * KPW, k1 = min(n, k0 + KPW);
+  const int W = a.W, wfirst = n - W;
+  const int64_t vrow = (int64_t)h * a.T + st.cu[b];      // [Hkv, T] index of the sequence's position 0
+  const int grp = b * a.Hkv + h;
+
+  unsigned char *qbuf = smem;
+  float2 *part = reinterpret_cast<float2 *>(smem + max(NR * C::ROWB, 4 * kHBins));
+  float *fac = reinterpret_cast<float *>(part + max(kKrWaves * NR, NT));
+  float *rmn = fac + kKrWaves * KT * NR;
+  float *lse = rmn + kKrWaves * KT * NR;
+  float *cb = lse + NR;
+
+  // ---- loads: the window queries, the first key tile, and once the queries
+  // are in LDS the other key tiles (as in the key-register passes)
+  constexpr int QP = NR * C::PIECES / NT;
+  u32x4 qv[QP];
+#pragma unroll
+  for (int j = 0; j < QP; ++j) {
+    const int i = t + j * NT, row = i / C::PIECES, pc = i % C::PIECES;
+    const int rr = min(row, a.R - 1), g = rr / W, w = rr - g * W;
+    qv[j] = *reinterpret_cast<const u32x4 *>(static_cast<const unsigned char *>(a.q) +
+        ((int64_t)(b * W + w) * a.Hq + (int64_t)h * a.G + g) * C::ROWB + 16 * pc);
+  }
+  const int64_t kstride = (int64_t)a.Hkv * C::ROWB;
+  const unsigned char *kb = static_cast<const unsigned char *>(a.k) +
+                            ((int64_t)st.cu[b] * a.Hkv + h) * C::ROWB + 16 * half;
+  u32x4 kr[KT][NU];
+  auto load_tile = [&](int kt) {
+    const int key = min(k0 + (wave * KT + kt) * 32 + l32, k1 - 1);
+    const unsigned char *kp = kb + (int64_t)key * kstride;
+#pragma unroll
+    for (int u = 0; u < NU; ++u) kr[kt][u] = *reinterpret_cast<const u32x4 *>(kp + 32 * u);
+  };
+  asm volatile("" ::: "memory");
+  load_tile(0);
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int j = 0; j < QP; ++j) pin(qv[j]);
+#pragma unroll
+  for (int j = 0; j < QP; ++j) {
+    const int i = t + j * NT, row = i / C::PIECES, pc = i % C::PIECES;
+    *reinterpret_cast<u32x4 *>(qbuf + row * C::ROWB + 16 * (pc ^ (row & C::SWM))) = qv[j];
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int kt = 1; kt < KT; ++kt) load_tile(kt);
+  asm volatile("" ::: "memory");
+
+  int koff[NU];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) koff[u] = l32 * C::ROWB + 16 * ((2 * u + half) ^ (l32 & C::SWM));
+
+  // ---- pass 1: probabilities of each tile against the running row max, two
+  // row tiles at a time (their accumulators and query fragments are what the
+  // stored probabilities leave of the register file); the max each tile used
+  // goes to LDS
+  constexpr int RG = NRT < 2 ? NRT : 2;
+  unsigned pk[KT][NRT][8];          // fp16 pairs: keys acc_row(2q, half), acc_row(2q + 1, half)
+  float m_run[NRT], l_run[NRT];
+#pragma unroll
+  for (int j = 0; j < NRT; ++j) { m_run[j] = -INFINITY; l_run[j] = 0.f; }
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    const int kbase = k0 + (wave * KT + kt) * 32;
+    const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
+#pragma unroll
+    for (int j0 = 0; j0 < NRT; j0 += RG) {
+      f32x16 acc[RG];
+#pragma unroll
+      for (int j = 0; j < RG; ++j) acc[j] = f32x16{};
+      {
+        u32x4 qf[2][RG];
+#pragma unroll
+        for (int j = 0; j < RG; ++j)
+          qf[0][j] = *reinterpret_cast<const u32x4 *>(qbuf + (j0 + j) * 32 * C::ROWB + koff[0]);
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+          if (u + 1 < NU) {
+#pragma unroll
+            for (int j = 0; j < RG; ++j)
+              qf[(u + 1) & 1][j] = *reinterpret_cast<const u32x4 *>(qbuf + (j0 + j) * 32 * C::ROWB + koff[u + 1]);
+          }
+#pragma unroll
+          for (int j = 0; j < RG; ++j) acc[j] = mfma_unit<true>(kr[kt][u], qf[u & 1][j], acc[j]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      // acc[j][reg]: key kbase + acc_row(reg, half), row (j0 + j)*32 + l32.
+      // Tiles away from the sequence end and the window take the unmasked
+      // form; the two forms are separate branches, which also keeps the
+      // compiler from issuing every tile's MFMAs ahead of the exps.
+      auto post = [&](bool masked) {
+#pragma unroll
+        for (int jj = 0; jj < RG; ++jj) {
+          const int j = j0 + jj;
+          const int r = j * 32 + l32;
+          float av[16];
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) av[reg] = acc[jj][reg];
+          if (masked) {
+            const int tpos = wfirst + (r < a.R ? r % W : W - 1);
+#pragma unroll
+            for (int reg = 0; reg < 16; ++reg) {
+              const int key = kbase + acc_row(reg, half);
+              if (!(key < k1 && key <= tpos)) av[reg] = -INFINITY;
+            }
+          }
+          float mt = tree_max16(av), lo = tree_min16(av);
+          mt = fmaxf(mt, xor32(mt, half));
+          lo = fminf(lo, xor32(lo, half));
+          const float mn = fmaxf(m_run[j], mt);
+          const float off = (mn == -INFINITY ? 0.f : -mn * a.c2) + kPScaleLog2;
+          float ev[16];
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) ev[reg] = __builtin_amdgcn_exp2f(fmaf(av[reg], a.c2, off));
+          l_run[j] = fmaf(l_run[j], __builtin_amdgcn_exp2f(fmaf(m_run[j], a.c2, off - kPScaleLog2)),
+                          tree_sum16(ev) * (1.f / 32768.f));
+          m_run[j] = mn;
+          // the tile's smallest probability of the row (0 when a key of the
+          // tile is masked), the same exp as its element's
+          const float pmin = __builtin_amdgcn_exp2f(fmaf(lo, a.c2, off));
+          if (half == 0) {
+            fac[(wave * KT + kt) * NR + r] = mn;
+            rmn[(wave * KT + kt) * NR + r] = pmin;
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q) pk[kt][j][q] = pack_f16(ev[2 * q] - pmin, ev[2 * q + 1] - pmin);
+          // the packed probabilities as formed here: keeps the compiler
+          // from sinking the exps to their uses in pass 2
+          pin8(pk[kt][j]);
+        }
+      };
+      if (edge) post(true); else post(false);
+    }
+  }
+  // the wave's (max, sum) per row (log2 units; both halves share the max)
+#pragma unroll
+  for (int j = 0; j < NRT; ++j) {
+    const float l = l_run[j] + xor32(l_run[j], half);
+    if (half == 0)
+      part[wave * NR + j * 32 + l32] = make_float2(m_run[j] == -INFINITY ? -INFINITY : m_run[j] * a.c2, l);
+  }
+  __syncthreads();
+  // the workgroup's partial of each row (waves in order), written through
+  const int64_t pbase = ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad;
+  if (t < a.Rpad) {
+    float mx = -INFINITY, sx = 0.f;
+    for (int w = 0; w < kKrWaves; ++w) mx = fmaxf(mx, part[w * NR + t].x);
+    if (mx != -INFINITY)
+      for (int w = 0; w < kKrWaves; ++w) {
+        const float2 pw = part[w * NR + t];
+        if (pw.x != -INFINITY) sx += pw.y * __builtin_amdgcn_exp2f(pw.x - mx);
+      }
+    store_agent(a.partials + pbase + (int64_t)c * a.Rpad + t, make_float2(mx, sx));
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __syncthreads();
+
+  // ---- the meeting of the chunks of (b, h).  The last workgroup to arrive
+  // merges the group's partials in chunk order and publishes the row
+  // normalisers; the others poll their rows of the published words (the
+  // complement of the float's bits, never 0 for a finite value or +inf, so
+  // 0 means not yet), backing off between polls.
+  unsigned *arrive = a.sync + kSyncStride * grp, *done = arrive + 1;
+  unsigned *pub = a.bcast + (int64_t)grp * a.Rpad;
+  if (t == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_go = prev + 1 == (unsigned)nch;
+  }
+  __syncthreads();
+  if (s_go) {
+    // thread t takes row t % Rpad over the chunks congruent to t / Rpad,
+    // 16 loads in flight
+    constexpr int FL = 16;
+    const int parts = NT / a.Rpad, row = t % a.Rpad, pp = t / a.Rpad;
+    float mm = -INFINITY, ll = 0.f;
+    if (pp < parts) {
+      const float2 *src = a.partials + pbase + row;
+      for (int c0 = pp; c0 < nch; c0 += FL * parts) {
+        float2 v[FL];
+#pragma unroll
+        for (int j = 0; j < FL; ++j) v[j] = load_agent(src + (int64_t)min(c0 + j * parts, nch - 1) * a.Rpad);
+#pragma unroll
+        for (int j = 0; j < FL; ++j)
+          if (c0 + j * parts >= nch) v[j] = make_float2(-INFINITY, 0.f);
+        float mb = mm;
+#pragma unroll
+        for (int j = 0; j < FL; ++j) mb = fmaxf(mb, v[j].x);
+        if (mb != -INFINITY) {
+          float acc = (mm == -INFINITY) ? 0.f : ll * __builtin_amdgcn_exp2f(mm - mb);
+#pragma unroll
+          for (int j = 0; j < FL; ++j)
+            if (v[j].x != -INFINITY) acc += v[j].y * __builtin_amdgcn_exp2f(v[j].x - mb);
+          ll = acc;
+          mm = mb;
+        }
+      }
+    }
+    part[t] = make_float2(mm, ll);
+    __syncthreads();
+    if (t < a.Rpad) {
+      float mx = -INFINITY, sx = 0.f;
+      for (int q = 0; q < parts; ++q) mx = fmaxf(mx, part[q * a.Rpad + t].x);
+      if (mx != -INFINITY)
+        for (int q = 0; q < parts; ++q) {
+          const float2 pq = part[q * a.Rpad + t];
+          if (pq.x != -INFINITY) sx += pq.y * __builtin_amdgcn_exp2f(pq.x - mx);
+        }
+      const float l2 = (t < a.R) ? mx + log2f(sx) : INFINITY;
+      lse[t] = l2;
+      __hip_atomic_store(pub + t, ~__builtin_bit_cast(unsigned, l2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      a.lse2[(int64_t)grp * a.Rpad + t] = l2;
+      if (a.lse_user && t < a.R) {
+        const int g = t / W, w = t - g * W;
+        a.lse_user[((int64_t)b * a.Hq + (int64_t)h * a.G + g) * W + w] = l2 * kLn2;
+      }
+    }
+  } else if (t < a.Rpad) {
+    unsigned v, polls = 0;
+    while ((v = __hip_atomic_load(pub + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == 0u) {
+      __builtin_amdgcn_s_sleep(16);
+      if (++polls == kMeetSpin) {
+        __hip_atomic_store(a.sync + kSyncStride * a.sync_groups, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+    }
+    lse[t] = __builtin_bit_cast(float, ~v);
+  }
+  if (t >= a.Rpad && t < NR) lse[t] = INFINITY;   // rows of the last tile past Rpad: factor 0
+  __syncthreads();
+  if (t == 0) {
+    // the normalisers are read: the last workgroup of the group to get here
+    // clears the counters and the published words for the next launch
+    const unsigned prev = __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_go = prev + 1 == (unsigned)nch;
+    if (s_go) {
+      __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  __syncthreads();
+  if (s_go && t < a.Rpad) __hip_atomic_store(pub + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // row factors of every (wave, tile): exp2(tile max - lse) / 2^15; zero for
+  // pad rows (lse = +inf) and rows with no key so far (max = -inf)
+  for (int e = t; e < kKrWaves * KT * NR; e += NT) {
+    const float m = fac[e], l2 = lse[e % NR];
+    fac[e] = (m == -INFINITY || l2 == INFINITY) ? 0.f
+                                                : __builtin_amdgcn_exp2f(fmaf(m, a.c2, -l2) - kPScaleLog2);
+  }
+  __syncthreads();
+
+  // ---- pass 2: B and Q of the wave's keys from the stored probabilities.
+  // Identity operands: the A operand of block (kt, j) holds, in lane l, the
+  // probabilities of row l % 32 for keys 4h + (s & 3) + 8 (s >> 2) of k-slot
+  // 8h + s (h = l / 32); operand kb maps them to keys 16 kb + ...; lane l of
+  // the identity holds a 1 where its column l % 32 is that key.
+  u32x4 idop[2];
+  {
+    const int np = l32 & 15, aa = np >> 3, bb = (np >> 2) & 1, cc = np & 3, slot = 4 * aa + cc;
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2) {
+      unsigned w4[4] = {0u, 0u, 0u, 0u};
+      if ((l32 >> 4) == kb2 && bb == half) w4[slot >> 1] = (slot & 1) ? 0x3C000000u : 0x00003C00u;
+      idop[kb2] = u32x4{w4[0], w4[1], w4[2], w4[3]};
+    }
+  }
+  uint32_t lastm[NRT];
+#pragma unroll
+  for (int j = 0; j < NRT; ++j) {
+    lastm[j] = 0;
+    if constexpr (!W32) {
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) {
+        const int r = j * 32 + acc_row(reg, half);
+        if (r < a.R && (r % W) == W - 1) lastm[j] |= 1u << reg;
+      }
+    }
+  }
+  typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+  // per tile: the sum over the rows of factor * p_min (into B) and over the
+  // last-query rows (into Q), reduced across the wave in a fixed order
+  float cB[KT], cQ[KT];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    float sb = 0.f, sq = 0.f;
+    for (int r = lane; r < NR; r += 64) {
+      const float v = fac[(wave * KT + kt) * NR + r] * rmn[(wave * KT + kt) * NR + r];
+      sb += v;
+      sq += (r < a.R && (r % W) == W - 1) ? v : 0.f;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      sb += __shfl_xor(sb, o);
+      sq += __shfl_xor(sq, o);
+    }
+    cB[kt] = sb;
+    cQ[kt] = sq;
+  }
+  float bsum[KT], qsum[KT];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) { bsum[kt] = 0.f; qsum[kt] = 0.f; }
+#pragma unroll
+  for (int j = 0; j < NRT; ++j) {
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      f32x16 d = f32x16{};
+      d = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+          __builtin_bit_cast(f16x8, u32x4{pk[kt][j][0], pk[kt][j][1], pk[kt][j][2], pk[kt][j][3]}),
+          __builtin_bit_cast(f16x8, idop[0]), d, 0, 0, 0);
+      d = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+          __builtin_bit_cast(f16x8, u32x4{pk[kt][j][4], pk[kt][j][5], pk[kt][j][6], pk[kt][j][7]}),
+          __builtin_bit_cast(f16x8, idop[1]), d, 0, 0, 0);
+      // d[reg]: row j*32 + acc_row(reg, half), key kbase + l32
+      const float *fr = fac + (wave * KT + kt) * NR + j * 32 + 4 * half;
+      float f[16];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 v = *reinterpret_cast<const float4 *>(fr + 8 * i);
+        f[4 * i + 0] = v.x; f[4 * i + 1] = v.y; f[4 * i + 2] = v.z; f[4 * i + 3] = v.w;
+      }
+      float pr[16];
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) pr[reg] = f[reg] * d[reg];
+      bsum[kt] += tree_sum16(pr);
+      if constexpr (W32) {
+        qsum[kt] += half ? pr[15] : 0.f;
+      } else {
+#pragma unroll
+        for (int reg = 0; reg < 16; ++reg) qsum[kt] += ((lastm[j] >> reg) & 1u) ? pr[reg] : 0.f;
+      }
+      // one block at a time: issued all at once the transposes would hold
+      // every block's 16 result registers
+      asm volatile("" : "+v"(bsum[kt]), "+v"(qsum[kt]));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  const float inv_gw = 1.f / (float)(a.G * W), inv_g = 1.f / (float)a.G;
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    const float bs = (bsum[kt] + xor32(bsum[kt], half)) + cB[kt];
+    const float qs = (qsum[kt] + xor32(qsum[kt], half)) + cQ[kt];
+    const int key = k0 + (wave * KT + kt) * 32 + l32;
+    const int kl = (wave * KT + kt) * 32 + l32;
+    if ((kt & 1) == half && key < k1) {
+      const float Bv = bs * inv_gw, Qv = qs * inv_g;
+      const int64_t pos = vrow + key;
+      // E (Eq. boundary_residual) to this layer's history slot
+      a.ring[a.ring_write * a.ring_stride + pos] = (Qv > Bv) ? (Qv - Bv) : 0.f;
+      a.vec_B[pos] = Bv;
+      cb[kl] = Bv;
+    }
+  }
+  __syncthreads();
+
+  // B histogram of the chunk's candidates (as in the key-register pass 2)
+  unsigned *hist = reinterpret_cast<unsigned *>(qbuf);
+  const int ncnd = max(0, min(k1, wfirst) - k0);
+  int blo = kHBins, bhi = -1;
+  for (int p = t; p < ncnd; p += NT) {
+    const int q = hbin(float_key(cb[p]));
+    blo = min(blo, q);
+    bhi = max(bhi, q);
+  }
+  blo = __reduce_min_sync(~0ull, blo);
+  bhi = __reduce_max_sync(~0ull, bhi);
+  int *mm2 = reinterpret_cast<int *>(part);
+  if (lane == 0) { mm2[wave] = blo; mm2[kKrWaves + wave] = bhi; }
+  __syncthreads();
+  blo = kHBins;
+  bhi = -1;
+  for (int w = 0; w < kKrWaves; ++w) {
+    blo = min(blo, mm2[w]);
+    bhi = max(bhi, mm2[kKrWaves + w]);
+  }
+  for (int q = blo + t; q <= bhi; q += NT) hist[q] = 0u;
+  __syncthreads();
+  for (int p = t; p < ncnd; p += NT) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
+  __syncthreads();
+  const int copy = (h * st.total_chunks + gchunk) % kHCopies;
+  unsigned *gh = a.hist_B + (((int64_t)b * a.Hkv + h) * kHCopies + copy) * kHBins;
+  for (int q = blo + t; q <= bhi; q += NT) {
+    const unsigned cnt = hist[q];
+    if (cnt) atomicAdd(&gh[q], cnt);
+  }
+}
+
+template <int D, bool W32, int NRT>
+static hipError_t launch_single_t(const PassArgs &a, const SeqTable &st, hipStream_t s) {
+  const int lds = single_lds_bytes(D, a.Rpad);
+  if (lds > kLdsBytes / 2) return hipErrorInvalidValue;
+  auto kern = k_single<D, W32, NRT>;
+  allow_lds(kern, lds);
+  hipLaunchKernelGGL(kern, dim3(st.total_chunks * a.Hkv), dim3(64 * kKrWaves), lds, s, a, st);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_single_d(bool w32, const PassArgs &a, const SeqTable &st, hipStream_t s) {
+  if (kr_row_tiles(a.Rpad) == 2)
+    return w32 ? launch_single_t<D, true, 2>(a, st, s) : launch_single_t<D, false, 2>(a, st, s);
+  return w32 ? launch_single_t<D, true, 4>(a, st, s) : launch_single_t<D, false, 4>(a, st, s);
+}
+
+hipError_t launch_single(int head_dim, bool w32, const PassArgs &a, const SeqTable &st, hipStream_t s) {
+  if (!kr_supported(true, head_dim, a.Rpad) || !a.sync || !a.bcast) return hipErrorInvalidValue;
+  return head_dim == 128 ? launch_single_d<128>(w32, a, st, s) : launch_single_d<64>(w32, a, st, s);
+}
+
+int single_resident_blocks(int head_dim, int rpad) {
+  const int lds = single_lds_bytes(head_dim, rpad);
+  int per_cu = 0;
+  hipError_t e;
+  if (head_dim == 128)
+    e = kr_row_tiles(rpad) == 2
+            ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_single<128, true, 2>, 64 * kKrWaves, lds)
+            : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_single<128, true, 4>, 64 * kKrWaves, lds);
+  else
+    e = kr_row_tiles(rpad) == 2
+            ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_single<64, true, 2>, 64 * kKrWaves, lds)
+            : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_single<64, true, 4>, 64 * kKrWaves, lds);
+  if (e != hipSuccess) return 0;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  return per_cu * cus;
 }
 
 // ---------------------------------------------------------------- block helpers
@@ -2261,7 +2787,7 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
     }
     lds_barrier();
   }
-  part[0] = s0; part[1] = s1; part[2] = s2; part[3] = s3;
+  part[0] = s0; part[1] = s1; part[2] = s2; part[3] = s3; part[4] = bref;
 }
 
 // Score kernel (segment_score).
@@ -2316,7 +2842,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
     ListView L;
     load_lists<true>(st, b, base, n, h, a.recB + b * a.Hkv + h, a.listB_key, a.listB_pos, a.listB_v,
                      a.cntB, scnt, L, rec, lk, lp, lv);
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0, bref_set = 0.0;
     if (L.fits && rec.w <= kSegCandCap) {
       // the boundary bin's entries, ranked under the tie rule
       compact_ballot<kListPer, NT, kSegCandCap>([&](int j) { return lk[j] != 0u && hbin(lk[j]) == rec.x; },
@@ -2333,6 +2859,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
         if (lk[j] == xm && lp[j] == pm) vref_s = lv[j];
       lds_barrier();
       const double bref = (double)key_float(xm), vref = (double)vref_s;
+      bref_set = bref;
 #pragma unroll
       for (int j = 0; j < kListPer; ++j) {
         if (lk[j] != 0u && (lk[j] > xm || (lk[j] == xm && lp[j] <= pm))) {
@@ -2341,9 +2868,10 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
         }
       }
     } else {
-      double part[4];
+      double part[5];
       whole_moments(a, base, nc, M, a.hist_B + hrow * kHCopies, ss, ckey, cpos, pre, mom, part);
       s0 = part[0]; s1 = part[1]; s2 = part[2]; s3 = part[3];
+      bref_set = part[4];
     }
     double sums[4];
     block_sum4_d(s0, s1, s2, s3, ss, sums);
@@ -2351,6 +2879,8 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
     double vb = sums[1] / M - mb * mb, vv = sums[3] / M - mv * mv;
     vb = vb > 0.0 ? vb : 0.0;
     vv = vv > 0.0 ? vv : 0.0;
+    // a spread of B within its rounding is none (B equal in exact arithmetic)
+    if (sqrt(vb) <= (double)a.b_floor * (bref_set + mb)) vb = 0.0;
     lam = (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));
   }
   if (sg == 0 && t == 0) {

@@ -17,10 +17,12 @@ RTOL = {"fp32": 1e-5, "bf16": 1e-2}
 # A (sequence, KV head) whose oracle gaps at the M-th (scale-matching set)
 # and K-th (kept set) boundaries both exceed GAP_TOL relative must have
 # exactly the oracle's kept set.  The GPU's scores come from the same exact
-# inputs in fp32 with hardware exp2 and differ from the fp64 oracle by about
-# 1e-6 relative; GAP_TOL leaves a hundredfold margin.  Closer boundaries may
-# swap positions whose pooled scores agree within RTOL of the K-th score.
-GAP_TOL = 1e-4
+# inputs in fp32 with hardware exp2; the single-read pass keeps the window-row
+# probabilities between its two halves in fp16 (relative rounding at most
+# 2^-11 per element), which leaves B within about 2e-4 of the oracle near the
+# selection boundaries.  GAP_TOL leaves a fivefold margin.  Closer boundaries
+# may swap positions whose pooled scores agree within RTOL of the K-th score.
+GAP_TOL = 1e-3
 
 
 def log(*a):
@@ -147,6 +149,96 @@ def check_idx(name, got, r, wl, rtol, hb=None, strict=False, stats=None):
                     f"K-th {pK:.9g}")
             stats["swaps"] += len(gs - os_)
     return stats
+
+
+def _lambda_of(B, V, sel, gamma, eps):
+    """lambda = gamma Std(B) / (Std(V) + eps) over the set sel (population
+    Std, in fp64; Eq. lambda_solution)."""
+    return gamma * float(np.std(B[sel])) / (float(np.std(V[sel])) + eps)
+
+
+def lambda_choices(r, b, h, s0, nc, gamma=1.0, eps=1e-12, max_band=10):
+    """The lambdas of every scale-matching set that resolves a tie at the
+    oracle's M-th boundary within GAP_TOL: the positions whose B is within
+    GAP_TOL relative of the M-th largest form a band, the set takes every
+    position above the band and any subset of the band of the remaining size.
+    One value (the oracle's) when the boundary is not tied."""
+    from itertools import combinations
+    M = int(r["m_count"][b, h])
+    lam = float(r["lambda"][b, h])
+    if M == 0 or M >= nc or lam == 0.0:
+        return [lam]
+    B = np.asarray(r["B"][h, s0:s0 + nc], np.float64)
+    V = np.asarray(r["V"][h, s0:s0 + nc], np.float64)
+    bM = float(np.sort(B)[nc - M])
+    tol = GAP_TOL * abs(bM)
+    above = np.nonzero(B > bM + tol)[0]
+    band = np.nonzero(np.abs(B - bM) <= tol)[0]
+    need = M - len(above)
+    if len(band) <= need or len(band) > max_band:
+        return [lam]
+    return [lam] + [_lambda_of(B, V, np.concatenate([above, list(c)]).astype(np.int64), gamma, eps)
+                    for c in combinations(band.tolist(), need)]
+
+
+def check_lambda(name, got, r, wl, rtol, gamma=1.0, eps=1e-12, B_gpu=None, V_gpu=None,
+                 stats=None):
+    """lambda of every (sequence, KV head) within rtol of the oracle's, or,
+    given the GPU's own window score B_gpu [Hkv, T] (and evidence V_gpu), of
+    what the GPU's B and V allow: the set the GPU's B selects may differ from
+    the oracle's only in positions tied within GAP_TOL at the M-th boundary,
+    and on that set, with dB and dV the largest deviations of the GPU's B and
+    V from the oracle's there (each checked against the oracle on its own),
+    Std(B) and Std(V) can move by at most dB and dV (Std is 1-Lipschitz in
+    the max norm), which bounds gamma Std(B) / (Std(V) + eps) to an interval
+    that lambda must meet within rtol.  The interval is wide only where the
+    set's B or V are nearly constant (identical keys, constant evidence),
+    where lambda is ill-conditioned.  Without B_gpu, lambda must be within
+    rtol of the fp64 lambda of some set resolving a tie of at most a few
+    positions."""
+    got = np.asarray(got, np.float64)
+    worst = 0.0
+    for b, (s0, s1) in enumerate(seq_slices(wl)):
+        nc = (s1 - s0) - wl.window
+        for h in range(wl.num_kv_heads):
+            g = float(got[b, h])
+            want = float(r["lambda"][b, h])
+            err = abs(g - want) / max(abs(want), 1e-300)
+            if abs(g - want) <= rtol * abs(want):
+                worst = max(worst, err)
+                continue
+            M = int(r["m_count"][b, h])
+            if B_gpu is not None and 0 < M < nc:
+                Bref = np.asarray(r["B"][h, s0:s0 + nc], np.float64)
+                Vref = np.asarray(r["V"][h, s0:s0 + nc], np.float64)
+                Bg = np.asarray(B_gpu[h, s0:s0 + nc], np.float64)
+                sel_g = np.lexsort((np.arange(nc), -Bg))[:M]
+                sel_o = np.lexsort((np.arange(nc), -Bref))[:M]
+                bM = float(Bref[sel_o[-1]])
+                diff = np.setxor1d(sel_g, sel_o)
+                assert np.all(np.abs(Bref[diff] - bM) <= GAP_TOL * abs(bM)), (
+                    f"{name} b{b} h{h}: the GPU's scale-matching set differs from the oracle's "
+                    f"outside the tie at its M-th boundary")
+                sb, sv = float(np.std(Bref[sel_g])), float(np.std(Vref[sel_g]))
+                dB = float(np.max(np.abs(Bg[sel_g] - Bref[sel_g])))
+                dV = 0.0
+                if V_gpu is not None:
+                    Vg = np.asarray(V_gpu[h, s0:s0 + nc], np.float64)
+                    dV = float(np.max(np.abs(Vg[sel_g] - Vref[sel_g])))
+                lo = gamma * max(sb - dB, 0.0) / (sv + dV + eps)
+                hi = gamma * (sb + dB) / (max(sv - dV, 0.0) + eps)
+                assert lo * (1 - rtol) <= g <= hi * (1 + rtol), (
+                    f"{name} b{b} h{h}: lambda {g:.9g} vs oracle {want:.9g}, outside "
+                    f"[{lo:.9g}, {hi:.9g}] that the GPU's B and V allow on the set its B selects "
+                    f"({len(diff) // 2} swaps in the tie)")
+                if stats is not None:
+                    stats["lambda_by_interval"] = stats.get("lambda_by_interval", 0) + 1
+                continue
+            alts = lambda_choices(r, b, h, s0, nc, gamma, eps)
+            assert any(abs(g - x) <= rtol * abs(x) for x in alts), (
+                f"{name} b{b} h{h}: lambda {g:.9g} vs oracle {want:.9g} (rel {err:.3g}); the "
+                f"{len(alts) - 1} sets resolving a tie at the M-th boundary give {alts[1:6]}")
+    return worst
 
 
 def box_pool(x, k):
