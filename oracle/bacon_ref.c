@@ -114,6 +114,56 @@ int bacon_ref_topk(int n, const double *x, int k, int32_t *out_idx) {
   return cnt;
 }
 
+/* App. B, AdaKV as the backbone: its head-wise budget allocation for one
+ * (layer, sequence), kept unchanged under BACON (App. B, Implementation
+ * Details).  Read here as AdaKV's published rule: every KV head keeps its top
+ * f = floor(alpha K) positions by the backbone score A; the other H (K - f)
+ * slots of the layer's budget go to the highest scores over the union of
+ * every head's remaining positions (ties: score desc, head asc, position
+ * asc); K_h = f + the head's share of the union.  With K >= n_cand every head
+ * keeps all its candidates, and K_h = K. */
+typedef struct { double v; int32_t h, i; } hvi;
+
+static int cmp_union(const void *a, const void *b) {
+  const hvi *x = (const hvi *)a, *y = (const hvi *)b;
+  if (x->v > y->v) return -1;
+  if (x->v < y->v) return 1;
+  if (x->h != y->h) return (x->h < y->h) ? -1 : 1;
+  return (x->i < y->i) ? -1 : (x->i > y->i);
+}
+
+void bacon_ref_adaptive_budgets(int num_heads, int n_cand, const double *A, long a_stride,
+                                int budget, double floor_alpha, int32_t *out) {
+  if (budget >= n_cand) {
+    for (int h = 0; h < num_heads; ++h) out[h] = budget;
+    return;
+  }
+  long ff = (long)floor(floor_alpha * (double)budget);
+  if (ff < 0) ff = 0;
+  if (ff > budget) ff = budget;
+  const int f = (int)ff;
+  /* the union: every head's positions after its own top f */
+  hvi *u = (hvi *)malloc(sizeof(hvi) * (size_t)num_heads * (size_t)n_cand);
+  vi_pair *p = (vi_pair *)malloc(sizeof(vi_pair) * (size_t)n_cand);
+  long nu = 0;
+  for (int h = 0; h < num_heads; ++h) {
+    for (int i = 0; i < n_cand; ++i) { p[i].v = A[h * a_stride + i]; p[i].i = i; }
+    qsort(p, (size_t)n_cand, sizeof(vi_pair), cmp_desc);
+    for (int j = f; j < n_cand; ++j) {
+      u[nu].v = p[j].v;
+      u[nu].h = h;
+      u[nu].i = p[j].i;
+      ++nu;
+    }
+  }
+  qsort(u, (size_t)nu, sizeof(hvi), cmp_union);
+  const long R = (long)num_heads * (long)(budget - f);
+  for (int h = 0; h < num_heads; ++h) out[h] = f;
+  for (long j = 0; j < R && j < nu; ++j) out[u[j].h] += 1;
+  free(p);
+  free(u);
+}
+
 /* Sec. 4.4: M = min(rho K, |I|) (Eq. scale_matching_size), the scale-matching
  * set = TopK of B over I (Eq. scale_matching_set), and the closed-form
  * minimiser lambda = gamma Std(B) / (Std(V) + eps) (Eq. lambda_solution). */

@@ -105,6 +105,12 @@ void bacon_ref_persistence(int n, int cnt, const double *const *prev, double *T)
  * ascending order and returns their count. */
 int bacon_ref_topk(int n, const double *x, int k, int32_t *out_idx);
 
+/* AdaKV's head-wise allocation of one (layer, sequence): K_h [num_heads] from
+ * the backbone score A (head h at A + h*a_stride, n_cand positions), the
+ * per-head budget K and the floor fraction alpha. */
+void bacon_ref_adaptive_budgets(int num_heads, int n_cand, const double *A, long a_stride,
+                                int budget, double floor_alpha, int32_t *out);
+
 /* lambda over the candidate prefix [0, n_cand) with budget K. */
 double bacon_ref_lambda(int n_cand, const double *B, const double *V, int budget,
                         double rho, double gamma, double eps,

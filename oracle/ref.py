@@ -66,6 +66,8 @@ def lib() -> C.CDLL:
         L.bacon_ref_lambda.restype = C.c_double
         L.bacon_ref_pool.argtypes = [C.c_int, C.c_int, _dp, _dp]
         L.bacon_ref_pool_max.argtypes = [C.c_int, C.c_int, _dp, _dp]
+        L.bacon_ref_adaptive_budgets.argtypes = [C.c_int, C.c_int, _dp, C.c_long, C.c_int,
+                                                 C.c_double, _ip]
         L.bacon_ref_layer.argtypes = [C.POINTER(_Cfg), C.c_int, C.c_int, _ip, _ip, _fp, _fp,
                                       _dp, C.POINTER(_Out)]
         L.bacon_ref_layer.restype = C.c_int
@@ -170,6 +172,16 @@ def pool_max(x: np.ndarray, kernel: int) -> np.ndarray:
     return out
 
 
+def adaptive_budgets(A: np.ndarray, budget: int, floor_alpha: float) -> np.ndarray:
+    """AdaKV's head-wise allocation of one (layer, sequence): K_h from the
+    backbone scores A [H, n_cand] (App. B; see bacon_ref_adaptive_budgets)."""
+    A = np.ascontiguousarray(A, dtype=np.float64)
+    H, n = A.shape
+    out = np.zeros(H, np.int32)
+    lib().bacon_ref_adaptive_budgets(H, n, _d(A), n, int(budget), float(floor_alpha), _i(out))
+    return out
+
+
 # ---------------------------------------------------------------- whole layers
 
 @dataclass
@@ -235,6 +247,31 @@ class Prompt:
                                    _f(q_win), _f(k), _d(self.e_hist), C.byref(out))
         if rc != 0:
             raise ValueError("oracle rejected the layer arguments")
+        return r
+
+    def layer_adaptive(self, layer: int, q_win: np.ndarray, k: np.ndarray, floor_alpha: float,
+                       budgets=None) -> dict:
+        """One layer on the AdaKV backbone (App. B): the head-wise budgets
+        K_{b,h} are AdaKV's allocation of each sequence's H_kv K_b slots by
+        the backbone score, the mean pool of B over the candidates (the
+        SnapKV-style window score, with this prompt's pool width); BACON then
+        keeps the top K_{b,h} of its own score in each head.  Runs the layer
+        once for B (E and the history are the same under any budgets) and
+        again with the allocation."""
+        bud = self.budgets if budgets is None else np.ascontiguousarray(budgets, dtype=np.int32)
+        r0 = self.layer(layer, q_win, k, budgets=bud)
+        bh = np.zeros((self.batch, self.Hkv), np.int32)
+        for b in range(self.batch):
+            s0, s1 = int(self.cu[b]), int(self.cu[b + 1])
+            nc = (s1 - s0) - self.W
+            if nc <= 0:
+                bh[b] = bud[b]
+                continue
+            A = np.stack([pool(r0["B"][h, s0:s0 + nc], self.cfg.pool_kernel)
+                          for h in range(self.Hkv)])
+            bh[b] = adaptive_budgets(A, int(bud[b]), floor_alpha)
+        r = self.layer(layer, q_win, k, budgets=bud, head_budgets=bh)
+        r["alloc_budgets"] = bh
         return r
 
     def _bh(self, r: dict) -> np.ndarray:
