@@ -85,7 +85,26 @@ enum { BACON_TERM_E = 1, BACON_TERM_L = 2, BACON_TERM_T = 4 };
 /* Method parameters.  Defaults (bacon_default_params): radius 5 and
  * persist_m 4 (Sec. 4.3), rho 2 (Sec. 4.4), gamma 1 and eps 1e-12 (the paper
  * gives no value), pool_kernel 7, use_last_query 1, terms E|L|T,
- * pool_mode BACON_POOL_MEAN_S. */
+ * pool_mode BACON_POOL_MEAN_S, head_alloc BACON_ALLOC_GIVEN, alloc_floor 0.2. */
+/* Head-wise budgets of the fused calls (App. B: BACON keeps the backbone's
+ * allocation and changes only the score within a head).
+ *   BACON_ALLOC_GIVEN     the batch's budgets (per sequence or per head).
+ *   BACON_ALLOC_ADAPTIVE  AdaKV's allocation of each layer: every KV head
+ *                         keeps its top floor(alloc_floor K_b) positions by
+ *                         the backbone score (B mean-pooled over the
+ *                         candidates with pool_kernel); the sequence's other
+ *                         H_kv K_b - H_kv floor(alloc_floor K_b) slots go to
+ *                         the highest scores over every head's remaining
+ *                         positions (ties: score desc, head asc, position
+ *                         asc).  Head h then keeps its K_{b,h} best of S.
+ *                         The batch gives budgets per sequence (no
+ *                         head_budgets), num_kv_heads <= 32, and the
+ *                         compacted cache holds one head per row: sequence
+ *                         b's H_kv (K_b + W) rows in head order, head h's
+ *                         K_{b,h} kept rows then its W window rows (the same
+ *                         bytes as the [rows, Hkv, d] layout).  idx keeps its
+ *                         layout with K_{b,h} entries per (b, h). */
+typedef enum { BACON_ALLOC_GIVEN = 0, BACON_ALLOC_ADAPTIVE = 1 } bacon_head_alloc;
 /* Pooling of the score over the candidate set before the top-K.  The method
  * itself does not pool; the average pool of S is the SnapKV convention it is
  * used with, and the variants serve ablations.  All use a centred window of
@@ -111,6 +130,8 @@ typedef struct {
   int32_t use_last_query;  /* 1 = BACON; 0 = window score only (S = B)       */
   uint32_t terms;          /* subset of BACON_TERM_E|L|T included in V       */
   int32_t pool_mode;       /* BACON_POOL_MEAN_S (default), _MAX_S, _MEAN_B   */
+  int32_t head_alloc;      /* BACON_ALLOC_GIVEN (default) or _ADAPTIVE       */
+  float alloc_floor;       /* alpha of the adaptive allocation, in [0, 1]    */
 } bacon_params;
 
 /* Static shape of the model and the largest batch a context will see. */
@@ -190,6 +211,19 @@ bacon_status bacon_select_topk(bacon_ctx *ctx, const bacon_batch *batch, const f
 bacon_status bacon_compact(bacon_ctx *ctx, const bacon_batch *batch, const void *d_k,
                            const void *d_v, const int32_t *d_idx, void *d_k_out,
                            void *d_v_out, void *stream);
+
+/* AdaKV's head-wise allocation of one layer (see BACON_ALLOC_ADAPTIVE) from a
+ * window score d_B [Hkv, T] (bacon_score's): writes K_{b,h} to d_budgets
+ * [batch, Hkv] (int32, device), for a later call's batch.head_budgets.  Uses
+ * the context's pool_kernel and alloc_floor; the batch gives per-sequence
+ * budgets.  UNSUPPORTED with more than 32 KV heads. */
+bacon_status bacon_allocate_heads(bacon_ctx *ctx, const bacon_batch *batch, const float *d_B,
+                                  int32_t *d_budgets, void *stream);
+
+/* Where the fused calls under BACON_ALLOC_ADAPTIVE write each layer's budgets:
+ * d_budgets [num_layers, max_batch, Hkv] int32 (device), layer l at offset
+ * l * max_batch * Hkv, or NULL to stop.  The caller keeps ownership. */
+bacon_status bacon_alloc_output(bacon_ctx *ctx, int32_t *d_budgets);
 
 /* The whole pass for one layer: score, calibrate, select and compact, with the
  * intermediates kept in the workspace.  Same ordering rule as calibrate. */
@@ -287,8 +321,10 @@ bacon_status bacon_debug_capture(bacon_ctx *ctx, float *d_B, float *d_V, float *
 
 /* Test instrumentation: waits for the device, then returns the context's
  * device error word: 0, or 1 if a meeting of the single-read K pass ran out
- * of its bounded wait (the results of that call are then unspecified; the
- * next bacon_begin_prompt clears the word); -1 if it cannot be read.
+ * of its bounded wait, or 2 if an adaptive allocation failed its own check
+ * (its budgets were then left uniform) (the results of that call are then
+ * unspecified; the next bacon_begin_prompt clears the word); -1 if it cannot
+ * be read.
  * Synchronises the device, unlike every other call. */
 int32_t bacon_debug_device_errors(bacon_ctx *ctx);
 

@@ -344,8 +344,10 @@ int bacon_ref_layer(const bacon_ref_cfg *c, int layer, int batch,
   const int pairs = batch * c->num_kv_heads;
   for (int b = 0; b < batch; ++b)
     if (cu[b + 1] - cu[b] < c->window) return -1;
+  /* a budget may be 0 (a head-wise allocation such as AdaKV's, App. B, can
+   * leave a head without slots): that head keeps no position */
   for (int p = 0; p < pairs; ++p)
-    if (budgets[p] < 1) return -1;
+    if (budgets[p] < 0) return -1;
   const long T = cu[batch];
   /* kept indices of (b, h) start after those of every earlier pair */
   long *idx_off = (long *)malloc(sizeof(long) * (size_t)(pairs + 1));

@@ -23,6 +23,7 @@ ENTRY_POINTS = [
     "bacon_begin_prompt", "bacon_score", "bacon_calibrate", "bacon_select_topk",
     "bacon_compact", "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_compress_prompt",
     "bacon_window_lse", "bacon_window_lse_static", "bacon_debug_capture", "bacon_debug_device_errors",
+    "bacon_allocate_heads", "bacon_alloc_output",
     "bacon_idx_count",
     "bacon_kept_rows",
     "bacon_profile_enable", "bacon_profile_read", "bacon_status_string", "bacon_last_error",
@@ -32,11 +33,14 @@ ENTRY_POINTS = [
 class Params(C.Structure):
     _fields_ = [("radius", C.c_int32), ("persist_m", C.c_int32), ("rho", C.c_double),
                 ("gamma", C.c_float), ("eps", C.c_float), ("pool_kernel", C.c_int32),
-                ("use_last_query", C.c_int32), ("terms", C.c_uint32), ("pool_mode", C.c_int32)]
+                ("use_last_query", C.c_int32), ("terms", C.c_uint32), ("pool_mode", C.c_int32),
+                ("head_alloc", C.c_int32), ("alloc_floor", C.c_float)]
 
 
 # pooling of the score before the top-K (bacon_pool_mode)
 POOL_MEAN_S, POOL_MAX_S, POOL_MEAN_B = 0, 1, 2
+# head-wise budgets of the fused calls (bacon_head_alloc)
+ALLOC_GIVEN, ALLOC_ADAPTIVE = 0, 1
 
 
 class Shape(C.Structure):
@@ -90,6 +94,8 @@ def lib() -> C.CDLL:
         L.bacon_compress_prompt.argtypes = [vp, C.POINTER(Batch), C.c_int32, C.c_int32, vp, vp, vp,
                                             vp, vp, vp, vp, vp, vp]
         L.bacon_debug_capture.argtypes = [vp, vp, vp, vp]
+        L.bacon_allocate_heads.argtypes = [vp, C.POINTER(Batch), vp, vp, vp]
+        L.bacon_alloc_output.argtypes = [vp, vp]
         L.bacon_debug_device_errors.argtypes = [vp]
         L.bacon_debug_device_errors.restype = C.c_int32
         L.bacon_window_lse_static.argtypes = [C.POINTER(Shape), C.POINTER(Batch), vp, vp, vp, vp]
@@ -107,7 +113,7 @@ def lib() -> C.CDLL:
                      "bacon_calibrate", "bacon_select_topk", "bacon_compact",
                      "bacon_compress_layer", "bacon_compress_layer_lse", "bacon_window_lse",
                      "bacon_compress_prompt", "bacon_debug_capture", "bacon_window_lse_static",
-                     "bacon_profile_enable"):
+                     "bacon_allocate_heads", "bacon_alloc_output", "bacon_profile_enable"):
             getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -289,6 +295,21 @@ class Context:
     def bacon_debug_device_errors(self) -> int:
         """Test instrumentation: the device error word (synchronises)."""
         return int(lib().bacon_debug_device_errors(self._h))
+
+    def bacon_allocate_heads(self, batch: BatchLayout, B, out=None):
+        """AdaKV's head-wise budgets K_{b,h} [batch, Hkv] (int32 device tensor)
+        from a window score B [Hkv, T]."""
+        import torch
+        bud = out if out is not None else torch.empty(
+            (batch.c.batch, self.shape.num_kv_heads), dtype=torch.int32, device=B.device)
+        _check(lib().bacon_allocate_heads(self._h, C.byref(batch.c), _ptr(B), _ptr(bud), _stream()))
+        return bud
+
+    def bacon_alloc_output(self, budgets=None):
+        """Where the fused calls under the adaptive allocation write each
+        layer's budgets: an int32 device tensor [num_layers, max_batch, Hkv],
+        or None to stop."""
+        _check(lib().bacon_alloc_output(self._h, _ptr(budgets)))
 
     def bacon_debug_capture(self, B=None, V=None, lam=None):
         """Test instrumentation: per-layer copies of B, V [L, Hkv, T] and lambda

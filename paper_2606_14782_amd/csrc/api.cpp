@@ -84,6 +84,10 @@ bacon_status check_params(const bacon_params *p) {
   if (p->terms & ~7u) return fail(BACON_ERR_INVALID, "terms has unknown bits");
   if (p->pool_mode < BACON_POOL_MEAN_S || p->pool_mode > BACON_POOL_MEAN_B)
     return fail(BACON_ERR_INVALID, "pool_mode must be 0, 1 or 2");
+  if (p->head_alloc != BACON_ALLOC_GIVEN && p->head_alloc != BACON_ALLOC_ADAPTIVE)
+    return fail(BACON_ERR_INVALID, "head_alloc must be 0 or 1");
+  if (!(p->alloc_floor >= 0.f && p->alloc_floor <= 1.f))
+    return fail(BACON_ERR_INVALID, "alloc_floor must be in [0, 1]");
   return BACON_OK;
 }
 
@@ -145,10 +149,10 @@ const char *kKernelNames[] = {"window_lse",    "lse_merge",     "window_score", 
                               "calib_elem",    "compact",       "window_lse_kr",
                               "window_score_calib_kr", "window_score_calib_lse_kr",
                               "segment_calib_cand", "segment_score_final",
-                              "window_score_calib_lse", "window_score_single"};
+                              "window_score_calib_lse", "window_score_single", "head_alloc"};
 enum KernelId { KI_LSE, KI_MERGE, KI_SCORE, KI_FUSED, KI_SEGCAL, KI_SEGSCORE, KI_SEGCAND, KI_FINAL,
                 KI_SEL_CALIB, KI_SEL_TOPK, KI_ELEM, KI_COMPACT, KI_LSE_KR, KI_FUSED_KR, KI_DUAL_KR,
-                KI_SEL_A, KI_SEL_B, KI_DUAL, KI_SINGLE, KI_COUNT };
+                KI_SEL_A, KI_SEL_B, KI_DUAL, KI_SINGLE, KI_ALLOC, KI_COUNT };
 
 }  // namespace
 
@@ -167,6 +171,7 @@ struct bacon_ctx {
   int single_cap = -1;       // single-read workgroups the device holds at once (-1: not yet asked)
   // test instrumentation (bacon_debug_capture): per-layer copies of B, V, lambda
   float *cap_B = nullptr, *cap_V = nullptr, *cap_lambda = nullptr;
+  int32_t *alloc_out = nullptr;   // [num_layers, max_batch, Hkv] budgets of the adaptive allocation
   // profiling
   bool prof = false;
   std::vector<hipEvent_t> ev_pool;
@@ -176,6 +181,17 @@ struct bacon_ctx {
   int64_t launches[KI_COUNT] = {};
   double ms[KI_COUNT] = {};
 };
+
+namespace {
+
+// The device error word (after the meeting counters of the single-read pass):
+// 1 if a meeting ran out, 2 if an allocation failed its check.
+unsigned *error_word(bacon_ctx *c) {
+  return reinterpret_cast<unsigned *>(c->ws + c->L.sync) +
+         (size_t)kSyncStride * c->shape.max_batch * c->shape.num_kv_heads;
+}
+
+}  // namespace
 
 namespace {
 
@@ -463,6 +479,8 @@ void bacon_default_params(bacon_params *p) {
   p->pool_mode = BACON_POOL_MEAN_S;
   p->use_last_query = 1;
   p->terms = BACON_TERM_E | BACON_TERM_L | BACON_TERM_T;
+  p->head_alloc = BACON_ALLOC_GIVEN;
+  p->alloc_floor = 0.2f;
 }
 
 size_t bacon_workspace_bytes(const bacon_shape *shape, const bacon_params *params) {
@@ -622,6 +640,40 @@ bacon_status bacon_select_topk(bacon_ctx *c, const bacon_batch *bt, const float 
   return timed(c, KI_SEL_TOPK, s, [&] { return launch_select(SEL_TOPK, max_len(bt), a, st, s); });
 }
 
+bacon_status bacon_allocate_heads(bacon_ctx *c, const bacon_batch *bt, const float *d_B,
+                                  int32_t *d_budgets, void *stream) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  TRY(check_batch(c, bt));
+  TRY(check_ptr(d_B, "B", 4));
+  TRY(check_ptr(d_budgets, "budgets", 4));
+  if (bt->head_budgets)
+    return fail(BACON_ERR_INVALID, "the adaptive allocation takes per-sequence budgets, not head_budgets");
+  if (c->shape.num_kv_heads > 32)
+    return fail(BACON_ERR_UNSUPPORTED, "the adaptive allocation takes at most 32 KV heads");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int chunk = 0;
+  const SeqTable st = make_table(c, bt, &chunk);
+  AllocArgs a{};
+  a.Hkv = c->shape.num_kv_heads;
+  a.W = c->shape.window;
+  a.pool_half = c->params.pool_kernel / 2;
+  a.T = bt->cu_seqlens[bt->batch];
+  a.alpha = c->params.alloc_floor;
+  a.vec_B = d_B;
+  a.vec_A = reinterpret_cast<float *>(c->ws + c->L.vec_pb);
+  a.hb = reinterpret_cast<int2 *>(c->ws + c->L.hb);
+  a.out = d_budgets;
+  a.err = error_word(c);
+  return timed(c, KI_ALLOC, s, [&] { return launch_alloc(a, st, s); });
+}
+
+bacon_status bacon_alloc_output(bacon_ctx *c, int32_t *d_budgets) {
+  if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
+  if (d_budgets) TRY(check_ptr(d_budgets, "budgets", 4));
+  c->alloc_out = d_budgets;
+  return BACON_OK;
+}
+
 bacon_status bacon_compact(bacon_ctx *c, const bacon_batch *bt, const void *d_k, const void *d_v,
                            const int32_t *d_idx, void *d_k_out, void *d_v_out, void *stream) {
   if (!c) return fail(BACON_ERR_INVALID, "ctx is NULL");
@@ -655,6 +707,7 @@ namespace {
 struct LayerRun {
   int layer = 0;
   bool bf16 = false, w32 = false, kr = false, single = false;
+  bool adaptive = false;   // head-wise budgets from the adaptive allocation
   int chunk = 0, kmax = 0;
   SeqTable st{};
   PassArgs a{};
@@ -705,6 +758,18 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
   }
   r.kmax = 0;
   for (int b = 0; b < bt->batch; ++b) r.kmax = std::max(r.kmax, batch_seq_rows(bt, c->shape.num_kv_heads, b));
+  r.adaptive = c->params.head_alloc == BACON_ALLOC_ADAPTIVE;
+  if (r.adaptive) {
+    if (bt->head_budgets)
+      return fail(BACON_ERR_INVALID, "the adaptive allocation takes per-sequence budgets, not head_budgets");
+    if (c->shape.num_kv_heads > 32)
+      return fail(BACON_ERR_UNSUPPORTED, "the adaptive allocation takes at most 32 KV heads");
+    // a head may take up to all H_kv K_b slots of its sequence, at most its candidates
+    for (int b = 0; b < bt->batch; ++b) {
+      const int nc = bt->cu_seqlens[b + 1] - bt->cu_seqlens[b] - c->shape.window;
+      r.kmax = std::max(r.kmax, (int)std::min<int64_t>(nc, (int64_t)c->shape.num_kv_heads * bt->budgets[b]));
+    }
+  }
   if (final_lds_bytes(r.kmax, c->shape.window) > (size_t)kLdsBytes)
     return fail(BACON_ERR_UNSUPPORTED, "budget %d needs more LDS than a CU has", r.kmax);
   const int par = layer & 1;
@@ -763,6 +828,7 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
   g.k_out = d_k_out;
   g.v_out = d_v_out;
   g.row_bytes = c->shape.head_dim * (r.bf16 ? 2 : 4);
+  g.flat_heads = r.adaptive;
   // final workgroups per (sequence, KV head): about one round over the CUs
   g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
   return BACON_OK;
@@ -796,6 +862,32 @@ bacon_status stage_pass(bacon_ctx *c, const LayerRun &r, bool lse_merged, const 
   if (next)   // fp32 keys: the next layer's pass 1 in a launch of its own
     return timed(c, KI_LSE, s, [&] { return launch_pass(PASS_LSE, r.bf16, d, false, *next, r.st, s); });
   return BACON_OK;
+}
+
+// The adaptive allocation's budget table of a layer (by layer parity, where
+// given head budgets go otherwise).
+int2 *alloc_table(bacon_ctx *c, int layer) {
+  return reinterpret_cast<int2 *>(c->ws + c->L.hb + (size_t)(layer & 1) * c->L.hb_stride);
+}
+
+// Head-wise budgets of r's layer from its window score (adaptive allocation
+// only), before its calibration reads them.
+bacon_status stage_alloc(bacon_ctx *c, const LayerRun &r, hipStream_t s) {
+  if (!r.adaptive) return BACON_OK;
+  AllocArgs a{};
+  a.Hkv = c->shape.num_kv_heads;
+  a.W = c->shape.window;
+  a.pool_half = c->params.pool_kernel / 2;
+  a.T = r.g.T;
+  a.alpha = c->params.alloc_floor;
+  a.vec_B = r.g.vec_B;
+  a.vec_A = r.g.vec_pB;   // free until this layer's calibration writes the pooled B there
+  a.hb = alloc_table(c, r.layer);
+  a.out = c->alloc_out ? c->alloc_out + (size_t)r.layer * c->shape.max_batch * c->shape.num_kv_heads
+                       : nullptr;
+  a.sb = r.g.sb;
+  a.err = error_word(c);
+  return timed(c, KI_ALLOC, s, [&] { return launch_alloc(a, r.st, s); });
 }
 
 // Calibration of r's layer, with the previous layer's candidate lists and the
@@ -849,7 +941,9 @@ bacon_status compress(bacon_ctx *c, int32_t layer, const bacon_batch *bt, const 
   TRY(plan_layer(c, layer, bt, d_q_win, d_k, d_v, d_lse, d_idx, d_k_out, d_v_out, r));
   hipStream_t s = static_cast<hipStream_t>(stream);
   TRY(head_table(c, bt, s, &r.g.hb, layer & 1));
+  if (r.adaptive) r.g.hb = alloc_table(c, layer);
   TRY(stage_pass(c, r, false, nullptr, s));
+  TRY(stage_alloc(c, r, s));
   TRY(stage_a(c, r, nullptr, nullptr, s));
   TRY(stage_b(c, r, nullptr, s));
   TRY(stage_capture(c, r, bt, s));
@@ -927,6 +1021,7 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
   for (int i = 0; i < num_layers; ++i) {
     LayerRun &r = runs[i];
     TRY(head_table(c, lbt(i), s, &r.g.hb, r.layer & 1));
+    if (r.adaptive) r.g.hb = alloc_table(c, r.layer);
     if (layer_batch) TRY(seq_table(c, r.st, s, &r.g.sb, r.layer & 1));
     const LayerRun *prev = (overlap && i > 0) ? &runs[i - 1] : nullptr;
     // the next layer's pass 1 rides in this layer's pass-2 launch, unless the
@@ -934,6 +1029,7 @@ bacon_status bacon_compress_prompt(bacon_ctx *c, const bacon_batch *bt, int32_t 
     const PassArgs *next = (!r.lse && !r.single && i + 1 < num_layers && !runs[i + 1].single)
                                ? &runs[i + 1].a : nullptr;
     TRY(stage_pass(c, r, merged, next, s));
+    TRY(stage_alloc(c, r, s));
     TRY(stage_a(c, r, prev, next, s));
     TRY(stage_b(c, r, prev, s));
     TRY(stage_capture(c, r, lbt(i), s));

@@ -141,6 +141,25 @@ struct SegArgs {
   const int4 *sb;                // optional [B] (budget, idx base, kept-row base, 0) of this
                                  // layer's batch, when it differs from the SeqTable's (a
                                  // per-layer budget schedule: a launch holds two layers' jobs)
+  // compacted cache one head per row: sequence b's rows start at Hkv times
+  // its kept-row base, head h's block (K_h kept rows, then W window rows) at
+  // its idx offset plus h W rows (the head-wise allocation, whose budgets
+  // the host does not know)
+  int flat_heads;
+};
+
+// Head-wise budget allocation of one layer (AdaKV's rule): K_{b,h} from the
+// pooled window score of every KV head of a sequence.
+struct AllocArgs {
+  int Hkv, W, pool_half;
+  int64_t T;
+  double alpha;                  // floor fraction: every head keeps floor(alpha K) at least
+  const float *vec_B;            // [Hkv, T]
+  float *vec_A;                  // [Hkv, T] scratch: the pooled B
+  int2 *hb;                      // out [B, Hkv] (K_{b,h}, idx offset in the sequence)
+  int32_t *out;                  // optional out [B, Hkv] K_{b,h}
+  const int4 *sb;                // optional per-layer sequence table (budget K_b in .x)
+  unsigned *err;                 // optional error word (set to 2 if the search fails)
 };
 
 struct ElemArgs {           // split calibrate: E, T, L, ring update
@@ -250,6 +269,8 @@ hipError_t launch_segscore(const SegArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_segcand(const SegArgs &a, const SeqTable &st, hipStream_t s);
 // LDS of the final workgroup for budgets up to max_budget.
 size_t final_lds_bytes(int max_budget, int window);
+size_t alloc_lds_bytes(int hkv);
+hipError_t launch_alloc(const AllocArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_segfinal(const SegArgs &a, const SeqTable &st, int max_budget, hipStream_t s);
 hipError_t launch_compact(const CompactArgs &a, const SeqTable &st, hipStream_t s);
 hipError_t launch_zero(unsigned *p, int64_t n, hipStream_t s);

@@ -1318,8 +1318,8 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   __syncthreads();
   if (s_go) {
     // thread t takes row t % Rpad over the chunks congruent to t / Rpad,
-    // 16 loads in flight
-    constexpr int FL = 16;
+    // 32 loads in flight (every chunk of a 32K sequence at Rpad = 128)
+    constexpr int FL = 32;
     const int parts = NT / a.Rpad, row = t % a.Rpad, pp = t / a.Rpad;
     float mm = -INFINITY, ll = 0.f;
     if (pp < parts) {
@@ -3046,7 +3046,7 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
   const int K = head_budget(st, a.hb, a.Hkv, b, h, a.sb);   // this head's budget
-  const int C = seq_budget(st, a.sb, b);                   // rows per head of the sequence, less W
+  const int C = a.flat_heads ? K : seq_budget(st, a.sb, b);  // rows of the head's block, less W
   const int kept = min(K, nc);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
   int32_t *idx = a.idx + head_idx_base(st, a.hb, a.Hkv, b, h, a.sb);
@@ -3137,7 +3137,10 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
       const int q = q0 + u * NT;
       if (q < total) {
         const int rr = r0 + q / pieces, p = q % pieces;
-        const int64_t dst = ((int64_t)(seq_kept_base(st, a.sb, b) + rr) * a.Hkv + h) * a.row_bytes + 16 * p;
+        const int64_t row = a.flat_heads
+            ? (int64_t)a.Hkv * seq_kept_base(st, a.sb, b) + a.hb[b * a.Hkv + h].y + (int64_t)h * a.W + rr
+            : (int64_t)(seq_kept_base(st, a.sb, b) + rr) * a.Hkv + h;
+        const int64_t dst = row * a.row_bytes + 16 * p;
         const u32x4 z = u32x4{0u, 0u, 0u, 0u};
         *reinterpret_cast<u32x4 *>(ko + dst) = srcs[u] >= 0 ? kv[u] : z;
         *reinterpret_cast<u32x4 *>(vo + dst) = srcs[u] >= 0 ? vv[u] : z;
@@ -3256,6 +3259,166 @@ hipError_t launch_segfinal(const SegArgs &a, const SeqTable &st, int max_budget,
   if (final_lds_bytes(max_budget, a.W) > (size_t)kLdsBytes || a.parts < 1) return hipErrorInvalidValue;
   allow_lds(k_segfinal, lds);
   hipLaunchKernelGGL(k_segfinal, dim3(a.parts, st.batch, a.Hkv), dim3(kSegThreads), lds, s, a, st);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- head-wise allocation
+// AdaKV's budget allocation of one (layer, sequence) (App. B: the backbone's
+// head-wise budgets, kept under BACON).  Every KV head keeps its top
+// f = floor(alpha K) positions by the backbone score A, the mean pool of B
+// over the candidates; the other H (K - f) slots go to the highest A over the
+// union of every head's remaining positions (ties: score desc, head asc,
+// position asc).  Counted without sorting: with g_h(x) the head's entries
+// above key x, the union's slots above x number F(x) = sum_h max(0, g_h(x) - f),
+// so a radix search over the key digits (per-head histograms in LDS) finds
+// the boundary key tau with F(above tau) < H (K - f) <= F(tau); the tie at tau
+// goes to the lower heads, and K_h = f + the head's share.  One workgroup per
+// sequence; A is written to a [Hkv, T] buffer between the passes.
+constexpr int kAllocThreads = 1024;
+constexpr int kAllocDigits = 1024;       // bins of a radix level (10 bits)
+constexpr int kAllocTile = 4096;         // positions of B staged per round of the pool
+constexpr int kMaxAllocHeads = 32;
+
+size_t alloc_lds_bytes(int hkv) { return (size_t)hkv * kAllocDigits * sizeof(unsigned); }
+
+__global__ __launch_bounds__(kAllocThreads) void k_alloc(AllocArgs a, SeqTable st) {
+  constexpr int NT = kAllocThreads;
+  extern __shared__ __align__(16) unsigned hist[];      // [Hkv][kAllocDigits]
+  __shared__ float tile[kAllocTile + 2 * kPoolHalo];
+  __shared__ SelSharedT<NT> ss;
+  __shared__ unsigned above[kMaxAllocHeads], eq[kMaxAllocHeads];
+  __shared__ int kh_s[kMaxAllocHeads];
+  const int t = threadIdx.x, b = blockIdx.x, H = a.Hkv;
+  const int n = st.cu[b + 1] - st.cu[b];
+  const int nc = n - a.W;
+  const int K = seq_budget(st, a.sb, b);
+  int2 *tab = a.hb + (int64_t)b * H;
+  if (nc <= K) {
+    // every head keeps all its candidates: the budgets stay uniform
+    for (int h = t; h < H; h += NT) {
+      tab[h] = make_int2(K, h * K);
+      if (a.out) a.out[(int64_t)b * H + h] = K;
+    }
+    return;
+  }
+  const int f = (int)min((double)K, floor(a.alpha * (double)K));
+  const unsigned R = (unsigned)H * (unsigned)(K - f);
+  const int ph = a.pool_half;
+  const int64_t T = a.T, s0 = st.cu[b];
+
+  // pass 0: A = the mean pool of B over the candidates (truncated at the
+  // ends), written out, and the histograms of its top key digit
+  for (int e = t; e < H * kAllocDigits; e += NT) hist[e] = 0u;
+  for (int h = 0; h < H; ++h) {
+    const float *B = a.vec_B + (int64_t)h * T + s0;
+    float *A = a.vec_A + (int64_t)h * T + s0;
+    for (int i0 = 0; i0 < nc; i0 += kAllocTile) {
+      __syncthreads();
+      const int lo = max(0, i0 - ph), hi = min(nc, i0 + kAllocTile + ph);
+      for (int j = lo + t; j < hi; j += NT) tile[j - lo] = B[j];
+      __syncthreads();
+      for (int i = i0 + t; i < min(nc, i0 + kAllocTile); i += NT) {
+        const int w0 = max(0, i - ph), w1 = min(nc - 1, i + ph);
+        float acc = 0.f;
+        for (int j = w0; j <= w1; ++j) acc += tile[j - lo];
+        const float v = acc / (float)(w1 - w0 + 1);
+        A[i] = v;
+        atomicAdd(&hist[h * kAllocDigits + (float_key(v) >> 22)], 1u);
+      }
+    }
+  }
+  for (int h = t; h < H; h += NT) above[h] = 0u;
+  __syncthreads();
+
+  // radix levels over key bits 31..22, 21..12, 11..2, 1..0
+  unsigned prefix = 0u;
+  for (int lev = 0; lev < 4; ++lev) {
+    const int shift = lev == 3 ? 0 : 22 - 10 * lev;
+    const int width = lev == 3 ? 2 : 10;
+    if (lev > 0) {
+      for (int e = t; e < H * kAllocDigits; e += NT) hist[e] = 0u;
+      __syncthreads();
+      const int pshift = shift + width;
+      for (int h = 0; h < H; ++h) {
+        const float *A = a.vec_A + (int64_t)h * T + s0;
+        for (int i = t; i < nc; i += NT) {
+          const unsigned k = float_key(A[i]);
+          if ((k >> pshift) == prefix)
+            atomicAdd(&hist[h * kAllocDigits + ((k >> shift) & ((1u << width) - 1u))], 1u);
+        }
+      }
+      __syncthreads();
+    }
+    // suffix sums per head in place: hist[h][x] = entries of head h with
+    // this level's digit >= x (under the prefix)
+    for (int h = 0; h < H; ++h) {
+      const unsigned v = hist[h * kAllocDigits + (kAllocDigits - 1 - t)];
+      const unsigned inc = block_excl_scan_u<NT>(v, ss) + v;
+      hist[h * kAllocDigits + (kAllocDigits - 1 - t)] = inc;
+      __syncthreads();
+    }
+    // F(x) at this thread's digit; the boundary is the largest x with F >= R
+    unsigned F = 0u;
+    for (int h = 0; h < H; ++h) {
+      const unsigned g = above[h] + hist[h * kAllocDigits + t];
+      F += g > (unsigned)f ? g - (unsigned)f : 0u;
+    }
+    // (some digit always qualifies: F at digit 0 counts the union at or
+    // below the previous boundary; the clamp only keeps indexes in range)
+    const unsigned xb = max(block_reduce_u<1, NT>(F >= R ? (unsigned)t + 1u : 0u, ss), 1u) - 1u;
+    // the entries above the boundary digit join `above`; the boundary digit's
+    // own count is kept for the last level
+    if (t < H) {
+      const unsigned at = hist[t * kAllocDigits + xb];
+      const unsigned up = xb + 1 < (unsigned)kAllocDigits ? hist[t * kAllocDigits + xb + 1] : 0u;
+      eq[t] = at - up;
+      above[t] += up;
+    }
+    prefix = (prefix << width) | xb;
+    __syncthreads();
+  }
+
+  // the tie at tau: each head's entries equal to tau beyond its floor, taken
+  // in head order until the union's slots are filled
+  if (t == 0) {
+    unsigned got = 0u;
+    for (int h = 0; h < H; ++h) got += above[h] > (unsigned)f ? above[h] - (unsigned)f : 0u;
+    unsigned need = got < R ? R - got : 0u;
+    int off = 0;
+    bool ok = true;
+    for (int h = 0; h < H; ++h) {
+      const unsigned g = above[h], ge = g + eq[h];
+      const unsigned hi2 = ge > (unsigned)f ? ge - (unsigned)f : 0u;
+      const unsigned lo2 = g > (unsigned)f ? g - (unsigned)f : 0u;
+      const unsigned take = min(hi2 - lo2, need);
+      need -= take;
+      kh_s[h] = f + (int)(lo2 + take);
+      ok = ok && kh_s[h] <= nc;
+      off += kh_s[h];
+    }
+    // the budgets fill the sequence's H K slots exactly (its idx region and
+    // compacted rows); anything else would be a fault of the search above,
+    // reported on the error word with the budgets left uniform
+    if (!ok || off != H * K) {
+      for (int h = 0; h < H; ++h) kh_s[h] = K;
+      if (a.err) __hip_atomic_store(a.err, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    off = 0;
+    for (int h = 0; h < H; ++h) {
+      tab[h] = make_int2(kh_s[h], off);
+      off += kh_s[h];
+    }
+  }
+  __syncthreads();
+  if (a.out)
+    for (int h = t; h < H; h += NT) a.out[(int64_t)b * H + h] = kh_s[h];
+}
+
+hipError_t launch_alloc(const AllocArgs &a, const SeqTable &st, hipStream_t s) {
+  if (a.Hkv < 1 || a.Hkv > kMaxAllocHeads || !a.vec_B || !a.vec_A || !a.hb) return hipErrorInvalidValue;
+  const size_t lds = alloc_lds_bytes(a.Hkv);
+  allow_lds(k_alloc, lds);
+  hipLaunchKernelGGL(k_alloc, dim3(st.batch), dim3(kAllocThreads), lds, s, a, st);
   return hipGetLastError();
 }
 

@@ -51,6 +51,7 @@ def test_defaults_follow_the_paper():
     assert p.gamma == 1.0 and p.use_last_query == 1 and p.terms == 7
     assert p.pool_kernel % 2 == 1
     assert p.pool_mode == bacon.POOL_MEAN_S
+    assert p.head_alloc == bacon.ALLOC_GIVEN and abs(p.alloc_floor - 0.2) < 1e-7
 
 
 @pytest.mark.parametrize("kw,expect_zero", [
@@ -72,7 +73,8 @@ def test_workspace_size_validates_shape(kw, expect_zero):
 @pytest.mark.parametrize("kw", [{"radius": -1}, {"radius": 17}, {"persist_m": 17}, {"rho": 0.0},
                                 {"gamma": -1.0}, {"pool_kernel": 4}, {"pool_kernel": 35},
                                 {"use_last_query": 2}, {"terms": 8}, {"pool_mode": -1},
-                                {"pool_mode": 3}])
+                                {"pool_mode": 3}, {"head_alloc": 2}, {"alloc_floor": -0.1},
+                                {"alloc_floor": 1.5}])
 def test_bad_params_rejected(kw):
     assert _ws(_shape(), bacon.default_params(**kw)) == 0
 
@@ -189,6 +191,18 @@ def test_calls_reject_bad_batches_and_order_before_enqueueing():
     assert L.bacon_score(h, 9, C.byref(good.c), fake, fake, None, fake, fake,
                          None) == bacon.ERR_INVALID
     assert b"layer" in L.bacon_last_error()
+    # adaptive allocation: NULL or misaligned pointers, head budgets given,
+    # and the output switch
+    assert L.bacon_allocate_heads(h, C.byref(good.c), None, fake, None) == bacon.ERR_INVALID
+    assert L.bacon_allocate_heads(h, C.byref(good.c), fake, C.c_void_p(0x200002),
+                                  None) == bacon.ERR_INVALID
+    hb = bacon.BatchLayout([0, 1000, 3000], [64, 128], head_budgets=np.full((2, 2), 8))
+    assert L.bacon_allocate_heads(h, C.byref(hb.c), fake, fake, None) == bacon.ERR_INVALID
+    assert b"per-sequence" in L.bacon_last_error()
+    assert L.bacon_allocate_heads(None, C.byref(good.c), fake, fake, None) == bacon.ERR_INVALID
+    assert L.bacon_alloc_output(h, C.c_void_p(0x200002)) == bacon.ERR_INVALID
+    assert L.bacon_alloc_output(h, fake) == bacon.OK
+    assert L.bacon_alloc_output(h, None) == bacon.OK
     # too long a sequence for the select kernel
     big = _init(_shape(max_total_tokens=70000, max_batch=1))[1]
     assert L.bacon_select_topk(big, C.byref(_batch([0, 40000], [4]).c), fake, fake,

@@ -134,3 +134,22 @@ def _box(x, k):
     num = np.convolve(x, ones, mode="full")[h:h + n]
     den = np.convolve(np.ones(n), ones, mode="full")[h:h + n]
     return num / den
+
+
+def test_zero_budget_head(oracle):
+    """A head the allocation leaves without slots keeps nothing (lambda 0:
+    its scale-matching set is empty); the other heads select as with their
+    own budgets everywhere."""
+    wl = inputs.Workload("pin", 2, 4, 2, 16, 4, 3, "fp32", (70, 45), (8, 6),
+                         ((5, 40), (5, 30)), 1, 98)
+    hb = np.array([[0, 5], [3, 0]], np.int32)
+    p = oracle.Prompt.for_workload(wl)
+    u = oracle.Prompt.for_workload(wl.with_(budgets=(5, 3)))
+    for l in range(wl.num_layers):
+        x = inputs.layer_inputs(wl, l)
+        r = p.layer(l, x["q_win"], x["k"], head_budgets=hb)
+        ru = u.layer(l, x["q_win"], x["k"])
+        assert r["n_kept"][0, 0] == 0 and r["n_kept"][1, 1] == 0
+        assert r["lambda"][0, 0] == 0.0 and r["m_count"][0, 0] == 0
+        assert np.array_equal(p.idx_of(r, 0, 1), u.idx_of(ru, 0, 1))
+        assert np.array_equal(p.idx_of(r, 1, 0), u.idx_of(ru, 1, 0))
