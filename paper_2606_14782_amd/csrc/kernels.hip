@@ -1190,8 +1190,11 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+  // the next tile now; each later tile when the tile two before it starts,
+  // so that the chunks sharing a CU receive their keys interleaved
+  constexpr int EARLY = KT < 2 ? KT : 2;
 #pragma unroll
-  for (int kt = 1; kt < KT; ++kt) load_tile(kt);
+  for (int kt = 1; kt < EARLY; ++kt) load_tile(kt);
   asm volatile("" ::: "memory");
 
   int koff[NU];
@@ -1209,6 +1212,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   for (int j = 0; j < NRT; ++j) { m_run[j] = -INFINITY; l_run[j] = 0.f; }
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
+    if (kt + EARLY < KT) load_tile(kt + EARLY);
     const int kbase = k0 + (wave * KT + kt) * 32;
     const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
 #pragma unroll
