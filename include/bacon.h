@@ -147,7 +147,9 @@ typedef struct {
 } bacon_shape;
 
 /* A packed batch.  The arrays live in HOST memory and are copied by the call.
- * cu_seqlens[0] = 0 and W <= N_b = cu_seqlens[b+1]-cu_seqlens[b] <= 32768.
+ * cu_seqlens[0] = 0 and W <= N_b = cu_seqlens[b+1]-cu_seqlens[b] <= 131072
+ * (bacon_calibrate and bacon_select_topk, whose select holds a sequence in
+ * LDS: <= 32768, UNSUPPORTED beyond).
  * Budgets: `head_budgets` [batch][num_kv_heads], when not NULL, gives every
  * (sequence, KV head) its own budget K_{b,h} >= 1 (a head-wise allocation of
  * the backbone method, Sec. 4 Preliminaries, kept as it is); otherwise every

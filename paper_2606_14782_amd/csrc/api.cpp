@@ -448,6 +448,9 @@ bacon_status check_lds(const bacon_ctx *c, const bacon_batch *bt, int chunk, boo
   const bool bf16 = c->shape.dtype == BACON_BF16;
   if (passes && pass_lds_bytes(PASS_FUSED, bf16, c->shape.head_dim, c->L.rpad, chunk) > kLdsBytes)
     return fail(BACON_ERR_UNSUPPORTED, "pass workgroup needs more LDS than a CU has");
+  if (sel_mode >= 0 && max_len(bt) > kMaxSelLen)
+    return fail(BACON_ERR_UNSUPPORTED, "the split calls select sequences of up to %d tokens (%d given); "
+                "the fused calls take up to %d", kMaxSelLen, max_len(bt), kMaxSeqLen);
   if (sel_mode >= 0 && select_lds_bytes(sel_mode, max_len(bt)) > (size_t)kLdsBytes)
     return fail(BACON_ERR_UNSUPPORTED, "select workgroup needs more LDS than a CU has");
   if (sel_mode == SEL_CALIB) {

@@ -7,12 +7,13 @@
 namespace bacon {
 
 constexpr int kMaxBatch = 64;       // sequences per batch (kernel-argument table)
-constexpr int kMaxSeqLen = 32768;   // positions per sequence held by the select kernel
+constexpr int kMaxSeqLen = 131072;  // positions per sequence (the segment select of the fused calls)
+constexpr int kMaxSelLen = 32768;   // positions per sequence of the split calls' block select (in LDS)
 constexpr int kMaxRows = 256;       // G*W window rows per KV head (8 row tiles of 32)
 constexpr int kMaxRing = 16;        // persistence depth m
 constexpr int kMaxChunk = 4096;     // keys per pass workgroup
 constexpr int kSelThreads = 1024;
-constexpr int kSelPer = kMaxSeqLen / kSelThreads;   // positions per select thread
+constexpr int kSelPer = kMaxSelLen / kSelThreads;   // positions per select thread
 constexpr int kHistBins = 2048;     // 11-bit digits of the block select
 constexpr int kSegLen = 2048;       // positions per segment of the histogram select
 constexpr int kSegThreads = 1024;

@@ -2081,7 +2081,7 @@ using SelShared = SelSharedT<kSelThreads>;
 // LDS: S padded by one word per kSelPer (thread-contiguous reads hit distinct
 // banks), reused as the slot table.
 __device__ __forceinline__ int pad32(int i) { return i + i / kSelPer; }
-constexpr int kArrWords = kMaxSeqLen + kMaxSeqLen / kSelPer + 64;
+constexpr int kArrWords = kMaxSelLen + kMaxSelLen / kSelPer + 64;
 
 template <int MODE>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) {
@@ -2093,7 +2093,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
   const int nc = n - a.W;                           // candidate set [0, nc)
   const int K = head_budget(st, a.hb, a.Hkv, b, h);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  // LDS: arr [pad32 extent of kMaxSeqLen], candidate list, then per-mode tables
+  // LDS: arr [pad32 extent of kMaxSelLen], candidate list, then per-mode tables
   unsigned *ckey = reinterpret_cast<unsigned *>(arr + kArrWords);
   int *cpos = reinterpret_cast<int *>(ckey + kCandCap);
 
@@ -2156,7 +2156,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
     if (calib) {
       auto keyB = [&](int j) -> unsigned {
         const int i = t + j * kSelThreads;
-        const unsigned kx = float_key(arr[pad32(i)]);   // i < kMaxSeqLen: inside arr
+        const unsigned kx = float_key(arr[pad32(i)]);   // i < kMaxSelLen: inside arr
         return i < nc ? kx : 0u;
       };
       auto posf = [&](int j) -> int { return t + j * kSelThreads; };
@@ -2341,7 +2341,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a, SeqTable st) 
 }
 
 size_t select_lds_bytes(int mode, int max_len) {
-  (void)max_len;   // arr always spans kMaxSeqLen so strided reads need no clamping
+  (void)max_len;   // arr always spans kMaxSelLen so strided reads need no clamping
   size_t bytes = (size_t)kArrWords * sizeof(float) +                              // arr (padded)
                  2 * kCandCap * sizeof(unsigned);                                // candidate list
   if (mode != SEL_TOPK) bytes += 2 * kEdgeCap * sizeof(float);                   // boundary tables
@@ -2401,14 +2401,14 @@ constexpr int kSegWinJ = (kSegWin + kSegThreads - 1) / kSegThreads;
 constexpr int kMaxRadius = 16;                             // largest coherence radius
 constexpr int kSegE = kSegWin + 2 * kMaxRadius;            // E over the window and the radius
 constexpr int kSegEJ = (kSegE + kSegThreads - 1) / kSegThreads;
-constexpr int kAllPer = kMaxSeqLen / kSegThreads;          // positions of a sequence per thread
+constexpr int kAllPer = kMaxSelLen / kSegThreads;          // positions per thread of the register fallback
 constexpr int kHPer = kHBins / kSegThreads;                // histogram bins per thread
 constexpr int kListPer = 4;                                // list entries per thread
 constexpr int kListSpec = 2;                               // of them loaded before the counts are known
 constexpr int kListCap = kListPer * kSegThreads;           // list entries of a (sequence, KV head)
 constexpr int kMaxSegs = kMaxSeqLen / kSegLen;             // segments of a sequence
 constexpr int kMomChunk = 4096;                            // scale-matching entries per LDS round
-static_assert(kAllPer <= 32 && kHPer % 4 == 0 && kMaxSegs <= kSegThreads / 64, "select layout");
+static_assert(kAllPer <= 32 && kHPer % 4 == 0 && kMaxSegs <= 64, "select layout");
 
 __device__ __forceinline__ int find_seg(const SeqTable &st, int seg) {
   int b = 0;
@@ -2496,6 +2496,68 @@ __device__ __forceinline__ void hist_threshold(const unsigned *gh, KeyF key, Pos
   } else {
     block_threshold<PER>(key, pos, k, xk, pthr, ss, ckey, cpos);
   }
+}
+
+// Exact top-k threshold (xk, pthr) over the positions [0, n) of a sequence
+// longer than the register form holds (n > kAllPer * NT), its keys read from
+// global memory once per step: the boundary bin from the histogram gh (key
+// bits 30..18; the method's scores are non-negative, so bit 31 is set), then
+// LDS histograms of bits 17..7 and 6..0 of the keys inside it, then the
+// position of the need-th key equal to the threshold (position ascending)
+// from counts over contiguous ranges of positions.  Kept iff key > xk, or
+// key == xk and position <= pthr.  1 <= k <= the count of nonzero keys.
+// keyf(i) is the key of position i (0: not a candidate).  Ends with a barrier.
+template <int COPIES, typename KeyF>
+__device__ __forceinline__ void stream_threshold(const unsigned *gh, KeyF keyf, int n, int k,
+                                                 unsigned &xk, int &pthr,
+                                                 SelSharedT<kSegThreads> &ss) {
+  constexpr int NT = kSegThreads;
+  const int t = threadIdx.x;
+  unsigned cb[kHPer];
+  load_bins<COPIES>(gh, cb);
+  bins_boundary<kHPer, NT>(cb, k, ss);
+  const unsigned beta = (unsigned)ss.bc_i[0];
+  int need = k - ss.bc_i[1];
+  lds_barrier();
+  unsigned digit[2];
+#pragma unroll
+  for (int lev = 0; lev < 2; ++lev) {
+    for (int q = t; q < kHistBins; q += NT) ss.hist[q] = 0u;
+    lds_barrier();
+    for (int i = t; i < n; i += NT) {
+      const unsigned x = keyf(i);
+      if (x == 0u || (unsigned)hbin(x) != beta) continue;
+      if (lev == 0) {
+        atomicAdd(&ss.hist[(x >> 7) & (kHistBins - 1)], 1u);
+      } else if (((x >> 7) & (kHistBins - 1)) == digit[0]) {
+        atomicAdd(&ss.hist[x & 127u], 1u);
+      }
+    }
+    lds_barrier();
+    hist_boundary<NT>(need, ss);
+    digit[lev] = (unsigned)ss.bc_i[0];
+    need -= ss.bc_i[1];
+    lds_barrier();
+  }
+  xk = 0x80000000u | (beta << 18) | (digit[0] << 7) | digit[1];
+  // the need-th position (ascending) among the keys equal to xk
+  const int ch = (n + NT - 1) / NT;
+  const int i0 = min(n, t * ch), i1 = min(n, i0 + ch);
+  if (t == 0) ss.bc_i[2] = n - 1;   // in range whatever the counts say
+  unsigned c = 0;
+  for (int i = i0; i < i1; ++i) c += keyf(i) == xk ? 1u : 0u;
+  const unsigned ex = block_excl_scan_u<NT>(c, ss);
+  if (ex < (unsigned)need && (unsigned)need <= ex + c) {
+    unsigned r = ex;
+    for (int i = i0; i < i1; ++i)
+      if (keyf(i) == xk && ++r == (unsigned)need) {
+        ss.bc_i[2] = i;
+        break;
+      }
+  }
+  lds_barrier();
+  pthr = ss.bc_i[2];
+  lds_barrier();
 }
 
 // The lists of the nseg segments of a (sequence, KV head) as one sequence of
@@ -2673,11 +2735,12 @@ __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) 
 // Loads the selection record and the segments' lists of a (sequence, KV
 // head) into registers as one sequence of entries e = t + j*NT in (segment,
 // slot) order, which is position order.  First round: kListSpec slots per
-// thread, every slot a segment may hold up to cs = kListSpec*NT/nseg, loaded
-// with the counts in flight alongside.  When a count exceeds cs, a second
-// round loads the exact entries from the counts' prefix (up to kListCap).
-// Entries that do not exist get key 0.  `fits` is false when the lists
-// exceed kListCap.  scnt is LDS for kMaxSegs + 1 values.  Ends with a barrier.
+// thread, every slot a segment may hold up to cs = kListSpec*NT/nseg (a
+// multiple of 64; none beyond 32 segments), loaded with the counts in flight
+// alongside.  When a count exceeds cs, a second round loads the exact entries
+// from the counts' prefix (up to kListCap).  Entries that do not exist get
+// key 0.  `fits` is false when the lists exceed kListCap.  scnt is LDS for
+// kMaxSegs values.  Ends with a barrier.
 template <bool WITH_V>
 __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t base, int n, int h,
                                            const int4 *recp, const unsigned *lkey, const int *lpos,
@@ -2692,10 +2755,11 @@ __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t ba
   rec = *recp;                                   // first: it heads the longest chain
   // unconditional (clamped) so that no branch waits for the loads in flight
   int c = cnts[(int64_t)h * st.total_segs + st.seg_base[b] + min(tt, L.nseg - 1)];
+  const int csd = max(cs, 64);    // the addressing only (no first round when cs is 0)
 #pragma unroll
   for (int j = 0; j < kListSpec; ++j) {
-    const int e = tt + j * NT, s = min(e / cs, L.nseg - 1);
-    const int64_t o = base + min(s * kSegLen + (e - s * cs), n - 1);
+    const int e = tt + j * NT, s = min(e / csd, L.nseg - 1);
+    const int64_t o = base + min(s * kSegLen + (e - s * csd), n - 1);
     k[j] = lkey[o];
     p[j] = lpos[o];
     if constexpr (WITH_V) v[j] = lv[o];
@@ -2708,9 +2772,8 @@ __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t ba
   if (t < kMaxSegs) scnt[t] = t < L.nseg ? c : 0;
   lds_barrier();
   // every thread reads all counts: no second barrier, no wait for the lists
-  bool over = false;
-#pragma unroll
-  for (int s = 0; s < kMaxSegs; ++s) over |= scnt[s] > cs;
+  bool over = cs == 0;
+  for (int s = 0; s < L.nseg; ++s) over |= scnt[s] > cs;
   if (!over) {
     L.fits = true;
 #pragma unroll
@@ -2720,25 +2783,85 @@ __device__ __forceinline__ void load_lists(const SeqTable &st, int b, int64_t ba
     }
     return;
   }
-  // second round: exact entries after the counts' prefix
-  int pre[kMaxSegs + 1];
-  pre[0] = 0;
-#pragma unroll
-  for (int s = 0; s < kMaxSegs; ++s) pre[s + 1] = pre[s] + scnt[s];
-  const int total = pre[kMaxSegs];
+  // second round: exact entries after the counts' prefix (inclusive, in
+  // place), each entry's segment found by bisection
+  lds_barrier();
+  if (t < 64) {
+    const unsigned c0 = t < kMaxSegs ? (unsigned)scnt[t] : 0u;
+    const unsigned inc = wave_incl_sum_u(c0);
+    if (t < kMaxSegs) scnt[t] = (int)inc;
+  }
+  lds_barrier();
+  const int total = scnt[L.nseg - 1];
   L.fits = total <= kListCap;
   if (!L.fits) return;
 #pragma unroll
   for (int j = 0; j < kListPer; ++j) {
     const int e = t + j * NT;
-    int s = 0;
-#pragma unroll
-    for (int q = 1; q < kMaxSegs; ++q) s += (e >= pre[q]) ? 1 : 0;
-    const int64_t o = base + min(s * kSegLen + (e - pre[s]), n - 1);
+    int lo = 0, hi = L.nseg - 1;          // the first segment whose prefix exceeds e
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (scnt[mid] > e) hi = mid; else lo = mid + 1;
+    }
+    const int before = lo > 0 ? scnt[lo - 1] : 0;
+    const int64_t o = base + min(lo * kSegLen + (e - before), n - 1);
     k[j] = e < total ? lkey[o] : 0u;
     p[j] = lpos[o];
     if constexpr (WITH_V) v[j] = lv[o];
   }
+}
+
+// whole_moments beyond the register form (nc > kAllPer * NT): the threshold
+// from global memory, then the members' moments in one more pass.
+__device__ __forceinline__ void whole_moments_stream(const SegArgs &a, int64_t base, int nc,
+                                                                int M, const unsigned *gh,
+                                                                SelSharedT<kSegThreads> &ss,
+                                                                double *part) {
+  constexpr int NT = kSegThreads;
+  const int t = threadIdx.x;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  unsigned xm;
+  int pm;
+  stream_threshold<kHCopies>(gh, [&](int i) { return float_key(a.vec_B[base + i]); }, nc, M, xm, pm, ss);
+  const double bref = (double)key_float(xm), vref = (double)a.vec_V[base + pm];
+  for (int i = t; i < nc; i += NT) {
+    const float bv = a.vec_B[base + i];
+    const unsigned x = float_key(bv);
+    if (x > xm || (x == xm && i <= pm)) {
+      const double db = (double)bv - bref, dv = (double)a.vec_V[base + i] - vref;
+      s0 += db; s1 += db * db; s2 += dv; s3 += dv * dv;
+    }
+  }
+  part[0] = s0; part[1] = s1; part[2] = s2; part[3] = s3; part[4] = bref;
+}
+
+// whole_topk beyond the register form: the threshold from global memory,
+// then the members in position order over contiguous ranges of positions.
+__device__ __forceinline__ void whole_topk_stream(const SegArgs &a, int64_t base, int nc,
+                                                             int kept, const unsigned *gh, int32_t *idx,
+                                                             int *tbl, SelSharedT<kSegThreads> &ss) {
+  constexpr int NT = kSegThreads;
+  const int t = threadIdx.x;
+  unsigned xk;
+  int pk;
+  stream_threshold<1>(gh, [&](int i) { return a.vec_S[base + i]; }, nc, kept, xk, pk, ss);
+  const int ch = (nc + NT - 1) / NT;
+  const int i0 = min(nc, t * ch), i1 = min(nc, i0 + ch);
+  auto member = [&](int i) {
+    const unsigned x = a.vec_S[base + i];
+    return x != 0u && (x > xk || (x == xk && i <= pk));
+  };
+  unsigned c = 0;
+  for (int i = i0; i < i1; ++i) c += member(i) ? 1u : 0u;
+  unsigned o = block_excl_scan_u<NT>(c, ss);
+  for (int i = i0; i < i1; ++i)
+    if (member(i)) {
+      if (o < (unsigned)kept) {
+        if (idx) idx[o] = i;
+        tbl[o] = i;
+      }
+      ++o;
+    }
 }
 
 // Scale-matching set and the thread's part of its moments over every
@@ -2873,7 +2996,10 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
       }
     } else {
       double part[5];
-      whole_moments(a, base, nc, M, a.hist_B + hrow * kHCopies, ss, ckey, cpos, pre, mom, part);
+      if (nc > kAllPer * kSegThreads)
+        whole_moments_stream(a, base, nc, M, a.hist_B + hrow * kHCopies, ss, part);
+      else
+        whole_moments(a, base, nc, M, a.hist_B + hrow * kHCopies, ss, ckey, cpos, pre, mom, part);
       s0 = part[0]; s1 = part[1]; s2 = part[2]; s3 = part[3];
       bref_set = part[4];
     }
@@ -3093,7 +3219,11 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
         }
       }
     } else {
-      whole_topk(a, base, nc, kept, a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, part == 0 ? idx : nullptr,
+      if (nc > kAllPer * kSegThreads)
+        whole_topk_stream(a, base, nc, kept, a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins,
+                          part == 0 ? idx : nullptr, tbl, ss);
+      else
+        whole_topk(a, base, nc, kept, a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, part == 0 ? idx : nullptr,
                  tbl, ss, ckey, cpos, pre);
     }
   }

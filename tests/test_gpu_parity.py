@@ -838,3 +838,67 @@ def test_exact_ties_resolve_by_lowest_position(n, K, distinct, params, monkeypat
     monkeypatch.setenv("BACON_SINGLE", "1")
     run_case(f"exact-ties-{params}-n{n}-d{distinct}/single", wl, gpu_kw=kw, orc_kw=kw,
              make=_tied_inputs(wl, distinct), split=False)
+
+
+LONG_CASES = {
+    # one GPU's share of the paper's extreme contexts (budget 1024): the
+    # single-read pass (every chunk of the sequence fits on the GPU at once)
+    "long-n65536": lambda: inputs.Workload(
+        "long", 3, 16, 4, 128, 32, 7, "bf16", (65536,), (1024,), ((32, 65000),), 8, 41,
+        frame_rank=8, frame_len=256),
+    "long-n131072": lambda: inputs.Workload(
+        "long", 3, 8, 2, 128, 32, 7, "bf16", (131072,), (1024,), ((32, 130000),), 8, 42,
+        frame_rank=8, frame_len=256),
+    # more chunks than the GPU holds at once: the two-K-pass path
+    "long-n65536-h8": lambda: inputs.Workload(
+        "long", 3, 32, 8, 128, 32, 7, "bf16", (65536,), (512,), ((32, 65000),), 8, 43),
+    # a long sequence among short ones
+    "long-ragged": lambda: inputs.Workload(
+        "long", 3, 8, 2, 128, 32, 7, "bf16", (3000, 98304, 20000), (256, 1024, 128),
+        ((32, 2800), (32, 98000), (32, 19000)), 8, 44),
+}
+
+
+@pytest.mark.parametrize("name", list(LONG_CASES))
+def test_long_sequences(name):
+    """Sequences beyond 32768 tokens (up to 131072) through the fused call:
+    64 select segments per sequence, scores and kept sets against the oracle.
+    (The split calls' block select holds at most 32768 positions.)"""
+    run_case(name, LONG_CASES[name](), split=False)
+
+
+@pytest.mark.parametrize("name", ["long-n131072", "long-ragged"])
+def test_long_prompt_call_equals_layer_calls(name):
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = LONG_CASES[name]()
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+    qs = [P.to_dev(x["q_win"], wl) for x in xs]
+    ks = [P.to_dev(x["k"], wl) for x in xs]
+    vs = [P.to_dev(x["v"], wl) for x in xs]
+    a, b = P.make_ctx(wl), P.make_ctx(wl)
+    a.bacon_begin_prompt(batch)
+    want = [a.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l]) for l in range(wl.num_layers)]
+    b.bacon_begin_prompt(batch)
+    got = b.bacon_compress_prompt(0, batch, qs, ks, vs)
+    torch.cuda.synchronize()
+    for l in range(wl.num_layers):
+        for i, what in enumerate(("idx", "k_out", "v_out")):
+            assert torch.equal(got[l][i], want[l][i]), f"{name} L{l} {what}"
+
+
+@pytest.mark.parametrize("n,K,params", [(65536, 300, "residual-only"),
+                                        (131072, 1024, "window-score")])
+def test_long_exact_ties_take_the_streamed_select(n, K, params, monkeypatch):
+    """Identical keys over a sequence beyond 32768 tokens: every candidate
+    falls in one histogram bin, so the scale-matching set (with the evidence
+    term) and the top-K take the select that streams the sequence from memory
+    (no register copy fits); on the two-K-pass path the equal scores are
+    bit-equal and the kept set must be the lowest positions exactly."""
+    monkeypatch.setenv("BACON_SINGLE", "0")
+    kw = TIE_PARAMS[params]
+    wl = inputs.Workload("ties", 2, 4, 2, 64, 8, 1, "bf16", (n,), (K,), ((0, 0),), 0, 23)
+    worst, stats = run_case(f"long-ties-n{n}", wl, gpu_kw=kw, orc_kw=kw, make=_tied_inputs(wl, 1),
+                            strict=True, split=False)
+    assert stats["strict"] == stats["pairs"]
