@@ -48,6 +48,7 @@ _NAMES = [
     (r"bacon::k_select<1>", "select_calib"),
     (r"bacon::k_select<2>", "select_topk"),
     (r"bacon::k_elem\b", "calib_elem"),
+    (r"bacon::k_alloc\b", "head_alloc"),
 ]
 
 

@@ -167,7 +167,7 @@ struct bacon_ctx {
   std::vector<int32_t> cu;
   int chunk_stages_override = 0;
   bool kr_off = false;   // key-register passes switched off (streaming passes only)
-  bool single_off = false;   // single-read pass switched off (two K passes)
+  int single_mode = -1;      // single-read pass: -1 where it pays, 0 never, 1 wherever it can run
   int single_cap = -1;       // single-read workgroups the device holds at once (-1: not yet asked)
   // test instrumentation (bacon_debug_capture): per-layer copies of B, V, lambda
   float *cap_B = nullptr, *cap_V = nullptr, *cap_lambda = nullptr;
@@ -515,7 +515,7 @@ bacon_status bacon_init(bacon_ctx **ctx, const bacon_shape *shape, const bacon_p
   c->L = L;
   if (const char *e = std::getenv("BACON_CHUNK_STAGES")) c->chunk_stages_override = std::atoi(e);
   if (const char *e = std::getenv("BACON_KEY_REGISTERS")) c->kr_off = std::atoi(e) == 0;
-  if (const char *e = std::getenv("BACON_SINGLE")) c->single_off = std::atoi(e) == 0;
+  if (const char *e = std::getenv("BACON_SINGLE")) c->single_mode = std::atoi(e) == 0 ? 0 : 1;
   *ctx = c;
   return BACON_OK;
 }
@@ -751,13 +751,19 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
   // One read of K (the single-read pass) when its meeting can complete:
   // workgroups run in grid order, chunk-major with the KV heads innermost,
   // so at most the groups of one sequence are incomplete at a time, and
-  // all their chunks must fit on the GPU at once.  With normalisers given
-  // by the caller the key-register pass 2 alone already reads K once.
-  if (r.kr && !d_lse && !c->single_off) {
+  // all their chunks must fit on the GPU at once.  It pays where the whole
+  // grid is resident at once and fills at least half of the GPU's slots:
+  // a grid that runs in rounds stalls at every sequence split across them,
+  // and a small one leaves the GPU idle through the meeting, where the two-
+  // pass path overlaps two layers in each launch.  With normalisers given by
+  // the caller the key-register pass 2 alone already reads K once.
+  if (r.kr && !d_lse && c->single_mode != 0) {
     if (c->single_cap < 0) c->single_cap = single_resident_blocks(c->shape.head_dim, c->L.rpad);
     int nmax = 0;
     for (int b = 0; b < bt->batch; ++b) nmax = std::max(nmax, r.st.chunk_base[b + 1] - r.st.chunk_base[b]);
-    r.single = (int64_t)nmax * c->shape.num_kv_heads <= c->single_cap;
+    const int64_t hkv = c->shape.num_kv_heads, grid = (int64_t)r.st.total_chunks * hkv;
+    r.single = (int64_t)nmax * hkv <= c->single_cap &&
+               (c->single_mode == 1 || (grid <= c->single_cap && 2 * grid >= c->single_cap));
   }
   r.kmax = 0;
   for (int b = 0; b < bt->batch; ++b) r.kmax = std::max(r.kmax, batch_seq_rows(bt, c->shape.num_kv_heads, b));

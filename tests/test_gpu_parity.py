@@ -735,6 +735,15 @@ def test_near_ties_with_pooling(n, K, distinct):
     run_case(f"ties-n{n}-d{distinct}", wl, make=_tied_inputs(wl, distinct))
 
 
+@pytest.mark.parametrize("n,K,distinct", [(600, 40, 1), (3000, 100, 3), (20000, 256, 2)])
+def test_near_ties_single_pass(n, K, distinct, monkeypatch):
+    """The near-tie cases on the single-read pass (forced): equal keys differ
+    there in the last bits of B as well."""
+    monkeypatch.setenv("BACON_SINGLE", "1")
+    wl = inputs.Workload("ties", 3, 4, 2, 64, 8, 5, "bf16", (n,), (K,), ((0, 0),), 0, 21)
+    run_case(f"ties-single-n{n}-d{distinct}", wl, make=_tied_inputs(wl, distinct), split=False)
+
+
 def _constant_evidence_inputs(wl):
     """Layer 0: keys of one vector on [0, n/2) and another on the rest, the
     last window query aligned with the first and the other rows with the
@@ -766,18 +775,23 @@ def _constant_evidence_inputs(wl):
 
 def test_constant_evidence_on_the_scale_matching_set():
     """V constant (and positive) over the scale-matching set while B varies,
-    so lambda = gamma Std_M(B) / eps (Eq. lambda_solution).  The split call's
-    two-pass score gives identical keys bit-equal probabilities, so its
-    Std_M(V) is exactly 0 (moments of shifted values) and its lambda agrees
-    with the oracle's within rtol.  The fused call's single-read pass stores
-    each probability relative to its tile's running maximum, so identical keys
-    in tiles with different maxima round differently and its Std_M(V) is a
-    rounding residue: its lambda is held to the interval its B and V allow,
-    and its kept set to the oracle's."""
+    so lambda = gamma Std_M(B) / eps (Eq. lambda_solution).  The two-pass
+    score (the split call, and the fused call on this small grid) gives
+    identical keys bit-equal probabilities, so Std_M(V) is exactly 0 (moments
+    of shifted values) and lambda agrees with the oracle's within rtol.  The
+    single-read pass (forced for a second fused run) stores each probability
+    relative to its tile's running maximum, so identical keys in tiles with
+    different maxima round differently and its Std_M(V) is a rounding
+    residue: its lambda is held to the interval its B and V allow, and its
+    kept set to the oracle's."""
     from paper_2606_14782_amd import bacon
     kw = dict(terms=4, persist_m=1)
     wl = inputs.Workload("const-v", 2, 1, 1, 64, 8, 1, "bf16", (1000,), (32,), ((0, 0),), 0, 28)
     run_case("const-v", wl, gpu_kw=kw, orc_kw=kw, make=_constant_evidence_inputs(wl))
+    with pytest.MonkeyPatch.context() as mp:
+        mp.setenv("BACON_SINGLE", "1")
+        run_case("const-v/single", wl, gpu_kw=kw, orc_kw=kw, make=_constant_evidence_inputs(wl),
+                 split=False)
     orc = ref.Prompt.for_workload(wl, P.oracle_params(**kw))
     ctx = P.make_ctx(wl, P.params_for(wl, **kw))
     batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
@@ -902,3 +916,46 @@ def test_long_exact_ties_take_the_streamed_select(n, K, params, monkeypatch):
     worst, stats = run_case(f"long-ties-n{n}", wl, gpu_kw=kw, orc_kw=kw, make=_tied_inputs(wl, 1),
                             strict=True, split=False)
     assert stats["strict"] == stats["pairs"]
+
+
+SINGLE_FORCED = ["llava-n2048", "ragged-b8", "llava-small", "ragged-small", "video-small",
+                 "batch64", "gqa3-w8-d64", "w1-budget1", "pool33-r16-segments", "M-over-segment",
+                 "pool-max-s", "pool-mean-b", "large-budget-whole-sequence", "window-score-only",
+                 "gamma0", "radius0-m0"]
+
+
+@pytest.mark.parametrize("name", SINGLE_FORCED)
+def test_single_pass_forced(name, monkeypatch):
+    """The single-read pass forced (BACON_SINGLE=1) where the library would
+    take the two-K-pass path: small grids, and batches whose grid runs in
+    rounds (every sequence's chunks still fit on the GPU at once)."""
+    monkeypatch.setenv("BACON_SINGLE", "1")
+    if name in CASES:
+        wl = CASES[name]()
+        run_case(name + "/single", wl.with_(num_layers=min(wl.num_layers, 5)), split=False)
+    else:
+        c = EDGE[name]
+        run_case(name + "/single", c["wl"], c.get("gpu"), c.get("orc"), split=False)
+
+
+@pytest.mark.parametrize("name", ["ragged-b8", "llava-n2048"])
+def test_single_pass_forced_prompt_call(name, monkeypatch):
+    import torch
+    from paper_2606_14782_amd import bacon
+    monkeypatch.setenv("BACON_SINGLE", "1")
+    wl = CASES[name]().with_(num_layers=3)
+    batch = bacon.BatchLayout(wl.cu_seqlens, wl.budgets_arr)
+    xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+    qs = [P.to_dev(x["q_win"], wl) for x in xs]
+    ks = [P.to_dev(x["k"], wl) for x in xs]
+    vs = [P.to_dev(x["v"], wl) for x in xs]
+    a, b = P.make_ctx(wl), P.make_ctx(wl)
+    a.bacon_begin_prompt(batch)
+    want = [a.bacon_compress_layer(l, batch, qs[l], ks[l], vs[l]) for l in range(wl.num_layers)]
+    b.bacon_begin_prompt(batch)
+    got = b.bacon_compress_prompt(0, batch, qs, ks, vs)
+    torch.cuda.synchronize()
+    for l in range(wl.num_layers):
+        for i, what in enumerate(("idx", "k_out", "v_out")):
+            assert torch.equal(got[l][i], want[l][i]), f"{name} L{l} {what}"
+    assert a.bacon_debug_device_errors() == 0 and b.bacon_debug_device_errors() == 0
