@@ -169,6 +169,7 @@ struct bacon_ctx {
   bool kr_off = false;   // key-register passes switched off (streaming passes only)
   int single_mode = -1;      // single-read pass: -1 where it pays, 0 never, 1 wherever it can run
   int single_cap = -1;       // single-read workgroups the device holds at once (-1: not yet asked)
+  int cus = -1;              // compute units of the device (-1: not yet asked)
   // test instrumentation (bacon_debug_capture): per-layer copies of B, V, lambda
   float *cap_B = nullptr, *cap_V = nullptr, *cap_lambda = nullptr;
   int32_t *alloc_out = nullptr;   // [num_layers, max_batch, Hkv] budgets of the adaptive allocation
@@ -839,7 +840,23 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
   g.row_bytes = c->shape.head_dim * (r.bf16 ? 2 : 4);
   g.flat_heads = r.adaptive;
   // final workgroups per (sequence, KV head): about one round over the CUs
-  g.parts = std::max(1, std::min(8, 256 / std::max(1, bt->batch * c->shape.num_kv_heads)));
+  // (in a prompt call the score workgroups of the next layer share the
+  // launch: fewer parts where that lets both fit in one round of the CUs)
+  if (c->cus < 0) {
+    int dev = 0;
+    c->cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) {
+      int n = 0;
+      if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) c->cus = n;
+    }
+  }
+  {
+    const int hkv = c->shape.num_kv_heads, heads = std::max(1, bt->batch * hkv);
+    const int score_wgs = r.st.total_segs * hkv;
+    g.parts = std::max(1, std::min(8, c->cus / heads));
+    if (score_wgs + g.parts * heads > c->cus && score_wgs + heads <= c->cus)
+      g.parts = (c->cus - score_wgs) / heads;
+  }
   return BACON_OK;
 }
 

@@ -3305,9 +3305,16 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
 //    that they hold CUs only briefly.
 //  * k_sel_b: [0, nfinal) the final top-K and compaction of the previous
 //    layer (parts per sequence), then the scores of this layer.
+// The jobs of one launch in grid order, the longest first: workgroups are
+// dispatched in that order, and those that find no CU free wait for one.
 __global__ __launch_bounds__(kSegThreads) void k_sel_a(SegArgs g, SegArgs gp, PassArgs m, SeqTable st,
                                                       int ncand, int nmerge) {
-  const int x = blockIdx.x, h = blockIdx.y;
+  const int h = blockIdx.y, nseg = st.total_segs;
+  if ((int)blockIdx.x < nseg) {
+    segcal_body(g, st, blockIdx.x, h);
+    return;
+  }
+  const int x = blockIdx.x - nseg;
   if (x < ncand) {
     segcand_body(gp, st, x, h);
   } else if (x < ncand + nmerge) {
@@ -3318,17 +3325,18 @@ __global__ __launch_bounds__(kSegThreads) void k_sel_a(SegArgs g, SegArgs gp, Pa
     const int grp = threadIdx.x / kMergeThreads;
     const int rg = (q - b * per_seq) * groups + grp;
     merge_rows(m, st, rg, b, h, threadIdx.x % kMergeThreads, mrg[grp], rg * kMergeRows < m.Rpad);
-  } else {
-    segcal_body(g, st, x - ncand - nmerge, h);
   }
 }
 
 __global__ __launch_bounds__(kSegThreads) void k_sel_b(SegArgs g, SegArgs gp, SeqTable st, int nfinal) {
-  const int x = blockIdx.x, h = blockIdx.y;
-  if (x < nfinal)
+  const int h = blockIdx.y, nseg = st.total_segs;
+  if ((int)blockIdx.x < nseg) {
+    segscore_body(g, st, blockIdx.x, h);
+  } else {
+    const int x = blockIdx.x - nseg;
     final_body(gp, st, x % gp.parts, x / gp.parts, h);
-  else
-    segscore_body(g, st, x - nfinal, h);
+  }
+  (void)nfinal;
 }
 
 size_t final_lds_bytes(int max_budget, int window) {
