@@ -231,3 +231,50 @@ def test_adaptive_prompt_call_equals_layer_calls(name):
     for l in range(wl.num_layers):
         for i, what in enumerate(("idx", "k_out", "v_out")):
             assert torch.equal(got[l][i], want[l][i]), f"{name} L{l} {what}"
+
+
+def test_adaptive_with_a_per_layer_budget_schedule():
+    """The adaptive allocation on a per-layer budget schedule (the backbone's
+    layer-wise budgets, each layer's H K_l slots allocated across its heads):
+    the prompt call with one batch per layer equals the per-layer calls bit
+    for bit, and each layer's budgets fill its own slots."""
+    import torch
+    from paper_2606_14782_amd import bacon
+    wl = CASES["ragged-small"]()
+    rng = np.random.default_rng(31)
+    sched = [tuple(int(x) for x in rng.choice([16, 64, 200], size=wl.batch))
+             for _ in range(wl.num_layers)]
+    batches = [bacon.BatchLayout(wl.cu_seqlens, np.asarray(s, np.int32)) for s in sched]
+    xs = [inputs.layer_inputs(wl, l) for l in range(wl.num_layers)]
+    qs = [P.to_dev(x["q_win"], wl) for x in xs]
+    ks = [P.to_dev(x["k"], wl) for x in xs]
+    vs = [P.to_dev(x["v"], wl) for x in xs]
+    prm = P.params_for(wl, head_alloc=bacon.ALLOC_ADAPTIVE, alloc_floor=0.2)
+    a, b = P.make_ctx(wl, prm), P.make_ctx(wl, prm)
+    ka = torch.zeros((wl.num_layers, wl.batch, wl.num_kv_heads), dtype=torch.int32, device="cuda")
+    kb = torch.zeros_like(ka)
+    a.bacon_alloc_output(ka)
+    b.bacon_alloc_output(kb)
+    a.bacon_begin_prompt(batches[0])
+    want = [a.bacon_compress_layer(l, batches[l], qs[l], ks[l], vs[l]) for l in range(wl.num_layers)]
+    b.bacon_begin_prompt(batches[0])
+    got = b.bacon_compress_prompt(0, batches[0], qs, ks, vs, layer_batches=batches)
+    torch.cuda.synchronize()
+    assert torch.equal(ka, kb)
+    for l in range(wl.num_layers):
+        for i, what in enumerate(("idx", "k_out", "v_out")):
+            assert torch.equal(got[l][i], want[l][i]), f"L{l} {what}"
+        kh = ka[l].cpu().numpy()
+        for bb, (s0, s1) in enumerate(P.seq_slices(wl)):
+            K = sched[l][bb]
+            if (s1 - s0) - wl.window > K:
+                assert kh[bb].sum() == wl.num_kv_heads * K, (l, bb)
+    assert a.bacon_debug_device_errors() == 0 and b.bacon_debug_device_errors() == 0
+
+
+def test_adaptive_on_a_long_sequence(monkeypatch):
+    """131072 tokens, budget 1024, two KV heads (the single-read pass): the
+    allocation and the kept sets against the oracle."""
+    wl = inputs.Workload("long", 2, 8, 2, 128, 32, 7, "bf16", (131072,), (1024,), ((32, 130000),),
+                         8, 45, frame_rank=8, frame_len=256)
+    run_adaptive("long-adaptive", wl, 0.2)
