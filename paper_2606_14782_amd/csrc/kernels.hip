@@ -36,6 +36,7 @@
 namespace bacon {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -74,6 +75,25 @@ __device__ __forceinline__ f32x16 mfma_unit(u32x4 a, u32x4 b, f32x16 c) {
 __device__ __forceinline__ float xor32(float v, int half) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return __uint_as_float(half ? r[0] : r[1]);
+}
+
+// Sum over the wave's 64 lanes through DPP moves (pairs, quads, half rows,
+// rows) and four lane reads: the same order, and so the same value, in every
+// lane.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f<0xB1>(v);    // quad_perm(1, 0, 3, 2)
+  v += dpp_f<0x4E>(v);    // quad_perm(2, 3, 0, 1)
+  v += dpp_f<0x141>(v);   // row_half_mirror
+  v += dpp_f<0x140>(v);   // row_mirror
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
 }
 
 // Pairwise (tree) sum and max of 16 values: depth 4 instead of a 16-long chain.
@@ -1071,21 +1091,24 @@ hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const Pass
 //    each tile used and p_min go to LDS.
 //  * The chunks of a (sequence, KV head) meet once: each publishes its
 //    per-row (max, sum) partial through to memory (agent-scope stores),
-//    counts itself on the group's arrival counter, and when all have arrived
-//    every workgroup merges all partials in chunk order into the same row
-//    normalisers.  The last workgroup to finish reading resets the counters.
+//    counts itself on the group's arrival counter; the last to arrive merges
+//    all partials in chunk order into the row normalisers and publishes them,
+//    and the others poll for them.  The last workgroup to finish reading
+//    resets the counters and the published words at its end.
 //    The waits are bounded: one that runs out sets the error word and goes
 //    on.  Workgroups are dispatched in grid order, chunk-major with the KV
 //    heads innermost, so the groups not yet complete are those of one
 //    sequence; the host launches this pass only when their chunks fit on the
 //    GPU at once.
 //  * Pass 2 turns each stored 32x32 block around with two MFMAs against the
-//    identity (a lane per key, the rows in registers), weights every row by
-//    exp2(tile max - lse) / 2^15 and sums the rows in-lane, and adds the
-//    tile's sum of the weighted p_min: B and Q without a second read of K or
-//    a second exp.  The tail (E to the history, B out,
-//    the B histogram) is that of the key-register pass 2.
+//    identity (a lane per key, the rows in registers) and sums its rows,
+//    each weighted by exp2(tile max - lse) / 2^15, with two more MFMAs whose
+//    other operand holds the row weights in fp16 as high and low parts; it
+//    adds the tile's sum of the weighted p_min: B and Q without a second
+//    read of K or a second exp.  The tail (E to the history, B out, the B
+//    histogram) is that of the key-register pass 2.
 constexpr float kPScaleLog2 = 15.f;          // stored probabilities are p * 2^15 (<= 2^15)
+constexpr int kWScaleLog2 = 12;              // pass 2's fp16 row factors are scaled by 2^(15 + this)
 constexpr unsigned kMeetSpin = 1u << 20;     // polls of a published word before giving up
 
 __device__ __forceinline__ void store_agent(float2 *p, float2 v) {
@@ -1105,6 +1128,20 @@ __device__ __forceinline__ float load_agent(const float *p) {
                                                      __HIP_MEMORY_SCOPE_AGENT));
 }
 
+// A device-scope atomic add whose old value is awaited only by await_vm():
+// the compiler's own form of a one-lane atomic waits for the return at once.
+// The vector atomic is the form the compiler emits for a relaxed agent-scope
+// add (old value returned); the compiler does not count it among its own
+// outstanding loads, which only makes its later waits stricter.
+__device__ __forceinline__ unsigned atomic_add_deferred(unsigned *p, unsigned v) {
+  unsigned r;
+  asm volatile("global_atomic_add %0, %1, %2, off sc0" : "=v"(r) : "v"(p), "v"(v) : "memory");
+  return r;
+}
+__device__ __forceinline__ void await_vm(unsigned &r) {
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(r) : : "memory");
+}
+
 __device__ __forceinline__ void pin8(unsigned (&v)[8]) {
   asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),
                "+v"(v[7]));
@@ -1119,15 +1156,18 @@ __device__ __forceinline__ unsigned pack_f16(float lo, float hi) {
 // LDS map of a single-read workgroup (bytes), NR = 32 * row tiles:
 //   qbuf  max(NR * ROWB, 4 * kHBins)      window queries; the B histogram after pass 2
 //   part  max(kKrWaves * NR, NT) float2   per-wave row partials; merge scratch
-//   fac   kKrWaves * KT * NR floats       the max each tile used; then its row factors
+//   fac   kKrWaves * KT * NR floats       the max each tile used
 //   rmn   kKrWaves * KT * NR floats       p_min * 2^15 of each row in each tile
 //   lse   NR floats                       merged row normalisers (log2 units)
 //   cb    KPW floats                      B of the chunk's keys
+//   wf    4 * kKrWaves * KT * NR + 32 fp16 the row factors as pass 2's operand:
+//                                         high and low parts, and the same on the
+//                                         last-query rows only; then zeros
 int single_lds_bytes(int head_dim, int rpad) {
   const int nr = 32 * kr_row_tiles(rpad), rowb = head_dim * 2, kpw = kr_keys(true, head_dim);
   const int kt = kpw / (32 * kKrWaves);
   return std::max(nr * rowb, 4 * kHBins) + 8 * std::max(kKrWaves * nr, 64 * kKrWaves) +
-         8 * kKrWaves * kt * nr + 4 * nr + 4 * kpw;
+         8 * kKrWaves * kt * nr + 4 * nr + 4 * kpw + 2 * (4 * kKrWaves * kt * nr + 32);
 }
 
 template <int D, bool W32, int NRT>
@@ -1154,6 +1194,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   float *rmn = fac + kKrWaves * KT * NR;
   float *lse = rmn + kKrWaves * KT * NR;
   float *cb = lse + NR;
+  _Float16 *wf = reinterpret_cast<_Float16 *>(cb + KPW);   // [4][kKrWaves * KT * NR] then 32 zeros
 
   // ---- loads: the window queries, the first key tile, and once the queries
   // are in LDS the other key tiles (as in the key-register passes)
@@ -1186,6 +1227,8 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
     const int i = t + j * NT, row = i / C::PIECES, pc = i % C::PIECES;
     *reinterpret_cast<u32x4 *>(qbuf + row * C::ROWB + 16 * (pc ^ (row & C::SWM))) = qv[j];
   }
+  // the zeros that pass 2's idle factor lanes read
+  if (t < 32) wf[4 * kKrWaves * KT * NR + t] = (_Float16)0.f;
   __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -1380,32 +1423,69 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   }
   if (t >= a.Rpad && t < NR) lse[t] = INFINITY;   // rows of the last tile past Rpad: factor 0
   __syncthreads();
-  if (t == 0) {
-    // the normalisers are read: the last workgroup of the group to get here
-    // clears the counters and the published words for the next launch
-    const unsigned prev = __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_go = prev + 1 == (unsigned)nch;
-    if (s_go) {
-      __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // the normalisers are read: count this workgroup out of the meeting now;
+  // the last of the group to get here clears the counters and the published
+  // words for the next launch, at its end (the count's return is awaited
+  // there)
+  unsigned done_prev = 0;
+  if (t == 0) done_prev = atomic_add_deferred(done, 1u);
+
+  // ---- row factors of the wave's own tiles (each wave reads and writes only
+  // its tiles' rows, so no workgroup barrier): exp2(tile max - lse) / 2^15,
+  // zero for pad rows (lse = +inf) and rows with no key so far (max = -inf).
+  // The same times 2^(15 + kWScaleLog2) in fp16 as a high and a low part
+  // (their sum within about 2^-22 of it) form pass 2's contraction operand,
+  // again on the last-query rows only; and per tile the sums over the rows
+  // of factor * p_min (into B) and over the last-query rows (into Q), in a
+  // fixed order.
+  constexpr int NE = kKrWaves * KT * NR;
+  constexpr int RL = NR / 64;       // rows per lane
+  float cB[KT], cQ[KT];
+  {
+    float l2r[RL];
+    bool lastq[RL];
+#pragma unroll
+    for (int q = 0; q < RL; ++q) {
+      const int r = lane + 64 * q;
+      l2r[q] = lse[r];
+      lastq[q] = r < a.R && (r % W) == W - 1;
+    }
+    constexpr float kWScale = (float)(1 << (15 + kWScaleLog2));
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      float sb = 0.f, sq = 0.f;
+#pragma unroll
+      for (int q = 0; q < RL; ++q) {
+        const int e = (wave * KT + kt) * NR + lane + 64 * q;
+        const float m = fac[e], pm = rmn[e];
+        const bool zero = m == -INFINITY || l2r[q] == INFINITY;
+        const float f = zero ? 0.f : __builtin_amdgcn_exp2f(fmaf(m, a.c2, -l2r[q]) - kPScaleLog2);
+        const float fs = f * kWScale;
+        const _Float16 hi = (_Float16)fs;
+        const _Float16 lo = (_Float16)(fs - (float)hi);
+        wf[e] = hi;
+        wf[NE + e] = lo;
+        wf[2 * NE + e] = lastq[q] ? hi : (_Float16)0.f;
+        wf[3 * NE + e] = lastq[q] ? lo : (_Float16)0.f;
+        const float v = f * pm;
+        sb += v;
+        sq += lastq[q] ? v : 0.f;
+      }
+      cB[kt] = wave_sum(sb);
+      cQ[kt] = wave_sum(sq);
     }
   }
-  __syncthreads();
-  if (s_go && t < a.Rpad) __hip_atomic_store(pub + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  // row factors of every (wave, tile): exp2(tile max - lse) / 2^15; zero for
-  // pad rows (lse = +inf) and rows with no key so far (max = -inf)
-  for (int e = t; e < kKrWaves * KT * NR; e += NT) {
-    const float m = fac[e], l2 = lse[e % NR];
-    fac[e] = (m == -INFINITY || l2 == INFINITY) ? 0.f
-                                                : __builtin_amdgcn_exp2f(fmaf(m, a.c2, -l2) - kPScaleLog2);
-  }
-  __syncthreads();
 
-  // ---- pass 2: B and Q of the wave's keys from the stored probabilities.
-  // Identity operands: the A operand of block (kt, j) holds, in lane l, the
-  // probabilities of row l % 32 for keys 4h + (s & 3) + 8 (s >> 2) of k-slot
-  // 8h + s (h = l / 32); operand kb maps them to keys 16 kb + ...; lane l of
-  // the identity holds a 1 where its column l % 32 is that key.
+  // ---- pass 2: B and Q of the wave's keys from the stored probabilities,
+  // on the matrix cores.  Per block (kt, j): two fp16 MFMAs against identity
+  // operands transpose the block (a lane per key; the A operand of block
+  // (kt, j) holds, in lane l, the probabilities of row l % 32 for keys
+  // 4h + (s & 3) + 8 (s >> 2) of k-slot 8h + s, h = l / 32, and lane l of
+  // the identity holds a 1 where its column l % 32 is that key), and two
+  // 16x16x32 MFMAs contract it over the rows with the row factors: four
+  // factor columns (high part, low part, and the two on the last-query rows
+  // only) in the A operand, the transposed block in the B operand, so that
+  // the four output registers of lane l < 32 are those sums for key l.
   u32x4 idop[2];
   {
     const int np = l32 & 15, aa = np >> 3, bb = (np >> 2) & 1, cc = np & 3, slot = 4 * aa + cc;
@@ -1416,84 +1496,69 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
       idop[kb2] = u32x4{w4[0], w4[1], w4[2], w4[3]};
     }
   }
-  uint32_t lastm[NRT];
-#pragma unroll
-  for (int j = 0; j < NRT; ++j) {
-    lastm[j] = 0;
-    if constexpr (!W32) {
-#pragma unroll
-      for (int reg = 0; reg < 16; ++reg) {
-        const int r = j * 32 + acc_row(reg, half);
-        if (r < a.R && (r % W) == W - 1) lastm[j] |= 1u << reg;
-      }
-    }
-  }
   typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
   // per tile: the sum over the rows of factor * p_min (into B) and over the
   // last-query rows (into Q), reduced across the wave in a fixed order
-  float cB[KT], cQ[KT];
+  // The factor operand of the 16x16x32 contractions: lane l holds column
+  // m = l % 16 for k-slots 8 g + i (g = l / 16), and lane group g of the B
+  // operand holds keys 16 (g & 1) + n (n = l % 16) of half g >> 1.  Output
+  // rows 0..3 take the four factor columns over the lane groups of keys
+  // 0..15, rows 4..7 over those of keys 16..31; the others read zeros.
+  const int g16 = lane >> 4, m16 = lane & 15;
+  const bool wact = (g16 & 1) ? (m16 >= 4 && m16 < 8) : (m16 < 4);
+  const _Float16 *wcol = wact ? wf + (m16 & 3) * NE : wf + 4 * NE;
+  const int wstep = wact ? 1 : 0;
+  auto transpose = [&](int kt, int j) {
+    f32x16 d = f32x16{};
+    d = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+        __builtin_bit_cast(f16x8, u32x4{pk[kt][j][0], pk[kt][j][1], pk[kt][j][2], pk[kt][j][3]}),
+        __builtin_bit_cast(f16x8, idop[0]), d, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+        __builtin_bit_cast(f16x8, u32x4{pk[kt][j][4], pk[kt][j][5], pk[kt][j][6], pk[kt][j][7]}),
+        __builtin_bit_cast(f16x8, idop[1]), d, 0, 0, 0);
+    return d;
+  };
+  // blocks in order kt-major; each block's transposes are issued before the
+  // previous block's contraction, which waits on their results otherwise
+  f32x4 acc2[KT];
+  constexpr int NB = KT * NRT;
+  f32x16 dn = transpose(0, 0);
 #pragma unroll
-  for (int kt = 0; kt < KT; ++kt) {
-    float sb = 0.f, sq = 0.f;
-    for (int r = lane; r < NR; r += 64) {
-      const float v = fac[(wave * KT + kt) * NR + r] * rmn[(wave * KT + kt) * NR + r];
-      sb += v;
-      sq += (r < a.R && (r % W) == W - 1) ? v : 0.f;
+  for (int blk = 0; blk < NB; ++blk) {
+    const int kt = blk / NRT, j = blk % NRT;
+    const f32x16 d = dn;
+    if (blk + 1 < NB) dn = transpose((blk + 1) / NRT, (blk + 1) % NRT);
+    // d[reg]: row j*32 + acc_row(reg, half), key kbase + l32: k-slot 8h + i
+    // of the two contractions is row acc_row(i, h) and acc_row(8 + i, h)
+    f16x8 bo[2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) bo[g][i] = (_Float16)d[8 * g + i];
+    // the factor operand: rows acc_row(0..7, h) are two runs of four,
+    // 4h + 0..3 and 8 + 4h + 0..3 (and 16, 24 further for the second)
+    const _Float16 *wr = wcol + wstep * ((wave * KT + kt) * NR + j * 32 + 4 * (g16 >> 1));
+    f16x8 ao[2];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const uint2 lo4 = *reinterpret_cast<const uint2 *>(wr + wstep * (16 * g));
+      const uint2 hi4 = *reinterpret_cast<const uint2 *>(wr + wstep * (16 * g + 8));
+      ao[g] = __builtin_bit_cast(f16x8, u32x4{lo4.x, lo4.y, hi4.x, hi4.y});
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      sb += __shfl_xor(sb, o);
-      sq += __shfl_xor(sq, o);
-    }
-    cB[kt] = sb;
-    cQ[kt] = sq;
-  }
-  float bsum[KT], qsum[KT];
-#pragma unroll
-  for (int kt = 0; kt < KT; ++kt) { bsum[kt] = 0.f; qsum[kt] = 0.f; }
-#pragma unroll
-  for (int j = 0; j < NRT; ++j) {
-#pragma unroll
-    for (int kt = 0; kt < KT; ++kt) {
-      f32x16 d = f32x16{};
-      d = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-          __builtin_bit_cast(f16x8, u32x4{pk[kt][j][0], pk[kt][j][1], pk[kt][j][2], pk[kt][j][3]}),
-          __builtin_bit_cast(f16x8, idop[0]), d, 0, 0, 0);
-      d = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-          __builtin_bit_cast(f16x8, u32x4{pk[kt][j][4], pk[kt][j][5], pk[kt][j][6], pk[kt][j][7]}),
-          __builtin_bit_cast(f16x8, idop[1]), d, 0, 0, 0);
-      // d[reg]: row j*32 + acc_row(reg, half), key kbase + l32
-      const float *fr = fac + (wave * KT + kt) * NR + j * 32 + 4 * half;
-      float f[16];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float4 v = *reinterpret_cast<const float4 *>(fr + 8 * i);
-        f[4 * i + 0] = v.x; f[4 * i + 1] = v.y; f[4 * i + 2] = v.z; f[4 * i + 3] = v.w;
-      }
-      float pr[16];
-#pragma unroll
-      for (int reg = 0; reg < 16; ++reg) pr[reg] = f[reg] * d[reg];
-      bsum[kt] += tree_sum16(pr);
-      if constexpr (W32) {
-        qsum[kt] += half ? pr[15] : 0.f;
-      } else {
-#pragma unroll
-        for (int reg = 0; reg < 16; ++reg) qsum[kt] += ((lastm[j] >> reg) & 1u) ? pr[reg] : 0.f;
-      }
-      // one block at a time: issued all at once the transposes would hold
-      // every block's 16 result registers
-      asm volatile("" : "+v"(bsum[kt]), "+v"(qsum[kt]));
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    if (j == 0) acc2[kt] = f32x4{};
+    acc2[kt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ao[0], bo[0], acc2[kt], 0, 0, 0);
+    acc2[kt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ao[1], bo[1], acc2[kt], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
   const float inv_gw = 1.f / (float)(a.G * W), inv_g = 1.f / (float)a.G;
+  constexpr float kUnscale = 1.f / (float)(1 << (15 + kWScaleLog2));
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
-    const float bs = (bsum[kt] + xor32(bsum[kt], half)) + cB[kt];
-    const float qs = (qsum[kt] + xor32(qsum[kt], half)) + cQ[kt];
     const int key = k0 + (wave * KT + kt) * 32 + l32;
     const int kl = (wave * KT + kt) * 32 + l32;
-    if ((kt & 1) == half && key < k1) {
+    if (half == 0 && key < k1) {
+      const float bs = fmaf(acc2[kt][0] + acc2[kt][1], kUnscale, cB[kt]);
+      const float qs = fmaf(acc2[kt][2] + acc2[kt][3], kUnscale, cQ[kt]);
       const float Bv = bs * inv_gw, Qv = qs * inv_g;
       const int64_t pos = vrow + key;
       // E (Eq. boundary_residual) to this layer's history slot
@@ -1527,7 +1592,16 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   for (int q = blo + t; q <= bhi; q += NT) hist[q] = 0u;
   __syncthreads();
   for (int p = t; p < ncnd; p += NT) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
+  if (t == 0) {
+    await_vm(done_prev);
+    s_go = done_prev + 1 == (unsigned)nch;
+    if (s_go) {
+      __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
   __syncthreads();
+  if (s_go && t < a.Rpad) __hip_atomic_store(pub + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int copy = (h * st.total_chunks + gchunk) % kHCopies;
   unsigned *gh = a.hist_B + (((int64_t)b * a.Hkv + h) * kHCopies + copy) * kHBins;
   for (int q = blo + t; q <= bhi; q += NT) {
