@@ -96,6 +96,33 @@ __device__ __forceinline__ float wave_sum(float v) {
   return (r0 + r1) + (r2 + r3);
 }
 
+// Sums over the wave's 64 lanes of eight values at once: lane swaps 32 and
+// 16 apart and a DPP exchange 8 apart each halve the values a lane carries
+// (keeping the ones its lane group ends with), then three DPP steps sum
+// within groups of 8 lanes, where value k ends (lanes 8k..8k+7).  Each sum
+// is formed in one fixed order.
+__device__ __forceinline__ void wave_sum8(const float (&x)[8], float (&s)[8], int lane) {
+  const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+  float y[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[i]), __float_as_uint(x[i + 4]), false, false);
+    y[i] = (b5 ? x[i + 4] : x[i]) + __uint_as_float(b5 ? r[0] : r[1]);
+  }
+  float z[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(y[i]), __float_as_uint(y[i + 2]), false, false);
+    z[i] = (b4 ? y[i + 2] : y[i]) + __uint_as_float(b4 ? r[0] : r[1]);
+  }
+  float w = (b3 ? z[1] : z[0]) + dpp_f<0x128>(b3 ? z[0] : z[1]);   // row_ror:8
+  w += dpp_f<0xB1>(w);
+  w += dpp_f<0x4E>(w);
+  w += dpp_f<0x141>(w);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) s[k] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), 8 * k));
+}
+
 // Pairwise (tree) sum and max of 16 values: depth 4 instead of a 16-long chain.
 __device__ __forceinline__ float tree_sum16(const float *x) {
   const float a0 = (x[0] + x[1]) + (x[2] + x[3]), a1 = (x[4] + x[5]) + (x[6] + x[7]);
@@ -1154,12 +1181,11 @@ __device__ __forceinline__ unsigned pack_f16(float lo, float hi) {
 }
 
 // LDS map of a single-read workgroup (bytes), NR = 32 * row tiles:
-//   qbuf  max(NR * ROWB, 4 * kHBins)      window queries; the B histogram after pass 2
+//   qbuf  max(NR * ROWB, 4 * kHBins)      window queries; the B histogram after pass 1
 //   part  max(kKrWaves * NR, NT) float2   per-wave row partials; merge scratch
 //   fac   kKrWaves * KT * NR floats       the max each tile used
 //   rmn   kKrWaves * KT * NR floats       p_min * 2^15 of each row in each tile
 //   lse   NR floats                       merged row normalisers (log2 units)
-//   cb    KPW floats                      B of the chunk's keys
 //   wf    4 * kKrWaves * KT * NR + 32 fp16 the row factors as pass 2's operand:
 //                                         high and low parts, and the same on the
 //                                         last-query rows only; then zeros
@@ -1167,7 +1193,7 @@ int single_lds_bytes(int head_dim, int rpad) {
   const int nr = 32 * kr_row_tiles(rpad), rowb = head_dim * 2, kpw = kr_keys(true, head_dim);
   const int kt = kpw / (32 * kKrWaves);
   return std::max(nr * rowb, 4 * kHBins) + 8 * std::max(kKrWaves * nr, 64 * kKrWaves) +
-         8 * kKrWaves * kt * nr + 4 * nr + 4 * kpw + 2 * (4 * kKrWaves * kt * nr + 32);
+         8 * kKrWaves * kt * nr + 4 * nr + 2 * (4 * kKrWaves * kt * nr + 32);
 }
 
 template <int D, bool W32, int NRT>
@@ -1193,8 +1219,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   float *fac = reinterpret_cast<float *>(part + max(kKrWaves * NR, NT));
   float *rmn = fac + kKrWaves * KT * NR;
   float *lse = rmn + kKrWaves * KT * NR;
-  float *cb = lse + NR;
-  _Float16 *wf = reinterpret_cast<_Float16 *>(cb + KPW);   // [4][kKrWaves * KT * NR] then 32 zeros
+  _Float16 *wf = reinterpret_cast<_Float16 *>(lse + NR);   // [4][kKrWaves * KT * NR] then 32 zeros
 
   // ---- loads: the window queries, the first key tile, and once the queries
   // are in LDS the other key tiles (as in the key-register passes)
@@ -1336,6 +1361,11 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
       part[wave * NR + j * 32 + l32] = make_float2(m_run[j] == -INFINITY ? -INFINITY : m_run[j] * a.c2, l);
   }
   __syncthreads();
+  // every wave is past pass 1: the window queries' space holds the B
+  // histogram of the chunk from here (cleared now, counted in pass 2's tail;
+  // the barriers of the meeting order the two)
+  unsigned *hist = reinterpret_cast<unsigned *>(qbuf);
+  for (int q = 4 * t; q < kHBins; q += 4 * NT) *reinterpret_cast<uint4 *>(hist + q) = make_uint4(0u, 0u, 0u, 0u);
   // the workgroup's partial of each row (waves in order), written through
   const int64_t pbase = ((int64_t)h * st.total_chunks + st.chunk_base[b]) * a.Rpad;
   if (t < a.Rpad) {
@@ -1451,6 +1481,8 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
       lastq[q] = r < a.R && (r % W) == W - 1;
     }
     constexpr float kWScale = (float)(1 << (15 + kWScaleLog2));
+    static_assert(KT == 4, "the p_min sums of a wave are eight values");
+    float sx[8];
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) {
       float sb = 0.f, sq = 0.f;
@@ -1471,8 +1503,15 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
         sb += v;
         sq += lastq[q] ? v : 0.f;
       }
-      cB[kt] = wave_sum(sb);
-      cQ[kt] = wave_sum(sq);
+      sx[kt] = sb;
+      sx[4 + kt] = sq;
+    }
+    float ss[8];
+    wave_sum8(sx, ss, lane);
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      cB[kt] = ss[kt];
+      cQ[kt] = ss[4 + kt];
     }
   }
 
@@ -1552,10 +1591,12 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   }
   const float inv_gw = 1.f / (float)(a.G * W), inv_g = 1.f / (float)a.G;
   constexpr float kUnscale = 1.f / (float)(1 << (15 + kWScaleLog2));
+  // B, E, and the B histogram of the chunk's candidates (keys before the
+  // window) with the range of bins it touched
+  int blo = kHBins, bhi = -1;
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
     const int key = k0 + (wave * KT + kt) * 32 + l32;
-    const int kl = (wave * KT + kt) * 32 + l32;
     if (half == 0 && key < k1) {
       const float bs = fmaf(acc2[kt][0] + acc2[kt][1], kUnscale, cB[kt]);
       const float qs = fmaf(acc2[kt][2] + acc2[kt][3], kUnscale, cQ[kt]);
@@ -1564,34 +1605,18 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
       // E (Eq. boundary_residual) to this layer's history slot
       a.ring[a.ring_write * a.ring_stride + pos] = (Qv > Bv) ? (Qv - Bv) : 0.f;
       a.vec_B[pos] = Bv;
-      cb[kl] = Bv;
+      if (key < wfirst) {
+        const int q = hbin(float_key(Bv));
+        atomicAdd(&hist[q], 1u);
+        blo = min(blo, q);
+        bhi = max(bhi, q);
+      }
     }
-  }
-  __syncthreads();
-
-  // B histogram of the chunk's candidates (as in the key-register pass 2)
-  unsigned *hist = reinterpret_cast<unsigned *>(qbuf);
-  const int ncnd = max(0, min(k1, wfirst) - k0);
-  int blo = kHBins, bhi = -1;
-  for (int p = t; p < ncnd; p += NT) {
-    const int q = hbin(float_key(cb[p]));
-    blo = min(blo, q);
-    bhi = max(bhi, q);
   }
   blo = __reduce_min_sync(~0ull, blo);
   bhi = __reduce_max_sync(~0ull, bhi);
   int *mm2 = reinterpret_cast<int *>(part);
   if (lane == 0) { mm2[wave] = blo; mm2[kKrWaves + wave] = bhi; }
-  __syncthreads();
-  blo = kHBins;
-  bhi = -1;
-  for (int w = 0; w < kKrWaves; ++w) {
-    blo = min(blo, mm2[w]);
-    bhi = max(bhi, mm2[kKrWaves + w]);
-  }
-  for (int q = blo + t; q <= bhi; q += NT) hist[q] = 0u;
-  __syncthreads();
-  for (int p = t; p < ncnd; p += NT) atomicAdd(&hist[hbin(float_key(cb[p]))], 1u);
   if (t == 0) {
     await_vm(done_prev);
     s_go = done_prev + 1 == (unsigned)nch;
@@ -1602,6 +1627,12 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   }
   __syncthreads();
   if (s_go && t < a.Rpad) __hip_atomic_store(pub + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  blo = kHBins;
+  bhi = -1;
+  for (int w = 0; w < kKrWaves; ++w) {
+    blo = min(blo, mm2[w]);
+    bhi = max(bhi, mm2[kKrWaves + w]);
+  }
   const int copy = (h * st.total_chunks + gchunk) % kHCopies;
   unsigned *gh = a.hist_B + (((int64_t)b * a.Hkv + h) * kHCopies + copy) * kHBins;
   for (int q = blo + t; q <= bhi; q += NT) {
