@@ -1136,6 +1136,10 @@ hipError_t launch_krpass(int mode, bool bf16, int head_dim, bool w32, const Pass
 //    histogram) is that of the key-register pass 2.
 constexpr float kPScaleLog2 = 15.f;          // stored probabilities are p * 2^15 (<= 2^15)
 constexpr int kWScaleLog2 = 12;              // pass 2's fp16 row factors are scaled by 2^(15 + this)
+// The factor operand's columns lie a multiple of 4 KiB plus 32 bytes apart,
+// so that the four lanes that read the same rows of different columns use
+// different LDS banks.
+constexpr int kWPad = 16;
 constexpr unsigned kMeetSpin = 1u << 20;     // polls of a published word before giving up
 
 __device__ __forceinline__ void store_agent(float2 *p, float2 v) {
@@ -1186,14 +1190,15 @@ __device__ __forceinline__ unsigned pack_f16(float lo, float hi) {
 //   fac   kKrWaves * KT * NR floats       the max each tile used
 //   rmn   kKrWaves * KT * NR floats       p_min * 2^15 of each row in each tile
 //   lse   NR floats                       merged row normalisers (log2 units)
-//   wf    4 * kKrWaves * KT * NR + 32 fp16 the row factors as pass 2's operand:
-//                                         high and low parts, and the same on the
-//                                         last-query rows only; then zeros
+//   wf    4 * (kKrWaves * KT * NR + kWPad)  the row factors as pass 2's operand
+//         + 32 fp16                       (four columns: high and low parts, and
+//                                         the same on the last-query rows only;
+//                                         then zeros)
 int single_lds_bytes(int head_dim, int rpad) {
   const int nr = 32 * kr_row_tiles(rpad), rowb = head_dim * 2, kpw = kr_keys(true, head_dim);
   const int kt = kpw / (32 * kKrWaves);
   return std::max(nr * rowb, 4 * kHBins) + 8 * std::max(kKrWaves * nr, 64 * kKrWaves) +
-         8 * kKrWaves * kt * nr + 4 * nr + 2 * (4 * kKrWaves * kt * nr + 32);
+         8 * kKrWaves * kt * nr + 4 * nr + 2 * (4 * (kKrWaves * kt * nr + kWPad) + 32);
 }
 
 template <int D, bool W32, int NRT>
@@ -1253,7 +1258,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
     *reinterpret_cast<u32x4 *>(qbuf + row * C::ROWB + 16 * (pc ^ (row & C::SWM))) = qv[j];
   }
   // the zeros that pass 2's idle factor lanes read
-  if (t < 32) wf[4 * kKrWaves * KT * NR + t] = (_Float16)0.f;
+  if (t < 32) wf[4 * (kKrWaves * KT * NR + kWPad) + t] = (_Float16)0.f;
   __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -1469,6 +1474,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   // of factor * p_min (into B) and over the last-query rows (into Q), in a
   // fixed order.
   constexpr int NE = kKrWaves * KT * NR;
+  constexpr int WS = NE + kWPad;    // column stride of the factor operand
   constexpr int RL = NR / 64;       // rows per lane
   float cB[KT], cQ[KT];
   {
@@ -1496,9 +1502,9 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
         const _Float16 hi = (_Float16)fs;
         const _Float16 lo = (_Float16)(fs - (float)hi);
         wf[e] = hi;
-        wf[NE + e] = lo;
-        wf[2 * NE + e] = lastq[q] ? hi : (_Float16)0.f;
-        wf[3 * NE + e] = lastq[q] ? lo : (_Float16)0.f;
+        wf[WS + e] = lo;
+        wf[2 * WS + e] = lastq[q] ? hi : (_Float16)0.f;
+        wf[3 * WS + e] = lastq[q] ? lo : (_Float16)0.f;
         const float v = f * pm;
         sb += v;
         sq += lastq[q] ? v : 0.f;
@@ -1545,7 +1551,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   // 0..15, rows 4..7 over those of keys 16..31; the others read zeros.
   const int g16 = lane >> 4, m16 = lane & 15;
   const bool wact = (g16 & 1) ? (m16 >= 4 && m16 < 8) : (m16 < 4);
-  const _Float16 *wcol = wact ? wf + (m16 & 3) * NE : wf + 4 * NE;
+  const _Float16 *wcol = wact ? wf + (m16 & 3) * WS : wf + 4 * WS;
   const int wstep = wact ? 1 : 0;
   auto transpose = [&](int kt, int j) {
     f32x16 d = f32x16{};
