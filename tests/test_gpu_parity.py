@@ -606,6 +606,11 @@ EDGE = {
     # a 256-query window with one head per group
     "w256-mha": dict(wl=inputs.Workload("edge", 2, 2, 2, 64, 256, 5, "bf16", (1200,), (50,),
                                         ((10, 800),), 3, 21)),
+    # d = 64 with a 32-query window: two and four row tiles (G = 2 and 4)
+    "d64-w32-g2": dict(wl=inputs.Workload("edge", 3, 4, 2, 64, 32, 7, "bf16", (1500, 700), (64, 32),
+                                          ((20, 1200), (5, 500)), 2, 31)),
+    "d64-w32-g4": dict(wl=inputs.Workload("edge", 3, 8, 2, 64, 32, 7, "bf16", (2100, 333), (90, 17),
+                                          ((40, 1800), (0, 200)), 2, 32)),
     # the largest batch: 64 sequences of ragged lengths and budgets
     "batch64": dict(wl=_batch64()),
     # large budgets: scale-matching set and kept set of thousands of positions
@@ -921,7 +926,7 @@ def test_long_exact_ties_take_the_streamed_select(n, K, params, monkeypatch):
 SINGLE_FORCED = ["llava-n2048", "ragged-b8", "llava-small", "ragged-small", "video-small",
                  "batch64", "gqa3-w8-d64", "w1-budget1", "pool33-r16-segments", "M-over-segment",
                  "pool-max-s", "pool-mean-b", "large-budget-whole-sequence", "window-score-only",
-                 "gamma0", "radius0-m0"]
+                 "gamma0", "radius0-m0", "d64-w32-g2", "d64-w32-g4"]
 
 
 @pytest.mark.parametrize("name", SINGLE_FORCED)
