@@ -3298,6 +3298,10 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
       tbl[j] = j;
     }
   } else if (kept > 0) {
+    // rows no member fills stay empty: the selection below sets exactly
+    // `kept` of them, and this keeps a table row from ever holding a stale
+    // position (the barriers of the list loads order it before those writes)
+    for (int j = t; j < kept; j += NT) tbl[j] = -1;
     int4 rec;
     unsigned lk[kListPer];
     int lp[kListPer];
@@ -3372,7 +3376,8 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
     for (int u = 0; u < BATCH; ++u) {
       const int q = min(q0 + u * NT, total - 1);
       const int rr = r0 + q / pieces, p = q % pieces;
-      srcs[u] = tbl[rr];
+      const int src = tbl[rr];
+      srcs[u] = (src >= 0 && src < n) ? src : -1;   // anything else is an empty row
       const int64_t so = ((int64_t)(st.cu[b] + max(srcs[u], 0)) * a.Hkv + h) * a.row_bytes + 16 * p;
       kv[u] = *reinterpret_cast<const u32x4 *>(ks + so);
       vv[u] = *reinterpret_cast<const u32x4 *>(vs + so);
