@@ -1467,16 +1467,19 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
 
   // ---- row factors of the wave's own tiles (each wave reads and writes only
   // its tiles' rows, so no workgroup barrier): exp2(tile max - lse) / 2^15,
-  // zero for pad rows (lse = +inf) and rows with no key so far (max = -inf).
-  // The same times 2^(15 + kWScaleLog2) in fp16 as a high and a low part
-  // (their sum within about 2^-22 of it) form pass 2's contraction operand,
-  // again on the last-query rows only; and per tile the sums over the rows
-  // of factor * p_min (into B) and over the last-query rows (into Q), in a
-  // fixed order.
+  // zero for pad rows (lse = +inf) and rows with no key so far (max = -inf;
+  // exp2 of -inf is 0).  The same times 2^(15 + kWScaleLog2) in fp16 as a
+  // high and a low part (their sum within about 2^-22 of it) form pass 2's
+  // contraction operand for B; Q takes the last-query rows: with a 32-query
+  // window, row 31 of every row tile, whose factors pass 2 applies in fp32
+  // (fq), else two more operand columns on those rows only.  Per tile also
+  // the sums over the rows of factor * p_min (into B) and over the
+  // last-query rows (into Q), in a fixed order.
   constexpr int NE = kKrWaves * KT * NR;
   constexpr int WS = NE + kWPad;    // column stride of the factor operand
   constexpr int RL = NR / 64;       // rows per lane
   float cB[KT], cQ[KT];
+  float fq[KT][NRT];                // W32: the factors of rows 32 j + 31
   {
     float l2r[RL];
     bool lastq[RL];
@@ -1496,18 +1499,26 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
       for (int q = 0; q < RL; ++q) {
         const int e = (wave * KT + kt) * NR + lane + 64 * q;
         const float m = fac[e], pm = rmn[e];
-        const bool zero = m == -INFINITY || l2r[q] == INFINITY;
-        const float f = zero ? 0.f : __builtin_amdgcn_exp2f(fmaf(m, a.c2, -l2r[q]) - kPScaleLog2);
+        const float f = __builtin_amdgcn_exp2f(fmaf(m, a.c2, -l2r[q]) - kPScaleLog2);
         const float fs = f * kWScale;
         const _Float16 hi = (_Float16)fs;
         const _Float16 lo = (_Float16)(fs - (float)hi);
         wf[e] = hi;
         wf[WS + e] = lo;
-        wf[2 * WS + e] = lastq[q] ? hi : (_Float16)0.f;
-        wf[3 * WS + e] = lastq[q] ? lo : (_Float16)0.f;
+        if constexpr (!W32) {
+          wf[2 * WS + e] = lastq[q] ? hi : (_Float16)0.f;
+          wf[3 * WS + e] = lastq[q] ? lo : (_Float16)0.f;
+        }
         const float v = f * pm;
         sb += v;
         sq += lastq[q] ? v : 0.f;
+        if constexpr (W32) {
+          // rows 64 q + 31 and 64 q + 63 are row tiles 2q and 2q + 1's row 31
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj)
+            if (2 * q + jj < NRT)
+              fq[kt][2 * q + jj] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 31 + 32 * jj));
+        }
       }
       sx[kt] = sb;
       sx[4 + kt] = sq;
@@ -1550,7 +1561,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   // rows 0..3 take the four factor columns over the lane groups of keys
   // 0..15, rows 4..7 over those of keys 16..31; the others read zeros.
   const int g16 = lane >> 4, m16 = lane & 15;
-  const bool wact = (g16 & 1) ? (m16 >= 4 && m16 < 8) : (m16 < 4);
+  const bool wact = ((g16 & 1) ? (m16 >= 4 && m16 < 8) : (m16 < 4)) && (!W32 || (m16 & 3) < 2);
   const _Float16 *wcol = wact ? wf + (m16 & 3) * WS : wf + 4 * WS;
   const int wstep = wact ? 1 : 0;
   auto transpose = [&](int kt, int j) {
@@ -1566,6 +1577,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   // blocks in order kt-major; each block's transposes are issued before the
   // previous block's contraction, which waits on their results otherwise
   f32x4 acc2[KT];
+  float qacc[KT];                   // W32: Q of key l % 32 in the lanes of the second half
   constexpr int NB = KT * NRT;
   f32x16 dn = transpose(0, 0);
 #pragma unroll
@@ -1573,6 +1585,8 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
     const int kt = blk / NRT, j = blk % NRT;
     const f32x16 d = dn;
     if (blk + 1 < NB) dn = transpose((blk + 1) / NRT, (blk + 1) % NRT);
+    // register 15 of the second half's lanes is row acc_row(15, 1) = 31
+    if constexpr (W32) qacc[kt] = fmaf(fq[kt][j], d[15], j == 0 ? 0.f : qacc[kt]);
     // d[reg]: row j*32 + acc_row(reg, half), key kbase + l32: k-slot 8h + i
     // of the two contractions is row acc_row(i, h) and acc_row(8 + i, h)
     f16x8 bo[2];
@@ -1603,9 +1617,11 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
     const int key = k0 + (wave * KT + kt) * 32 + l32;
+    float qw = 0.f;
+    if constexpr (W32) qw = xor32(qacc[kt], half);
     if (half == 0 && key < k1) {
       const float bs = fmaf(acc2[kt][0] + acc2[kt][1], kUnscale, cB[kt]);
-      const float qs = fmaf(acc2[kt][2] + acc2[kt][3], kUnscale, cQ[kt]);
+      const float qs = W32 ? qw + cQ[kt] : fmaf(acc2[kt][2] + acc2[kt][3], kUnscale, cQ[kt]);
       const float Bv = bs * inv_gw, Qv = qs * inv_g;
       const int64_t pos = vrow + key;
       // E (Eq. boundary_residual) to this layer's history slot
