@@ -52,12 +52,21 @@ _NAMES = [
 ]
 
 
+def _code_only(text: str) -> str:
+    """The source with comments and blank lines removed (no string literal in
+    the kernel sources holds a comment marker)."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = (re.sub(r"//.*", "", ln).rstrip() for ln in text.splitlines())
+    return "\n".join(ln for ln in lines if ln)
+
+
 def source_sha() -> str:
-    """Hash of the kernel sources; counters taken on other sources are stale."""
+    """Hash of the kernel sources' code (comments aside); counters taken on
+    other code are stale."""
     h = hashlib.sha256()
     for f in ("kernels.hip", "internal.h"):
-        with open(os.path.join(HERE, "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(HERE, "csrc", f), encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -1538,10 +1538,11 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   // (kt, j) holds, in lane l, the probabilities of row l % 32 for keys
   // 4h + (s & 3) + 8 (s >> 2) of k-slot 8h + s, h = l / 32, and lane l of
   // the identity holds a 1 where its column l % 32 is that key), and two
-  // 16x16x32 MFMAs contract it over the rows with the row factors: four
-  // factor columns (high part, low part, and the two on the last-query rows
-  // only) in the A operand, the transposed block in the B operand, so that
-  // the four output registers of lane l < 32 are those sums for key l.
+  // 16x16x32 MFMAs contract it over the rows with the row factors: the
+  // factor columns (high part, low part, and without a 32-query window the
+  // two on the last-query rows only) in the A operand, the transposed block
+  // in the B operand, so that the output registers of lane l < 32 are those
+  // sums for key l.
   u32x4 idop[2];
   {
     const int np = l32 & 15, aa = np >> 3, bb = (np >> 2) & 1, cc = np & 3, slot = 4 * aa + cc;
@@ -1553,13 +1554,12 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
     }
   }
   typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-  // per tile: the sum over the rows of factor * p_min (into B) and over the
-  // last-query rows (into Q), reduced across the wave in a fixed order
   // The factor operand of the 16x16x32 contractions: lane l holds column
   // m = l % 16 for k-slots 8 g + i (g = l / 16), and lane group g of the B
   // operand holds keys 16 (g & 1) + n (n = l % 16) of half g >> 1.  Output
-  // rows 0..3 take the four factor columns over the lane groups of keys
-  // 0..15, rows 4..7 over those of keys 16..31; the others read zeros.
+  // rows 0..3 take the factor columns over the lane groups of keys 0..15,
+  // rows 4..7 over those of keys 16..31; the other lanes (and, with a
+  // 32-query window, columns 2 and 3) read zeros.
   const int g16 = lane >> 4, m16 = lane & 15;
   const bool wact = ((g16 & 1) ? (m16 >= 4 && m16 < 8) : (m16 < 4)) && (!W32 || (m16 & 3) < 2);
   const _Float16 *wcol = wact ? wf + (m16 & 3) * WS : wf + 4 * WS;
