@@ -1263,12 +1263,11 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-  // the next tile now; each later tile when the tile two before it starts,
-  // so that the chunks sharing a CU receive their keys interleaved
-  constexpr int EARLY = KT < 2 ? KT : 2;
-#pragma unroll
-  for (int kt = 1; kt < EARLY; ++kt) load_tile(kt);
-  asm volatile("" ::: "memory");
+  // each later tile's keys are requested when the tile before it starts: one
+  // tile in flight per wave.  With two, every workgroup's requests go out at
+  // once and the second workgroup of each CU receives its keys last (about
+  // 1 us later in the launch)
+  constexpr int EARLY = 1;
 
   int koff[NU];
 #pragma unroll
