@@ -788,8 +788,6 @@ __device__ __forceinline__ void krpass_body(const PassArgs &a, const SeqTable &s
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-#pragma unroll
-  for (int kt = 1; kt < KT; ++kt) load_tile(kt);
   asm volatile("" ::: "memory");
 
   // byte offsets of this lane's operand pieces 2u + half of query row l32 of a
@@ -831,6 +829,7 @@ __device__ __forceinline__ void krpass_body(const PassArgs &a, const SeqTable &s
     for (int j = 0; j < NRT; ++j) { m_run[j] = -INFINITY; l_run[j] = 0.f; }
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) {
+      if (kt + 1 < KT) load_tile(kt + 1);
       f32x16 acc[NRT];
 #pragma unroll
       for (int j = 0; j < NRT; ++j) acc[j] = f32x16{};
@@ -914,6 +913,7 @@ __device__ __forceinline__ void krpass_body(const PassArgs &a, const SeqTable &s
     const float inv_gw = 1.f / (float)(a.G * W), inv_g = 1.f / (float)a.G;
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) {
+      if (kt + 1 < KT) load_tile(kt + 1);
       const int kbase = k0 + (wave * KT + kt) * 32, key = kbase + l32;
       const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
       float bsum = 0.f, qsum = 0.f;
@@ -1263,11 +1263,11 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-  // each later tile's keys are requested when the tile before it starts: one
-  // tile in flight per wave.  With two, every workgroup's requests go out at
-  // once and the second workgroup of each CU receives its keys last (about
-  // 1 us later in the launch)
-  constexpr int EARLY = 1;
+  // each later tile's keys are requested when the wave starts that tile
+  // (the other waves of the SIMD cover the wait).  Requested further ahead,
+  // every workgroup's requests go out at once and the second workgroup of
+  // each CU receives its keys last: about 1.5 us later in the launch with
+  // two tiles ahead, 0.5 us with one
 
   int koff[NU];
 #pragma unroll
@@ -1284,7 +1284,7 @@ __global__ __launch_bounds__(64 * kKrWaves, 2) void k_single(PassArgs a, SeqTabl
   for (int j = 0; j < NRT; ++j) { m_run[j] = -INFINITY; l_run[j] = 0.f; }
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
-    if (kt + EARLY < KT) load_tile(kt + EARLY);
+    if (kt > 0) load_tile(kt);
     const int kbase = k0 + (wave * KT + kt) * 32;
     const bool edge = (kbase + 31 >= k1) || (kbase + 31 > wfirst);
 #pragma unroll
