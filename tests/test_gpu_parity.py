@@ -611,6 +611,10 @@ EDGE = {
                                           ((20, 1200), (5, 500)), 2, 31)),
     "d64-w32-g4": dict(wl=inputs.Workload("edge", 3, 8, 2, 64, 32, 7, "bf16", (2100, 333), (90, 17),
                                           ((40, 1800), (0, 200)), 2, 32)),
+    # G = 3 with a 32-query window: 96 window rows in four row tiles, the last
+    # tile all pad rows (their weights are 0, also on the last-query row)
+    "g3-w32-pad-rows": dict(wl=inputs.Workload("edge", 3, 6, 2, 128, 32, 7, "bf16", (1800, 650),
+                                               (70, 24), ((30, 1500), (8, 400)), 2, 33)),
     # the largest batch: 64 sequences of ragged lengths and budgets
     "batch64": dict(wl=_batch64()),
     # large budgets: scale-matching set and kept set of thousands of positions
@@ -926,7 +930,7 @@ def test_long_exact_ties_take_the_streamed_select(n, K, params, monkeypatch):
 SINGLE_FORCED = ["llava-n2048", "ragged-b8", "llava-small", "ragged-small", "video-small",
                  "batch64", "gqa3-w8-d64", "w1-budget1", "pool33-r16-segments", "M-over-segment",
                  "pool-max-s", "pool-mean-b", "large-budget-whole-sequence", "window-score-only",
-                 "gamma0", "radius0-m0", "d64-w32-g2", "d64-w32-g4"]
+                 "gamma0", "radius0-m0", "d64-w32-g2", "d64-w32-g4", "g3-w32-pad-rows"]
 
 
 @pytest.mark.parametrize("name", SINGLE_FORCED)
