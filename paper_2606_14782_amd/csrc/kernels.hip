@@ -2695,15 +2695,15 @@ struct ListView {
 };
 
 // Calibration kernel (segment_calib).
-__device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st, int gs, int h) {
+__device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st, int gs, int h, int b) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
-  __shared__ float Bs[kSegWin], Vs[kSegWin];
-  __shared__ float Es[kSegE];
+  constexpr int TAPS = 8;                           // window taps read per round
+  __shared__ float Bs[kSegWin + TAPS], Vs[kSegWin + TAPS];
+  __shared__ float Es[kSegE + TAPS];
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[PER * NW + 1];
   const int t = threadIdx.x;
   const int wave = t >> 6;
-  const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
@@ -2772,15 +2772,42 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
           for (int j = 0; j < kSegWinJ; ++j) tv[j] += (l0 + i < a.ring_cnt) ? x[i][j] : 0.f;
       }
     }
+    // E is 0 outside the sequence in LDS, so that a neighbourhood sum needs
+    // no per-position bounds
 #pragma unroll
-    for (int j = 0; j < kSegEJ; ++j)
-      if (tt + j * NT < kSegE) Es[tt + j * NT] = ev[j];
+    for (int j = 0; j < kSegEJ; ++j) {
+      const int u = w0 - kMaxRadius + tt + j * NT;
+      if (tt + j * NT < kSegE) Es[tt + j * NT] = (u >= 0 && u < n) ? ev[j] : 0.f;
+    }
+    if (t < TAPS) Es[kSegE + t] = 0.f;
     lds_barrier();
     // V = E + L + T (Eq. structurally_calibrated_evidence, per the terms
     // mask), L = P_r E over the sequence-truncated neighbourhood
     // (Eq. intra_layer_coherence), T the mean of the earlier layers' E
-    // (Eq. inter_layer_persistence)
+    // (Eq. inter_layer_persistence).  The neighbourhood's taps are read
+    // TAPS at a time for all of the thread's positions and summed in
+    // position order; a tap outside the sequence adds 0.
     const float inv_cnt = a.ring_cnt ? 1.f / (float)a.ring_cnt : 0.f;
+    float ls[kSegWinJ];
+#pragma unroll
+    for (int j = 0; j < kSegWinJ; ++j) ls[j] = 0.f;
+    if (use_l) {
+      for (int d0 = -r; d0 <= r; d0 += TAPS) {
+        float e[kSegWinJ][TAPS];
+#pragma unroll
+        for (int j = 0; j < kSegWinJ; ++j) {
+          const int q = min(tt + j * NT, kSegWin - 1);
+#pragma unroll
+          for (int k = 0; k < TAPS; ++k) e[j][k] = Es[q + kMaxRadius + d0 + k];
+        }
+#pragma unroll
+        for (int k = 0; k < TAPS; ++k) {
+          const bool in = d0 + k <= r;                 // uniform
+#pragma unroll
+          for (int j = 0; j < kSegWinJ; ++j) ls[j] += in ? e[j][k] : 0.f;
+        }
+      }
+    }
 #pragma unroll
     for (int j = 0; j < kSegWinJ; ++j) {
       const int q = tt + j * NT;
@@ -2789,33 +2816,62 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
         float v = ((a.terms & 1u) ? Es[q + kMaxRadius] : 0.f) + (use_t ? tv[j] * inv_cnt : 0.f);
         if (use_l && u >= 0 && u < n) {
           const int lo = max(0, u - r), hi = min(n - 1, u + r);
-          float sum = 0.f;
-          for (int x = lo; x <= hi; ++x) sum += Es[x - w0 + kMaxRadius];
-          v += sum / (float)(hi - lo + 1);
+          v += ls[j] / (float)(hi - lo + 1);
         }
-        Bs[q] = bv[j];
-        Vs[q] = v;
+        // B and V are 0 outside the candidates: the pool windows need no
+        // per-position bounds either
+        const bool cand = u >= 0 && u < nc;
+        Bs[q] = cand ? bv[j] : 0.f;
+        Vs[q] = cand ? v : 0.f;
       }
+    }
+    if (t < TAPS) {
+      Bs[kSegWin + t] = 0.f;
+      Vs[kSegWin + t] = 0.f;
     }
   }
   lds_barrier();
 
-  // V, and the pooled B and V over I (truncated windows), of the segment's candidates
+  // V, and the pooled B and V over I (truncated windows), of the segment's
+  // candidates; the window's taps TAPS at a time, summed in position order
+  // (a tap outside the candidates adds 0)
   const int hp = a.pool_half;
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
-  float xb[PER], xv[PER];
+  float xb[PER], xv[PER], sb[PER], sv[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int q = t + j * NT;
+    xb[j] = Bs[kPoolHalo + q];
+    xv[j] = Vs[kPoolHalo + q];
+    sb[j] = 0.f;
+    sv[j] = 0.f;
+  }
+  for (int d0 = -hp; d0 <= hp; d0 += TAPS) {
+    float pb[PER][TAPS], pv[PER][TAPS];
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+#pragma unroll
+      for (int k = 0; k < TAPS; ++k) {
+        pb[j][k] = Bs[kPoolHalo + t + j * NT + d0 + k];
+        pv[j][k] = Vs[kPoolHalo + t + j * NT + d0 + k];
+      }
+#pragma unroll
+    for (int k = 0; k < TAPS; ++k) {
+      const bool in = d0 + k <= hp;                    // uniform
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        sb[j] += in ? pb[j][k] : 0.f;
+        sv[j] += in ? pv[j][k] : 0.f;
+      }
+    }
+  }
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int q = t + j * NT, i = i0 + q;
-    xb[j] = Bs[kPoolHalo + q];
-    xv[j] = Vs[kPoolHalo + q];
     if (q < ncand) {
-      const int lo = max(0, i - hp), hi = min(nc - 1, i + hp);
-      float sb = 0.f, sv = 0.f;
-      for (int u = lo - w0; u <= hi - w0; ++u) { sb += Bs[u]; sv += Vs[u]; }
-      const float cnt = (float)(hi - lo + 1);
-      a.vec_pB[base + i] = sb / cnt;
-      a.vec_pV[base + i] = sv / cnt;
+      const float cnt = (float)(min(nc - 1, i + hp) - max(0, i - hp) + 1);
+      a.vec_pB[base + i] = sb[j] / cnt;
+      a.vec_pV[base + i] = sv[j] / cnt;
       a.vec_V[base + i] = xv[j];
     }
   }
@@ -2855,7 +2911,7 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
 }
 
 __global__ __launch_bounds__(kSegThreads) void k_segcal(SegArgs a, SeqTable st) {
-  segcal_body(a, st, blockIdx.x, blockIdx.y);
+  segcal_body(a, st, blockIdx.x, blockIdx.y, find_seg(st, blockIdx.x));
 }
 
 // Loads the selection record and the segments' lists of a (sequence, KV
@@ -3046,7 +3102,7 @@ __device__ __attribute__((noinline)) void whole_moments(const SegArgs &a, int64_
 // Score kernel (segment_score).
 // (The select bodies take their arguments by value: a reference to a kernel
 // argument that reaches an out-of-line call costs a stack copy and spills.)
-__device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int gs, int h) {
+__device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int gs, int h, int b) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ unsigned hist[kHBins];
   __shared__ unsigned ckey[kSegCandCap];
@@ -3058,7 +3114,6 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
   __shared__ float vref_s;
   const int t = threadIdx.x;
   const int wave = t >> 6;
-  const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
@@ -3199,13 +3254,12 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
 
 // Candidate kernel (segment_cand): the boundary bin of the top-K of the
 // pooled score and the segment's list of entries at or above it.
-__device__ __forceinline__ void segcand_body(SegArgs a, const SeqTable &st, int gs, int h) {
+__device__ __forceinline__ void segcand_body(SegArgs a, const SeqTable &st, int gs, int h, int b) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[PER * NW + 1];
   const int t = threadIdx.x;
   const int wave = t >> 6;
-  const int b = find_seg(st, gs);
   const int sg = gs - st.seg_base[b];
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
@@ -3415,11 +3469,11 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
 }
 
 __global__ __launch_bounds__(kSegThreads) void k_segscore(SegArgs a, SeqTable st) {
-  segscore_body(a, st, blockIdx.x, blockIdx.y);
+  segscore_body(a, st, blockIdx.x, blockIdx.y, find_seg(st, blockIdx.x));
 }
 
 __global__ __launch_bounds__(kSegThreads) void k_segcand(SegArgs a, SeqTable st) {
-  segcand_body(a, st, blockIdx.x, blockIdx.y);
+  segcand_body(a, st, blockIdx.x, blockIdx.y, find_seg(st, blockIdx.x));
 }
 
 __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st) {
@@ -3442,12 +3496,12 @@ __global__ __launch_bounds__(kSegThreads) void k_sel_a(SegArgs g, SegArgs gp, Pa
                                                       int ncand, int nmerge) {
   const int h = blockIdx.y, nseg = st.total_segs;
   if ((int)blockIdx.x < nseg) {
-    segcal_body(g, st, blockIdx.x, h);
+    segcal_body(g, st, blockIdx.x, h, find_seg(st, blockIdx.x));
     return;
   }
   const int x = blockIdx.x - nseg;
   if (x < ncand) {
-    segcand_body(gp, st, x, h);
+    segcand_body(gp, st, x, h, find_seg(st, x));
   } else if (x < ncand + nmerge) {
     constexpr int groups = kSegThreads / kMergeThreads;
     __shared__ float2 mrg[groups][kMergeParts][kMergeRows];
@@ -3460,9 +3514,19 @@ __global__ __launch_bounds__(kSegThreads) void k_sel_a(SegArgs g, SegArgs gp, Pa
 }
 
 __global__ __launch_bounds__(kSegThreads) void k_sel_b(SegArgs g, SegArgs gp, SeqTable st, int nfinal) {
-  const int h = blockIdx.y, nseg = st.total_segs;
+  const int h = blockIdx.y, nseg = st.total_segs, batch = st.batch;
+  // both table words in one round of scalar loads (the job split below
+  // would otherwise wait for each in turn); a batch of one sequence takes a
+  // copy of the score body with b = 0, whose per-sequence table reads sit at
+  // fixed kernel-argument offsets and need no sequence search first.  (Not
+  // in k_sel_a: there the copies' scalar registers would cost the second
+  // workgroup per CU, and they did not pay.)
+  asm volatile("" ::"s"(nseg), "s"(batch));
   if ((int)blockIdx.x < nseg) {
-    segscore_body(g, st, blockIdx.x, h);
+    if (batch == 1)
+      segscore_body(g, st, blockIdx.x, h, 0);
+    else
+      segscore_body(g, st, blockIdx.x, h, find_seg(st, blockIdx.x));
   } else {
     const int x = blockIdx.x - nseg;
     final_body(gp, st, x % gp.parts, x / gp.parts, h);
