@@ -1827,6 +1827,42 @@ __device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, do
   lds_barrier();
 }
 
+// Scale-matching factor lambda (Eq. lambda_solution) from each thread's
+// partial moment sums over the scale-matching set of size M: sum of B - bref,
+// of its square, of V - vref and of its square.  The partials go through
+// LDS (sc: 2 * NT double2) to wave 0, which sums them in a fixed order
+// (thread w*64 + lane into lane `lane` for w ascending, then across the
+// lanes) and forms lambda; the other waves wait at the barrier rather than
+// each repeat the double-precision reduction and arithmetic.  Ends with a
+// barrier; returns lambda in every thread.
+template <int NT>
+__device__ __forceinline__ float block_lambda(double s0, double s1, double s2, double s3, int M,
+                                              double bref, float gamma, float eps, float b_floor,
+                                              double2 *sc, float *lam_s) {
+  const int t = threadIdx.x;
+  sc[t] = make_double2(s0, s1);
+  sc[NT + t] = make_double2(s2, s3);
+  lds_barrier();
+  if (t < 64) {
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) {
+      const double2 x = sc[w * 64 + t], y = sc[NT + w * 64 + t];
+      a0 += x.x; a1 += x.y; a2 += y.x; a3 += y.y;
+    }
+    a0 = wave_sum_d(a0); a1 = wave_sum_d(a1); a2 = wave_sum_d(a2); a3 = wave_sum_d(a3);
+    const double mb = a0 / M, mv = a2 / M;
+    double vb = a1 / M - mb * mb, vv = a3 / M - mv * mv;
+    vb = vb > 0.0 ? vb : 0.0;
+    vv = vv > 0.0 ? vv : 0.0;
+    // a spread of B within its rounding is none (B equal in exact arithmetic)
+    if (sqrt(vb) <= (double)b_floor * (bref + mb)) vb = 0.0;
+    if (t == 0) *lam_s = (float)((double)gamma * sqrt(vb) / (sqrt(vv) + (double)eps));
+  }
+  lds_barrier();
+  return *lam_s;
+}
+
 // Exclusive prefix sum over threads in index order.
 template <int NT>
 __device__ __forceinline__ unsigned block_excl_scan_u(unsigned v, SelSharedT<NT> &ss) {
@@ -3109,7 +3145,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
   __shared__ int cpos[kSegCandCap];
   __shared__ SelSharedT<NT> ss;
   __shared__ unsigned pre[kAllPer * NW + 1];
-  __shared__ float2 mom[kMomChunk];
+  __shared__ __align__(16) float2 mom[kMomChunk];
   __shared__ __align__(16) int scnt[kMaxSegs];
   __shared__ float vref_s;
   const int t = threadIdx.x;
@@ -3184,15 +3220,9 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
       s0 = part[0]; s1 = part[1]; s2 = part[2]; s3 = part[3];
       bref_set = part[4];
     }
-    double sums[4];
-    block_sum4_d(s0, s1, s2, s3, ss, sums);
-    const double mb = sums[0] / M, mv = sums[2] / M;
-    double vb = sums[1] / M - mb * mb, vv = sums[3] / M - mv * mv;
-    vb = vb > 0.0 ? vb : 0.0;
-    vv = vv > 0.0 ? vv : 0.0;
-    // a spread of B within its rounding is none (B equal in exact arithmetic)
-    if (sqrt(vb) <= (double)a.b_floor * (bref_set + mb)) vb = 0.0;
-    lam = (float)((double)a.gamma * sqrt(vb) / (sqrt(vv) + (double)a.eps));
+    // the moment scratch is free here (its fallback user is done)
+    lam = block_lambda<NT>(s0, s1, s2, s3, M, bref_set, a.gamma, a.eps, a.b_floor,
+                           reinterpret_cast<double2 *>(mom), &vref_s);
   }
   if (sg == 0 && t == 0) {
     a.lambda_ws[b * a.Hkv + h] = lam;
