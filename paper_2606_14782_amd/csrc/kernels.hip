@@ -2851,8 +2851,10 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
         const int u = w0 + q;
         float v = ((a.terms & 1u) ? Es[q + kMaxRadius] : 0.f) + (use_t ? tv[j] * inv_cnt : 0.f);
         if (use_l && u >= 0 && u < n) {
+          // the mean through the hardware reciprocal (within an ulp or two
+          // of the quotient; an IEEE division costs ten instructions a wave)
           const int lo = max(0, u - r), hi = min(n - 1, u + r);
-          v += ls[j] / (float)(hi - lo + 1);
+          v += ls[j] * __builtin_amdgcn_rcpf((float)(hi - lo + 1));
         }
         // B and V are 0 outside the candidates: the pool windows need no
         // per-position bounds either
@@ -2905,9 +2907,9 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
   for (int j = 0; j < PER; ++j) {
     const int q = t + j * NT, i = i0 + q;
     if (q < ncand) {
-      const float cnt = (float)(min(nc - 1, i + hp) - max(0, i - hp) + 1);
-      a.vec_pB[base + i] = sb[j] / cnt;
-      a.vec_pV[base + i] = sv[j] / cnt;
+      const float inv = __builtin_amdgcn_rcpf((float)(min(nc - 1, i + hp) - max(0, i - hp) + 1));
+      a.vec_pB[base + i] = sb[j] * inv;
+      a.vec_pV[base + i] = sv[j] * inv;
       a.vec_V[base + i] = xv[j];
     }
   }
