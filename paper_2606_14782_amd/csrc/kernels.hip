@@ -2572,6 +2572,50 @@ constexpr int kMaxSegs = kMaxSeqLen / kSegLen;             // segments of a sequ
 constexpr int kMomChunk = 4096;                            // scale-matching entries per LDS round
 static_assert(kAllPer <= 32 && kHPer % 4 == 0 && kMaxSegs <= 64, "select layout");
 
+// Budget fields of the select kernels.  The sequence table sits in the
+// kernel arguments, the optional per-sequence (sb) and per-head (hb) tables
+// in global memory; read through one conditional expression, the two are
+// merged into a generic load of a selected pointer, whose wait also waits
+// for every global load the wave has in flight.  The kernel-argument word is
+// taken apart (a scalar load behind an empty asm), and a table only when it
+// is given, waited for inside its branch: where no table is given, no wait
+// for global loads follows.
+__device__ __forceinline__ int kern_word(const int32_t &w) {
+  int v = w;
+  asm volatile("" : "+s"(v));
+  return v;
+}
+__device__ __forceinline__ int table_word(const int *p) {
+  int v = *p;
+  asm volatile("" : "+v"(v));
+  return v;
+}
+__device__ __forceinline__ int sel_seq_budget(const SeqTable &st, const int4 *sb, int b) {
+  int v = kern_word(st.budget[b]);
+  if (sb) v = table_word(&sb[b].x);
+  return v;
+}
+__device__ __forceinline__ int sel_seq_kept_base(const SeqTable &st, const int4 *sb, int b) {
+  int v = kern_word(st.kept_base[b]);
+  if (sb) v = table_word(&sb[b].z);
+  return v;
+}
+__device__ __forceinline__ int sel_head_budget(const SeqTable &st, const int2 *hb, int Hkv, int b, int h,
+                                               const int4 *sb) {
+  int v = sel_seq_budget(st, sb, b);
+  if (hb) v = table_word(&hb[b * Hkv + h].x);
+  return v;
+}
+__device__ __forceinline__ int64_t sel_head_idx_base(const SeqTable &st, const int2 *hb, int Hkv, int b,
+                                                     int h, const int4 *sb) {
+  int v = kern_word(st.idx_base[b]);
+  if (sb) v = table_word(&sb[b].y);
+  int w;
+  if (hb) w = table_word(&hb[b * Hkv + h].y);
+  else w = h * sel_seq_budget(st, sb, b);
+  return (int64_t)v + w;
+}
+
 __device__ __forceinline__ int find_seg(const SeqTable &st, int seg) {
   int b = 0;
   while (b + 1 < st.batch && st.seg_base[b + 1] <= seg) ++b;
@@ -2748,7 +2792,7 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
   const int64_t base = (int64_t)h * a.T + st.cu[b];
   const int r = a.radius;
   const bool use_l = (a.terms & 2u) != 0;
-  int M = scale_set_size(a.rho, head_budget(st, a.hb, a.Hkv, b, h, a.sb));
+  int M = scale_set_size(a.rho, sel_head_budget(st, a.hb, a.Hkv, b, h, a.sb));
   M = max(0, min(M, nc));
   const bool calib = M > 0 && a.use_last_query;
   // the bins of the B histogram (accumulated by the fused pass, in kHCopies
@@ -3177,7 +3221,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
     }
   }
 
-  int M = scale_set_size(a.rho, head_budget(st, a.hb, a.Hkv, b, h, a.sb));
+  int M = scale_set_size(a.rho, sel_head_budget(st, a.hb, a.Hkv, b, h, a.sb));
   M = max(0, min(M, nc));
   float lam = 0.f;
   if (M > 0 && a.use_last_query) {
@@ -3298,7 +3342,7 @@ __device__ __forceinline__ void segcand_body(SegArgs a, const SeqTable &st, int 
   const int i0 = sg * kSegLen;
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  const int kept = min(head_budget(st, a.hb, a.Hkv, b, h, a.sb), nc);
+  const int kept = min(sel_head_budget(st, a.hb, a.Hkv, b, h, a.sb), nc);
   if (kept <= 0 || kept == nc) return;               // none or all kept: no list needed
   unsigned cb[kHPer];
   load_bins<1>(a.hist_S + ((int64_t)b * a.Hkv + h) * kHBins, cb);
@@ -3387,11 +3431,11 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
   const int wave = t >> 6;
   const int n = st.cu[b + 1] - st.cu[b];
   const int nc = n - a.W;
-  const int K = head_budget(st, a.hb, a.Hkv, b, h, a.sb);   // this head's budget
-  const int C = a.flat_heads ? K : seq_budget(st, a.sb, b);  // rows of the head's block, less W
+  const int K = sel_head_budget(st, a.hb, a.Hkv, b, h, a.sb);   // this head's budget
+  const int C = a.flat_heads ? K : sel_seq_budget(st, a.sb, b);  // rows of the head's block, less W
   const int kept = min(K, nc);
   const int64_t base = (int64_t)h * a.T + st.cu[b];
-  int32_t *idx = a.idx + head_idx_base(st, a.hb, a.Hkv, b, h, a.sb);
+  int32_t *idx = a.idx + sel_head_idx_base(st, a.hb, a.Hkv, b, h, a.sb);
   if (kept > 0 && kept == nc) {
     // every candidate is kept
     for (int j = t; j < nc; j += NT) {
@@ -3469,6 +3513,7 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
   const unsigned char *vs = static_cast<const unsigned char *>(a.v);
   unsigned char *ko = static_cast<unsigned char *>(a.k_out);
   unsigned char *vo = static_cast<unsigned char *>(a.v_out);
+  const int kept_base = sel_seq_kept_base(st, a.sb, b);
   constexpr int BATCH = 4;
   for (int q0 = t; q0 < total; q0 += BATCH * NT) {
     u32x4 kv[BATCH], vv[BATCH];
@@ -3489,8 +3534,8 @@ __device__ __forceinline__ void final_body(SegArgs a, const SeqTable &st, int pa
       if (q < total) {
         const int rr = r0 + q / pieces, p = q % pieces;
         const int64_t row = a.flat_heads
-            ? (int64_t)a.Hkv * seq_kept_base(st, a.sb, b) + a.hb[b * a.Hkv + h].y + (int64_t)h * a.W + rr
-            : (int64_t)(seq_kept_base(st, a.sb, b) + rr) * a.Hkv + h;
+            ? (int64_t)a.Hkv * kept_base + a.hb[b * a.Hkv + h].y + (int64_t)h * a.W + rr
+            : (int64_t)(kept_base + rr) * a.Hkv + h;
         const int64_t dst = row * a.row_bytes + 16 * p;
         const u32x4 z = u32x4{0u, 0u, 0u, 0u};
         *reinterpret_cast<u32x4 *>(ko + dst) = srcs[u] >= 0 ? kv[u] : z;
