@@ -2864,30 +2864,40 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
     // V = E + L + T (Eq. structurally_calibrated_evidence, per the terms
     // mask), L = P_r E over the sequence-truncated neighbourhood
     // (Eq. intra_layer_coherence), T the mean of the earlier layers' E
-    // (Eq. inter_layer_persistence).  The neighbourhood's taps are read
-    // TAPS at a time for all of the thread's positions and summed in
-    // position order; a tap outside the sequence adds 0.
-    const float inv_cnt = a.ring_cnt ? 1.f / (float)a.ring_cnt : 0.f;
-    float ls[kSegWinJ];
-#pragma unroll
-    for (int j = 0; j < kSegWinJ; ++j) ls[j] = 0.f;
+    // (Eq. inter_layer_persistence).  The neighbourhood sums are taken for
+    // three consecutive window positions per thread, whose 2r + 1 taps
+    // overlap (2r + 3 LDS reads instead of 3 (2r + 1)), each summed in
+    // position order (a tap outside the sequence adds 0), and pass through
+    // Vs to the layout of the loads.
     if (use_l) {
-      for (int d0 = -r; d0 <= r; d0 += TAPS) {
-        float e[kSegWinJ][TAPS];
-#pragma unroll
-        for (int j = 0; j < kSegWinJ; ++j) {
-          const int q = min(tt + j * NT, kSegWin - 1);
-#pragma unroll
-          for (int k = 0; k < TAPS; ++k) e[j][k] = Es[q + kMaxRadius + d0 + k];
+      const int q0 = 3 * t;
+      if (q0 < kSegWin) {
+        const float *ep = Es + q0 + kMaxRadius - r;   // ep[k]: tap k of position q0 (k <= 2r)
+        float s0, s1, s2;
+        if (r == 0) {
+          s0 = ep[0]; s1 = ep[1]; s2 = ep[2];
+        } else {
+          s0 = ep[0];
+          s1 = ep[1];
+          s0 += s1;
+          s2 = 0.f;
+#pragma unroll 4
+          for (int k = 2; k <= 2 * r; ++k) {
+            const float x = ep[k];
+            s0 += x; s1 += x; s2 += x;
+          }
+          const float x = ep[2 * r + 1];
+          s1 += x;
+          s2 += x;
+          s2 += ep[2 * r + 2];
         }
-#pragma unroll
-        for (int k = 0; k < TAPS; ++k) {
-          const bool in = d0 + k <= r;                 // uniform
-#pragma unroll
-          for (int j = 0; j < kSegWinJ; ++j) ls[j] += in ? e[j][k] : 0.f;
-        }
+        Vs[q0] = s0;
+        if (q0 + 1 < kSegWin) Vs[q0 + 1] = s1;
+        if (q0 + 2 < kSegWin) Vs[q0 + 2] = s2;
       }
+      lds_barrier();
     }
+    const float inv_cnt = a.ring_cnt ? 1.f / (float)a.ring_cnt : 0.f;
 #pragma unroll
     for (int j = 0; j < kSegWinJ; ++j) {
       const int q = tt + j * NT;
@@ -2898,7 +2908,7 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
           // the mean through the hardware reciprocal (within an ulp or two
           // of the quotient; an IEEE division costs ten instructions a wave)
           const int lo = max(0, u - r), hi = min(n - 1, u + r);
-          v += ls[j] * __builtin_amdgcn_rcpf((float)(hi - lo + 1));
+          v += Vs[q] * __builtin_amdgcn_rcpf((float)(hi - lo + 1));
         }
         // B and V are 0 outside the candidates: the pool windows need no
         // per-position bounds either
@@ -2915,46 +2925,39 @@ __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st
   lds_barrier();
 
   // V, and the pooled B and V over I (truncated windows), of the segment's
-  // candidates; the window's taps TAPS at a time, summed in position order
-  // (a tap outside the candidates adds 0)
+  // candidates: two consecutive candidates per thread, whose 2hp + 1 taps
+  // overlap, each summed in position order (a tap outside the candidates
+  // adds 0)
   const int hp = a.pool_half;
   const int ncand = max(0, min(i0 + kSegLen, nc) - i0);
-  float xb[PER], xv[PER], sb[PER], sv[PER];
+  float xb[PER], xv[PER];
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     const int q = t + j * NT;
     xb[j] = Bs[kPoolHalo + q];
     xv[j] = Vs[kPoolHalo + q];
-    sb[j] = 0.f;
-    sv[j] = 0.f;
   }
-  for (int d0 = -hp; d0 <= hp; d0 += TAPS) {
-    float pb[PER][TAPS], pv[PER][TAPS];
-#pragma unroll
-    for (int j = 0; j < PER; ++j)
-#pragma unroll
-      for (int k = 0; k < TAPS; ++k) {
-        pb[j][k] = Bs[kPoolHalo + t + j * NT + d0 + k];
-        pv[j][k] = Vs[kPoolHalo + t + j * NT + d0 + k];
-      }
-#pragma unroll
-    for (int k = 0; k < TAPS; ++k) {
-      const bool in = d0 + k <= hp;                    // uniform
-#pragma unroll
-      for (int j = 0; j < PER; ++j) {
-        sb[j] += in ? pb[j][k] : 0.f;
-        sv[j] += in ? pv[j][k] : 0.f;
-      }
+  {
+    static_assert(PER == 2, "two consecutive candidates per thread");
+    const int q0 = 2 * t;
+    const float *bp = Bs + kPoolHalo + q0 - hp, *vp = Vs + kPoolHalo + q0 - hp;   // tap k of q0 (k <= 2hp)
+    float b0 = bp[0], v0 = vp[0], b1 = 0.f, v1 = 0.f;
+#pragma unroll 4
+    for (int k = 1; k <= 2 * hp; ++k) {
+      const float x = bp[k], y = vp[k];
+      b0 += x; b1 += x; v0 += y; v1 += y;
     }
-  }
+    b1 += bp[2 * hp + 1];
+    v1 += vp[2 * hp + 1];
 #pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int q = t + j * NT, i = i0 + q;
-    if (q < ncand) {
-      const float inv = __builtin_amdgcn_rcpf((float)(min(nc - 1, i + hp) - max(0, i - hp) + 1));
-      a.vec_pB[base + i] = sb[j] * inv;
-      a.vec_pV[base + i] = sv[j] * inv;
-      a.vec_V[base + i] = xv[j];
+    for (int j = 0; j < 2; ++j) {
+      const int q = q0 + j, i = i0 + q;
+      if (q < ncand) {
+        const float inv = __builtin_amdgcn_rcpf((float)(min(nc - 1, i + hp) - max(0, i - hp) + 1));
+        a.vec_pB[base + i] = (j ? b1 : b0) * inv;
+        a.vec_pV[base + i] = (j ? v1 : v0) * inv;
+        a.vec_V[base + i] = Vs[kPoolHalo + q];
+      }
     }
   }
   if (!calib) return;
