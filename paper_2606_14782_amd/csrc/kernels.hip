@@ -1830,27 +1830,34 @@ __device__ __forceinline__ void block_sum4_d(double v0, double v1, double v2, do
 // Scale-matching factor lambda (Eq. lambda_solution) from each thread's
 // partial moment sums over the scale-matching set of size M: sum of B - bref,
 // of its square, of V - vref and of its square.  The partials go through
-// LDS (sc: 2 * NT double2) to wave 0, which sums them in a fixed order
-// (thread w*64 + lane into lane `lane` for w ascending, then across the
-// lanes) and forms lambda; the other waves wait at the barrier rather than
-// each repeat the double-precision reduction and arithmetic.  Ends with a
-// barrier; returns lambda in every thread.
+// LDS (sc: 4 * NT doubles, one row per sum); wave k < 4 sums row k in a
+// fixed order (thread w*64 + lane into lane `lane` for w ascending, then
+// across the lanes), and wave 0 forms lambda from the four totals; the
+// other waves wait at the barriers rather than each repeat the
+// double-precision reduction and arithmetic.  Ends with a barrier; returns
+// lambda in every thread.
 template <int NT>
 __device__ __forceinline__ float block_lambda(double s0, double s1, double s2, double s3, int M,
                                               double bref, float gamma, float eps, float b_floor,
-                                              double2 *sc, float *lam_s) {
-  const int t = threadIdx.x;
-  sc[t] = make_double2(s0, s1);
-  sc[NT + t] = make_double2(s2, s3);
+                                              double *sc, SelSharedT<NT> &ss, float *lam_s) {
+  static_assert(NT >= 256, "four reducing waves");
+  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  sc[t] = s0;
+  sc[NT + t] = s1;
+  sc[2 * NT + t] = s2;
+  sc[3 * NT + t] = s3;
   lds_barrier();
-  if (t < 64) {
-    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  if (wave < 4) {
+    const double *row = sc + wave * NT;
+    double acc = 0.0;
 #pragma unroll
-    for (int w = 0; w < NT / 64; ++w) {
-      const double2 x = sc[w * 64 + t], y = sc[NT + w * 64 + t];
-      a0 += x.x; a1 += x.y; a2 += y.x; a3 += y.y;
-    }
-    a0 = wave_sum_d(a0); a1 = wave_sum_d(a1); a2 = wave_sum_d(a2); a3 = wave_sum_d(a3);
+    for (int w = 0; w < NT / 64; ++w) acc += row[w * 64 + lane];
+    acc = wave_sum_d(acc);
+    if (lane == 0) ss.bc_d[wave] = acc;
+  }
+  lds_barrier();
+  if (wave == 0) {
+    const double a0 = ss.bc_d[0], a1 = ss.bc_d[1], a2 = ss.bc_d[2], a3 = ss.bc_d[3];
     const double mb = a0 / M, mv = a2 / M;
     double vb = a1 / M - mb * mb, vv = a3 / M - mv * mv;
     vb = vb > 0.0 ? vb : 0.0;
@@ -2581,7 +2588,9 @@ static_assert(kAllPer <= 32 && kHPer % 4 == 0 && kMaxSegs <= 64, "select layout"
 // is given, waited for inside its branch: where no table is given, no wait
 // for global loads follows.
 __device__ __forceinline__ int kern_word(const int32_t &w) {
-  int v = w;
+  // (uniform: the read-first-lane is free, and lets the scalar constraint
+  // hold wherever the compiler placed the load)
+  int v = __builtin_amdgcn_readfirstlane(w);
   asm volatile("" : "+s"(v));
   return v;
 }
@@ -3271,7 +3280,7 @@ __device__ __forceinline__ void segscore_body(SegArgs a, const SeqTable &st, int
     }
     // the moment scratch is free here (its fallback user is done)
     lam = block_lambda<NT>(s0, s1, s2, s3, M, bref_set, a.gamma, a.eps, a.b_floor,
-                           reinterpret_cast<double2 *>(mom), &vref_s);
+                           reinterpret_cast<double *>(mom), ss, &vref_s);
   }
   if (sg == 0 && t == 0) {
     a.lambda_ws[b * a.Hkv + h] = lam;
