@@ -559,6 +559,16 @@ EDGE = {
     "m1-pool1-r9": dict(wl=inputs.Workload("edge", 4, 4, 2, 64, 16, 1, "bf16", (600,), (32,),
                                            ((40, 500),), 2, 12),
                         gpu=dict(radius=9, persist_m=1), orc=dict(radius=9, persist_m=1)),
+    # the calibration kernel sums the neighbourhoods of three consecutive
+    # window positions and the pools of two consecutive candidates per
+    # thread: radius 1 runs its shared-tap loop once, radius 2 with pool 5
+    # twice, on lengths whose segments end in a partial thread
+    "radius1-pool3": dict(wl=inputs.Workload("edge", 3, 4, 2, 64, 16, 3, "bf16", (2500, 701), (48, 20),
+                                             ((40, 2000), (10, 600)), 2, 34),
+                          gpu=dict(radius=1), orc=dict(radius=1)),
+    "radius2-pool5-ragged": dict(wl=inputs.Workload("edge", 3, 4, 2, 64, 16, 5, "bf16", (4099, 1030),
+                                                    (64, 24), ((100, 3900), (0, 900)), 2, 35),
+                                 gpu=dict(radius=2), orc=dict(radius=2)),
     "window-score-only": dict(wl=inputs.Workload("edge", 2, 8, 2, 128, 32, 7, "bf16", (1000,),
                                                  (64,), ((30, 800),), 3, 13),
                               gpu=dict(use_last_query=0), orc=dict(use_last_query=0)),
