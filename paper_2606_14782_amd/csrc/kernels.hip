@@ -2786,7 +2786,10 @@ struct ListView {
 // Calibration kernel (segment_calib).
 __device__ __forceinline__ void segcal_body(const SegArgs &a, const SeqTable &st, int gs, int h, int b) {
   constexpr int NT = kSegThreads, PER = kSegPer, NW = NT / 64;
-  constexpr int TAPS = 8;                           // window taps read per round
+  // zeroed slots past the end of the LDS windows: the neighbourhood sums of
+  // the last window positions read E up to two slots past its window (at
+  // the largest radius)
+  constexpr int TAPS = 8;
   __shared__ float Bs[kSegWin + TAPS], Vs[kSegWin + TAPS];
   __shared__ float Es[kSegE + TAPS];
   __shared__ SelSharedT<NT> ss;
