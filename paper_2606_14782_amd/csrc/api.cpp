@@ -839,9 +839,11 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
   g.v_out = d_v_out;
   g.row_bytes = c->shape.head_dim * (r.bf16 ? 2 : 4);
   g.flat_heads = r.adaptive;
-  // final workgroups per (sequence, KV head): about one round over the CUs
+  // final workgroups per (sequence, KV head): up to eight, but no more than
+  // keep the launch to the rounds over the CUs that one part per head needs
   // (in a prompt call the score workgroups of the next layer share the
-  // launch: fewer parts where that lets both fit in one round of the CUs)
+  // launch, one 1024-thread workgroup per CU: a batch whose score
+  // workgroups alone fill the CUs takes more rounds with every part)
   if (c->cus < 0) {
     int dev = 0;
     c->cus = 256;
@@ -853,9 +855,10 @@ bacon_status plan_layer(bacon_ctx *c, int32_t layer, const bacon_batch *bt, cons
   {
     const int hkv = c->shape.num_kv_heads, heads = std::max(1, bt->batch * hkv);
     const int score_wgs = r.st.total_segs * hkv;
-    g.parts = std::max(1, std::min(8, c->cus / heads));
-    if (score_wgs + g.parts * heads > c->cus && score_wgs + heads <= c->cus)
-      g.parts = (c->cus - score_wgs) / heads;
+    auto rounds = [&](int p) { return (score_wgs + p * heads + c->cus - 1) / c->cus; };
+    int p = std::max(1, std::min(8, c->cus / heads));
+    while (p > 1 && rounds(p) > rounds(1)) --p;
+    g.parts = p;
   }
   return BACON_OK;
 }
