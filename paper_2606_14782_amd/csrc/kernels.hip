@@ -3574,24 +3574,25 @@ __global__ __launch_bounds__(kSegThreads) void k_segfinal(SegArgs a, SeqTable st
 
 // Launches that carry work of two or three layers (a prompt's layers in
 // flight at once; the jobs of one launch share no buffer, see the host's
-// schedule).  Columns of workgroups, per KV head (blockIdx.y):
-//  * k_sel_a: [0, ncand) the candidate lists of the previous layer (gp),
-//    [ncand, ncand + nmerge) the next layer's row normalisers (m; each
-//    workgroup takes kSegThreads / kMergeThreads row groups of a sequence),
-//    then the calibration of this layer (g).  The short jobs come first, so
-//    that they hold CUs only briefly.
-//  * k_sel_b: [0, nfinal) the final top-K and compaction of the previous
-//    layer (parts per sequence), then the scores of this layer.
-// The jobs of one launch in grid order, the longest first: workgroups are
-// dispatched in that order, and those that find no CU free wait for one.
+// schedule):
+//  * k_sel_a, jobs along blockIdx.y and KV heads along blockIdx.x: [0, nseg)
+//    the calibration of this layer (g), [nseg, nseg + ncand) the candidate
+//    lists of the previous layer (gp), then the next layer's row
+//    normalisers (m; each workgroup takes kSegThreads / kMergeThreads row
+//    groups of a sequence).  Workgroups are dispatched x first, so every
+//    head's calibration (the longest job) is dispatched before any shorter
+//    one, and a grid beyond one round of the CUs leaves short jobs waiting.
+//  * k_sel_b, jobs along blockIdx.x per KV head (blockIdx.y): [0, nfinal)
+//    the final top-K and compaction of the previous layer (parts per
+//    sequence), then the scores of this layer.
 __global__ __launch_bounds__(kSegThreads) void k_sel_a(SegArgs g, SegArgs gp, PassArgs m, SeqTable st,
                                                       int ncand, int nmerge) {
-  const int h = blockIdx.y, nseg = st.total_segs;
-  if ((int)blockIdx.x < nseg) {
-    segcal_body(g, st, blockIdx.x, h, find_seg(st, blockIdx.x));
+  const int h = blockIdx.x, job = blockIdx.y, nseg = st.total_segs;
+  if (job < nseg) {
+    segcal_body(g, st, job, h, find_seg(st, job));
     return;
   }
-  const int x = blockIdx.x - nseg;
+  const int x = job - nseg;
   if (x < ncand) {
     segcand_body(gp, st, x, h, find_seg(st, x));
   } else if (x < ncand + nmerge) {
@@ -3647,7 +3648,7 @@ hipError_t launch_sel_a(const SegArgs &g, const SegArgs *gp, const PassArgs *m, 
     nmerge = st.batch * ((m->Rpad / kMergeRows + groups - 1) / groups);
   }
   const int ncand = gp ? st.total_segs : 0;
-  dim3 grid(ncand + nmerge + st.total_segs, g.Hkv), block(kSegThreads);
+  dim3 grid(g.Hkv, ncand + nmerge + st.total_segs), block(kSegThreads);
   hipLaunchKernelGGL(k_sel_a, grid, block, 0, s, g, gp ? *gp : g, m ? *m : PassArgs{}, st, ncand,
                      nmerge);
   return hipGetLastError();
